@@ -1,0 +1,37 @@
+"""Plain, slow, fp64 CPU oracle for the action-expert per-tick forward.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  The product path
+(the HIP library and its Python binding) never imports, calls or links it, and
+this package imports nothing from the product path.
+
+What it computes (the expert of Sec. 3.1, "Action Expert with Per-Layer Cache
+Attention", run once per control tick as in Sec. 3.3):
+
+* ``expert.py``  -- RMSNorm, rotary encoding, the joint attention of Eq. (1)
+  over [cached backbone K/V ; the expert's own K/V], the output projection, the
+  SwiGLU block, and the mean-pool + linear waypoint head.
+* ``fp8.py``     -- decoding of OCP FP8 E4M3 (e4m3fn) codes, used only to build
+  the diagnostic reference for the fp8-stored cache.
+
+Every function is the plain definition evaluated in float64 on the exact values
+the GPU receives (inputs are rounded to the stored dtype first, then upcast).
+Readings of points the paper leaves open are listed at the top of each module.
+Parity status: every function is pinned by the ``-m "not gpu"`` tests in
+``tests/test_oracle_pins.py``; no function is "parity unpinned" except the
+end-to-end composition, which has no printed worked example in the paper and is
+pinned only through its pinned parts and invariants (see those tests).
+"""
+
+from .expert import (  # noqa: F401
+    ExpertShape,
+    rmsnorm,
+    rope_cos_sin,
+    apply_rope,
+    joint_attention,
+    swiglu_ffn,
+    expert_layer,
+    waypoint_head,
+    expert_forward,
+)
+from .fp8 import e4m3fn_decode  # noqa: F401
