@@ -1,0 +1,182 @@
+/*
+ * fsx.h -- C ABI of the action-expert fast path (MI355X / gfx950).
+ *
+ * The method (Sec. 3.1, "Action Expert with Per-Layer Cache Attention"): a small
+ * transformer (the "action expert") runs once per control tick.  At each of its
+ * layers it projects its own tokens into the frozen backbone's attention geometry
+ * (H heads of width Dh), attends jointly over [the backbone's cached keys/values
+ * of that layer ; its own keys/values] (Eq. (1)), projects back to width d and
+ * applies a SwiGLU block; a head regresses waypoints.  The backbone never attends
+ * to expert tokens, so the cache is read-only for the expert and can be kept as
+ * standing state that the slow system extends by appending rows every K ticks
+ * (Sec. 3.3, "Asynchronous Deployment").
+ *
+ * This header exposes exactly that per-tick path:
+ *   fsx_expert_create      -- pack the expert's weights into library-owned device memory
+ *   fsx_expert_forward     -- one tick: all layers + head, for a batch of agents
+ *   fsx_cache_append_rows  -- append new cached K/V rows (the slow system's output)
+ * plus destroy / error / introspection helpers.
+ *
+ * Conventions shared by every call
+ *   - All functions return an fsx_status (0 = FSX_OK).  Argument and shape checks
+ *     run before any GPU work is enqueued; on error nothing is enqueued and
+ *     fsx_last_error() (thread-local) holds a message.
+ *   - "device" pointers are HIP device memory of the current device; "host"
+ *     pointers are ordinary CPU memory.  No call keeps a caller pointer after it
+ *     returns, except that enqueued GPU work reads/writes the caller's device
+ *     buffers later in stream order.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Work is
+ *     enqueued on it asynchronously; GPU faults surface at the caller's next
+ *     synchronisation of that stream.
+ *   - Matrices use the nn.Linear layout [out][in], row-major, densely packed.
+ *   - No exception crosses this boundary.
+ */
+#ifndef FSX_H
+#define FSX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FSX_OK = 0,
+  FSX_E_INVALID = 1,     /* bad argument, NULL pointer, inconsistent shapes */
+  FSX_E_UNSUPPORTED = 2, /* valid request the library does not implement */
+  FSX_E_CAPACITY = 3,    /* batch/rows beyond what was provisioned, or ring full under FSX_APPEND_ERROR */
+  FSX_E_OOM = 4,         /* device allocation failed */
+  FSX_E_HIP = 5          /* a HIP runtime call or kernel launch failed */
+} fsx_status;
+
+typedef enum {
+  FSX_F32 = 0,      /* IEEE binary32 */
+  FSX_BF16 = 1,     /* bfloat16 */
+  FSX_FP8_E4M3 = 2  /* OCP FP8 E4M3 ("e4m3fn": bias 7, max 448, no inf); cache only */
+} fsx_dtype;
+
+enum { FSX_APPEND_RING = 0, FSX_APPEND_ERROR = 1 };
+
+/* Flags of fsx_expert_cfg.flags. */
+enum {
+  FSX_FLAG_GENERIC = 1,     /* force the simple per-op kernels instead of the fused tick kernel */
+  FSX_FLAG_MULTI_LAUNCH = 2 /* run the fused path as one launch per phase instead of one persistent launch */
+};
+
+#define FSX_MAX_BATCH 64
+
+/* Sizes of the expert (Sec. 3.1: 32 layers, width d = 512, backbone geometry 32 heads x 128,
+ * 10 expert tokens, 5 (x, y) waypoints).  The FFN width is not given by the paper. */
+typedef struct {
+  int32_t n_layers;         /* > 0 */
+  int32_t d_model;          /* d  (expert width) */
+  int32_t n_heads;          /* H  (backbone heads) */
+  int32_t head_dim;         /* Dh (backbone head width); A = H * Dh */
+  int32_t d_ffn;            /* SwiGLU hidden width */
+  int32_t n_expert_tokens;  /* T: tokens pooled by the waypoint head */
+  int32_t n_out;            /* head outputs (10 = 5 waypoints x (x, y)) */
+  int32_t max_batch;        /* agents per forward, 1..FSX_MAX_BATCH */
+  int32_t max_frame_tokens; /* F: extra current-frame tokens per agent, >= 0 */
+  int32_t dtype;            /* fsx_dtype of weights and tokens: FSX_F32 or FSX_BF16 */
+  float rope_base;          /* rotary base for expert q/k (pairs j, j+Dh/2); 0 = no rotary */
+  float rms_eps;            /* RMSNorm epsilon */
+  int32_t flags;            /* FSX_FLAG_* */
+} fsx_expert_cfg;
+
+/* One layer's parameters, DEVICE pointers, elements of cfg.dtype (norm gains always fp32). */
+typedef struct {
+  const void* wq;          /* [A][d] */
+  const void* wk;          /* [A][d] */
+  const void* wv;          /* [A][d] */
+  const void* wo;          /* [d][A] */
+  const void* w_gate;      /* [d_ffn][d] */
+  const void* w_up;        /* [d_ffn][d] */
+  const void* w_down;      /* [d][d_ffn] */
+  const float* attn_norm;  /* [d] RMSNorm gain before attention */
+  const float* ffn_norm;   /* [d] RMSNorm gain before the FFN */
+} fsx_layer_weights;
+
+/* The backbone's per-layer KV cache for a batch of agents (Sec. 3.1, Sec. 3.3).
+ * Each (agent, layer) owns a ring of `capacity` rows; a row holds one cached token's
+ * keys (or values) for all heads, [H][Dh].  Keys are stored already rotated.
+ * The valid rows of agent b are ring slots (start[b] + i) mod capacity, i < len[b]. */
+typedef struct {
+  int32_t dtype;           /* FSX_F32 | FSX_BF16 | FSX_FP8_E4M3 */
+  int32_t batch;           /* agents described by this descriptor */
+  int32_t n_layers;        /* must equal the expert's */
+  int32_t n_heads;         /* must equal the expert's */
+  int32_t head_dim;        /* must equal the expert's */
+  int32_t reserved;        /* 0 */
+  int64_t capacity;        /* ring rows per (agent, layer) */
+  void* k;                 /* DEVICE [batch][n_layers][capacity][H][Dh] */
+  void* v;                 /* DEVICE, same layout */
+  const float* k_scale;    /* FP8 only: DEVICE [batch][n_layers][H], stored value = code * scale */
+  const float* v_scale;    /* FP8 only: DEVICE [batch][n_layers][H] */
+  int64_t* start;          /* HOST [batch]: ring slot of the oldest valid row */
+  int64_t* len;            /* HOST [batch]: valid rows, 0..capacity */
+  int64_t* pos;            /* HOST [batch]: position of the agent's expert token 0 (rotary angle) */
+} fsx_cache_desc;
+
+typedef struct fsx_expert fsx_expert;
+
+/* Pack an expert's weights into library-owned device memory.
+ *   cfg        sizes and dtype (validated; FSX_E_INVALID / FSX_E_UNSUPPORTED on bad values)
+ *   layers     HOST array of cfg.n_layers descriptors (DEVICE weight pointers)
+ *   final_norm DEVICE [d] fp32 gain of the RMSNorm before the head
+ *   head_w     DEVICE [n_out][d] (cfg.dtype) waypoint head weight, no bias
+ *   stream     used for the packing copies; the call synchronises it before returning,
+ *              so the caller may free its weight buffers afterwards
+ *   out        receives the handle (NULL on failure)
+ * Allocates the packed weights and a workspace sized for cfg.max_batch agents of
+ * T + max_frame_tokens tokens. */
+int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weights* layers, const float* final_norm,
+                      const void* head_w, void* stream, fsx_expert** out);
+
+/* One control tick for `batch` agents (Sec. 3.1, Eq. (1); Sec. 3.3: the expert reads the cache as-is).
+ *   cache          descriptor; only rows (start+i) mod capacity, i < len[b], are read.  The
+ *                  cache is never written.  batch <= cache->batch.
+ *   tokens         DEVICE [batch][S][d] (cfg.dtype), S = T + n_frame_tokens; rows < T are the
+ *                  expert tokens, the rest current-frame tokens.  Token t of agent b sits at
+ *                  rotary position pos[b] + t.
+ *   n_frame_tokens 0..cfg.max_frame_tokens
+ *   waypoints      DEVICE [batch][n_out] fp32 output
+ *   hidden         DEVICE [n_layers][batch][S][d] fp32 output of every layer, or NULL
+ * Uses only library-owned workspace; allocates nothing.  Calls that overlap on one
+ * expert handle (e.g. from two streams) race on its workspace. */
+int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, const void* tokens, int32_t batch,
+                       int32_t n_frame_tokens, float* waypoints, float* hidden, void* stream);
+
+/* Append n_rows new cached rows to every (agent, layer) of the cache (Sec. 3.3: every K ticks the
+ * slow system appends the current frame's tokens through an incremental forward).
+ *   k_rows, v_rows DEVICE [cache->batch][n_layers][n_rows][H][Dh] in cache->dtype (fp8: codes
+ *                  already scaled by the cache's k_scale / v_scale)
+ *   policy         FSX_APPEND_RING: when a ring is full the oldest rows are overwritten (start
+ *                  advances); FSX_APPEND_ERROR: FSX_E_CAPACITY if any agent would exceed
+ *                  capacity, and nothing is written.
+ * The row copy is enqueued on `stream` (bit-exact); len/start/pos in the descriptor are
+ * updated on the host before returning (pos advances by n_rows), so later calls enqueued
+ * on the same stream see the new rows. */
+int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, const void* v_rows, int32_t n_rows,
+                          int32_t policy, void* stream);
+
+/* Free the packed weights and the workspace (synchronises the device first). NULL is a no-op. */
+void fsx_expert_destroy(fsx_expert* ex);
+
+/* Message of the calling thread's last failed call ("" if none). */
+const char* fsx_last_error(void);
+
+/* Introspection of a handle (any pointer may be NULL):
+ *   path          0 = fused tick kernel (bf16 weights), 1 = simple per-op kernels
+ *   weight_bytes  bytes of the packed weight matrices the tick streams (excludes fp32 norm gains)
+ *   workspace_bytes device workspace owned by the handle */
+int fsx_expert_info(const fsx_expert* ex, int32_t* path, int64_t* weight_bytes, int64_t* workspace_bytes);
+
+/* Library version, "major.minor.patch". */
+const char* fsx_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FSX_H */

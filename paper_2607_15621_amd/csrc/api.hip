@@ -1,0 +1,407 @@
+// C ABI of the expert tick: validation, weight packing, workspace, split planning and the per-tick
+// launch sequence.  See include/fsx.h for the contract of every entry point.
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+
+using namespace fsx;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                          \
+  do {                                                                                         \
+    hipError_t e_ = (expr);                                                                    \
+    if (e_ != hipSuccess) return fail(FSX_E_HIP, std::string(#expr ": ") + hipGetErrorString(e_)); \
+  } while (0)
+
+int esize(int dtype) { return dtype == FSX_F32 ? 4 : (dtype == FSX_BF16 ? 2 : 1); }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int KSPLIT_MAX = 8;
+
+}  // namespace
+
+struct fsx_expert {
+  fsx_expert_cfg cfg{};
+  int path = 0;  // 0 fused bf16 path, 1 per-op path
+  int device = 0;
+  int A = 0, S_max = 0, M_max = 0, items_max = 0;
+  void* wbuf = nullptr;    // packed (fused) or copied (per-op) weight matrices
+  float* fbuf = nullptr;   // norm gains: [n_layers][2][d] then final [d]
+  void* head_w = nullptr;  // [n_out][d] cfg.dtype
+  void* wsbuf = nullptr;   // workspace
+  int64_t weight_bytes = 0, ws_bytes = 0;
+  std::vector<FastWeights> fw;
+  std::vector<GenericWeights> gw;
+  Workspace ws{};
+  GenericWorkspace gws{};
+  const float* final_norm = nullptr;
+};
+
+static void free_expert(fsx_expert* ex) {
+  if (!ex) return;
+  if (ex->wbuf) (void)hipFree(ex->wbuf);
+  if (ex->fbuf) (void)hipFree(ex->fbuf);
+  if (ex->head_w) (void)hipFree(ex->head_w);
+  if (ex->wsbuf) (void)hipFree(ex->wsbuf);
+  delete ex;
+}
+
+static int validate_cfg(const fsx_expert_cfg* c) {
+  if (!c) return fail(FSX_E_INVALID, "cfg is NULL");
+  if (c->n_layers <= 0 || c->d_model <= 0 || c->n_heads <= 0 || c->head_dim <= 0 || c->d_ffn <= 0)
+    return fail(FSX_E_INVALID, "n_layers, d_model, n_heads, head_dim and d_ffn must be positive");
+  if (c->head_dim % 2) return fail(FSX_E_INVALID, "head_dim must be even (rotary pairs)");
+  if (c->n_expert_tokens <= 0 || c->n_out <= 0) return fail(FSX_E_INVALID, "n_expert_tokens and n_out must be positive");
+  if (c->max_batch <= 0 || c->max_batch > FSX_MAX_BATCH) return fail(FSX_E_INVALID, "max_batch must be in 1..64");
+  if (c->max_frame_tokens < 0) return fail(FSX_E_INVALID, "max_frame_tokens must be >= 0");
+  if (c->dtype != FSX_F32 && c->dtype != FSX_BF16) return fail(FSX_E_UNSUPPORTED, "weights must be F32 or BF16");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_base >= 0.f)) return fail(FSX_E_INVALID, "rms_eps and rope_base must be >= 0");
+  if ((int64_t)c->n_heads * c->head_dim > (1 << 20) || c->d_model > (1 << 16) || c->d_ffn > (1 << 18))
+    return fail(FSX_E_UNSUPPORTED, "sizes beyond the supported range");
+  return FSX_OK;
+}
+
+extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weights* layers, const float* final_norm,
+                                 const void* head_w, void* stream, fsx_expert** out) {
+  if (!out) return fail(FSX_E_INVALID, "out is NULL");
+  *out = nullptr;
+  int rc = validate_cfg(cfg);
+  if (rc) return rc;
+  if (!layers || !final_norm || !head_w) return fail(FSX_E_INVALID, "layers, final_norm and head_w must be non-NULL");
+  const fsx_expert_cfg& c = *cfg;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const fsx_layer_weights& w = layers[l];
+    if (!w.wq || !w.wk || !w.wv || !w.wo || !w.w_gate || !w.w_up || !w.w_down || !w.attn_norm || !w.ffn_norm)
+      return fail(FSX_E_INVALID, "layer " + std::to_string(l) + " has a NULL pointer");
+  }
+  hipStream_t s = (hipStream_t)stream;
+  fsx_expert* ex = new fsx_expert();
+  ex->cfg = c;
+  if (hipGetDevice(&ex->device) != hipSuccess) {
+    delete ex;
+    return fail(FSX_E_HIP, "hipGetDevice failed");
+  }
+  const int d = c.d_model, F = c.d_ffn, H = c.n_heads, Dh = c.head_dim;
+  const int A = H * Dh;
+  ex->A = A;
+  ex->S_max = c.n_expert_tokens + c.max_frame_tokens;
+  ex->M_max = c.max_batch * ex->S_max;
+  const bool fused_ok = c.dtype == FSX_BF16 && Dh == 128 && d % 32 == 0 && F % 32 == 0;
+  ex->path = (fused_ok && !(c.flags & FSX_FLAG_GENERIC)) ? 0 : 1;
+  const int es = esize(c.dtype);
+  const int64_t per_layer = (int64_t)4 * A * d + (int64_t)3 * F * d;  // elements
+  ex->weight_bytes = (per_layer * c.n_layers + (int64_t)c.n_out * d) * es;
+
+  int last = FSX_OK;
+  auto cleanup = [&](int code) {
+    free_expert(ex);
+    return last != FSX_OK ? last : code;
+  };
+  auto ok = [&](hipError_t e, const char* what) -> bool {
+    if (e != hipSuccess) {
+      last = e == hipErrorOutOfMemory ? FSX_E_OOM : FSX_E_HIP;
+      fail(last, std::string(what) + ": " + hipGetErrorString(e));
+      return false;
+    }
+    return true;
+  };
+
+  if (!ok(hipMalloc(&ex->wbuf, (size_t)(per_layer * c.n_layers * es)), "hipMalloc(weights)")) return cleanup(FSX_E_OOM);
+  if (!ok(hipMalloc((void**)&ex->fbuf, sizeof(float) * ((size_t)2 * c.n_layers * d + d)), "hipMalloc(norms)"))
+    return cleanup(FSX_E_OOM);
+  if (!ok(hipMalloc(&ex->head_w, (size_t)c.n_out * d * es), "hipMalloc(head)")) return cleanup(FSX_E_OOM);
+
+  // norm gains and head
+  for (int l = 0; l < c.n_layers; ++l) {
+    if (!ok(hipMemcpyAsync(ex->fbuf + (size_t)(2 * l) * d, layers[l].attn_norm, sizeof(float) * d,
+                           hipMemcpyDeviceToDevice, s), "copy attn_norm") ||
+        !ok(hipMemcpyAsync(ex->fbuf + (size_t)(2 * l + 1) * d, layers[l].ffn_norm, sizeof(float) * d,
+                           hipMemcpyDeviceToDevice, s), "copy ffn_norm"))
+      return cleanup(FSX_E_HIP);
+  }
+  ex->final_norm = ex->fbuf + (size_t)2 * c.n_layers * d;
+  if (!ok(hipMemcpyAsync((void*)ex->final_norm, final_norm, sizeof(float) * d, hipMemcpyDeviceToDevice, s),
+          "copy final_norm") ||
+      !ok(hipMemcpyAsync(ex->head_w, head_w, (size_t)c.n_out * d * es, hipMemcpyDeviceToDevice, s), "copy head"))
+    return cleanup(FSX_E_HIP);
+
+  char* wp = (char*)ex->wbuf;
+  if (ex->path == 0) {
+    for (int l = 0; l < c.n_layers; ++l) {
+      const fsx_layer_weights& w = layers[l];
+      const void* ptrs[7] = {w.wq, w.wk, w.wv, w.wo, w.w_gate, w.w_up, w.w_down};
+      for (const void* p : ptrs)
+        if (!aligned16(p)) {
+          fail(FSX_E_INVALID, "bf16 weight pointers must be 16-byte aligned");
+          return cleanup(FSX_E_INVALID);
+        }
+      FastWeights f{};
+      const size_t sq = (size_t)A * d * 2;  // bytes of one [A][d] bf16 matrix
+      f.wqkv = (const uint4*)wp;
+      bool good = ok(launch_pack((const uint16_t*)w.wq, nullptr, A, d, PACK_ROPE_PAIRS, Dh, wp, s), "pack wq") &&
+                  ok(launch_pack((const uint16_t*)w.wk, nullptr, A, d, PACK_ROPE_PAIRS, Dh, wp + sq, s), "pack wk") &&
+                  ok(launch_pack((const uint16_t*)w.wv, nullptr, A, d, PACK_PLAIN, 0, wp + 2 * sq, s), "pack wv");
+      wp += 3 * sq;
+      f.wo = (const uint4*)wp;
+      good = good && ok(launch_pack((const uint16_t*)w.wo, nullptr, d, A, PACK_PLAIN, 0, wp, s), "pack wo");
+      wp += sq;
+      f.wgu = (const uint4*)wp;
+      good = good && ok(launch_pack((const uint16_t*)w.w_gate, (const uint16_t*)w.w_up, 2 * F, d, PACK_SWIGLU_PAIRS, 0,
+                                    wp, s), "pack gate/up");
+      wp += (size_t)2 * F * d * 2;
+      f.wd = (const uint4*)wp;
+      good = good && ok(launch_pack((const uint16_t*)w.w_down, nullptr, d, F, PACK_PLAIN, 0, wp, s), "pack down");
+      wp += (size_t)F * d * 2;
+      if (!good) return cleanup(FSX_E_HIP);
+      f.attn_norm = ex->fbuf + (size_t)(2 * l) * d;
+      f.ffn_norm = ex->fbuf + (size_t)(2 * l + 1) * d;
+      ex->fw.push_back(f);
+    }
+  } else {
+    for (int l = 0; l < c.n_layers; ++l) {
+      const fsx_layer_weights& w = layers[l];
+      GenericWeights g{};
+      const size_t n_ad = (size_t)A * d * es, n_fd = (size_t)F * d * es;
+      const void* src[7] = {w.wq, w.wk, w.wv, w.wo, w.w_gate, w.w_up, w.w_down};
+      const size_t sz[7] = {n_ad, n_ad, n_ad, n_ad, n_fd, n_fd, n_fd};
+      const void** dst[7] = {&g.wq, &g.wk, &g.wv, &g.wo, &g.wg, &g.wu, &g.wd};
+      for (int i = 0; i < 7; ++i) {
+        if (!ok(hipMemcpyAsync(wp, src[i], sz[i], hipMemcpyDeviceToDevice, s), "copy weights")) return cleanup(FSX_E_HIP);
+        *dst[i] = wp;
+        wp += sz[i];
+      }
+      g.attn_norm = ex->fbuf + (size_t)(2 * l) * d;
+      g.ffn_norm = ex->fbuf + (size_t)(2 * l + 1) * d;
+      ex->gw.push_back(g);
+    }
+  }
+
+  // workspace
+  const int M = ex->M_max;
+  const int n_tt_max = (ex->S_max + 15) / 16;
+  ex->items_max = std::max(16384, 2 * c.max_batch * H * n_tt_max + 64);
+  std::vector<std::pair<void**, size_t>> parts;
+  if (ex->path == 0) {
+    parts = {{(void**)&ex->ws.h, (size_t)M * d * 4},
+             {(void**)&ex->ws.xb, (size_t)M * d * 2},
+             {(void**)&ex->ws.q, (size_t)M * A * 4},
+             {(void**)&ex->ws.kself, (size_t)M * A * 2},
+             {(void**)&ex->ws.vself, (size_t)M * A * 2},
+             {(void**)&ex->ws.attn, (size_t)M * A * 2},
+             {(void**)&ex->ws.z, (size_t)M * F * 2},
+             {(void**)&ex->ws.part, (size_t)KSPLIT_MAX * M * d * 4},
+             {(void**)&ex->ws.att_o, (size_t)ex->items_max * 16 * Dh * 4},
+             {(void**)&ex->ws.att_ml, (size_t)ex->items_max * 32 * 4},
+             {(void**)&ex->ws.rope, (size_t)M * Dh * 4}};
+  } else {
+    parts = {{(void**)&ex->gws.h, (size_t)M * d * 4},   {(void**)&ex->gws.x, (size_t)M * d * 4},
+             {(void**)&ex->gws.q, (size_t)M * A * 4},   {(void**)&ex->gws.k, (size_t)M * A * 4},
+             {(void**)&ex->gws.v, (size_t)M * A * 4},   {(void**)&ex->gws.attn, (size_t)M * A * 4},
+             {(void**)&ex->gws.g, (size_t)M * F * 4},   {(void**)&ex->gws.u, (size_t)M * F * 4},
+             {(void**)&ex->gws.rope, (size_t)M * Dh * 4}};
+  }
+  size_t total = 0;
+  for (auto& p : parts) total += (p.second + 255) & ~(size_t)255;
+  if (!ok(hipMalloc(&ex->wsbuf, total), "hipMalloc(workspace)")) return cleanup(FSX_E_OOM);
+  ex->ws_bytes = (int64_t)total;
+  char* q = (char*)ex->wsbuf;
+  for (auto& p : parts) {
+    *p.first = q;
+    q += (p.second + 255) & ~(size_t)255;
+  }
+  if (!ok(hipStreamSynchronize(s), "hipStreamSynchronize(create)")) return cleanup(FSX_E_HIP);
+  *out = ex;
+  g_err.clear();
+  return FSX_OK;
+}
+
+static int validate_cache(const fsx_expert* ex, const fsx_cache_desc* c, int batch) {
+  if (!c) return fail(FSX_E_INVALID, "cache is NULL");
+  if (c->dtype != FSX_F32 && c->dtype != FSX_BF16 && c->dtype != FSX_FP8_E4M3)
+    return fail(FSX_E_INVALID, "cache dtype must be F32, BF16 or FP8_E4M3");
+  if (ex && (c->n_layers != ex->cfg.n_layers || c->n_heads != ex->cfg.n_heads || c->head_dim != ex->cfg.head_dim))
+    return fail(FSX_E_INVALID, "cache geometry (n_layers, n_heads, head_dim) differs from the expert's");
+  if (c->batch <= 0 || c->batch > FSX_MAX_BATCH) return fail(FSX_E_INVALID, "cache batch must be in 1..64");
+  if (batch > c->batch) return fail(FSX_E_INVALID, "batch exceeds the cache descriptor's batch");
+  if (c->capacity < 0 || c->capacity > (int64_t)INT32_MAX) return fail(FSX_E_INVALID, "capacity out of range");
+  if (!c->start || !c->len || !c->pos) return fail(FSX_E_INVALID, "start, len and pos must be non-NULL host arrays");
+  bool any = false;
+  for (int b = 0; b < batch; ++b) {
+    if (c->len[b] < 0 || c->len[b] > c->capacity)
+      return fail(FSX_E_CAPACITY, "len[" + std::to_string(b) + "] outside 0..capacity");
+    if (c->len[b] > 0 && (c->start[b] < 0 || c->start[b] >= c->capacity))
+      return fail(FSX_E_INVALID, "start[" + std::to_string(b) + "] outside 0..capacity-1");
+    if (c->pos[b] < 0 || c->pos[b] > ((int64_t)1 << 40)) return fail(FSX_E_INVALID, "pos out of range");
+    any = any || c->len[b] > 0;
+  }
+  if (any && (!c->k || !c->v)) return fail(FSX_E_INVALID, "cache k/v pointers are NULL");
+  if (any && c->dtype == FSX_FP8_E4M3 && (!c->k_scale || !c->v_scale))
+    return fail(FSX_E_INVALID, "fp8 cache needs k_scale and v_scale");
+  if (any && (!aligned16(c->k) || !aligned16(c->v))) return fail(FSX_E_INVALID, "cache k/v must be 16-byte aligned");
+  return FSX_OK;
+}
+
+extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, const void* tokens, int32_t batch,
+                                  int32_t n_frame_tokens, float* waypoints, float* hidden, void* stream) {
+  if (!ex) return fail(FSX_E_INVALID, "expert handle is NULL");
+  if (!tokens || !waypoints) return fail(FSX_E_INVALID, "tokens and waypoints must be non-NULL");
+  const fsx_expert_cfg& c = ex->cfg;
+  if (batch <= 0) return fail(FSX_E_INVALID, "batch must be positive");
+  if (batch > c.max_batch) return fail(FSX_E_CAPACITY, "batch exceeds max_batch");
+  if (n_frame_tokens < 0 || n_frame_tokens > c.max_frame_tokens)
+    return fail(FSX_E_CAPACITY, "n_frame_tokens outside 0..max_frame_tokens");
+  int rc = validate_cache(ex, cache, batch);
+  if (rc) return rc;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev != ex->device) return fail(FSX_E_INVALID, "current device differs from the one the expert was created on");
+  if (ex->path == 0 && cache->dtype == FSX_F32) return fail(FSX_E_UNSUPPORTED, "the bf16 expert reads BF16 or FP8 caches");
+  if (ex->path == 0 && !aligned16(tokens)) return fail(FSX_E_INVALID, "tokens must be 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+
+  TickParams tp{};
+  tp.B = batch;
+  tp.S = c.n_expert_tokens + n_frame_tokens;
+  tp.T = c.n_expert_tokens;
+  tp.M = batch * tp.S;
+  tp.n_tt = (tp.S + 15) / 16;
+  int64_t rows = 0;
+  for (int b = 0; b < batch; ++b) {
+    tp.pos[b] = cache->pos[b];
+    tp.start[b] = cache->len[b] > 0 ? cache->start[b] : 0;
+    tp.len[b] = (int32_t)cache->len[b];
+    rows += cache->len[b];
+  }
+  Dims dm{};
+  dm.d = c.d_model; dm.H = c.n_heads; dm.Dh = c.head_dim; dm.A = ex->A; dm.F = c.d_ffn; dm.n_layers = c.n_layers;
+  dm.n_out = c.n_out; dm.eps = c.rms_eps; dm.rope_base = c.rope_base;
+  CacheView cv{};
+  cv.k = cache->k; cv.v = cache->v; cv.k_scale = cache->k_scale; cv.v_scale = cache->v_scale;
+  cv.cap = cache->capacity; cv.n_layers = cache->n_layers; cv.layer = 0; cv.dtype = cache->dtype;
+
+  if (ex->path == 1) {
+    HIP_TRY(generic_tick(ex->gw.data(), ex->final_norm, ex->head_w, c.dtype, tokens, cv, tp, dm, ex->gws, waypoints,
+                         hidden, s));
+    g_err.clear();
+    return FSX_OK;
+  }
+
+  // split plan: chunk rows (multiple of 32) so that the work items number about 2048
+  const int target = 2048;
+  const int64_t work = rows * dm.H * tp.n_tt;
+  int64_t cr = (work + target - 1) / target;
+  cr = std::max<int64_t>(32, ((cr + 31) / 32) * 32);
+  int n_items = 0;
+  for (;;) {
+    int64_t slots = 0;
+    for (int b = 0; b < batch; ++b) slots += (tp.len[b] + cr - 1) / cr + 1;
+    const int64_t items = slots * dm.H * tp.n_tt;
+    if (items <= ex->items_max) {
+      n_items = (int)items;
+      break;
+    }
+    cr *= 2;
+  }
+  tp.chunk_rows = (int)cr;
+  tp.n_items = n_items;
+  tp.chunk_prefix[0] = 0;
+  for (int b = 0; b < batch; ++b) tp.chunk_prefix[b + 1] = tp.chunk_prefix[b] + (int)((tp.len[b] + cr - 1) / cr) + 1;
+  const int wpg = n_items >= 1024 ? 4 : 1;
+  auto kspl = [](int KB) { return KB % 8 == 0 ? 8 : (KB % 4 == 0 ? 4 : (KB % 2 == 0 ? 2 : 1)); };
+  const int ks_o = kspl(dm.A / 32), ks_d = kspl(dm.F / 32);
+
+  HIP_TRY(launch_embed(tokens, c.dtype, ex->fw[0].attn_norm, tp, dm, ex->ws, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const FastWeights& w = ex->fw[l];
+    cv.layer = l;
+    HIP_TRY(launch_gemm_qkv(w, tp, dm, ex->ws, s));
+    HIP_TRY(launch_attention(cv, tp, dm, ex->ws, wpg, s));
+    HIP_TRY(launch_combine(tp, dm, ex->ws, s));
+    HIP_TRY(launch_gemm_o(w, tp, dm, ex->ws, ks_o, s));
+    HIP_TRY(launch_reduce_norm(tp, dm, ex->ws, ks_o, w.ffn_norm, nullptr, s));
+    HIP_TRY(launch_gemm_gu(w, tp, dm, ex->ws, s));
+    HIP_TRY(launch_gemm_down(w, tp, dm, ex->ws, ks_d, s));
+    const float* gnext = l + 1 < c.n_layers ? ex->fw[l + 1].attn_norm : ex->final_norm;
+    HIP_TRY(launch_reduce_norm(tp, dm, ex->ws, ks_d, gnext, hidden ? hidden + (int64_t)l * tp.M * dm.d : nullptr, s));
+  }
+  HIP_TRY(launch_head(tp, dm, ex->ws, ex->final_norm, ex->head_w, c.dtype, waypoints, s));
+  g_err.clear();
+  return FSX_OK;
+}
+
+extern "C" int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, const void* v_rows, int32_t n_rows,
+                                     int32_t policy, void* stream) {
+  int rc = validate_cache(nullptr, cache, cache ? cache->batch : 0);
+  if (rc) return rc;
+  if (n_rows < 0) return fail(FSX_E_INVALID, "n_rows must be >= 0");
+  if (policy != FSX_APPEND_RING && policy != FSX_APPEND_ERROR) return fail(FSX_E_INVALID, "unknown append policy");
+  if (n_rows == 0) {
+    g_err.clear();
+    return FSX_OK;
+  }
+  if (!k_rows || !v_rows || !cache->k || !cache->v) return fail(FSX_E_INVALID, "row and cache pointers must be non-NULL");
+  if (n_rows > cache->capacity) return fail(FSX_E_CAPACITY, "n_rows exceeds the ring capacity");
+  if (cache->n_layers <= 0 || cache->n_heads <= 0 || cache->head_dim <= 0)
+    return fail(FSX_E_INVALID, "cache geometry must be positive");
+  const int64_t row_bytes = (int64_t)cache->n_heads * cache->head_dim * esize(cache->dtype);
+  if (row_bytes % 16) return fail(FSX_E_UNSUPPORTED, "a cache row must be a multiple of 16 bytes");
+  if (!aligned16(k_rows) || !aligned16(v_rows) || !aligned16(cache->k) || !aligned16(cache->v))
+    return fail(FSX_E_INVALID, "row and cache buffers must be 16-byte aligned");
+  const int B = cache->batch;
+  if (policy == FSX_APPEND_ERROR)
+    for (int b = 0; b < B; ++b)
+      if (cache->len[b] + n_rows > cache->capacity)
+        return fail(FSX_E_CAPACITY, "agent " + std::to_string(b) + ": ring full (policy FSX_APPEND_ERROR)");
+  std::vector<int64_t> first(B);
+  for (int b = 0; b < B; ++b) {
+    const int64_t st = cache->len[b] > 0 ? cache->start[b] : 0;
+    first[b] = (st + cache->len[b]) % cache->capacity;
+  }
+  HIP_TRY(launch_append(*cache, k_rows, v_rows, n_rows, first.data(), (hipStream_t)stream));
+  for (int b = 0; b < B; ++b) {
+    const int64_t st = cache->len[b] > 0 ? cache->start[b] : first[b];
+    const int64_t nl = cache->len[b] + n_rows;
+    if (nl <= cache->capacity) {
+      cache->start[b] = st;
+      cache->len[b] = nl;
+    } else {  // ring: the oldest rows were overwritten
+      cache->start[b] = (st + (nl - cache->capacity)) % cache->capacity;
+      cache->len[b] = cache->capacity;
+    }
+    cache->pos[b] += n_rows;
+  }
+  g_err.clear();
+  return FSX_OK;
+}
+
+extern "C" void fsx_expert_destroy(fsx_expert* ex) {
+  if (!ex) return;
+  (void)hipDeviceSynchronize();
+  free_expert(ex);
+}
+
+extern "C" const char* fsx_last_error(void) { return g_err.c_str(); }
+
+extern "C" int fsx_expert_info(const fsx_expert* ex, int32_t* path, int64_t* weight_bytes, int64_t* workspace_bytes) {
+  if (!ex) return fail(FSX_E_INVALID, "expert handle is NULL");
+  if (path) *path = ex->path;
+  if (weight_bytes) *weight_bytes = ex->weight_bytes;
+  if (workspace_bytes) *workspace_bytes = ex->ws_bytes;
+  return FSX_OK;
+}
+
+extern "C" const char* fsx_version(void) { return "0.1.0"; }

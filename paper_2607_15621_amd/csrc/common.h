@@ -1,0 +1,104 @@
+// Device-side building blocks shared by the kernels of the expert tick (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/fsx.h"
+
+namespace fsx {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
+typedef __attribute__((__vector_size__(2 * sizeof(_Float16)))) _Float16 f16x2;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+constexpr int WAVE = 64;
+constexpr float LOG2E = 1.4426950408889634f;
+
+// ---------------------------------------------------------------- scalar conversions
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// round-to-nearest-even float -> bf16 bits (finite inputs; NaN stays NaN)
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// two floats -> packed bf16x2 (RNE), low half = a
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+}
+
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+  _Float16 ha = (_Float16)a, hb = (_Float16)b;
+  return (uint32_t)__builtin_bit_cast(uint16_t, ha) | ((uint32_t)__builtin_bit_cast(uint16_t, hb) << 16);
+}
+
+// OCP E4M3 (e4m3fn) pair -> f16x2, exact (every E4M3 value is an fp16 value).  `word` selects
+// bytes 0-1 (false) or 2-3 (true) of `packed`.
+__device__ __forceinline__ uint32_t e4m3x2_to_f16x2(uint32_t packed, bool word) {
+  f16x2 r = word ? __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(packed, 1.0f, true)
+                 : __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(packed, 1.0f, false);
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+__device__ __forceinline__ float e4m3_to_f32(uint8_t c) {
+  uint32_t p = c;
+  f16x2 r = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p, 1.0f, false);
+  return (float)r[0];
+}
+
+// ---------------------------------------------------------------- MFMA (16x16x32, fp32 accumulate)
+// Operand layout (wave64): lane l holds A[row = l%16][k = 8*(l/16) + j] and
+// B[k = 8*(l/16) + j][col = l%16], j = 0..7; the result lane l holds
+// C[row = 4*(l/16) + i][col = l%16], i = 0..3.
+
+__device__ __forceinline__ f32x4 mfma_bf16(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4 mfma_f16(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                0, 0);
+}
+
+// ---------------------------------------------------------------- cross-lane helpers
+
+__device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v, m, WAVE); }
+__device__ __forceinline__ float shfl(float v, int src) { return __shfl(v, src, WAVE); }
+
+// Transpose an 8x8 block of 16-bit values held as 8 x uint4 (in[j] = row j, 8 columns) into
+// out[k] = column k as 8 values (element j = in[j][k]).
+__device__ __forceinline__ void transpose8x8_b16(const uint4 in[8], uint4 out[8]) {
+  const uint32_t* w = reinterpret_cast<const uint32_t*>(in);  // w[j*4 + k/2]
+  uint32_t* o = reinterpret_cast<uint32_t*>(out);            // o[k*4 + j/2]
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+#pragma unroll
+    for (int jp = 0; jp < 4; ++jp) {
+      uint32_t lo = w[(2 * jp) * 4 + k / 2];
+      uint32_t hi = w[(2 * jp + 1) * 4 + k / 2];
+      o[k * 4 + jp] = __builtin_amdgcn_perm(hi, lo, (k & 1) ? 0x07060302u : 0x05040100u);
+    }
+  }
+}
+
+__device__ __forceinline__ float block_sum(float v, float* scratch /* >= 16 floats */) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += shfl_xor(v, m);
+  const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
+  const int nw = (blockDim.x + WAVE - 1) / WAVE;
+  __syncthreads();
+  if (lane == 0) scratch[wave] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += scratch[i];
+  return t;
+}
+
+}  // namespace fsx

@@ -1,0 +1,655 @@
+// Kernels of the bf16 expert tick on gfx950 (Sec. 3.1, Eq. (1); Sec. 3.3).
+//
+// One tick, per layer:
+//   qkv   : x = RMSNorm(h) (bf16) times the packed [3A][d] projection on MFMA; epilogue applies the
+//           rotary rotation to q and k and folds 1/sqrt(Dh) * log2(e) into q.
+//   attn  : split-K ("flash-decode") joint attention.  A work item is (agent, head, chunk of cached
+//           rows, tile of 16 queries); the expert's own keys/values form one extra chunk per agent, so
+//           Eq. (1)'s single softmax over [cache ; own rows] is the log-sum-exp merge of the items.
+//   comb  : merges the items of each (agent, head) and writes the attention output (bf16).
+//   o     : output projection, split-K partial sums.
+//   norm  : h += sum of partials; x = RMSNorm(h) * gain (bf16) for the next projection.
+//   gu    : gate/up projection on MFMA with SwiGLU in the epilogue.
+//   down  : down projection, split-K partials; then norm again with the next layer's gain.
+// The head pools the first T tokens after a final RMSNorm and applies a d -> n_out map.
+
+#include "common.h"
+#include "kernels.h"
+
+namespace fsx {
+
+// =====================================================================================================
+// Weight packing.  A [N][K] bf16 matrix (nn.Linear layout) becomes N/16 x K/32 blocks of 1 KiB; block
+// (nt, kb) sits at element offset (nt*K/32 + kb)*512 and its 16-byte slot l (l = 0..63) holds
+// W[row(nt*16 + l%16)][kb*32 + 8*(l/16) + j], j = 0..7 -- exactly the B operand of a 16x16x32 MFMA for
+// output columns nt*16.. and k = kb*32.., so one wave reads a block with one fully coalesced 1 KiB load.
+// row() pairs rows for fused epilogues:
+//   PACK_ROPE_PAIRS  : within each head of width Dh, tile tau holds channels [8tau, 8tau+8) in columns
+//                      0..7 and [Dh/2 + 8tau, ...) in columns 8..15, so rotary partners are lanes l, l^8.
+//   PACK_SWIGLU_PAIRS: tile tau holds gate rows [8tau, 8tau+8) (from a) in columns 0..7 and the same up
+//                      rows (from b) in columns 8..15.
+// =====================================================================================================
+__global__ void k_pack(const uint16_t* __restrict__ a, const uint16_t* __restrict__ b, int N, int K, int kind,
+                       int param, uint4* __restrict__ dst) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int KB = K / 32;
+  const int64_t total = (int64_t)(N / 16) * KB * 64;
+  if (i >= total) return;
+  const int l = (int)(i & 63);
+  const int64_t blk = i >> 6;
+  const int kb = (int)(blk % KB);
+  const int nt = (int)(blk / KB);
+  const int n = nt * 16 + (l & 15);
+  const int kcol = kb * 32 + 8 * (l >> 4);
+  const uint16_t* src = a;
+  int64_t row = n;
+  if (kind == PACK_ROPE_PAIRS) {
+    const int Dh = param, half = Dh / 2;
+    const int head = n / Dh, p = n % Dh, tau = p / 16, c = p % 16;
+    row = (int64_t)head * Dh + (c < 8 ? 8 * tau + c : half + 8 * tau + (c - 8));
+  } else if (kind == PACK_SWIGLU_PAIRS) {
+    const int tau = n / 16, c = n % 16;
+    row = 8 * tau + (c & 7);
+    src = c < 8 ? a : b;
+  }
+  dst[i] = *reinterpret_cast<const uint4*>(src + row * K + kcol);
+}
+
+hipError_t launch_pack(const uint16_t* a, const uint16_t* b, int N, int K, int kind, int param, void* dst,
+                       hipStream_t s) {
+  const int64_t total = (int64_t)(N / 16) * (K / 32) * 64;
+  const int64_t blocks = (total + 255) / 256;
+  hipLaunchKernelGGL(k_pack, dim3((unsigned)blocks), dim3(256), 0, s, a, b, N, K, kind, param, (uint4*)dst);
+  return hipGetLastError();
+}
+
+// =====================================================================================================
+// Embed: h = tokens (fp32), x = bf16(RMSNorm(h) * g), rotary table cos/sin(p * base^(-2j/Dh)) in fp64.
+// One workgroup per token row.
+// =====================================================================================================
+__global__ __launch_bounds__(256) void k_embed(const void* __restrict__ tokens, int tok_dtype,
+                                               const float* __restrict__ g0, TickParams tp, Dims dm,
+                                               Workspace ws) {
+  __shared__ float red[16];
+  const int m = blockIdx.x;
+  const int b = m / tp.S, t = m % tp.S;
+  const int d = dm.d;
+  float ss = 0.f;
+  for (int n = threadIdx.x; n < d; n += blockDim.x) {
+    const int64_t idx = (int64_t)m * d + n;
+    const float v = tok_dtype == FSX_BF16 ? bf16_to_f32(((const uint16_t*)tokens)[idx]) : ((const float*)tokens)[idx];
+    ws.h[idx] = v;
+    ss += v * v;
+  }
+  ss = block_sum(ss, red);
+  const float r = 1.0f / sqrtf(ss / (float)d + dm.eps);
+  for (int n = threadIdx.x; n < d; n += blockDim.x) {
+    const int64_t idx = (int64_t)m * d + n;
+    ws.xb[idx] = f32_to_bf16(ws.h[idx] * r * g0[n]);
+  }
+  const int half = dm.Dh / 2;
+  for (int j = threadIdx.x; j < half; j += blockDim.x) {
+    double cs = 1.0, sn = 0.0;
+    if (dm.rope_base > 0.f) {
+      const double theta = pow((double)dm.rope_base, -2.0 * (double)j / (double)dm.Dh);
+      const double ang = (double)(tp.pos[b] + t) * theta;
+      cs = cos(ang);
+      sn = sin(ang);
+    }
+    ws.rope[((int64_t)m * half + j) * 2 + 0] = (float)cs;
+    ws.rope[((int64_t)m * half + j) * 2 + 1] = (float)sn;
+  }
+}
+
+hipError_t launch_embed(const void* tokens, int tok_dtype, const float* g0, const TickParams& tp, const Dims& dm,
+                        const Workspace& ws, hipStream_t s) {
+  hipLaunchKernelGGL(k_embed, dim3(tp.M), dim3(256), 0, s, tokens, tok_dtype, g0, tp, dm, ws);
+  return hipGetLastError();
+}
+
+// =====================================================================================================
+// Projection GEMM: y[m][n] = sum_k x[m][k] W[n][k], x bf16 [M][K], W packed (above).
+// Workgroup = 4 waves on one 16-column tile and one split-K range; the waves interleave its k-blocks,
+// then reduce their accumulators through LDS.  Each lane streams one 16-byte weight slot per k-block
+// (1 KiB coalesced per wave) and multiplies it by up to MT 16-row tiles of x.
+// =====================================================================================================
+enum { EPI_QKV = 0, EPI_SWIGLU = 1, EPI_PARTIAL = 2 };
+
+struct GemmArgs {
+  const uint16_t* x;
+  int ldx;
+  const uint4* w;
+  int M, K, N, ksplit;
+  float* out_f;      // QKV: q [M][A]; PARTIAL: [ksplit][M][N]
+  uint16_t* out_k;   // QKV
+  uint16_t* out_v;   // QKV
+  uint16_t* out_z;   // SWIGLU: [M][N/2]
+  const float* rope; // [M][Dh/2][2]
+  int A, Dh;
+  float q_scale;
+};
+
+template <int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x4 s, int row0, int nt, int ks, int c, int grp) {
+  const int n = nt * 16 + c;
+  if constexpr (EPI == EPI_PARTIAL) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = row0 + 4 * grp + i;
+      if (row < g.M) g.out_f[((int64_t)ks * g.M + row) * g.N + n] = s[i];
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float up = shfl_xor(s[i], 8);
+      const int row = row0 + 4 * grp + i;
+      if (c < 8 && row < g.M) {
+        const float gt = s[i];
+        const float zz = gt / (1.0f + expf(-gt)) * up;
+        g.out_z[(int64_t)row * (g.N / 2) + nt * 8 + c] = f32_to_bf16(zz);
+      }
+    }
+  } else {
+    const int A = g.A, Dh = g.Dh, half = Dh / 2;
+    const int sec = n / A;  // 0 = q, 1 = k, 2 = v (uniform across the tile)
+    const int nl = n - sec * A;
+    if (sec == 2) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = row0 + 4 * grp + i;
+        if (row < g.M) g.out_v[(int64_t)row * A + nl] = f32_to_bf16(s[i]);
+      }
+    } else {
+      const int head = nl / Dh, p = nl % Dh;
+      const int j = 8 * (p / 16) + (c & 7);
+      const int dch = c < 8 ? j : half + j;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float other = shfl_xor(s[i], 8);
+        const int row = row0 + 4 * grp + i;
+        const int rrow = row < g.M ? row : 0;
+        const float cs = g.rope[((int64_t)rrow * half + j) * 2 + 0];
+        const float sn = g.rope[((int64_t)rrow * half + j) * 2 + 1];
+        const float r = c < 8 ? s[i] * cs - other * sn : s[i] * cs + other * sn;
+        if (row < g.M) {
+          const int64_t o = (int64_t)row * A + head * Dh + dch;
+          if (sec == 0)
+            g.out_f[o] = r * g.q_scale;
+          else
+            g.out_k[o] = f32_to_bf16(r);
+        }
+      }
+    }
+  }
+}
+
+template <int MT, int EPI>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
+  __shared__ f32x4 red[4][MT][WAVE];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c = lane & 15, grp = lane >> 4;
+  const int n_tiles = g.N / 16;
+  const int nt = blockIdx.x % n_tiles, ks = blockIdx.x / n_tiles;
+  const int KB = g.K / 32;
+  const int kbs = KB / g.ksplit;
+  const int kb0 = ks * kbs, kb1 = kb0 + kbs;
+  const uint4* wt = g.w + (int64_t)nt * KB * WAVE + lane;
+  const int n_mt = (g.M + 15) / 16;
+  for (int mg = 0; mg < n_mt; mg += MT) {
+    f32x4 acc[MT];
+    const uint16_t* xr[MT];
+    bool ok[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int row = (mg + mt) * 16 + c;
+      ok[mt] = row < g.M;
+      xr[mt] = g.x + (int64_t)(ok[mt] ? row : 0) * g.ldx + 8 * grp;
+    }
+    for (int kb = kb0 + wave; kb < kb1; kb += 4) {
+      const uint4 wv = wt[(int64_t)kb * WAVE];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const uint4 xv = ok[mt] ? *reinterpret_cast<const uint4*>(xr[mt] + kb * 32) : make_uint4(0, 0, 0, 0);
+        acc[mt] = mfma_bf16(xv, wv, acc[mt]);
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) red[wave][mt][lane] = acc[mt];
+    __syncthreads();
+    for (int mt = wave; mt < MT; mt += 4) {
+      const f32x4 s = red[0][mt][lane] + red[1][mt][lane] + red[2][mt][lane] + red[3][mt][lane];
+      gemm_epilogue<EPI>(g, s, (mg + mt) * 16, nt, ks, c, grp);
+    }
+    __syncthreads();
+  }
+}
+
+template <int EPI>
+static hipError_t gemm_dispatch(const GemmArgs& g, hipStream_t s) {
+  const int n_mt = (g.M + 15) / 16;
+  const int groups = (n_mt + 7) / 8;
+  const int mt = (n_mt + groups - 1) / groups;
+  const dim3 grid((unsigned)((g.N / 16) * g.ksplit)), block(256);
+  switch (mt) {
+    case 1: hipLaunchKernelGGL((k_gemm<1, EPI>), grid, block, 0, s, g); break;
+    case 2: hipLaunchKernelGGL((k_gemm<2, EPI>), grid, block, 0, s, g); break;
+    case 3: hipLaunchKernelGGL((k_gemm<3, EPI>), grid, block, 0, s, g); break;
+    case 4: hipLaunchKernelGGL((k_gemm<4, EPI>), grid, block, 0, s, g); break;
+    case 5: hipLaunchKernelGGL((k_gemm<5, EPI>), grid, block, 0, s, g); break;
+    case 6: hipLaunchKernelGGL((k_gemm<6, EPI>), grid, block, 0, s, g); break;
+    case 7: hipLaunchKernelGGL((k_gemm<7, EPI>), grid, block, 0, s, g); break;
+    default: hipLaunchKernelGGL((k_gemm<8, EPI>), grid, block, 0, s, g); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_qkv(const FastWeights& w, const TickParams& tp, const Dims& dm, const Workspace& ws,
+                           hipStream_t s) {
+  GemmArgs g{};
+  g.x = ws.xb; g.ldx = dm.d; g.w = w.wqkv; g.M = tp.M; g.K = dm.d; g.N = 3 * dm.A; g.ksplit = 1;
+  g.out_f = ws.q; g.out_k = ws.kself; g.out_v = ws.vself; g.rope = ws.rope; g.A = dm.A; g.Dh = dm.Dh;
+  g.q_scale = LOG2E / sqrtf((float)dm.Dh);
+  return gemm_dispatch<EPI_QKV>(g, s);
+}
+
+hipError_t launch_gemm_o(const FastWeights& w, const TickParams& tp, const Dims& dm, const Workspace& ws,
+                         int ksplit, hipStream_t s) {
+  GemmArgs g{};
+  g.x = ws.attn; g.ldx = dm.A; g.w = w.wo; g.M = tp.M; g.K = dm.A; g.N = dm.d; g.ksplit = ksplit;
+  g.out_f = ws.part;
+  return gemm_dispatch<EPI_PARTIAL>(g, s);
+}
+
+hipError_t launch_gemm_gu(const FastWeights& w, const TickParams& tp, const Dims& dm, const Workspace& ws,
+                          hipStream_t s) {
+  GemmArgs g{};
+  g.x = ws.xb; g.ldx = dm.d; g.w = w.wgu; g.M = tp.M; g.K = dm.d; g.N = 2 * dm.F; g.ksplit = 1;
+  g.out_z = ws.z;
+  return gemm_dispatch<EPI_SWIGLU>(g, s);
+}
+
+hipError_t launch_gemm_down(const FastWeights& w, const TickParams& tp, const Dims& dm, const Workspace& ws,
+                            int ksplit, hipStream_t s) {
+  GemmArgs g{};
+  g.x = ws.z; g.ldx = dm.F; g.w = w.wd; g.M = tp.M; g.K = dm.F; g.N = dm.d; g.ksplit = ksplit;
+  g.out_f = ws.part;
+  return gemm_dispatch<EPI_PARTIAL>(g, s);
+}
+
+// =====================================================================================================
+// Split-K joint attention (Eq. (1)).  One wave = one work item = (agent b, head h, chunk of rows, query
+// tile tt).  Per 32-row tile:
+//   S^T = K Q^T on MFMA (A operand: 16 cached rows x 32 channels straight from memory, 16-byte loads;
+//   B operand: the 16 queries, kept in registers), scores already in log2 units (q is pre-scaled),
+//   online softmax with the row max reduced over the 4 lanes sharing a query (xor 16, xor 32),
+//   P (bf16/f16) re-used in place as the A operand of O += P V: the lane's own 8 scores are rows
+//   {4g..4g+3, 16+4g..16+4g+3}, and V is loaded as those 8 rows x 8 channels per lane (each load
+//   instruction reads 4 whole 256-byte rows) and transposed 8x8 in registers, so MFMA k (k = 0..7)
+//   produces output channels 8c + k.
+// The item writes its unnormalised output, running max and sum; k_combine merges them.
+// fp8 rows are decoded to fp16 in registers (exact) and use fp16 MFMA; the per-(agent, layer, head)
+// scales multiply the scores (keys) and the partial output (values).
+// =====================================================================================================
+struct AttnArgs {
+  CacheView cv;
+  const float* q;
+  const uint16_t* kself;
+  const uint16_t* vself;
+  float* att_o;
+  float* att_ml;
+  uint16_t* attn_out;  // [M][A] bf16 (combine output)
+  int H, Dh, A;
+};
+
+template <int KT>  // 0: bf16 operands, 1: f16 operands
+__device__ __forceinline__ void load_q_frag(const float* __restrict__ q, int64_t row, bool valid, int grp,
+                                            uint4 qf[4]) {
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
+    if (valid) {
+      const float4* p = reinterpret_cast<const float4*>(q + row + 32 * kb + 8 * grp);
+      lo = p[0];
+      hi = p[1];
+    }
+    if (KT == 0)
+      qf[kb] = make_uint4(pack_bf16x2(lo.x, lo.y), pack_bf16x2(lo.z, lo.w), pack_bf16x2(hi.x, hi.y),
+                          pack_bf16x2(hi.z, hi.w));
+    else
+      qf[kb] = make_uint4(pack_f16x2(lo.x, lo.y), pack_f16x2(lo.z, lo.w), pack_f16x2(hi.x, hi.y),
+                          pack_f16x2(hi.z, hi.w));
+  }
+}
+
+// 16-byte group of 8 consecutive channels of one row -> 8 x 16-bit MFMA operand values.
+template <int KT>
+__device__ __forceinline__ uint4 load8(const char* p) {
+  if constexpr (KT == 0) {
+    return *reinterpret_cast<const uint4*>(p);
+  } else {
+    const uint2 raw = *reinterpret_cast<const uint2*>(p);
+    return make_uint4(e4m3x2_to_f16x2(raw.x, false), e4m3x2_to_f16x2(raw.x, true), e4m3x2_to_f16x2(raw.y, false),
+                      e4m3x2_to_f16x2(raw.y, true));
+  }
+}
+
+// rows i in [i0, i1) of one (agent, head): row i lives at base + slot(i) * row_bytes, where
+// slot(i) = (start + i) mod cap for a ring and i for the expert's own rows.
+template <int KT, bool RING>
+__device__ void attn_rows(const char* __restrict__ kbase, const char* __restrict__ vbase, int64_t row_bytes,
+                          int64_t start, int64_t cap, int i0, int i1, const uint4 qf[4], float kscale, float vscale,
+                          int lane, float* __restrict__ out_o, float* __restrict__ out_ml, int Dh) {
+  constexpr int ES = KT == 0 ? 2 : 1;
+  const int c = lane & 15, grp = lane >> 4;
+  auto roff = [&](int i) -> int64_t {
+    int64_t slot = i;
+    if (RING) {
+      slot = start + i;
+      if (slot >= cap) slot -= cap;
+    }
+    return slot * row_bytes;
+  };
+  f32x4 o[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  for (int r0 = i0; r0 < i1; r0 += 32) {
+    uint4 kf[2][4];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      const int i = r0 + 16 * rt + c;
+      const char* p = kbase + roff(i < i1 ? i : i0);
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) kf[rt][kb] = load8<KT>(p + (32 * kb + 8 * grp) * ES);
+    }
+    uint4 vr[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int rr = r0 + (j < 4 ? 4 * grp + j : 16 + 4 * grp + (j - 4));
+      vr[j] = load8<KT>(vbase + roff(rr < i1 ? rr : i0) + 8 * c * ES);
+    }
+    f32x4 s[2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      s[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+        s[rt] = KT == 0 ? mfma_bf16(kf[rt][kb], qf[kb], s[rt]) : mfma_f16(kf[rt][kb], qf[kb], s[rt]);
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rr = r0 + 16 * rt + 4 * grp + i;
+        const float v = rr < i1 ? s[rt][i] * kscale : -INFINITY;
+        s[rt][i] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, shfl_xor(mx, 16));
+    mx = fmaxf(mx, shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = exp2f(m_run - m_new);
+    float p[8], ps = 0.f;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        p[rt * 4 + i] = exp2f(s[rt][i] - m_new);
+        ps += p[rt * 4 + i];
+      }
+    l_run = l_run * alpha + ps;
+    m_run = m_new;
+    uint4 pf;
+    if (KT == 0)
+      pf = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                      pack_bf16x2(p[6], p[7]));
+    else
+      pf = make_uint4(pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3]), pack_f16x2(p[4], p[5]), pack_f16x2(p[6], p[7]));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float a_i = shfl(alpha, 4 * grp + i);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) o[k][i] *= a_i;
+    }
+    uint4 vt[8];
+    transpose8x8_b16(vr, vt);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) o[k] = KT == 0 ? mfma_bf16(pf, vt[k], o[k]) : mfma_f16(pf, vt[k], o[k]);
+  }
+  float lt = l_run + shfl_xor(l_run, 16);
+  lt += shfl_xor(lt, 32);
+  if (grp == 0) {
+    out_ml[c * 2 + 0] = m_run;
+    out_ml[c * 2 + 1] = lt;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float4* dst = reinterpret_cast<float4*>(out_o + (4 * grp + i) * Dh + 8 * c);
+    dst[0] = make_float4(o[0][i] * vscale, o[1][i] * vscale, o[2][i] * vscale, o[3][i] * vscale);
+    dst[1] = make_float4(o[4][i] * vscale, o[5][i] * vscale, o[6][i] * vscale, o[7][i] * vscale);
+  }
+}
+
+template <int KT>
+__global__ __launch_bounds__(256) void k_attention(AttnArgs a, TickParams tp) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int item = blockIdx.x * (blockDim.x >> 6) + wave;
+  if (item >= tp.n_items) return;
+  const int tt = item % tp.n_tt;
+  const int rest = item / tp.n_tt;
+  const int h = rest % a.H;
+  const int cs = rest / a.H;
+  int b = 0;
+  while (b + 1 < tp.B && tp.chunk_prefix[b + 1] <= cs) ++b;
+  const int cidx = cs - tp.chunk_prefix[b];
+  const int nch = tp.chunk_prefix[b + 1] - tp.chunk_prefix[b] - 1;
+  const int grp = lane >> 4;
+  const int t = tt * 16 + (lane & 15);
+  const bool tv = t < tp.S;
+  const int64_t qrow = ((int64_t)b * tp.S + (tv ? t : 0)) * a.A + (int64_t)h * a.Dh;
+  float* out_o = a.att_o + (int64_t)item * 16 * a.Dh;
+  float* out_ml = a.att_ml + (int64_t)item * 32;
+  uint4 qf[4];
+  if (cidx == nch) {  // the expert's own rows (bf16)
+    load_q_frag<0>(a.q, qrow, tv, grp, qf);
+    const int64_t off = ((int64_t)b * tp.S * a.A + (int64_t)h * a.Dh) * 2;
+    attn_rows<0, false>((const char*)a.kself + off, (const char*)a.vself + off, (int64_t)a.A * 2, 0, 0, 0, tp.S, qf,
+                        1.f, 1.f, lane, out_o, out_ml, a.Dh);
+  } else {
+    const int i0 = cidx * tp.chunk_rows;
+    const int i1 = min(i0 + tp.chunk_rows, tp.len[b]);
+    const int64_t slab = ((int64_t)b * a.cv.n_layers + a.cv.layer) * a.cv.cap;
+    constexpr int ES = KT == 0 ? 2 : 1;
+    const int64_t off = (slab * a.A + (int64_t)h * a.Dh) * ES;
+    float ks = 1.f, vs = 1.f;
+    if (KT == 1) {
+      const int64_t si = ((int64_t)b * a.cv.n_layers + a.cv.layer) * a.H + h;
+      ks = a.cv.k_scale[si];
+      vs = a.cv.v_scale[si];
+    }
+    load_q_frag<KT>(a.q, qrow, tv, grp, qf);
+    attn_rows<KT, true>((const char*)a.cv.k + off, (const char*)a.cv.v + off, (int64_t)a.A * ES, tp.start[b],
+                        a.cv.cap, i0, i1, qf, ks, vs, lane, out_o, out_ml, a.Dh);
+  }
+}
+
+hipError_t launch_attention(const CacheView& cv, const TickParams& tp, const Dims& dm, const Workspace& ws,
+                            int waves_per_wg, hipStream_t s) {
+  AttnArgs a{};
+  a.cv = cv; a.q = ws.q; a.kself = ws.kself; a.vself = ws.vself; a.att_o = ws.att_o; a.att_ml = ws.att_ml;
+  a.H = dm.H; a.Dh = dm.Dh; a.A = dm.A;
+  const dim3 grid((unsigned)((tp.n_items + waves_per_wg - 1) / waves_per_wg)), block(64 * waves_per_wg);
+  if (cv.dtype == FSX_FP8_E4M3)
+    hipLaunchKernelGGL(k_attention<1>, grid, block, 0, s, a, tp);
+  else
+    hipLaunchKernelGGL(k_attention<0>, grid, block, 0, s, a, tp);
+  return hipGetLastError();
+}
+
+// Log-sum-exp merge of the work items of one (agent, head, query tile), in item order.
+__global__ __launch_bounds__(256) void k_combine(AttnArgs a, TickParams tp) {
+  const int tt = blockIdx.x % tp.n_tt;
+  const int rest = blockIdx.x / tp.n_tt;
+  const int h = rest % a.H;
+  const int b = rest / a.H;
+  const int first = tp.chunk_prefix[b], nslot = tp.chunk_prefix[b + 1] - first;
+  const int t = threadIdx.x >> 4, d0 = (threadIdx.x & 15) * 8;
+  float M = -INFINITY;
+  for (int sl = 0; sl < nslot; ++sl) {
+    const int64_t item = ((int64_t)(first + sl) * a.H + h) * tp.n_tt + tt;
+    M = fmaxf(M, a.att_ml[item * 32 + t * 2]);
+  }
+  float L = 0.f, acc[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+  for (int sl = 0; sl < nslot; ++sl) {
+    const int64_t item = ((int64_t)(first + sl) * a.H + h) * tp.n_tt + tt;
+    const float w = exp2f(a.att_ml[item * 32 + t * 2] - M);
+    L += a.att_ml[item * 32 + t * 2 + 1] * w;
+    const float4* po = reinterpret_cast<const float4*>(a.att_o + (item * 16 + t) * a.Dh + d0);
+    const float4 x0 = po[0], x1 = po[1];
+    acc[0] += x0.x * w; acc[1] += x0.y * w; acc[2] += x0.z * w; acc[3] += x0.w * w;
+    acc[4] += x1.x * w; acc[5] += x1.y * w; acc[6] += x1.z * w; acc[7] += x1.w * w;
+  }
+  const int tok = tt * 16 + t;
+  if (tok < tp.S) {
+    const float inv = 1.0f / L;
+    const uint4 out = make_uint4(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
+                                 pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv));
+    *reinterpret_cast<uint4*>(a.attn_out + ((int64_t)b * tp.S + tok) * a.A + (int64_t)h * a.Dh + d0) = out;
+  }
+}
+
+hipError_t launch_combine(const TickParams& tp, const Dims& dm, const Workspace& ws, hipStream_t s) {
+  AttnArgs a{};
+  a.att_o = ws.att_o; a.att_ml = ws.att_ml; a.attn_out = ws.attn; a.H = dm.H; a.Dh = dm.Dh; a.A = dm.A;
+  hipLaunchKernelGGL(k_combine, dim3((unsigned)(tp.B * dm.H * tp.n_tt)), dim3(256), 0, s, a, tp);
+  return hipGetLastError();
+}
+
+// =====================================================================================================
+// h += sum of split-K partials (fixed order), optional copy to the per-layer hidden output, then
+// x = bf16(RMSNorm(h) * gain) for the next projection.  One workgroup per token row.
+// =====================================================================================================
+__global__ __launch_bounds__(256) void k_reduce_norm(float* __restrict__ h, const float* __restrict__ part,
+                                                     uint16_t* __restrict__ xb, int M, int d, int ksplit,
+                                                     const float* __restrict__ gain, float eps,
+                                                     float* __restrict__ hidden) {
+  __shared__ float red[16];
+  const int m = blockIdx.x;
+  float ss = 0.f;
+  for (int n = threadIdx.x; n < d; n += blockDim.x) {
+    const int64_t idx = (int64_t)m * d + n;
+    float acc = 0.f;
+    for (int s = 0; s < ksplit; ++s) acc += part[((int64_t)s * M + m) * d + n];
+    const float v = h[idx] + acc;
+    h[idx] = v;
+    if (hidden) hidden[idx] = v;
+    ss += v * v;
+  }
+  ss = block_sum(ss, red);
+  const float r = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int n = threadIdx.x; n < d; n += blockDim.x) {
+    const int64_t idx = (int64_t)m * d + n;
+    xb[idx] = f32_to_bf16(h[idx] * r * gain[n]);
+  }
+}
+
+hipError_t launch_reduce_norm(const TickParams& tp, const Dims& dm, const Workspace& ws, int ksplit,
+                              const float* gain, float* hidden_layer, hipStream_t s) {
+  hipLaunchKernelGGL(k_reduce_norm, dim3(tp.M), dim3(256), 0, s, ws.h, (const float*)ws.part, ws.xb, tp.M, dm.d,
+                     ksplit, gain, dm.eps, hidden_layer);
+  return hipGetLastError();
+}
+
+// =====================================================================================================
+// Waypoint head: mean over the first T tokens of RMSNorm(h) * g_final, then W_head [n_out][d] (no bias).
+// One workgroup per agent.  Dynamic LDS: d floats.
+// =====================================================================================================
+__global__ __launch_bounds__(256) void k_head(const float* __restrict__ h, int S, int T, int d, float eps,
+                                              const float* __restrict__ gfin, const void* __restrict__ w,
+                                              int wdtype, int n_out, float* __restrict__ wp) {
+  extern __shared__ float xm[];
+  __shared__ float red[16];
+  const int b = blockIdx.x;
+  for (int n = threadIdx.x; n < d; n += blockDim.x) xm[n] = 0.f;
+  for (int t = 0; t < T; ++t) {
+    const float* hr = h + ((int64_t)b * S + t) * d;
+    float ss = 0.f;
+    for (int n = threadIdx.x; n < d; n += blockDim.x) ss += hr[n] * hr[n];
+    ss = block_sum(ss, red);
+    const float r = 1.0f / sqrtf(ss / (float)d + eps);
+    for (int n = threadIdx.x; n < d; n += blockDim.x) xm[n] += hr[n] * r * gfin[n];
+  }
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+  for (int o = wave; o < n_out; o += nw) {
+    float acc = 0.f;
+    for (int n = lane; n < d; n += WAVE) {
+      const float wv = wdtype == FSX_BF16 ? bf16_to_f32(((const uint16_t*)w)[(int64_t)o * d + n])
+                                          : ((const float*)w)[(int64_t)o * d + n];
+      acc += xm[n] * wv;
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) acc += shfl_xor(acc, m);
+    if (lane == 0) wp[(int64_t)b * n_out + o] = acc / (float)T;
+  }
+}
+
+hipError_t launch_head(const TickParams& tp, const Dims& dm, const Workspace& ws, const float* final_norm,
+                       const void* head_w, int head_dtype, float* waypoints, hipStream_t s) {
+  hipLaunchKernelGGL(k_head, dim3(tp.B), dim3(256), dm.d * sizeof(float), s, (const float*)ws.h, tp.S, tp.T, dm.d,
+                     dm.eps, final_norm, head_w, head_dtype, dm.n_out, waypoints);
+  return hipGetLastError();
+}
+
+// =====================================================================================================
+// Cache append (Sec. 3.3): copy n new rows of every (agent, layer) into ring slots
+// (first[b] + j) mod cap, bit-exact, 16 bytes per thread.
+// =====================================================================================================
+struct AppendArgs {
+  const uint4* ks;
+  const uint4* vs;
+  uint4* kc;
+  uint4* vc;
+  int64_t cap;
+  int64_t row_chunks;  // 16-byte chunks per row
+  int n_layers, n_rows, B;
+  int64_t first[FSX_MAX_BATCH];
+};
+
+__global__ __launch_bounds__(256) void k_append(AppendArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)a.B * a.n_layers * a.n_rows * a.row_chunks;
+  if (i >= total) return;
+  const int64_t ch = i % a.row_chunks;
+  int64_t r = i / a.row_chunks;
+  const int j = (int)(r % a.n_rows);
+  r /= a.n_rows;
+  const int l = (int)(r % a.n_layers);
+  const int b = (int)(r / a.n_layers);
+  int64_t slot = a.first[b] + j;
+  if (slot >= a.cap) slot -= a.cap;
+  const int64_t dst = (((int64_t)b * a.n_layers + l) * a.cap + slot) * a.row_chunks + ch;
+  a.kc[dst] = a.ks[i];
+  a.vc[dst] = a.vs[i];
+}
+
+hipError_t launch_append(const fsx_cache_desc& c, const void* k_rows, const void* v_rows, int n_rows,
+                         const int64_t* first, hipStream_t s) {
+  AppendArgs a{};
+  const int es = c.dtype == FSX_F32 ? 4 : (c.dtype == FSX_BF16 ? 2 : 1);
+  a.ks = (const uint4*)k_rows; a.vs = (const uint4*)v_rows; a.kc = (uint4*)c.k; a.vc = (uint4*)c.v;
+  a.cap = c.capacity; a.row_chunks = (int64_t)c.n_heads * c.head_dim * es / 16;
+  a.n_layers = c.n_layers; a.n_rows = n_rows; a.B = c.batch;
+  for (int b = 0; b < c.batch; ++b) a.first[b] = first[b];
+  const int64_t total = (int64_t)a.B * a.n_layers * a.n_rows * a.row_chunks;
+  if (total == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_append, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace fsx

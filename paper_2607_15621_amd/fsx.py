@@ -1,0 +1,190 @@
+"""Thin Python binding of libfsx (include/fsx.h): argument marshalling only.
+
+Every step of the expert tick runs in the HIP library; this module only turns
+torch tensors / numpy arrays into the raw pointers and sizes the C ABI takes,
+and turns non-zero status codes into exceptions.  If the library has not been
+built, loading it raises -- there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfsx.so")
+
+F32, BF16, FP8_E4M3 = 0, 1, 2
+APPEND_RING, APPEND_ERROR = 0, 1
+FLAG_GENERIC, FLAG_MULTI_LAUNCH = 1, 2
+MAX_BATCH = 64
+STATUS = {0: "FSX_OK", 1: "FSX_E_INVALID", 2: "FSX_E_UNSUPPORTED", 3: "FSX_E_CAPACITY", 4: "FSX_E_OOM",
+          5: "FSX_E_HIP"}
+SYMBOLS = ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_destroy",
+           "fsx_last_error", "fsx_expert_info", "fsx_version")
+
+
+class FsxError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class ExpertCfg(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("n_expert_tokens", ctypes.c_int32),
+                ("n_out", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("max_frame_tokens", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float),
+                ("flags", ctypes.c_int32)]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "attn_norm", "ffn_norm")]
+
+
+class CacheDescC(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("batch", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("capacity", ctypes.c_int64), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("k_scale", ctypes.c_void_p), ("v_scale", ctypes.c_void_p),
+                ("start", ctypes.POINTER(ctypes.c_int64)), ("len", ctypes.POINTER(ctypes.c_int64)),
+                ("pos", ctypes.POINTER(ctypes.c_int64))]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libfsx.so (built by ``paper_2607_15621_amd.build``); raises if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_15621_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        L.fsx_expert_create.argtypes = [ctypes.POINTER(ExpertCfg), ctypes.POINTER(LayerWeights), vp, vp, vp,
+                                        ctypes.POINTER(vp)]
+        L.fsx_expert_forward.argtypes = [vp, ctypes.POINTER(CacheDescC), vp, i32, i32, vp, vp, vp]
+        L.fsx_cache_append_rows.argtypes = [ctypes.POINTER(CacheDescC), vp, vp, i32, i32, vp]
+        L.fsx_expert_destroy.argtypes = [vp]
+        L.fsx_expert_destroy.restype = None
+        L.fsx_last_error.restype = ctypes.c_char_p
+        L.fsx_expert_info.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i64), ctypes.POINTER(i64)]
+        L.fsx_version.restype = ctypes.c_char_p
+        for n in ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_info"):
+            getattr(L, n).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().fsx_last_error().decode()
+
+
+def version() -> str:
+    return lib().fsx_version().decode()
+
+
+def _check(code: int):
+    if code != 0:
+        raise FsxError(code, last_error())
+
+
+def _ptr(t) -> int:
+    if t is None:
+        return 0
+    if isinstance(t, int):
+        return t
+    return int(t.data_ptr())
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+
+        return int(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return stream
+    return int(stream.cuda_stream)
+
+
+def make_cfg(n_layers, d_model, n_heads, head_dim, d_ffn, n_expert_tokens=10, n_out=10, max_batch=1,
+             max_frame_tokens=0, dtype=BF16, rope_base=10000.0, rms_eps=1e-6, flags=0) -> ExpertCfg:
+    return ExpertCfg(n_layers, d_model, n_heads, head_dim, d_ffn, n_expert_tokens, n_out, max_batch,
+                     max_frame_tokens, dtype, rope_base, rms_eps, flags)
+
+
+class Expert:
+    """Handle returned by fsx_expert_create; fsx_expert_destroy runs on close()."""
+
+    def __init__(self, handle: int, cfg: ExpertCfg):
+        self.handle = handle
+        self.cfg = cfg
+
+    def close(self):
+        if self.handle:
+            lib().fsx_expert_destroy(ctypes.c_void_p(self.handle))
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def expert_create(cfg: ExpertCfg, layers: Sequence[dict], final_norm, head_w, stream=None) -> Expert:
+    """fsx_expert_create.  layers: per layer a dict of device tensors (wq, wk, wv, wo, w_gate, w_up,
+    w_down, attn_norm, ffn_norm) in nn.Linear layout."""
+    arr = (LayerWeights * len(layers))()
+    for i, lw in enumerate(layers):
+        arr[i] = LayerWeights(*[_ptr(lw[n]) for n in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down",
+                                                        "attn_norm", "ffn_norm")])
+    out = ctypes.c_void_p(0)
+    _check(lib().fsx_expert_create(ctypes.byref(cfg), arr if len(layers) else None, _ptr(final_norm),
+                                   _ptr(head_w), _stream(stream), ctypes.byref(out)))
+    return Expert(out.value, cfg)
+
+
+def expert_info(ex: Expert):
+    path, wb, wsb = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().fsx_expert_info(ctypes.c_void_p(ex.handle), ctypes.byref(path), ctypes.byref(wb),
+                                 ctypes.byref(wsb)))
+    return {"path": path.value, "weight_bytes": wb.value, "workspace_bytes": wsb.value}
+
+
+class CacheDesc:
+    """fsx_cache_desc: device K/V tensors [batch][n_layers][capacity][H][Dh] plus host ring state.
+
+    start / len / pos are numpy int64 arrays that the C side reads, and updates in place on append.
+    """
+
+    def __init__(self, k, v, dtype: int, n_layers: int, n_heads: int, head_dim: int, capacity: int,
+                 lengths, positions=None, starts=None, k_scale=None, v_scale=None):
+        self.k, self.v, self.k_scale, self.v_scale = k, v, k_scale, v_scale
+        batch = len(lengths)
+        self.len = np.ascontiguousarray(np.asarray(lengths, dtype=np.int64))
+        self.pos = np.ascontiguousarray(np.asarray(lengths if positions is None else positions, dtype=np.int64))
+        self.start = np.ascontiguousarray(np.zeros(batch, np.int64) if starts is None else
+                                          np.asarray(starts, dtype=np.int64))
+        P = ctypes.POINTER(ctypes.c_int64)
+        self.c = CacheDescC(dtype, batch, n_layers, n_heads, head_dim, 0, capacity, _ptr(k), _ptr(v),
+                            _ptr(k_scale), _ptr(v_scale), self.start.ctypes.data_as(P),
+                            self.len.ctypes.data_as(P), self.pos.ctypes.data_as(P))
+
+
+def expert_forward(ex: Expert, cache: CacheDesc, tokens, batch: int, n_frame_tokens: int, waypoints,
+                   hidden=None, stream=None):
+    """fsx_expert_forward: one tick for `batch` agents (enqueued on `stream`)."""
+    _check(lib().fsx_expert_forward(ctypes.c_void_p(ex.handle), ctypes.byref(cache.c), _ptr(tokens), batch,
+                                    n_frame_tokens, _ptr(waypoints), _ptr(hidden), _stream(stream)))
+
+
+def cache_append_rows(cache: CacheDesc, k_rows, v_rows, n_rows: int, policy: int = APPEND_RING, stream=None):
+    """fsx_cache_append_rows: enqueue the row copy; host ring state is updated on return."""
+    _check(lib().fsx_cache_append_rows(ctypes.byref(cache.c), _ptr(k_rows), _ptr(v_rows), n_rows, policy,
+                                       _stream(stream)))
