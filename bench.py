@@ -1,0 +1,164 @@
+"""Benchmark of the expert tick on one MI355X (ticks/s, µs/tick, fraction of the HBM roofline).
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+Default workload: the full-size expert (32 layers, width 512, 32 heads x 128, SwiGLU 2048) on one agent
+with a 224-row cache per layer (a 40-frame history at 4 rows per frame plus 64 instruction rows), bf16.
+Inputs are seeded synthetic arrays, resident in HBM before the timed region.  Prints ONE JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+PAPER_EXPERT_MS = 7.5  # paper, Table 3: action expert per tick at a 40-frame history (RTX 3090 Ti)
+METRIC = "expert µs/tick and ticks/s at L=224/4096/B=16; achieved HBM GB/s vs peak"
+
+
+def algorithmic_bytes(wl, weight_bytes: int) -> int:
+    """Bytes one tick must read: packed weight matrices + the valid cache rows (K and V)."""
+    es = {"bf16": 2, "fp8": 1, "f32": 4}[wl.cache_dtype]
+    return int(weight_bytes) + sum(wl.lengths) * 2 * wl.n_layers * wl.attn_width * es
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_15621_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from rocprofv3 FETCH_SIZE/WRITE_SIZE counters, if taken on these sources."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        d = json.load(open(p))
+    except Exception:
+        return None
+    if d.get("source_hash") != source_hash():
+        return None
+    return d.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, budget_s: float = 15.0):
+    """The fp64 oracle on the host cores: as many full single-agent ticks as fit in ~budget_s."""
+    cores = len(os.sched_getaffinity(0))
+    for v in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
+        os.environ.setdefault(v, str(cores))
+    from harness import Model  # noqa: E402  (oracle is imported only on this leg)
+    import synth  # noqa: E402
+
+    one = wl.replace(batch=1, lengths=wl.lengths[:1])
+    model = Model(one)
+    tokens = synth.make_tokens(one)
+    slabs = {}
+    for l in range(one.n_layers):
+        slabs[l] = (synth.cache_slab(one, 0, l, "k").astype("float64"), synth.cache_slab(one, 0, l, "v").astype("float64"))
+    n, t0 = 0, time.perf_counter()
+    while True:
+        model.oracle_agent(tokens[0], lambda l: slabs[l], one.lengths[0])
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or (n >= 1 and el * (n + 1) / n > 2 * budget_s):
+            break
+    return {"value": round(n / el, 4), "unit": "ticks/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} full fp64 oracle tick(s) of one agent ({one.n_layers} layers, L={one.lengths[0]}, "
+                      f"S={one.seq}) in {el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="single_bf16_L224")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--multi-launch", action="store_true", help="one launch per phase instead of the tick kernel")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from gpu_inputs import Cache, Model, tokens_for
+    from paper_2607_15621_amd import fsx
+
+    wl = synth.WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    model = Model(wl)
+    flags = fsx.FLAG_MULTI_LAUNCH if args.multi_launch else 0
+    ex = model.create(flags=flags)
+    info = fsx.expert_info(ex)
+    cache = Cache(wl)
+    _, tok = tokens_for(wl)
+    wp = torch.zeros(wl.batch, wl.n_out, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        fsx.expert_forward(ex, cache.desc, tok, wl.batch, wl.n_frame_tokens, wp, None, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_s = e0.elapsed_time(e1) / 1e3
+    per_tick = gpu_s / args.steps
+    assert torch.isfinite(wp).all(), "non-finite waypoints"
+
+    nbytes = algorithmic_bytes(wl, info["weight_bytes"])
+    achieved = nbytes / per_tick / 1e9
+    value = wl.batch / per_tick  # agent-ticks per second
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "ticks/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(per_tick * 1e3, 5),
+        "us_per_tick": round(per_tick * 1e6, 2),
+        "wall_s": round(wall, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": round(value / (1000.0 / PAPER_EXPERT_MS), 3),
+        "dtype": "bf16" if wl.cache_dtype != "fp8" else "bf16 (fp8-e4m3 cache)",
+        "data": "synthetic (seeded N(0,1) tokens and cache, N(0,0.02^2) weights)",
+        "config": {"workload": wl.name, "agents": wl.batch, "cache_rows": list(wl.lengths)[:8],
+                   "layers": wl.n_layers, "d_model": wl.d_model, "heads": wl.n_heads, "head_dim": wl.head_dim,
+                   "d_ffn": wl.d_ffn, "expert_tokens": wl.n_expert_tokens, "frame_tokens": wl.n_frame_tokens,
+                   "launch": "multi" if args.multi_launch else "tick-kernel"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(wl.name),
+                     "algorithmic_bytes_per_launch": nbytes},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out), flush=True)
+    ex.close()
+
+
+if __name__ == "__main__":
+    main()

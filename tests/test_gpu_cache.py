@@ -1,0 +1,204 @@
+"""GPU tests of the cache side: append (bit-exact, ring wrap, error policy), batched agents, the fp8 cache.
+
+Append is checked byte for byte against host slicing of the generator's rows; forwards after an append
+are checked against the oracle over the rows the ring then holds.
+"""
+
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from harness import Cache, Model, rel_err, run_forward, tokens_for
+from paper_2607_15621_amd import fsx
+
+pytestmark = pytest.mark.gpu
+
+BF16_WP_TOL = 2e-2
+FP8_WP_TOL = 6e-2
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def small(wid, lengths, capacity, cache_dtype="bf16", n_layers=2):
+    return synth.Workload(name=f"small{wid}", wid=wid, n_layers=n_layers, d_model=128, n_heads=4, head_dim=128,
+                          d_ffn=256, n_expert_tokens=10, n_frame_tokens=0, batch=len(lengths),
+                          lengths=tuple(lengths), dtype="bf16", cache_dtype=cache_dtype, capacity=capacity)
+
+
+def rows_after_append(wl, b, l, kind, new_rows, capacity, start_len):
+    """The multiset of rows the ring holds after appending new_rows to the generator's slab (oldest evicted)."""
+    old = synth.cache_slab(wl, b, l, kind, rows=start_len)
+    allr = np.concatenate([old, new_rows], axis=0)
+    return allr[max(0, allr.shape[0] - capacity):]
+
+
+def device_rows(t, wl, b, l):
+    return t[b, l].float().cpu().numpy()
+
+
+def test_append_is_bit_exact_and_wraps_the_ring():
+    wl = small(50, lengths=(30, 64), capacity=64)
+    say("case append ring")
+    cache = Cache(wl)
+    before_k = cache.k.clone()
+    n = 4
+    k_new = synth.append_rows(wl, 0, "k", n)
+    v_new = synth.append_rows(wl, 0, "v", n)
+    kd = torch.from_numpy(k_new).to("cuda", torch.bfloat16)
+    vd = torch.from_numpy(v_new).to("cuda", torch.bfloat16)
+    fsx.cache_append_rows(cache.desc, kd, vd, n, fsx.APPEND_RING)
+    torch.cuda.synchronize()
+    # agent 0: rows 30..33 written, start 0, len 34; agent 1: full ring, slots 0..3 overwritten, start 4
+    assert list(cache.desc.len) == [34, 64] and list(cache.desc.start) == [0, 4] and list(cache.desc.pos) == [34, 68]
+    for l in range(wl.n_layers):
+        assert torch.equal(cache.k[0, l, 30:34].view(torch.int16), kd[0, l].view(torch.int16))
+        assert torch.equal(cache.k[1, l, 0:4].view(torch.int16), kd[1, l].view(torch.int16))
+        assert torch.equal(cache.v[1, l, 0:4].view(torch.int16), vd[1, l].view(torch.int16))
+        # untouched rows keep their bytes
+        assert torch.equal(cache.k[0, l, :30].view(torch.int16), before_k[0, l, :30].view(torch.int16))
+        assert torch.equal(cache.k[1, l, 4:].view(torch.int16), before_k[1, l, 4:].view(torch.int16))
+        assert torch.equal(cache.k[0, l, 34:].view(torch.int16), before_k[0, l, 34:].view(torch.int16))
+
+
+def test_append_error_policy_rejects_and_writes_nothing():
+    wl = small(51, lengths=(60,), capacity=62)
+    cache = Cache(wl)
+    before = cache.k.clone()
+    kd = torch.zeros((1, wl.n_layers, 4, wl.n_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(fsx.FsxError) as e:
+        fsx.cache_append_rows(cache.desc, kd, kd, 4, fsx.APPEND_ERROR)
+    assert e.value.code == 3
+    torch.cuda.synchronize()
+    assert torch.equal(cache.k, before) and list(cache.desc.len) == [60]
+    with pytest.raises(fsx.FsxError) as e:
+        fsx.cache_append_rows(cache.desc, kd, kd, 63, fsx.APPEND_RING)  # more rows than the ring holds
+    assert e.value.code == 3
+
+
+def test_forward_after_wrapping_append_matches_oracle():
+    wl = small(52, lengths=(64, 20), capacity=64)
+    say("case forward after wrap")
+    model = Model(wl)
+    ex = model.create()
+    cache = Cache(wl)
+    host_tok, tok = tokens_for(wl)
+    n = 6
+    k_new = synth.append_rows(wl, 0, "k", n)
+    v_new = synth.append_rows(wl, 0, "v", n)
+    fsx.cache_append_rows(cache.desc, torch.from_numpy(k_new).to("cuda", torch.bfloat16),
+                          torch.from_numpy(v_new).to("cuda", torch.bfloat16), n)
+    wp, _ = run_forward(ex, cache, tok, wl.batch, 0)
+    for b in range(wl.batch):
+        def rows(l, b=b):
+            return (rows_after_append(wl, b, l, "k", k_new[b, l], 64, wl.lengths[b]).astype(np.float64),
+                    rows_after_append(wl, b, l, "v", v_new[b, l], 64, wl.lengths[b]).astype(np.float64))
+        ref, _ = model.oracle_agent(host_tok[b], rows, cache.desc.pos[b])
+        err = rel_err(wp[b], ref)
+        say(f"  agent {b} err {err:.3e}")
+        assert err <= BF16_WP_TOL
+
+
+@pytest.mark.slow
+def test_batched_agents_then_append_match_oracle():
+    """16 agents x 1024 cached rows sharing the weights, then 4 rows appended per agent and layer."""
+    wl = synth.WORKLOADS["batched_bf16_B16_L1024"]
+    say("case batched_bf16_B16_L1024")
+    model = Model(wl)
+    ex = model.create()
+    cache = Cache(wl)
+    host_tok, tok = tokens_for(wl)
+    wp, _ = run_forward(ex, cache, tok, wl.batch, 0)
+    sample = (0, 9, 15)
+    for b in sample:
+        ref, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        err = rel_err(wp[b], ref)
+        say(f"  agent {b} err {err:.3e}")
+        assert err <= BF16_WP_TOL
+    n = wl.append_rows
+    k_new = synth.append_rows(wl, 0, "k", n)
+    v_new = synth.append_rows(wl, 0, "v", n)
+    kd = torch.from_numpy(k_new).to("cuda", torch.bfloat16)
+    vd = torch.from_numpy(v_new).to("cuda", torch.bfloat16)
+    fsx.cache_append_rows(cache.desc, kd, vd, n)
+    torch.cuda.synchronize()
+    assert all(int(x) == 1028 for x in cache.desc.len)
+    assert torch.equal(cache.k[:, :, 1024:1028].view(torch.int16), kd.view(torch.int16))
+    assert torch.equal(cache.v[:, :, 1024:1028].view(torch.int16), vd.view(torch.int16))
+    wp2, _ = run_forward(ex, cache, tok, wl.batch, 0)
+    for b in sample:
+        def rows(l, b=b):
+            return (rows_after_append(wl, b, l, "k", k_new[b, l], wl.capacity, 1024).astype(np.float64),
+                    rows_after_append(wl, b, l, "v", v_new[b, l], wl.capacity, 1024).astype(np.float64))
+        ref, _ = model.oracle_agent(host_tok[b], rows, cache.desc.pos[b])
+        err = rel_err(wp2[b], ref)
+        say(f"  after append agent {b} err {err:.3e}")
+        assert err <= BF16_WP_TOL
+
+
+def test_fp8_decode_of_every_code_on_the_gpu():
+    """All 254 finite E4M3 codes stored in the cache decode as the OCP definition says (both paths)."""
+    wl = small(60, lengths=(2,), capacity=2, cache_dtype="fp8", n_layers=1)
+    model = Model(wl)
+    codes = np.array([c for c in range(256) if c not in (0x7F, 0xFF)], np.uint8)
+    H, Dh = wl.n_heads, wl.head_dim
+    block = np.resize(codes, (2, H, Dh))
+    host_tok, tok = tokens_for(wl)
+    results = []
+    for flags in (0, fsx.FLAG_GENERIC):
+        ex = model.create(flags=flags)
+        cache = Cache(wl)
+        for kind, t in (("k", cache.k), ("v", cache.v)):
+            t[0, 0].copy_(torch.from_numpy(block if kind == "v" else np.flip(block, 0).copy()))
+        cache.k_scale.fill_(1.0 / 64)
+        cache.v_scale.fill_(1.0 / 32)
+        torch.cuda.synchronize()
+        wp, _ = run_forward(ex, cache, tok, 1, 0)
+        results.append(wp[0])
+    dec = oracle.e4m3fn_decode(block)
+    kv = (np.flip(dec, 0) / 64.0, dec / 32.0)
+    ref, _ = model.oracle_agent(host_tok[0], lambda l: kv, 2)
+    for wp in results:
+        assert rel_err(wp, ref) <= BF16_WP_TOL, rel_err(wp, ref)
+
+
+def test_small_fp8_cache_matches_oracle():
+    wl = small(61, lengths=(300, 45, 0), capacity=320, cache_dtype="fp8")
+    say("case small fp8")
+    model = Model(wl)
+    ex = model.create()
+    cache = Cache(wl, starts=(100, 310, 0))
+    host_tok, tok = tokens_for(wl)
+    wp, _ = run_forward(ex, cache, tok, wl.batch, 0)
+    for b in range(wl.batch):
+        ref, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        refd, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b, decoded=True), cache.desc.pos[b])
+        e, ed = rel_err(wp[b], ref), rel_err(wp[b], refd)
+        say(f"  agent {b} err vs source {e:.3e}, vs decoded {ed:.3e}")
+        assert e <= FP8_WP_TOL and ed <= BF16_WP_TOL
+
+
+@pytest.mark.slow
+def test_ragged_fp8_agents_match_oracle():
+    """8 agents with ragged histories (256..16384 rows) in an fp8 cache; sampled agents vs the oracle."""
+    wl = synth.WORKLOADS["ragged_fp8_B8"]
+    say("case ragged_fp8_B8", wl.lengths)
+    model = Model(wl)
+    ex = model.create()
+    cache = Cache(wl)
+    host_tok, tok = tokens_for(wl)
+    wp, _ = run_forward(ex, cache, tok, wl.batch, 0)
+    assert np.isfinite(wp).all()
+    for b in (7, 3):
+        ref, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        err = rel_err(wp[b], ref)
+        say(f"  agent {b} L={wl.lengths[b]} err {err:.3e}")
+        assert err <= FP8_WP_TOL
