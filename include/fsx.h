@@ -61,7 +61,8 @@ enum { FSX_APPEND_RING = 0, FSX_APPEND_ERROR = 1 };
 /* Flags of fsx_expert_cfg.flags. */
 enum {
   FSX_FLAG_GENERIC = 1,     /* force the simple per-op kernels instead of the fused tick kernel */
-  FSX_FLAG_MULTI_LAUNCH = 2 /* run the fused path as one launch per phase instead of one persistent launch */
+  FSX_FLAG_MULTI_LAUNCH = 2, /* run the fused path as one launch per phase instead of one persistent launch */
+  FSX_FLAG_TRACE = 4         /* tick kernel records per-workgroup phase timestamps (fsx_expert_trace) */
 };
 
 #define FSX_MAX_BATCH 64
@@ -82,6 +83,7 @@ typedef struct {
   float rope_base;          /* rotary base for expert q/k (pairs j, j+Dh/2); 0 = no rotary */
   float rms_eps;            /* RMSNorm epsilon */
   int32_t flags;            /* FSX_FLAG_* */
+  int32_t tick_timeout_us;  /* bound on any wait inside the tick kernel; 0 = 2 s */
 } fsx_expert_cfg;
 
 /* One layer's parameters, DEVICE pointers, elements of cfg.dtype (norm gains always fp32). */
@@ -160,6 +162,20 @@ int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, const void* 
 int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, const void* v_rows, int32_t n_rows,
                           int32_t policy, void* stream);
 
+/* Synchronise `stream` and report whether the ticks enqueued on this handle completed: FSX_OK, or
+ * FSX_E_HIP if a tick kernel gave up on a wait (its waypoints were then written as NaN).  The
+ * failure is reported once per failed tick and cleared by reporting it. */
+int fsx_expert_status(fsx_expert* ex, void* stream);
+
+/* Phase timestamps of the last tick of a handle created with FSX_FLAG_TRACE.  Synchronises `stream`,
+ * then copies n_wg x n_ev values into host_out (capacity `cap` values): for workgroup w, event e
+ * (0 start, 1 after the embedding, 2 + 16*l + p after phase p of layer l with p = 0 q/k/v projection,
+ * 1 attention, 2 output projection, 3 gate/up, 4 down, 2 + 16*l + 5 + k sub-phase mark k; 2 + 16*n_layers
+ * at the end) is the GPU real-time counter (100 MHz).  Sub-phase marks are written only by workgroups
+ * that reach them and keep older values otherwise.  FSX_E_UNSUPPORTED without the flag, FSX_E_CAPACITY
+ * if cap is short. */
+int fsx_expert_trace(fsx_expert* ex, uint64_t* host_out, int64_t cap, int32_t* n_wg, int32_t* n_ev, void* stream);
+
 /* Free the packed weights and the workspace (synchronises the device first). NULL is a no-op. */
 void fsx_expert_destroy(fsx_expert* ex);
 
@@ -167,7 +183,8 @@ void fsx_expert_destroy(fsx_expert* ex);
 const char* fsx_last_error(void);
 
 /* Introspection of a handle (any pointer may be NULL):
- *   path          0 = fused tick kernel (bf16 weights), 1 = simple per-op kernels
+ *   path          0 = fused bf16 path (one persistent launch per tick, or one launch per phase with
+ *                 FSX_FLAG_MULTI_LAUNCH), 1 = simple per-op kernels
  *   weight_bytes  bytes of the packed weight matrices the tick streams (excludes fp32 norm gains)
  *   workspace_bytes device workspace owned by the handle */
 int fsx_expert_info(const fsx_expert* ex, int32_t* path, int64_t* weight_bytes, int64_t* workspace_bytes);

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfsx.so")
-SOURCES = ["api.hip", "fast_kernels.hip", "generic_kernels.hip"]
+SOURCES = ["api.hip", "fast_kernels.hip", "generic_kernels.hip", "tick_kernel.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC",
@@ -36,7 +36,8 @@ def build(verbose: bool = False) -> str:
     with ThreadPoolExecutor(len(cmds)) as ex:
         outs = list(ex.map(_run, cmds))
     tmp = LIB + ".tmp"
-    outs.append(_run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]))
+    # -z defs: every symbol the library uses must be defined in it or in a library it links
+    outs.append(_run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,-z,defs", *objs, "-o", tmp]))
     os.replace(tmp, LIB)
     if verbose:
         for o in outs:

@@ -32,6 +32,19 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 constexpr int KSPLIT_MAX = 8;
 
+// split factor of the output projection: a divisor of H whose head group is at most 512 columns wide
+int pick_ks_o(int H, int Dh) {
+  for (int ks = 1; ks <= H; ++ks)
+    if (H % ks == 0 && (H / ks) * Dh <= 512 && ks >= std::min(H, KSPLIT_MAX)) return ks <= KSPLIT_MAX ? ks : -1;
+  return -1;
+}
+// split factor of the down projection: ranges of F/ks columns, a multiple of 32, at most 512
+int pick_ks_d(int F) {
+  for (int ks = KSPLIT_MAX; ks >= 1; --ks)
+    if ((F / 32) % ks == 0 && F / ks <= 512) return ks;
+  return -1;
+}
+
 }  // namespace
 
 struct fsx_expert {
@@ -49,6 +62,14 @@ struct fsx_expert {
   Workspace ws{};
   GenericWorkspace gws{};
   const float* final_norm = nullptr;
+  // persistent tick kernel
+  bool tick = false;
+  int ks_o = 8, ks_d = 8, n_att_cnt = 0, cu_count = 0;
+  TickArgs ta{};            // workspace pointers; per-forward fields are filled in forward
+  TickLayer* dlayers = nullptr;
+  uint64_t* trace = nullptr;
+  uint64_t epoch = 0;
+  uint64_t status_seen = 0;
 };
 
 static void free_expert(fsx_expert* ex) {
@@ -57,6 +78,8 @@ static void free_expert(fsx_expert* ex) {
   if (ex->fbuf) (void)hipFree(ex->fbuf);
   if (ex->head_w) (void)hipFree(ex->head_w);
   if (ex->wsbuf) (void)hipFree(ex->wsbuf);
+  if (ex->dlayers) (void)hipFree(ex->dlayers);
+  if (ex->trace) (void)hipFree(ex->trace);
   delete ex;
 }
 
@@ -152,19 +175,21 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
       FastWeights f{};
       const size_t sq = (size_t)A * d * 2;  // bytes of one [A][d] bf16 matrix
       f.wqkv = (const uint4*)wp;
-      bool good = ok(launch_pack((const uint16_t*)w.wq, nullptr, A, d, PACK_ROPE_PAIRS, Dh, wp, s), "pack wq") &&
-                  ok(launch_pack((const uint16_t*)w.wk, nullptr, A, d, PACK_ROPE_PAIRS, Dh, wp + sq, s), "pack wk") &&
-                  ok(launch_pack((const uint16_t*)w.wv, nullptr, A, d, PACK_PLAIN, 0, wp + 2 * sq, s), "pack wv");
+      // q/k/v and gate/up read RMSNorm outputs: their gains are folded into the packed weights
+      bool good =
+          ok(launch_pack((const uint16_t*)w.wq, nullptr, A, d, PACK_ROPE_PAIRS, Dh, w.attn_norm, wp, s), "pack wq") &&
+          ok(launch_pack((const uint16_t*)w.wk, nullptr, A, d, PACK_ROPE_PAIRS, Dh, w.attn_norm, wp + sq, s), "pack wk") &&
+          ok(launch_pack((const uint16_t*)w.wv, nullptr, A, d, PACK_PLAIN, 0, w.attn_norm, wp + 2 * sq, s), "pack wv");
       wp += 3 * sq;
       f.wo = (const uint4*)wp;
-      good = good && ok(launch_pack((const uint16_t*)w.wo, nullptr, d, A, PACK_PLAIN, 0, wp, s), "pack wo");
+      good = good && ok(launch_pack((const uint16_t*)w.wo, nullptr, d, A, PACK_PLAIN, 0, nullptr, wp, s), "pack wo");
       wp += sq;
       f.wgu = (const uint4*)wp;
       good = good && ok(launch_pack((const uint16_t*)w.w_gate, (const uint16_t*)w.w_up, 2 * F, d, PACK_SWIGLU_PAIRS, 0,
-                                    wp, s), "pack gate/up");
+                                    w.ffn_norm, wp, s), "pack gate/up");
       wp += (size_t)2 * F * d * 2;
       f.wd = (const uint4*)wp;
-      good = good && ok(launch_pack((const uint16_t*)w.w_down, nullptr, d, F, PACK_PLAIN, 0, wp, s), "pack down");
+      good = good && ok(launch_pack((const uint16_t*)w.w_down, nullptr, d, F, PACK_PLAIN, 0, nullptr, wp, s), "pack down");
       wp += (size_t)F * d * 2;
       if (!good) return cleanup(FSX_E_HIP);
       f.attn_norm = ex->fbuf + (size_t)(2 * l) * d;
@@ -203,7 +228,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
              {(void**)&ex->ws.vself, (size_t)M * A * 2},
              {(void**)&ex->ws.attn, (size_t)M * A * 2},
              {(void**)&ex->ws.z, (size_t)M * F * 2},
-             {(void**)&ex->ws.part, (size_t)KSPLIT_MAX * M * d * 4},
+             {(void**)&ex->ws.part, (size_t)KSPLIT_MAX * M * d * 4},  // split factors are <= KSPLIT_MAX
              {(void**)&ex->ws.att_o, (size_t)ex->items_max * 16 * Dh * 4},
              {(void**)&ex->ws.att_ml, (size_t)ex->items_max * 32 * 4},
              {(void**)&ex->ws.rope, (size_t)M * Dh * 4}};
@@ -214,6 +239,43 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
              {(void**)&ex->gws.g, (size_t)M * F * 4},   {(void**)&ex->gws.u, (size_t)M * F * 4},
              {(void**)&ex->gws.rope, (size_t)M * Dh * 4}};
   }
+  const int L = c.n_layers;
+  const int nflag_attn = c.max_batch * H;
+  if (ex->path == 0 && !(c.flags & FSX_FLAG_MULTI_LAUNCH)) {
+    ex->ks_o = pick_ks_o(H, Dh);
+    ex->ks_d = pick_ks_d(F);
+    auto pow2 = [](int v) { return v > 0 && (v & (v - 1)) == 0; };
+    ex->tick = d <= 512 && pow2(d) && ex->ks_o > 0 && ex->ks_d > 0 && pow2(A / ex->ks_o) && pow2(F / ex->ks_d) &&
+               c.n_expert_tokens <= 64;
+  }
+  if (ex->tick) {
+    TickArgs& t = ex->ta;
+    const size_t dt = (size_t)d / 16;
+    std::vector<std::pair<void**, size_t>> tp = {
+        {(void**)&t.h0, (size_t)M * d * 4},
+        {(void**)&t.hb0, (size_t)M * d * 2},
+        {(void**)&t.hbmid, (size_t)L * M * d * 2},
+        {(void**)&t.hbout, (size_t)L * M * d * 2},
+        {(void**)&t.ssq0, dt * M * 4},
+        {(void**)&t.hmid, (size_t)L * M * d * 4},
+        {(void**)&t.hout, (size_t)L * M * d * 4},
+        {(void**)&t.ssq_mid, (size_t)L * dt * M * 4},
+        {(void**)&t.ssq_out, (size_t)L * dt * M * 4},
+        {(void**)&t.attn, (size_t)L * M * A * 2},
+        {(void**)&t.z, (size_t)L * M * F * 2},
+        {(void**)&t.f_embed, (size_t)M * 8},
+        {(void**)&t.f_qkv, (size_t)3 * A / 16 * 8},
+        {(void**)&t.f_attn, (size_t)nflag_attn * 8},
+        {(void**)&t.f_hmid, dt * 8},
+        {(void**)&t.f_z, (size_t)2 * F / 16 * 8},
+        {(void**)&t.f_hout, dt * 8},
+        {(void**)&t.status, 256},
+        {(void**)&t.att_cnt, (size_t)nflag_attn * 4},
+        {(void**)&t.o_cnt, dt * 4},
+        {(void**)&t.d_cnt, dt * 4}};
+    parts.insert(parts.end(), tp.begin(), tp.end());
+    ex->n_att_cnt = nflag_attn;
+  }
   size_t total = 0;
   for (auto& p : parts) total += (p.second + 255) & ~(size_t)255;
   if (!ok(hipMalloc(&ex->wsbuf, total), "hipMalloc(workspace)")) return cleanup(FSX_E_OOM);
@@ -222,6 +284,46 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   for (auto& p : parts) {
     *p.first = q;
     q += (p.second + 255) & ~(size_t)255;
+  }
+  if (ex->tick) {
+    // flags, counters and status start at zero; stamps only grow, counters return to zero
+    TickArgs& t = ex->ta;
+    const size_t zbytes = (size_t)((char*)q - (char*)t.f_embed);
+    if (!ok(hipMemsetAsync(t.f_embed, 0, zbytes, s), "hipMemsetAsync(flags)")) return cleanup(FSX_E_HIP);
+    std::vector<TickLayer> tl(c.n_layers);
+    for (int l = 0; l < c.n_layers; ++l)
+      tl[l] = TickLayer{ex->fw[l].wqkv, ex->fw[l].wo, ex->fw[l].wgu, ex->fw[l].wd, ex->fw[l].attn_norm,
+                        ex->fw[l].ffn_norm};
+    if (!ok(hipMalloc((void**)&ex->dlayers, sizeof(TickLayer) * c.n_layers), "hipMalloc(layer table)") ||
+        !ok(hipMemcpyAsync(ex->dlayers, tl.data(), sizeof(TickLayer) * c.n_layers, hipMemcpyHostToDevice, s),
+            "copy layer table"))
+      return cleanup(FSX_E_HIP);
+    t.layers = ex->dlayers;
+    t.final_norm = ex->final_norm;
+    t.head_w = ex->head_w;
+    t.head_dtype = c.dtype;
+    t.q = ex->ws.q;
+    t.kself = ex->ws.kself;
+    t.vself = ex->ws.vself;
+    t.att_o = ex->ws.att_o;
+    t.att_ml = ex->ws.att_ml;
+    t.part = ex->ws.part;
+    t.rope = ex->ws.rope;
+    t.n_att_cnt = ex->n_att_cnt;
+    t.ks_o = ex->ks_o;
+    t.ks_d = ex->ks_d;
+    const uint64_t us = c.tick_timeout_us > 0 ? (uint64_t)c.tick_timeout_us : 2000000ull;
+    t.timeout_ticks = us * 100;  // the real-time counter runs at 100 MHz
+    hipDeviceProp_t prop;
+    if (!ok(hipGetDeviceProperties(&prop, ex->device), "hipGetDeviceProperties")) return cleanup(FSX_E_HIP);
+    ex->cu_count = prop.multiProcessorCount;
+    if (c.flags & FSX_FLAG_TRACE) {
+      const size_t nt = (size_t)ex->cu_count * trace_events(c.n_layers);
+      if (!ok(hipMalloc((void**)&ex->trace, nt * 8), "hipMalloc(trace)") ||
+          !ok(hipMemsetAsync(ex->trace, 0, nt * 8, s), "hipMemsetAsync(trace)"))
+        return cleanup(FSX_E_HIP);
+      t.trace = ex->trace;
+    }
   }
   if (!ok(hipStreamSynchronize(s), "hipStreamSynchronize(create)")) return cleanup(FSX_E_HIP);
   *out = ex;
@@ -320,6 +422,46 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
   tp.n_items = n_items;
   tp.chunk_prefix[0] = 0;
   for (int b = 0; b < batch; ++b) tp.chunk_prefix[b + 1] = tp.chunk_prefix[b] + (int)((tp.len[b] + cr - 1) / cr) + 1;
+  if (ex->tick) {
+    int per_cu = 0;
+    const int mt = tick_mt(tp.M);
+    HIP_TRY(tick_occupancy(mt, cache->dtype == FSX_FP8_E4M3 ? 1 : 0, &per_cu));
+    if (per_cu < 1) return fail(FSX_E_UNSUPPORTED, "tick kernel does not fit on a compute unit");
+    // attention units: (agent, range of rr rows, head, query tile).  One range per agent when the work is
+    // small; otherwise about 2 (medium) or 8 (large) units per workgroup, with an agent's ranges of equal size.
+    const int G = ex->cu_count;
+    int64_t lmax = 0;
+    for (int b = 0; b < batch; ++b) lmax = std::max<int64_t>(lmax, tp.len[b]);
+    const int64_t per_wg = rows * dm.H * tp.n_tt / G;
+    int64_t rr = std::max<int64_t>(32, (lmax + 31) / 32 * 32);
+    if (per_wg > 512) {
+      const int64_t target_pairs = std::max<int64_t>(1, (per_wg <= 8192 ? 2 : 8) * (int64_t)G / tp.n_tt);
+      const int64_t rr_t = std::max<int64_t>(128, (rows * dm.H + target_pairs - 1) / target_pairs);
+      const int64_t nr = (lmax + rr_t - 1) / rr_t;
+      rr = std::max<int64_t>(128, ((lmax + nr - 1) / nr + 31) / 32 * 32);
+    }
+    for (;;) {
+      int64_t slots = 0;
+      for (int b = 0; b < batch; ++b) slots += std::max<int64_t>(1, (tp.len[b] + rr - 1) / rr);
+      if (slots * dm.H * tp.n_tt <= ex->items_max) break;
+      rr *= 2;
+    }
+    tp.range_rows = (int)std::min<int64_t>(rr, INT32_MAX / 2);
+    tp.range_prefix[0] = 0;
+    for (int b = 0; b < batch; ++b)
+      tp.range_prefix[b + 1] = tp.range_prefix[b] + (int)std::max<int64_t>(1, (tp.len[b] + rr - 1) / rr);
+    tp.n_aunits = tp.range_prefix[batch] * dm.H;
+    TickArgs a = ex->ta;
+    a.tok_dtype = c.dtype;
+    a.tokens = tokens;
+    a.cv = cv;
+    a.waypoints = waypoints;
+    if (hidden) a.hout = hidden;
+    a.epoch = ++ex->epoch;
+    HIP_TRY(launch_tick(a, tp, dm, ex->cu_count, s));
+    g_err.clear();
+    return FSX_OK;
+  }
   const int wpg = n_items >= 1024 ? 4 : 1;
   auto kspl = [](int KB) { return KB % 8 == 0 ? 8 : (KB % 4 == 0 ? 4 : (KB % 2 == 0 ? 2 : 1)); };
   const int ks_o = kspl(dm.A / 32), ks_d = kspl(dm.F / 32);
@@ -388,6 +530,38 @@ extern "C" int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, 
   return FSX_OK;
 }
 
+extern "C" int fsx_expert_status(fsx_expert* ex, void* stream) {
+  if (!ex) return fail(FSX_E_INVALID, "expert handle is NULL");
+  HIP_TRY(hipStreamSynchronize((hipStream_t)stream));
+  if (!ex->tick) {
+    g_err.clear();
+    return FSX_OK;
+  }
+  uint64_t v = 0;
+  HIP_TRY(hipMemcpy(&v, ex->ta.status, sizeof(v), hipMemcpyDeviceToHost));
+  if (v != ex->status_seen) {
+    ex->status_seen = v;
+    return fail(FSX_E_HIP, "a tick kernel timed out waiting for another workgroup (tick " + std::to_string(v - 1) +
+                               "); its waypoints are NaN");
+  }
+  g_err.clear();
+  return FSX_OK;
+}
+
+extern "C" int fsx_expert_trace(fsx_expert* ex, uint64_t* host_out, int64_t cap, int32_t* n_wg, int32_t* n_ev,
+                                void* stream) {
+  if (!ex || !host_out) return fail(FSX_E_INVALID, "expert handle and host_out must be non-NULL");
+  if (!ex->trace) return fail(FSX_E_UNSUPPORTED, "the handle was not created with FSX_FLAG_TRACE");
+  const int64_t n = (int64_t)ex->cu_count * trace_events(ex->cfg.n_layers);
+  if (cap < n) return fail(FSX_E_CAPACITY, "host_out holds fewer than n_wg * n_ev values");
+  HIP_TRY(hipStreamSynchronize((hipStream_t)stream));
+  HIP_TRY(hipMemcpy(host_out, ex->trace, (size_t)n * 8, hipMemcpyDeviceToHost));
+  if (n_wg) *n_wg = ex->cu_count;
+  if (n_ev) *n_ev = trace_events(ex->cfg.n_layers);
+  g_err.clear();
+  return FSX_OK;
+}
+
 extern "C" void fsx_expert_destroy(fsx_expert* ex) {
   if (!ex) return;
   (void)hipDeviceSynchronize();
@@ -398,7 +572,7 @@ extern "C" const char* fsx_last_error(void) { return g_err.c_str(); }
 
 extern "C" int fsx_expert_info(const fsx_expert* ex, int32_t* path, int64_t* weight_bytes, int64_t* workspace_bytes) {
   if (!ex) return fail(FSX_E_INVALID, "expert handle is NULL");
-  if (path) *path = ex->path;
+  if (path) *path = ex->path;  // the tick kernel and the per-phase launches are both path 0
   if (weight_bytes) *weight_bytes = ex->weight_bytes;
   if (workspace_bytes) *workspace_bytes = ex->ws_bytes;
   return FSX_OK;

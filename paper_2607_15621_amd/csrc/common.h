@@ -88,6 +88,80 @@ __device__ __forceinline__ void transpose8x8_b16(const uint4 in[8], uint4 out[8]
   }
 }
 
+// ---------------------------------------------------------------- device-coherent accesses
+// Data exchanged between workgroups inside one launch is written with device-scope ("sc1") stores,
+// which write through the XCD's L2 to memory, and read with device-scope loads, which do not return
+// lines cached by another XCD's L2.  A producer waits for its stores to complete (stores_done) before
+// it publishes a flag; no L2 write-back or invalidate is needed.
+__device__ __forceinline__ void st_dev(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev_f(float* p, float v) { st_dev(reinterpret_cast<uint32_t*>(p), __float_as_uint(v)); }
+__device__ __forceinline__ void st_dev16(void* p, uint4 v) {
+  uint64_t* q = reinterpret_cast<uint64_t*>(p);
+  st_dev(q, (uint64_t)v.x | ((uint64_t)v.y << 32));
+  st_dev(q + 1, (uint64_t)v.z | ((uint64_t)v.w << 32));
+}
+__device__ __forceinline__ void st_dev_f4(float* p, float4 v) {
+  st_dev16(p, make_uint4(__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)));
+}
+__device__ __forceinline__ uint32_t ld_dev(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_dev(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev_f(const float* p) { return __uint_as_float(ld_dev(reinterpret_cast<const uint32_t*>(p))); }
+__device__ __forceinline__ uint4 ld_dev16(const void* p) {
+  const uint64_t* q = reinterpret_cast<const uint64_t*>(p);
+  const uint64_t a = ld_dev(q), b = ld_dev(q + 1);
+  return make_uint4((uint32_t)a, (uint32_t)(a >> 32), (uint32_t)b, (uint32_t)(b >> 32));
+}
+__device__ __forceinline__ float4 ld_dev_f4(const float* p) {
+  const uint4 u = ld_dev16(p);
+  return make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w));
+}
+__device__ __forceinline__ uint32_t atomic_add_dev(uint32_t* p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// wait until every vector memory operation this thread issued has completed
+__device__ __forceinline__ void stores_done() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Plain or device-coherent access, chosen at compile time.
+template <bool COH>
+__device__ __forceinline__ uint4 ld16(const void* p) {
+  if constexpr (COH) return ld_dev16(p);
+  else return *reinterpret_cast<const uint4*>(p);
+}
+template <bool COH>
+__device__ __forceinline__ float4 ldf4(const float* p) {
+  if constexpr (COH) return ld_dev_f4(p);
+  else return *reinterpret_cast<const float4*>(p);
+}
+template <bool COH>
+__device__ __forceinline__ float ldf(const float* p) {
+  if constexpr (COH) return ld_dev_f(p);
+  else return *p;
+}
+template <bool COH>
+__device__ __forceinline__ void stf(float* p, float v) {
+  if constexpr (COH) st_dev_f(p, v);
+  else *p = v;
+}
+template <bool COH>
+__device__ __forceinline__ void stf4(float* p, float4 v) {
+  if constexpr (COH) st_dev_f4(p, v);
+  else *reinterpret_cast<float4*>(p) = v;
+}
+template <bool COH>
+__device__ __forceinline__ void st16(void* p, uint4 v) {
+  if constexpr (COH) st_dev16(p, v);
+  else *reinterpret_cast<uint4*>(p) = v;
+}
+
 __device__ __forceinline__ float block_sum(float v, float* scratch /* >= 16 floats */) {
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) v += shfl_xor(v, m);

@@ -13,6 +13,7 @@
 //   down  : down projection, split-K partials; then norm again with the next layer's gain.
 // The head pools the first T tokens after a final RMSNorm and applies a d -> n_out map.
 
+#include "attn_device.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -28,9 +29,11 @@ namespace fsx {
 //                      0..7 and [Dh/2 + 8tau, ...) in columns 8..15, so rotary partners are lanes l, l^8.
 //   PACK_SWIGLU_PAIRS: tile tau holds gate rows [8tau, 8tau+8) (from a) in columns 0..7 and the same up
 //                      rows (from b) in columns 8..15.
+// When the projection reads an RMSNorm output, the norm's gain is folded into the packed weights
+// (x*r*g) W^T = r * (x (W diag(g))^T), so kernels feed bf16(x) and scale each output row by r.
 // =====================================================================================================
 __global__ void k_pack(const uint16_t* __restrict__ a, const uint16_t* __restrict__ b, int N, int K, int kind,
-                       int param, uint4* __restrict__ dst) {
+                       int param, const float* __restrict__ gain, uint4* __restrict__ dst) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int KB = K / 32;
   const int64_t total = (int64_t)(N / 16) * KB * 64;
@@ -52,19 +55,29 @@ __global__ void k_pack(const uint16_t* __restrict__ a, const uint16_t* __restric
     row = 8 * tau + (c & 7);
     src = c < 8 ? a : b;
   }
-  dst[i] = *reinterpret_cast<const uint4*>(src + row * K + kcol);
+  uint4 v = *reinterpret_cast<const uint4*>(src + row * K + kcol);
+  if (gain) {  // fold the RMSNorm gain of the input channels into the weight: W'[n][k] = W[n][k] * g[k]
+    uint32_t* w = reinterpret_cast<uint32_t*>(&v);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float lo = bf16_to_f32((uint16_t)(w[j] & 0xffffu)) * gain[kcol + 2 * j];
+      const float hi = bf16_to_f32((uint16_t)(w[j] >> 16)) * gain[kcol + 2 * j + 1];
+      w[j] = pack_bf16x2(lo, hi);
+    }
+  }
+  dst[i] = v;
 }
 
-hipError_t launch_pack(const uint16_t* a, const uint16_t* b, int N, int K, int kind, int param, void* dst,
-                       hipStream_t s) {
+hipError_t launch_pack(const uint16_t* a, const uint16_t* b, int N, int K, int kind, int param, const float* gain,
+                       void* dst, hipStream_t s) {
   const int64_t total = (int64_t)(N / 16) * (K / 32) * 64;
   const int64_t blocks = (total + 255) / 256;
-  hipLaunchKernelGGL(k_pack, dim3((unsigned)blocks), dim3(256), 0, s, a, b, N, K, kind, param, (uint4*)dst);
+  hipLaunchKernelGGL(k_pack, dim3((unsigned)blocks), dim3(256), 0, s, a, b, N, K, kind, param, gain, (uint4*)dst);
   return hipGetLastError();
 }
 
 // =====================================================================================================
-// Embed: h = tokens (fp32), x = bf16(RMSNorm(h) * g), rotary table cos/sin(p * base^(-2j/Dh)) in fp64.
+// Embed: h = tokens (fp32), x = bf16(h / rms(h)), rotary table cos/sin(p * base^(-2j/Dh)) in fp64.
 // One workgroup per token row.
 // =====================================================================================================
 __global__ __launch_bounds__(256) void k_embed(const void* __restrict__ tokens, int tok_dtype,
@@ -85,7 +98,7 @@ __global__ __launch_bounds__(256) void k_embed(const void* __restrict__ tokens, 
   const float r = 1.0f / sqrtf(ss / (float)d + dm.eps);
   for (int n = threadIdx.x; n < d; n += blockDim.x) {
     const int64_t idx = (int64_t)m * d + n;
-    ws.xb[idx] = f32_to_bf16(ws.h[idx] * r * g0[n]);
+    ws.xb[idx] = f32_to_bf16(ws.h[idx] * r);  // the gain is folded into the packed weights
   }
   const int half = dm.Dh / 2;
   for (int j = threadIdx.x; j < half; j += blockDim.x) {
@@ -278,18 +291,8 @@ hipError_t launch_gemm_down(const FastWeights& w, const TickParams& tp, const Di
 }
 
 // =====================================================================================================
-// Split-K joint attention (Eq. (1)).  One wave = one work item = (agent b, head h, chunk of rows, query
-// tile tt).  Per 32-row tile:
-//   S^T = K Q^T on MFMA (A operand: 16 cached rows x 32 channels straight from memory, 16-byte loads;
-//   B operand: the 16 queries, kept in registers), scores already in log2 units (q is pre-scaled),
-//   online softmax with the row max reduced over the 4 lanes sharing a query (xor 16, xor 32),
-//   P (bf16/f16) re-used in place as the A operand of O += P V: the lane's own 8 scores are rows
-//   {4g..4g+3, 16+4g..16+4g+3}, and V is loaded as those 8 rows x 8 channels per lane (each load
-//   instruction reads 4 whole 256-byte rows) and transposed 8x8 in registers, so MFMA k (k = 0..7)
-//   produces output channels 8c + k.
-// The item writes its unnormalised output, running max and sum; k_combine merges them.
-// fp8 rows are decoded to fp16 in registers (exact) and use fp16 MFMA; the per-(agent, layer, head)
-// scales multiply the scores (keys) and the partial output (values).
+// Split-K joint attention (Eq. (1)): one wave = one work item (see attn_device.h); k_combine merges the
+// items of each (agent, head, query tile).
 // =====================================================================================================
 struct AttnArgs {
   CacheView cv;
@@ -301,137 +304,6 @@ struct AttnArgs {
   uint16_t* attn_out;  // [M][A] bf16 (combine output)
   int H, Dh, A;
 };
-
-template <int KT>  // 0: bf16 operands, 1: f16 operands
-__device__ __forceinline__ void load_q_frag(const float* __restrict__ q, int64_t row, bool valid, int grp,
-                                            uint4 qf[4]) {
-#pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
-    if (valid) {
-      const float4* p = reinterpret_cast<const float4*>(q + row + 32 * kb + 8 * grp);
-      lo = p[0];
-      hi = p[1];
-    }
-    if (KT == 0)
-      qf[kb] = make_uint4(pack_bf16x2(lo.x, lo.y), pack_bf16x2(lo.z, lo.w), pack_bf16x2(hi.x, hi.y),
-                          pack_bf16x2(hi.z, hi.w));
-    else
-      qf[kb] = make_uint4(pack_f16x2(lo.x, lo.y), pack_f16x2(lo.z, lo.w), pack_f16x2(hi.x, hi.y),
-                          pack_f16x2(hi.z, hi.w));
-  }
-}
-
-// 16-byte group of 8 consecutive channels of one row -> 8 x 16-bit MFMA operand values.
-template <int KT>
-__device__ __forceinline__ uint4 load8(const char* p) {
-  if constexpr (KT == 0) {
-    return *reinterpret_cast<const uint4*>(p);
-  } else {
-    const uint2 raw = *reinterpret_cast<const uint2*>(p);
-    return make_uint4(e4m3x2_to_f16x2(raw.x, false), e4m3x2_to_f16x2(raw.x, true), e4m3x2_to_f16x2(raw.y, false),
-                      e4m3x2_to_f16x2(raw.y, true));
-  }
-}
-
-// rows i in [i0, i1) of one (agent, head): row i lives at base + slot(i) * row_bytes, where
-// slot(i) = (start + i) mod cap for a ring and i for the expert's own rows.
-template <int KT, bool RING>
-__device__ void attn_rows(const char* __restrict__ kbase, const char* __restrict__ vbase, int64_t row_bytes,
-                          int64_t start, int64_t cap, int i0, int i1, const uint4 qf[4], float kscale, float vscale,
-                          int lane, float* __restrict__ out_o, float* __restrict__ out_ml, int Dh) {
-  constexpr int ES = KT == 0 ? 2 : 1;
-  const int c = lane & 15, grp = lane >> 4;
-  auto roff = [&](int i) -> int64_t {
-    int64_t slot = i;
-    if (RING) {
-      slot = start + i;
-      if (slot >= cap) slot -= cap;
-    }
-    return slot * row_bytes;
-  };
-  f32x4 o[8];
-#pragma unroll
-  for (int k = 0; k < 8; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
-
-  for (int r0 = i0; r0 < i1; r0 += 32) {
-    uint4 kf[2][4];
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      const int i = r0 + 16 * rt + c;
-      const char* p = kbase + roff(i < i1 ? i : i0);
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) kf[rt][kb] = load8<KT>(p + (32 * kb + 8 * grp) * ES);
-    }
-    uint4 vr[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int rr = r0 + (j < 4 ? 4 * grp + j : 16 + 4 * grp + (j - 4));
-      vr[j] = load8<KT>(vbase + roff(rr < i1 ? rr : i0) + 8 * c * ES);
-    }
-    f32x4 s[2];
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      s[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-        s[rt] = KT == 0 ? mfma_bf16(kf[rt][kb], qf[kb], s[rt]) : mfma_f16(kf[rt][kb], qf[kb], s[rt]);
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int rr = r0 + 16 * rt + 4 * grp + i;
-        const float v = rr < i1 ? s[rt][i] * kscale : -INFINITY;
-        s[rt][i] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, shfl_xor(mx, 16));
-    mx = fmaxf(mx, shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
-    float p[8], ps = 0.f;
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        p[rt * 4 + i] = exp2f(s[rt][i] - m_new);
-        ps += p[rt * 4 + i];
-      }
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-    uint4 pf;
-    if (KT == 0)
-      pf = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
-                      pack_bf16x2(p[6], p[7]));
-    else
-      pf = make_uint4(pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3]), pack_f16x2(p[4], p[5]), pack_f16x2(p[6], p[7]));
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float a_i = shfl(alpha, 4 * grp + i);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) o[k][i] *= a_i;
-    }
-    uint4 vt[8];
-    transpose8x8_b16(vr, vt);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) o[k] = KT == 0 ? mfma_bf16(pf, vt[k], o[k]) : mfma_f16(pf, vt[k], o[k]);
-  }
-  float lt = l_run + shfl_xor(l_run, 16);
-  lt += shfl_xor(lt, 32);
-  if (grp == 0) {
-    out_ml[c * 2 + 0] = m_run;
-    out_ml[c * 2 + 1] = lt;
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float4* dst = reinterpret_cast<float4*>(out_o + (4 * grp + i) * Dh + 8 * c);
-    dst[0] = make_float4(o[0][i] * vscale, o[1][i] * vscale, o[2][i] * vscale, o[3][i] * vscale);
-    dst[1] = make_float4(o[4][i] * vscale, o[5][i] * vscale, o[6][i] * vscale, o[7][i] * vscale);
-  }
-}
 
 template <int KT>
 __global__ __launch_bounds__(256) void k_attention(AttnArgs a, TickParams tp) {
@@ -454,9 +326,9 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a, TickParams tp) {
   float* out_ml = a.att_ml + (int64_t)item * 32;
   uint4 qf[4];
   if (cidx == nch) {  // the expert's own rows (bf16)
-    load_q_frag<0>(a.q, qrow, tv, grp, qf);
+    load_q_frag<0, false>(a.q, qrow, tv, grp, qf);
     const int64_t off = ((int64_t)b * tp.S * a.A + (int64_t)h * a.Dh) * 2;
-    attn_rows<0, false>((const char*)a.kself + off, (const char*)a.vself + off, (int64_t)a.A * 2, 0, 0, 0, tp.S, qf,
+    attn_rows<0, false, false, false>((const char*)a.kself + off, (const char*)a.vself + off, (int64_t)a.A * 2, 0, 0, 0, tp.S, qf,
                         1.f, 1.f, lane, out_o, out_ml, a.Dh);
   } else {
     const int i0 = cidx * tp.chunk_rows;
@@ -470,8 +342,8 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a, TickParams tp) {
       ks = a.cv.k_scale[si];
       vs = a.cv.v_scale[si];
     }
-    load_q_frag<KT>(a.q, qrow, tv, grp, qf);
-    attn_rows<KT, true>((const char*)a.cv.k + off, (const char*)a.cv.v + off, (int64_t)a.A * ES, tp.start[b],
+    load_q_frag<KT, false>(a.q, qrow, tv, grp, qf);
+    attn_rows<KT, true, false, false>((const char*)a.cv.k + off, (const char*)a.cv.v + off, (int64_t)a.A * ES, tp.start[b],
                         a.cv.cap, i0, i1, qf, ks, vs, lane, out_o, out_ml, a.Dh);
   }
 }
@@ -532,7 +404,8 @@ hipError_t launch_combine(const TickParams& tp, const Dims& dm, const Workspace&
 
 // =====================================================================================================
 // h += sum of split-K partials (fixed order), optional copy to the per-layer hidden output, then
-// x = bf16(RMSNorm(h) * gain) for the next projection.  One workgroup per token row.
+// x = bf16(h / rms(h)) for the next projection (whose packed weights carry the norm gain).  One workgroup
+// per token row.
 // =====================================================================================================
 __global__ __launch_bounds__(256) void k_reduce_norm(float* __restrict__ h, const float* __restrict__ part,
                                                      uint16_t* __restrict__ xb, int M, int d, int ksplit,
@@ -554,7 +427,7 @@ __global__ __launch_bounds__(256) void k_reduce_norm(float* __restrict__ h, cons
   const float r = 1.0f / sqrtf(ss / (float)d + eps);
   for (int n = threadIdx.x; n < d; n += blockDim.x) {
     const int64_t idx = (int64_t)m * d + n;
-    xb[idx] = f32_to_bf16(h[idx] * r * gain[n]);
+    xb[idx] = f32_to_bf16(h[idx] * r);  // the gain is folded into the packed weights
   }
 }
 

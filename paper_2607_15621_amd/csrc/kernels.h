@@ -19,6 +19,11 @@ struct TickParams {
   int64_t start[FSX_MAX_BATCH];               // ring slot of the oldest valid row
   int32_t len[FSX_MAX_BATCH];                 // valid cache rows
   int32_t chunk_prefix[FSX_MAX_BATCH + 1];    // chunk slots before agent b (each agent: ceil(len/chunk_rows) + 1)
+  // tick kernel: attention units are (agent, row range of range_rows rows, head); agent b owns ranges
+  // range_prefix[b] .. range_prefix[b+1]-1 (at least one, which also holds the expert's own rows)
+  int32_t range_rows;
+  int32_t n_aunits;
+  int32_t range_prefix[FSX_MAX_BATCH + 1];
 };
 
 // Cache view of one layer.
@@ -35,8 +40,8 @@ struct CacheView {
 
 // ------------------------------------------------------------------ packing (create time)
 enum PackKind { PACK_PLAIN = 0, PACK_ROPE_PAIRS = 1, PACK_SWIGLU_PAIRS = 2 };
-hipError_t launch_pack(const uint16_t* a, const uint16_t* b, int N, int K, int kind, int param, void* dst,
-                       hipStream_t s);
+hipError_t launch_pack(const uint16_t* a, const uint16_t* b, int N, int K, int kind, int param, const float* gain,
+                       void* dst, hipStream_t s);
 
 // ------------------------------------------------------------------ fused-path phases
 struct FastWeights {
@@ -84,6 +89,70 @@ hipError_t launch_reduce_norm(const TickParams& tp, const Dims& dm, const Worksp
                               const float* gain, float* hidden_layer, hipStream_t s);
 hipError_t launch_head(const TickParams& tp, const Dims& dm, const Workspace& ws, const float* final_norm,
                        const void* head_w, int head_dtype, float* waypoints, hipStream_t s);
+
+// ------------------------------------------------------------------ persistent tick kernel
+struct TickLayer {
+  const uint4* wqkv;
+  const uint4* wo;
+  const uint4* wgu;
+  const uint4* wd;
+  const float* attn_norm;
+  const float* ffn_norm;
+};
+
+struct TickArgs {
+  const TickLayer* layers;  // device [n_layers]
+  const float* final_norm;
+  const void* head_w;
+  int head_dtype;
+  int tok_dtype;
+  const void* tokens;
+  CacheView cv;
+  float* waypoints;
+  // exchanged inside the launch, device-coherent accesses
+  float* q;
+  uint16_t* kself;
+  uint16_t* vself;
+  float* att_o;
+  float* att_ml;
+  uint32_t* att_cnt;
+  int n_att_cnt;
+  float* part;
+  uint32_t* o_cnt;
+  uint32_t* d_cnt;
+  // written once per launch (per layer)
+  float* h0;
+  uint16_t* hb0;     // [M][d] bf16 copy of h0
+  uint16_t* hbmid;   // [L][M][d] bf16 copy of hmid
+  uint16_t* hbout;   // [L][M][d] bf16 copy of hout
+  float* ssq0;
+  float* rope;
+  float* hmid;     // [L][M][d]
+  float* hout;     // [L][M][d] (the caller's hidden buffer when given)
+  float* ssq_mid;  // [L][d/16][M]
+  float* ssq_out;  // [L][d/16][M]
+  uint16_t* attn;  // [L][M][A]
+  uint16_t* z;     // [L][M][F]
+  // flags (stamps) and status
+  uint64_t* f_embed;
+  uint64_t* f_qkv;
+  uint64_t* f_attn;
+  uint64_t* f_hmid;
+  uint64_t* f_z;
+  uint64_t* f_hout;
+  uint64_t* status;
+  uint64_t epoch;
+  uint64_t timeout_ticks;  // real-time counter ticks (100 MHz)
+  int ks_o, ks_d;
+  uint64_t* trace;         // optional: [grid][2 + 5 * n_layers + 1] real-time stamps per workgroup
+};
+
+// per workgroup: start, after the embedding, 16 events per layer (5 phase ends, then 11 sub-phase marks), end
+__host__ __device__ inline int trace_events(int n_layers) { return 2 + 16 * n_layers + 1; }
+
+int tick_mt(int M);
+hipError_t tick_occupancy(int mt, int kt, int* blocks_per_cu);
+hipError_t launch_tick(const TickArgs& a, const TickParams& tp, const Dims& dm, int grid, hipStream_t s);
 
 // ------------------------------------------------------------------ cache append
 hipError_t launch_append(const fsx_cache_desc& c, const void* k_rows, const void* v_rows, int n_rows,

@@ -19,12 +19,12 @@ LIB_PATH = os.path.join(HERE, "libfsx.so")
 
 F32, BF16, FP8_E4M3 = 0, 1, 2
 APPEND_RING, APPEND_ERROR = 0, 1
-FLAG_GENERIC, FLAG_MULTI_LAUNCH = 1, 2
+FLAG_GENERIC, FLAG_MULTI_LAUNCH, FLAG_TRACE = 1, 2, 4
 MAX_BATCH = 64
 STATUS = {0: "FSX_OK", 1: "FSX_E_INVALID", 2: "FSX_E_UNSUPPORTED", 3: "FSX_E_CAPACITY", 4: "FSX_E_OOM",
           5: "FSX_E_HIP"}
-SYMBOLS = ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_destroy",
-           "fsx_last_error", "fsx_expert_info", "fsx_version")
+SYMBOLS = ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_status",
+           "fsx_expert_trace", "fsx_expert_destroy", "fsx_last_error", "fsx_expert_info", "fsx_version")
 
 
 class FsxError(RuntimeError):
@@ -38,7 +38,7 @@ class ExpertCfg(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("n_expert_tokens", ctypes.c_int32),
                 ("n_out", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("max_frame_tokens", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float),
-                ("flags", ctypes.c_int32)]
+                ("flags", ctypes.c_int32), ("tick_timeout_us", ctypes.c_int32)]
 
 
 class LayerWeights(ctypes.Structure):
@@ -70,12 +70,16 @@ def lib() -> ctypes.CDLL:
                                         ctypes.POINTER(vp)]
         L.fsx_expert_forward.argtypes = [vp, ctypes.POINTER(CacheDescC), vp, i32, i32, vp, vp, vp]
         L.fsx_cache_append_rows.argtypes = [ctypes.POINTER(CacheDescC), vp, vp, i32, i32, vp]
+        L.fsx_expert_status.argtypes = [vp, vp]
+        L.fsx_expert_trace.argtypes = [vp, ctypes.POINTER(ctypes.c_uint64), i64, ctypes.POINTER(i32),
+                                       ctypes.POINTER(i32), vp]
         L.fsx_expert_destroy.argtypes = [vp]
         L.fsx_expert_destroy.restype = None
         L.fsx_last_error.restype = ctypes.c_char_p
         L.fsx_expert_info.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i64), ctypes.POINTER(i64)]
         L.fsx_version.restype = ctypes.c_char_p
-        for n in ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_info"):
+        for n in ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_info",
+                  "fsx_expert_status", "fsx_expert_trace"):
             getattr(L, n).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -113,9 +117,10 @@ def _stream(stream) -> int:
 
 
 def make_cfg(n_layers, d_model, n_heads, head_dim, d_ffn, n_expert_tokens=10, n_out=10, max_batch=1,
-             max_frame_tokens=0, dtype=BF16, rope_base=10000.0, rms_eps=1e-6, flags=0) -> ExpertCfg:
+             max_frame_tokens=0, dtype=BF16, rope_base=10000.0, rms_eps=1e-6, flags=0,
+             tick_timeout_us=0) -> ExpertCfg:
     return ExpertCfg(n_layers, d_model, n_heads, head_dim, d_ffn, n_expert_tokens, n_out, max_batch,
-                     max_frame_tokens, dtype, rope_base, rms_eps, flags)
+                     max_frame_tokens, dtype, rope_base, rms_eps, flags, tick_timeout_us)
 
 
 class Expert:
@@ -182,6 +187,22 @@ def expert_forward(ex: Expert, cache: CacheDesc, tokens, batch: int, n_frame_tok
     """fsx_expert_forward: one tick for `batch` agents (enqueued on `stream`)."""
     _check(lib().fsx_expert_forward(ctypes.c_void_p(ex.handle), ctypes.byref(cache.c), _ptr(tokens), batch,
                                     n_frame_tokens, _ptr(waypoints), _ptr(hidden), _stream(stream)))
+
+
+def expert_status(ex: Expert, stream=None):
+    """fsx_expert_status: synchronise the stream; raise if a tick of this handle timed out."""
+    _check(lib().fsx_expert_status(ctypes.c_void_p(ex.handle), _stream(stream)))
+
+
+def expert_trace(ex: Expert, n_wg_max: int = 1024, stream=None) -> np.ndarray:
+    """fsx_expert_trace: [n_wg][n_events] real-time stamps (100 MHz) of the last tick."""
+    n_layers = ex.cfg.n_layers
+    cap = n_wg_max * (2 + 16 * n_layers + 1)
+    buf = np.zeros(cap, np.uint64)
+    nw, ne = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().fsx_expert_trace(ctypes.c_void_p(ex.handle), buf.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)),
+                                  cap, ctypes.byref(nw), ctypes.byref(ne), _stream(stream)))
+    return buf[: nw.value * ne.value].reshape(nw.value, ne.value)
 
 
 def cache_append_rows(cache: CacheDesc, k_rows, v_rows, n_rows: int, policy: int = APPEND_RING, stream=None):

@@ -29,7 +29,7 @@ class Model:
         self.wl = wl
         self.layers, self.final_norm, self.head_w = synth.make_weights(wl)
 
-    def create(self, max_batch=None, max_frame_tokens=None, flags=0, device="cuda") -> fsx.Expert:
+    def create(self, max_batch=None, max_frame_tokens=None, flags=0, device="cuda", tick_timeout_us=0) -> fsx.Expert:
         wl = self.wl
         td = torch_dtype(wl.dtype)
         self.dev_layers = []
@@ -40,7 +40,7 @@ class Model:
         self.dev_head = torch.from_numpy(self.head_w).to(device=device, dtype=td)
         cfg = fsx.make_cfg(wl.n_layers, wl.d_model, wl.n_heads, wl.head_dim, wl.d_ffn, wl.n_expert_tokens, wl.n_out,
                            max_batch or wl.batch, wl.n_frame_tokens if max_frame_tokens is None else max_frame_tokens,
-                           fsx_dtype(wl.dtype), wl.rope_base, wl.rms_eps, flags)
+                           fsx_dtype(wl.dtype), wl.rope_base, wl.rms_eps, flags, tick_timeout_us)
         ex = fsx.expert_create(cfg, self.dev_layers, self.dev_final, self.dev_head)
         torch.cuda.synchronize()
         # the library packed its own copy; the caller's tensors may go

@@ -1,0 +1,111 @@
+"""The persistent tick kernel: agreement with the per-phase launch path, consecutive ticks with new inputs,
+per-layer hidden outputs, and the bounded-wait failure path (forced from the host by a tiny wait limit)."""
+
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from harness import Cache, Model, rel_err, run_forward, tokens_for
+from paper_2607_15621_amd import fsx
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def small(wid, lengths, n_frame=0, capacity=400, n_layers=3, d_model=128, n_heads=4, d_ffn=256):
+    return synth.Workload(name=f"tick{wid}", wid=wid, n_layers=n_layers, d_model=d_model, n_heads=n_heads,
+                          head_dim=128, d_ffn=d_ffn, n_expert_tokens=10, n_frame_tokens=n_frame,
+                          batch=len(lengths), lengths=tuple(lengths), dtype="bf16", cache_dtype="bf16",
+                          capacity=capacity)
+
+
+@pytest.mark.parametrize("n_frame", [0, 30])
+def test_tick_kernel_and_per_phase_launches_match_oracle(n_frame):
+    wl = small(70 + n_frame, lengths=(17, 0, 250, 399), n_frame=n_frame)
+    say(f"case tick vs per-phase, n_frame={n_frame}")
+    model = Model(wl)
+    cache = Cache(wl, starts=(390, 0, 200, 1))
+    host_tok, tok = tokens_for(wl)
+    outs = {}
+    for name, flags in (("tick", 0), ("per-phase", fsx.FLAG_MULTI_LAUNCH)):
+        ex = model.create(flags=flags)
+        wp, hid = run_forward(ex, cache, tok, wl.batch, n_frame, with_hidden=True)
+        outs[name] = (wp, hid)
+        ex.close()
+    for b in range(wl.batch):
+        ref, ref_hid = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        for name, (wp, hid) in outs.items():
+            e = rel_err(wp[b], ref)
+            say(f"  {name} agent {b} err {e:.3e}")
+            assert e <= TOL, (name, b, e)
+            for l in range(wl.n_layers):
+                assert rel_err(hid[l, b], ref_hid[l]) <= TOL, (name, b, l)
+    assert rel_err(outs["tick"][0], outs["per-phase"][0]) <= 1e-2
+
+
+def test_consecutive_ticks_with_new_inputs():
+    """Each tick must see its own inputs: forward A, then B (new tokens and cache), then A again."""
+    wl_a = small(80, lengths=(64, 120))
+    wl_b = wl_a.replace(wid=81)  # other tokens and cache; the weights stay those of A
+    model = Model(wl_a)
+    ex = model.create()
+    cache_a = Cache(wl_a)
+    cache_b = Cache(wl_b)
+    host_a, tok_a = tokens_for(wl_a)
+    host_b, tok_b = tokens_for(wl_b)
+    for rnd, (cache, host, tok) in enumerate(((cache_a, host_a, tok_a), (cache_b, host_b, tok_b),
+                                              (cache_a, host_a, tok_a))):
+        wp, _ = run_forward(ex, cache, tok, wl_a.batch, 0)
+        for b in range(wl_a.batch):
+            ref, _ = model.oracle_agent(host[b], cache.oracle_rows(b), cache.desc.pos[b])
+            e = rel_err(wp[b], ref)
+            say(f"  round {rnd} agent {b} err {e:.3e}")
+            assert e <= TOL
+
+
+def test_many_ticks_are_bitwise_reproducible():
+    wl = small(82, lengths=(300,), n_layers=2)
+    model = Model(wl)
+    ex = model.create()
+    cache = Cache(wl)
+    _, tok = tokens_for(wl)
+    first, _ = run_forward(ex, cache, tok, 1, 0)
+    wp = torch.empty((1, wl.n_out), device="cuda")
+    for _ in range(50):
+        fsx.expert_forward(ex, cache.desc, tok, 1, 0, wp)
+    torch.cuda.synchronize()
+    fsx.expert_status(ex)
+    assert np.array_equal(wp.cpu().numpy(), first)
+
+
+def test_wait_limit_failure_is_reported_and_poisons_waypoints():
+    """A 1 us bound on every wait makes the tick give up: waypoints NaN, status reports it once."""
+    wl = small(83, lengths=(200, 50), n_layers=2)
+    model = Model(wl)
+    cache = Cache(wl)
+    host_tok, tok = tokens_for(wl)
+    ex_lim = model.create(tick_timeout_us=1)
+    wp, _ = run_forward(ex_lim, cache, tok, wl.batch, 0)
+    assert np.isnan(wp).all()
+    with pytest.raises(fsx.FsxError) as e:
+        fsx.expert_status(ex_lim)
+    assert e.value.code == 5 and "timed out" in str(e.value)
+    fsx.expert_status(ex_lim)  # reported once
+    ex_lim.close()
+    ex = model.create()  # an expert with the default bound works on the same inputs
+    wp2, _ = run_forward(ex, cache, tok, wl.batch, 0)
+    fsx.expert_status(ex)
+    for b in range(wl.batch):
+        ref, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        assert rel_err(wp2[b], ref) <= TOL
