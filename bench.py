@@ -143,7 +143,8 @@ def main():
         "wall_s": round(wall, 4),
         "higher_is_better": True,
         "scaling": "weak",
-        "vs_baseline": round(value / (1000.0 / PAPER_EXPERT_MS), 3),
+        # the paper's expert tick (another machine) is quoted for the 40-frame history only
+        "vs_baseline": round(value / (1000.0 / PAPER_EXPERT_MS), 3) if wl.name == "single_bf16_L224" else None,
         "dtype": "bf16" if wl.cache_dtype != "fp8" else "bf16 (fp8-e4m3 cache)",
         "data": "synthetic (seeded N(0,1) tokens and cache, N(0,0.02^2) weights)",
         "config": {"workload": wl.name, "agents": wl.batch, "cache_rows": list(wl.lengths)[:8],
