@@ -100,9 +100,10 @@ typedef struct {
 } fsx_layer_weights;
 
 /* The backbone's per-layer KV cache for a batch of agents (Sec. 3.1, Sec. 3.3).
- * Each (agent, layer) owns a ring of `capacity` rows; a row holds one cached token's
- * keys (or values) for all heads, [H][Dh].  Keys are stored already rotated.
- * The valid rows of agent b are ring slots (start[b] + i) mod capacity, i < len[b]. */
+ * Head-major, as a transformer's per-layer cache is usually kept: each (agent, layer, head) owns a
+ * contiguous ring of `capacity` rows of Dh elements (one cached token's key, or value, for that head).
+ * Keys are stored already rotated.  The valid rows of agent b are ring slots (start[b] + i) mod
+ * capacity, i < len[b], the same slots in every layer and head. */
 typedef struct {
   int32_t dtype;           /* FSX_F32 | FSX_BF16 | FSX_FP8_E4M3 */
   int32_t batch;           /* agents described by this descriptor */
@@ -111,7 +112,7 @@ typedef struct {
   int32_t head_dim;        /* must equal the expert's */
   int32_t reserved;        /* 0 */
   int64_t capacity;        /* ring rows per (agent, layer) */
-  void* k;                 /* DEVICE [batch][n_layers][capacity][H][Dh] */
+  void* k;                 /* DEVICE [batch][n_layers][H][capacity][Dh] */
   void* v;                 /* DEVICE, same layout */
   const float* k_scale;    /* FP8 only: DEVICE [batch][n_layers][H], stored value = code * scale */
   const float* v_scale;    /* FP8 only: DEVICE [batch][n_layers][H] */
@@ -149,10 +150,11 @@ int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weights* layers
 int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, const void* tokens, int32_t batch,
                        int32_t n_frame_tokens, float* waypoints, float* hidden, void* stream);
 
-/* Append n_rows new cached rows to every (agent, layer) of the cache (Sec. 3.3: every K ticks the
- * slow system appends the current frame's tokens through an incremental forward).
- *   k_rows, v_rows DEVICE [cache->batch][n_layers][n_rows][H][Dh] in cache->dtype (fp8: codes
- *                  already scaled by the cache's k_scale / v_scale)
+/* Append n_rows new cached rows to every (agent, layer, head) of the cache (Sec. 3.3: every K ticks
+ * the slow system appends the current frame's tokens through an incremental forward).
+ *   k_rows, v_rows DEVICE [cache->batch][n_layers][H][n_rows][Dh] in cache->dtype (fp8: codes
+ *                  already scaled by the cache's k_scale / v_scale); Dh elements must be a multiple
+ *                  of 16 bytes (FSX_E_UNSUPPORTED otherwise)
  *   policy         FSX_APPEND_RING: when a ring is full the oldest rows are overwritten (start
  *                  advances); FSX_APPEND_ERROR: FSX_E_CAPACITY if any agent would exceed
  *                  capacity, and nothing is written.

@@ -499,8 +499,8 @@ extern "C" int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, 
   if (n_rows > cache->capacity) return fail(FSX_E_CAPACITY, "n_rows exceeds the ring capacity");
   if (cache->n_layers <= 0 || cache->n_heads <= 0 || cache->head_dim <= 0)
     return fail(FSX_E_INVALID, "cache geometry must be positive");
-  const int64_t row_bytes = (int64_t)cache->n_heads * cache->head_dim * esize(cache->dtype);
-  if (row_bytes % 16) return fail(FSX_E_UNSUPPORTED, "a cache row must be a multiple of 16 bytes");
+  const int64_t head_row_bytes = (int64_t)cache->head_dim * esize(cache->dtype);
+  if (head_row_bytes % 16) return fail(FSX_E_UNSUPPORTED, "a cache row of one head must be a multiple of 16 bytes");
   if (!aligned16(k_rows) || !aligned16(v_rows) || !aligned16(cache->k) || !aligned16(cache->v))
     return fail(FSX_E_INVALID, "row and cache buffers must be 16-byte aligned");
   const int B = cache->batch;

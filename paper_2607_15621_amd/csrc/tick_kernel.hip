@@ -494,7 +494,7 @@ __device__ __forceinline__ void attn_tiles(const TickArgs& a, const TickParams& 
   m_run = -INFINITY;
   l_run = 0.f;
   if (part >= ntiles) return;
-  const int64_t crow = (int64_t)A * ES, srow = (int64_t)A * 2;
+  const int64_t crow = (int64_t)Dh * ES, srow = (int64_t)A * 2;
   uint4 kf[8], vr[8];
   // the first tile, when it is a cache tile, does not depend on this layer's projections: load it now
   int j = part;
@@ -655,9 +655,9 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
     U.i1 = min(U.i0 + tp.range_rows, tp.len[b]);
     U.nct = U.i1 > U.i0 ? (U.i1 - U.i0 + 31) / 32 : 0;
     U.nst = U.r == U.nr - 1 ? (tp.S + 31) / 32 : 0;
-    const int64_t slab = ((int64_t)b * a.cv.n_layers + l) * a.cv.cap;
-    U.kc = (const char*)a.cv.k + (slab * A + (int64_t)U.h * Dh) * ES;
-    U.vc = (const char*)a.cv.v + (slab * A + (int64_t)U.h * Dh) * ES;
+    const int64_t slab = (((int64_t)b * a.cv.n_layers + l) * H + U.h) * a.cv.cap;  // head-major (b, l, h) ring
+    U.kc = (const char*)a.cv.k + slab * Dh * ES;
+    U.vc = (const char*)a.cv.v + slab * Dh * ES;
     U.ks = (const char*)a.kself + ((int64_t)b * tp.S * A + (int64_t)U.h * Dh) * 2;
     U.vs = (const char*)a.vself + ((int64_t)b * tp.S * A + (int64_t)U.h * Dh) * 2;
     U.ksc = U.vsc = 1.f;

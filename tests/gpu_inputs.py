@@ -62,7 +62,7 @@ class Cache:
         cap = wl.capacity if capacity is None else capacity
         self.capacity = cap
         self.starts = [0] * B if starts is None else list(starts)
-        shape = (B, wl.n_layers, cap, wl.n_heads, wl.head_dim)
+        shape = (B, wl.n_layers, wl.n_heads, cap, wl.head_dim)  # head-major rings
         if wl.cache_dtype == "fp8":
             self.k = torch.zeros(shape, dtype=torch.uint8, device=device)
             self.v = torch.zeros(shape, dtype=torch.uint8, device=device)
@@ -97,7 +97,14 @@ class Cache:
                 t = torch.from_numpy(codes)
             else:
                 t = torch.from_numpy(src).to(dst.dtype)
-            dst[b, l].index_copy_(0, idx.to(dst.device), t.to(dst.device, non_blocking=False))
+            # generator slab [L][H][Dh] -> head-major [H][L][Dh] rows of the ring
+            t = t.permute(1, 0, 2).contiguous()
+            dst[b, l].index_copy_(1, idx.to(dst.device), t.to(dst.device, non_blocking=False))
+
+
+def head_major_rows(rows: np.ndarray, dtype, device="cuda"):
+    """Appended rows [B][n_layers][n][H][Dh] (generator order) -> device [B][n_layers][H][n][Dh]."""
+    return torch.from_numpy(np.ascontiguousarray(rows.transpose(0, 1, 3, 2, 4))).to(device, dtype)
 
 
 def tokens_for(wl: synth.Workload, device="cuda"):

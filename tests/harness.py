@@ -13,7 +13,7 @@ import oracle
 import synth
 from gpu_inputs import Cache as _Cache
 from gpu_inputs import Model as _Model
-from gpu_inputs import rel_err, run_forward, tokens_for  # noqa: F401
+from gpu_inputs import head_major_rows, rel_err, run_forward, tokens_for  # noqa: F401
 
 
 def shape_of(wl: synth.Workload) -> oracle.ExpertShape:

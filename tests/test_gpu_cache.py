@@ -14,7 +14,7 @@ import torch
 
 import oracle
 import synth
-from harness import Cache, Model, rel_err, run_forward, tokens_for
+from harness import Cache, Model, head_major_rows, rel_err, run_forward, tokens_for
 from paper_2607_15621_amd import fsx
 
 pytestmark = pytest.mark.gpu
@@ -41,10 +41,6 @@ def rows_after_append(wl, b, l, kind, new_rows, capacity, start_len):
     return allr[max(0, allr.shape[0] - capacity):]
 
 
-def device_rows(t, wl, b, l):
-    return t[b, l].float().cpu().numpy()
-
-
 def test_append_is_bit_exact_and_wraps_the_ring():
     wl = small(50, lengths=(30, 64), capacity=64)
     say("case append ring")
@@ -53,27 +49,29 @@ def test_append_is_bit_exact_and_wraps_the_ring():
     n = 4
     k_new = synth.append_rows(wl, 0, "k", n)
     v_new = synth.append_rows(wl, 0, "v", n)
-    kd = torch.from_numpy(k_new).to("cuda", torch.bfloat16)
-    vd = torch.from_numpy(v_new).to("cuda", torch.bfloat16)
+    kd = head_major_rows(k_new, torch.bfloat16)
+    vd = head_major_rows(v_new, torch.bfloat16)
     fsx.cache_append_rows(cache.desc, kd, vd, n, fsx.APPEND_RING)
     torch.cuda.synchronize()
     # agent 0: rows 30..33 written, start 0, len 34; agent 1: full ring, slots 0..3 overwritten, start 4
     assert list(cache.desc.len) == [34, 64] and list(cache.desc.start) == [0, 4] and list(cache.desc.pos) == [34, 68]
     for l in range(wl.n_layers):
-        assert torch.equal(cache.k[0, l, 30:34].view(torch.int16), kd[0, l].view(torch.int16))
-        assert torch.equal(cache.k[1, l, 0:4].view(torch.int16), kd[1, l].view(torch.int16))
-        assert torch.equal(cache.v[1, l, 0:4].view(torch.int16), vd[1, l].view(torch.int16))
+        assert torch.equal(cache.k[0, l, :, 30:34].view(torch.int16), kd[0, l].view(torch.int16))
+        assert torch.equal(cache.k[1, l, :, 0:4].view(torch.int16), kd[1, l].view(torch.int16))
+        assert torch.equal(cache.v[1, l, :, 0:4].view(torch.int16), vd[1, l].view(torch.int16))
+        # the bytes are the generator's rows of that (layer, head)
+        assert torch.equal(cache.k[1, l, 2, 0:4].float().cpu(), torch.from_numpy(k_new[1, l, :, 2]))
         # untouched rows keep their bytes
-        assert torch.equal(cache.k[0, l, :30].view(torch.int16), before_k[0, l, :30].view(torch.int16))
-        assert torch.equal(cache.k[1, l, 4:].view(torch.int16), before_k[1, l, 4:].view(torch.int16))
-        assert torch.equal(cache.k[0, l, 34:].view(torch.int16), before_k[0, l, 34:].view(torch.int16))
+        assert torch.equal(cache.k[0, l, :, :30].view(torch.int16), before_k[0, l, :, :30].view(torch.int16))
+        assert torch.equal(cache.k[1, l, :, 4:].view(torch.int16), before_k[1, l, :, 4:].view(torch.int16))
+        assert torch.equal(cache.k[0, l, :, 34:].view(torch.int16), before_k[0, l, :, 34:].view(torch.int16))
 
 
 def test_append_error_policy_rejects_and_writes_nothing():
     wl = small(51, lengths=(60,), capacity=62)
     cache = Cache(wl)
     before = cache.k.clone()
-    kd = torch.zeros((1, wl.n_layers, 4, wl.n_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+    kd = torch.zeros((1, wl.n_layers, wl.n_heads, 4, wl.head_dim), dtype=torch.bfloat16, device="cuda")
     with pytest.raises(fsx.FsxError) as e:
         fsx.cache_append_rows(cache.desc, kd, kd, 4, fsx.APPEND_ERROR)
     assert e.value.code == 3
@@ -94,8 +92,7 @@ def test_forward_after_wrapping_append_matches_oracle():
     n = 6
     k_new = synth.append_rows(wl, 0, "k", n)
     v_new = synth.append_rows(wl, 0, "v", n)
-    fsx.cache_append_rows(cache.desc, torch.from_numpy(k_new).to("cuda", torch.bfloat16),
-                          torch.from_numpy(v_new).to("cuda", torch.bfloat16), n)
+    fsx.cache_append_rows(cache.desc, head_major_rows(k_new, torch.bfloat16), head_major_rows(v_new, torch.bfloat16), n)
     wp, _ = run_forward(ex, cache, tok, wl.batch, 0)
     for b in range(wl.batch):
         def rows(l, b=b):
@@ -126,13 +123,13 @@ def test_batched_agents_then_append_match_oracle():
     n = wl.append_rows
     k_new = synth.append_rows(wl, 0, "k", n)
     v_new = synth.append_rows(wl, 0, "v", n)
-    kd = torch.from_numpy(k_new).to("cuda", torch.bfloat16)
-    vd = torch.from_numpy(v_new).to("cuda", torch.bfloat16)
+    kd = head_major_rows(k_new, torch.bfloat16)
+    vd = head_major_rows(v_new, torch.bfloat16)
     fsx.cache_append_rows(cache.desc, kd, vd, n)
     torch.cuda.synchronize()
     assert all(int(x) == 1028 for x in cache.desc.len)
-    assert torch.equal(cache.k[:, :, 1024:1028].view(torch.int16), kd.view(torch.int16))
-    assert torch.equal(cache.v[:, :, 1024:1028].view(torch.int16), vd.view(torch.int16))
+    assert torch.equal(cache.k[:, :, :, 1024:1028].view(torch.int16), kd.view(torch.int16))
+    assert torch.equal(cache.v[:, :, :, 1024:1028].view(torch.int16), vd.view(torch.int16))
     wp2, _ = run_forward(ex, cache, tok, wl.batch, 0)
     for b in sample:
         def rows(l, b=b):
@@ -157,7 +154,8 @@ def test_fp8_decode_of_every_code_on_the_gpu():
         ex = model.create(flags=flags)
         cache = Cache(wl)
         for kind, t in (("k", cache.k), ("v", cache.v)):
-            t[0, 0].copy_(torch.from_numpy(block if kind == "v" else np.flip(block, 0).copy()))
+            rows = block if kind == "v" else np.flip(block, 0)
+            t[0, 0].copy_(torch.from_numpy(np.ascontiguousarray(rows.transpose(1, 0, 2))))  # [H][rows][Dh]
         cache.k_scale.fill_(1.0 / 64)
         cache.v_scale.fill_(1.0 / 32)
         torch.cuda.synchronize()

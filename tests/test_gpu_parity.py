@@ -129,8 +129,8 @@ def test_small_permuted_cache_rows_give_same_waypoints():
     host_tok, tok = tokens_for(wl)
     wp, _ = run_forward(ex, cache, tok, 1, 0)
     perm = torch.randperm(200, generator=torch.Generator().manual_seed(0)).to(cache.k.device)
-    cache.k[0, :, :200] = cache.k[0, :, :200][:, perm]
-    cache.v[0, :, :200] = cache.v[0, :, :200][:, perm]
+    cache.k[0, :, :, :200] = cache.k[0, :, :, :200][:, :, perm]
+    cache.v[0, :, :, :200] = cache.v[0, :, :, :200][:, :, perm]
     torch.cuda.synchronize()
     wp2, _ = run_forward(ex, cache, tok, 1, 0)
     assert rel_err(wp2, wp) <= 1e-2
