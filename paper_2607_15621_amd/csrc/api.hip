@@ -251,19 +251,20 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   if (ex->tick) {
     TickArgs& t = ex->ta;
     const size_t dt = (size_t)d / 16;
+    const size_t Mp = ((size_t)M + 7) / 8 * 8, Ms = ((size_t)M + 31) / 32 * 32;
     std::vector<std::pair<void**, size_t>> tp = {
         {(void**)&t.h0, (size_t)M * d * 4},
-        {(void**)&t.hb0, (size_t)M * d * 2},
-        {(void**)&t.hbmid, (size_t)L * M * d * 2},
-        {(void**)&t.hbout, (size_t)L * M * d * 2},
-        {(void**)&t.ssq0, dt * M * 4},
+        {(void**)&t.hb0, Mp * d * 2},
+        {(void**)&t.hbmid, (size_t)L * Mp * d * 2},
+        {(void**)&t.hbout, (size_t)L * Mp * d * 2},
+        {(void**)&t.ssq0, dt * Ms * 4},
         {(void**)&t.hmid, (size_t)L * M * d * 4},
         {(void**)&t.hout, (size_t)L * M * d * 4},
-        {(void**)&t.ssq_mid, (size_t)L * dt * M * 4},
-        {(void**)&t.ssq_out, (size_t)L * dt * M * 4},
+        {(void**)&t.ssq_mid, (size_t)L * dt * Ms * 4},
+        {(void**)&t.ssq_out, (size_t)L * dt * Ms * 4},
         {(void**)&t.attn, (size_t)L * M * A * 2},
-        {(void**)&t.z, (size_t)L * M * F * 2},
-        {(void**)&t.f_embed, (size_t)M * 8},
+        {(void**)&t.z, (size_t)L * Mp * F * 2},
+        {(void**)&t.f_embed, (dt + (size_t)M) * 8},
         {(void**)&t.f_qkv, (size_t)3 * A / 16 * 8},
         {(void**)&t.f_attn, (size_t)nflag_attn * 8},
         {(void**)&t.f_hmid, dt * 8},
@@ -272,7 +273,8 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
         {(void**)&t.status, 256},
         {(void**)&t.att_cnt, (size_t)nflag_attn * 4},
         {(void**)&t.o_cnt, dt * 4},
-        {(void**)&t.d_cnt, dt * 4}};
+        {(void**)&t.d_cnt, dt * 4},
+        {(void**)&t.sched, (size_t)L * 4}};
     parts.insert(parts.end(), tp.begin(), tp.end());
     ex->n_att_cnt = nflag_attn;
   }
@@ -424,33 +426,42 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
   for (int b = 0; b < batch; ++b) tp.chunk_prefix[b + 1] = tp.chunk_prefix[b] + (int)((tp.len[b] + cr - 1) / cr) + 1;
   if (ex->tick) {
     int per_cu = 0;
-    const int mt = tick_mt(tp.M);
-    HIP_TRY(tick_occupancy(mt, cache->dtype == FSX_FP8_E4M3 ? 1 : 0, &per_cu));
+    HIP_TRY(tick_occupancy(cache->dtype == FSX_FP8_E4M3 ? 1 : 0, &per_cu));
     if (per_cu < 1) return fail(FSX_E_UNSUPPORTED, "tick kernel does not fit on a compute unit");
-    // attention units: (agent, range of rr rows, head, query tile).  One range per agent when the work is
-    // small; otherwise about 2 (medium) or 8 (large) units per workgroup, with an agent's ranges of equal size.
     const int G = ex->cu_count;
-    int64_t lmax = 0;
-    for (int b = 0; b < batch; ++b) lmax = std::max<int64_t>(lmax, tp.len[b]);
-    const int64_t per_wg = rows * dm.H * tp.n_tt / G;
-    int64_t rr = std::max<int64_t>(32, (lmax + 31) / 32 * 32);
-    if (per_wg > 512) {
-      const int64_t target_pairs = std::max<int64_t>(1, (per_wg <= 8192 ? 2 : 8) * (int64_t)G / tp.n_tt);
-      const int64_t rr_t = std::max<int64_t>(128, (rows * dm.H + target_pairs - 1) / target_pairs);
-      const int64_t nr = (lmax + rr_t - 1) / rr_t;
-      rr = std::max<int64_t>(128, ((lmax + nr - 1) / nr + 31) / 32 * 32);
-    }
+    tp.Mp = (tp.M + 7) / 8 * 8;
+    tp.Ms = (tp.M + 31) / 32 * 32;
+    // Attention units: (agent, range of rows, head).  Rows per unit (one head) aim at about one unit per
+    // workgroup for small work and 2 or 4 for larger work (units are handed out dynamically, so several
+    // per workgroup even out), never below 512 rows; an agent's ranges are equal, multiples of 32 rows.
+    const int64_t total_rh = rows * dm.H;
+    const int64_t per_wg = total_rh / G;
+    const int k_units = per_wg >= 4096 ? 4 : (per_wg >= 512 ? 2 : 1);
+    int64_t unit_rows = std::max<int64_t>(512, (total_rh + (int64_t)k_units * G - 1) / ((int64_t)k_units * G));
     for (;;) {
       int64_t slots = 0;
-      for (int b = 0; b < batch; ++b) slots += std::max<int64_t>(1, (tp.len[b] + rr - 1) / rr);
+      for (int b = 0; b < batch; ++b) slots += std::max<int64_t>(1, (tp.len[b] + unit_rows - 1) / unit_rows);
       if (slots * dm.H * tp.n_tt <= ex->items_max) break;
-      rr *= 2;
+      unit_rows *= 2;
     }
-    tp.range_rows = (int)std::min<int64_t>(rr, INT32_MAX / 2);
     tp.range_prefix[0] = 0;
-    for (int b = 0; b < batch; ++b)
-      tp.range_prefix[b + 1] = tp.range_prefix[b] + (int)std::max<int64_t>(1, (tp.len[b] + rr - 1) / rr);
-    tp.n_aunits = tp.range_prefix[batch] * dm.H;
+    for (int b = 0; b < batch; ++b) {
+      const int64_t nr = std::max<int64_t>(1, (tp.len[b] + unit_rows - 1) / unit_rows);
+      const int64_t rr = std::max<int64_t>(32, ((tp.len[b] + nr - 1) / nr + 31) / 32 * 32);
+      tp.range_rows[b] = (int)std::min<int64_t>(rr, INT32_MAX / 2);
+      tp.range_prefix[b + 1] = tp.range_prefix[b] + (int)nr;
+    }
+    // agents with the largest ranges first
+    std::vector<int> ord(batch);
+    for (int b = 0; b < batch; ++b) ord[b] = b;
+    std::stable_sort(ord.begin(), ord.end(), [&](int x, int y) { return tp.range_rows[x] > tp.range_rows[y]; });
+    tp.unit_prefix[0] = 0;
+    for (int k = 0; k < batch; ++k) {
+      const int b = ord[k];
+      tp.order[k] = b;
+      tp.unit_prefix[k + 1] = tp.unit_prefix[k] + (tp.range_prefix[b + 1] - tp.range_prefix[b]) * dm.H;
+    }
+    tp.n_units = tp.unit_prefix[batch];
     TickArgs a = ex->ta;
     a.tok_dtype = c.dtype;
     a.tokens = tokens;

@@ -127,8 +127,33 @@ __device__ __forceinline__ float4 ld_dev_f4(const float* p) {
 __device__ __forceinline__ uint32_t atomic_add_dev(uint32_t* p, uint32_t v) {
   return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// wait until every vector memory operation this thread issued has completed
-__device__ __forceinline__ void stores_done() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until every vector memory operation this thread issued has completed (s_waitcnt vmcnt(0), GFX9
+// encoding).  Through the builtin, so the compiler knows those loads are complete and adds no later wait
+// for them; the empty asm statements keep memory accesses from moving across it.
+__device__ __forceinline__ void vm_wait_all() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ void stores_done() { vm_wait_all(); }
+
+// Load through a pointer that addresses global memory.  A pointer the compiler cannot prove global (one
+// read from memory, such as a table of weight pointers) would otherwise give a flat load, which also counts
+// in the LDS counter, so every later LDS wait would wait for it too.
+// (Through a native vector type: a cast of a pointer to the class type uint4 loses its address space.)
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld_global(const uint4* p) {
+  const u32x4_t v = *(const __attribute__((address_space(1))) u32x4_t*)p;
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Direct load global -> LDS of 16 bytes per lane: lane l's 16 bytes at src land at lds_base + 16 l
+// (lds_base is wave-uniform).  No registers hold the data; completion is counted by vmcnt.
+__device__ __forceinline__ void load_lds16(const void* src, void* lds_base) {
+  typedef __attribute__((address_space(3))) void lds_void_t;
+  typedef const __attribute__((address_space(1))) void g_void_t;
+  __builtin_amdgcn_global_load_lds((g_void_t*)src, (lds_void_t*)lds_base, 16, 0, 0);
+}
 
 // Plain or device-coherent access, chosen at compile time.
 template <bool COH>

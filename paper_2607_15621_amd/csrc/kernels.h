@@ -12,18 +12,22 @@ namespace fsx {
 struct TickParams {
   int32_t B, S, T, M;                         // agents, tokens per agent, pooled tokens, rows = B*S
   int32_t n_tt;                               // ceil(S / 16): query tiles per (agent, head)
-  int32_t chunk_rows;                         // cache rows per attention work item
-  int32_t n_items;                            // attention work items
-  int32_t reserved;
+  int32_t chunk_rows;                         // per-phase path: cache rows per attention work item
+  int32_t n_items;                            // per-phase path: attention work items
+  int32_t Mp;                                 // M rounded up to 8: rows of tile-major activations
+  int32_t Ms;                                 // M rounded up to 32: rows of the sums of squares
+  int32_t n_units;                            // tick kernel: attention units
   int64_t pos[FSX_MAX_BATCH];                 // rotary position of token 0
   int64_t start[FSX_MAX_BATCH];               // ring slot of the oldest valid row
   int32_t len[FSX_MAX_BATCH];                 // valid cache rows
-  int32_t chunk_prefix[FSX_MAX_BATCH + 1];    // chunk slots before agent b (each agent: ceil(len/chunk_rows) + 1)
-  // tick kernel: attention units are (agent, row range of range_rows rows, head); agent b owns ranges
-  // range_prefix[b] .. range_prefix[b+1]-1 (at least one, which also holds the expert's own rows)
-  int32_t range_rows;
-  int32_t n_aunits;
+  int32_t chunk_prefix[FSX_MAX_BATCH + 1];    // per-phase path: chunk slots before agent b (ceil(len/chunk_rows) + 1 each)
+  // tick kernel: attention units are (agent, range of range_rows[b] rows, head); agent b owns range slots
+  // range_prefix[b] .. range_prefix[b+1]-1 (at least one, the last also holds the expert's own rows).  Units are
+  // numbered agent by agent in the order order[0..B-1]; the k-th agent's units start at unit_prefix[k].
   int32_t range_prefix[FSX_MAX_BATCH + 1];
+  int32_t range_rows[FSX_MAX_BATCH];
+  int32_t unit_prefix[FSX_MAX_BATCH + 1];
+  int32_t order[FSX_MAX_BATCH];
 };
 
 // Cache view of one layer.
@@ -120,19 +124,20 @@ struct TickArgs {
   float* part;
   uint32_t* o_cnt;
   uint32_t* d_cnt;
-  // written once per launch (per layer)
+  uint32_t* sched;   // [n_layers] attention units taken beyond the first G
+  // written once per launch (per layer); "tile-major" = [column tile][Mp rows][16 columns]
   float* h0;
-  uint16_t* hb0;     // [M][d] bf16 copy of h0
-  uint16_t* hbmid;   // [L][M][d] bf16 copy of hmid
-  uint16_t* hbout;   // [L][M][d] bf16 copy of hout
-  float* ssq0;
-  float* rope;
+  uint16_t* hb0;     // [d/16][Mp][16] bf16 copy of h0, tile-major
+  uint16_t* hbmid;   // [L][d/16][Mp][16] bf16 copy of hmid, tile-major
+  uint16_t* hbout;   // [L][d/16][Mp][16] bf16 copy of hout, tile-major
+  float* ssq0;     // [d/16][Ms] per-tile sums of squares of h0
+  float* rope;     // [M][Dh/2][2] cos, sin
   float* hmid;     // [L][M][d]
   float* hout;     // [L][M][d] (the caller's hidden buffer when given)
-  float* ssq_mid;  // [L][d/16][M]
-  float* ssq_out;  // [L][d/16][M]
+  float* ssq_mid;  // [L][d/16][Ms]
+  float* ssq_out;  // [L][d/16][Ms]
   uint16_t* attn;  // [L][M][A]
-  uint16_t* z;     // [L][M][F]
+  uint16_t* z;     // [L][F/8][Mp][8] SwiGLU output, tile-major
   // flags (stamps) and status
   uint64_t* f_embed;
   uint64_t* f_qkv;
@@ -144,14 +149,13 @@ struct TickArgs {
   uint64_t epoch;
   uint64_t timeout_ticks;  // real-time counter ticks (100 MHz)
   int ks_o, ks_d;
-  uint64_t* trace;         // optional: [grid][2 + 5 * n_layers + 1] real-time stamps per workgroup
+  uint64_t* trace;         // optional: [grid][trace_events(n_layers)] real-time stamps per workgroup
 };
 
 // per workgroup: start, after the embedding, 16 events per layer (5 phase ends, then 11 sub-phase marks), end
 __host__ __device__ inline int trace_events(int n_layers) { return 2 + 16 * n_layers + 1; }
 
-int tick_mt(int M);
-hipError_t tick_occupancy(int mt, int kt, int* blocks_per_cu);
+hipError_t tick_occupancy(int kt, int* blocks_per_cu);
 hipError_t launch_tick(const TickArgs& a, const TickParams& tp, const Dims& dm, int grid, hipStream_t s);
 
 // ------------------------------------------------------------------ cache append
