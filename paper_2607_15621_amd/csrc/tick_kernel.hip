@@ -328,8 +328,33 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
 }
 
 // ------------------------------------------------------------------------------------------ Q
+// One wave per projection unit: the wave holds the unit's 16-column tile for every k-block (K <= 512) in
+// registers and multiplies all staged row tiles, so the units of a workgroup run side by side with no
+// cross-wave reduction.
+__device__ __forceinline__ void load_unit_w_full(const uint4* __restrict__ wtile, int nkb, uint4 w[16]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) w[i] = i < nkb ? ld_global(wtile + (int64_t)i * WAVE + lane) : make_uint4(0, 0, 0, 0);
+}
+
+template <typename Epi>
+__device__ __forceinline__ void wave_gemm(const uint4 w[16], int nkb, int mt_n, TickLds& L, Epi epi) {
+  const int lane = threadIdx.x & 63, c = lane & 15, grp = lane >> 4;
+#pragma unroll
+  for (int mt = 0; mt < MTMAX; ++mt) {
+    if (mt < mt_n) {
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (i < nkb) acc = mfma_bf16(*reinterpret_cast<const uint4*>(&L.u.p.x[mt * 16 + c][i * 32 + 8 * grp]), w[i], acc);
+      epi(mt, acc, c, grp);
+    }
+  }
+}
+
 __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   const int G = gridDim.x, d = dm.d, M = tp.M, A = dm.A, Dh = dm.Dh, half = Dh / 2;
+  const int wave = threadIdx.x >> 6;
   const int n_units = 3 * A / 16;
   const TickLayer& W = a.layers[l];
   const int KB = d / 32;
@@ -337,13 +362,11 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
   const uint16_t* hbsrc = l == 0 ? a.hb0 : a.hbout + (int64_t)(l - 1) * tp.Mp * d;
   const float* ssq = l == 0 ? a.ssq0 : a.ssq_out + (int64_t)(l - 1) * (d / 16) * tp.Ms;
   bool waited = false;
-  for (int u0 = blockIdx.x; u0 < n_units; u0 += UMAX * G) {
-    uint4 w[UMAX][4];
-#pragma unroll
-    for (int k = 0; k < UMAX; ++k) {
-      const int u = u0 + k * G;
-      if (u < n_units) load_unit_w(W.wqkv + (int64_t)u * KB * WAVE, 0, KB, w[k]);
-    }
+  for (int u0 = blockIdx.x; u0 < n_units; u0 += 4 * G) {
+    const int u = u0 + wave * G;  // this wave's unit in this round
+    const bool mine = u < n_units;
+    uint4 w[16];
+    if (mine) load_unit_w_full(W.wqkv + (int64_t)u * KB * WAVE, KB, w);
     if (!waited) {
       TICK_SUB(l, 0);
       const bool ok = l == 0 ? wg_wait(a.f_embed, d / 16 + M, stamp_of(a, -1, dm.n_layers), a, L)
@@ -352,19 +375,16 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
       waited = true;
       TICK_SUB(l, 1);
     }
+    const int sec = (u * 16) / A;  // 0 q, 1 k, 2 v
+    const int nl0 = u * 16 - sec * A;
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
       // rotary rows ([M][Dh/2][2], 512 bytes each, one producer per row, complete before any projection
       // starts) are read with ordinary loads
       stage<16>(hbsrc, tp.Mp, m0, rows, d, ssq, tp.Ms, d, dm.eps, L, a.rope);
       TICK_SUB(l, 2);
-#pragma unroll
-      for (int k = 0; k < UMAX; ++k) {
-        const int u = u0 + k * G;
-        if (u >= n_units) break;
-        const int sec = (u * 16) / A;  // 0 q, 1 k, 2 v
-        const int nl0 = u * 16 - sec * A;
-        unit_gemm(w[k], KB, mt_n, L, [&](int mt, f32x4 s, int c, int grp) {
+      if (mine) {
+        wave_gemm(w, KB, mt_n, L, [&](int mt, f32x4 s, int c, int grp) {
           const int nl = nl0 + c;
           if (sec == 2) {
 #pragma unroll
@@ -398,6 +418,7 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
           }
         });
       }
+      __syncthreads();  // the next chunk overwrites the staged rows
     }
   }
   TICK_SUB(l, 3);
@@ -412,10 +433,11 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
 }
 
 // ------------------------------------------------------------------------------------------ A
-// Raw registers of one 32-row tile, as loaded: k[rt*4 + kb] = K row r0+16rt+c, channels 32kb+8grp..+7;
-// v[j] = V row r0 + (j<4 ? 4grp+j : 16+4grp+j-4), channels 8c..8c+7.  fp8 tiles hold the codes (8 bytes per
-// 8 channels) and are decoded only when the tile is used, so the loads of the following tiles stay in
-// flight meanwhile.
+// Raw registers of one 32-row tile, as loaded.  bf16: k[rt*4 + kb] = K row r0+16rt+c, channels 32kb+8grp..+7;
+// fp8: k[rt*2 + h] = K row r0+16rt+c, channels 64h+16grp..+15 (16 bytes; the k-blocks of the score MFMA then
+// hold channels 64(kb/2) + 16grp + 8(kb%2) + j, and the fp16 queries use the same order).  v[j] = V row
+// r0 + (j<4 ? 4grp+j : 16+4grp+j-4), channels 8c..8c+7.  fp8 tiles hold the codes and are decoded only when
+// the tile is used, so the loads of the following tiles stay in flight meanwhile.
 template <int KT>
 struct RawTile;
 template <>
@@ -425,7 +447,7 @@ struct RawTile<0> {
 };
 template <>
 struct RawTile<1> {
-  uint2 k[8];
+  uint4 k[4];
   uint2 v[8];
 };
 
@@ -445,12 +467,12 @@ __device__ __forceinline__ void load_cache_tile(const char* kb, const char* vb, 
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
     const char* p = kb + roff(r0 + 16 * rt + c);
+    if constexpr (KT == 0) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if constexpr (KT == 0)
-        t.k[rt * 4 + k] = *reinterpret_cast<const uint4*>(p + (32 * k + 8 * grp) * ES);
-      else
-        t.k[rt * 4 + k] = *reinterpret_cast<const uint2*>(p + (32 * k + 8 * grp) * ES);
+      for (int k = 0; k < 4; ++k) t.k[rt * 4 + k] = *reinterpret_cast<const uint4*>(p + (32 * k + 8 * grp) * 2);
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) t.k[rt * 2 + h] = *reinterpret_cast<const uint4*>(p + 64 * h + 16 * grp);
     }
   }
 #pragma unroll
@@ -483,7 +505,7 @@ __device__ __forceinline__ void load_own_tile(const char* ks, const char* vs, in
 }
 
 // Query fragments of query tiles tt0 .. tt0+nq-1 of agent b, head h (16 queries x 128 channels each, B operand
-// of S^T = K Q^T), as bf16 (F16 = false) or fp16.
+// of S^T = K Q^T): bf16 in plain channel order (F16 = false), or fp16 in the channel order of fp8 key tiles.
 template <int NQ, bool F16>
 __device__ __forceinline__ void load_q(const TickArgs& a, const TickParams& tp, const Dims& dm, int b, int h, int tt0,
                                        int nq, uint4 (&q)[NQ][4]) {
@@ -496,9 +518,10 @@ __device__ __forceinline__ void load_q(const TickArgs& a, const TickParams& tp, 
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
+      const int ch = F16 ? 64 * (kb >> 1) + 16 * grp + 8 * (kb & 1) : 32 * kb + 8 * grp;
       if (tv) {
-        lo = ld_dev_f4(row + 32 * kb + 8 * grp);
-        hi = ld_dev_f4(row + 32 * kb + 8 * grp + 4);
+        lo = ld_dev_f4(row + ch);
+        hi = ld_dev_f4(row + ch + 4);
       }
       if (F16)
         q[tt][kb] = make_uint4(pack_f16x2(lo.x, lo.y), pack_f16x2(lo.z, lo.w), pack_f16x2(hi.x, hi.y),
@@ -554,12 +577,16 @@ __device__ __forceinline__ void tile_compute(const RawTile<KT>& t, QF qf, int nq
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      kf[i] = make_uint4(e4m3x2_to_f16x2(t.k[i].x, false), e4m3x2_to_f16x2(t.k[i].x, true),
-                         e4m3x2_to_f16x2(t.k[i].y, false), e4m3x2_to_f16x2(t.k[i].y, true));
+    for (int i = 0; i < 4; ++i) {
+      kf[2 * i] = make_uint4(e4m3x2_to_f16x2(t.k[i].x, false), e4m3x2_to_f16x2(t.k[i].x, true),
+                             e4m3x2_to_f16x2(t.k[i].y, false), e4m3x2_to_f16x2(t.k[i].y, true));
+      kf[2 * i + 1] = make_uint4(e4m3x2_to_f16x2(t.k[i].z, false), e4m3x2_to_f16x2(t.k[i].z, true),
+                                 e4m3x2_to_f16x2(t.k[i].w, false), e4m3x2_to_f16x2(t.k[i].w, true));
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
       vr[i] = make_uint4(e4m3x2_to_f16x2(t.v[i].x, false), e4m3x2_to_f16x2(t.v[i].x, true),
                          e4m3x2_to_f16x2(t.v[i].y, false), e4m3x2_to_f16x2(t.v[i].y, true));
-    }
   }
   uint4 vt[8];
   transpose8x8_b16(vr, vt);
@@ -763,7 +790,13 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
     load_q<1, KT == 1>(a, tp, dm, U.b, U.h, tt0, nq, reinterpret_cast<uint4(&)[1][4]>(qr));
   else
     load_q_lds<KT == 1>(a, tp, dm, U.b, U.h, tt0, nq, L);
+  // LDS queries are in plain channel order; fp8 key tiles want the permuted order (see RawTile)
   auto qf = [&](int tt, int k) -> uint4 {
+    if (NQ == 1) return qr[k];
+    const int ch = KT == 1 ? 64 * (k >> 1) + 16 * grp + 8 * (k & 1) : 32 * k + 8 * grp;
+    return *reinterpret_cast<const uint4*>(&L.u.a.qs[tt * 16 + c16][ch]);
+  };
+  auto qf_own = [&](int tt, int k) -> uint4 {
     if (NQ == 1) return qr[k];
     return *reinterpret_cast<const uint4*>(&L.u.a.qs[tt * 16 + c16][32 * k + 8 * grp]);
   };
@@ -800,7 +833,7 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
     for (int j = first_own; j < U.nst; j += 4) {
       RawTile<0> t;
       load_own_tile(U.ks, U.vs, (int64_t)dm.A * 2, 32 * j, tp.S, t);
-      tile_compute<0, NQ>(t, qf, nq, 32 * j, tp.S, 1.f, o, m_run, l_run);
+      tile_compute<0, NQ>(t, qf_own, nq, 32 * j, tp.S, 1.f, o, m_run, l_run);
     }
   }
   const bool final_out = U.nr == 1;
