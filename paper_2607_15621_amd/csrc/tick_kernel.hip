@@ -32,13 +32,22 @@
 
 namespace fsx {
 
+// threadIdx.x, re-read at each use through an empty asm statement.  Otherwise the compiler hoists the
+// lane-dependent addresses of every phase out of the layer loop and keeps them all live at once, which
+// exhausts the register file; recomputing them where they are used costs a few instructions.
+__device__ __forceinline__ int tix() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
 constexpr int XSTR = 520;  // LDS row stride (bf16 elements) of staged activations: 512 + 8 padding
 constexpr int NTHR = 256;
 constexpr int UMAX = 4;    // projection units whose weights a wave holds in registers at once
 constexpr int MTMAX = 5;   // 16-row tiles per staged chunk (80 rows)
 constexpr int DH = 128;    // head width of the fused path
 constexpr int STW = 16 * DH + 32;  // LDS floats of one wave's attention state: O[16][128], (m, l)[16]
-constexpr int NQW = 5;     // query tiles a wave carries at once in the many-query attention variant
+constexpr int NQW = 3;     // query tiles a wave carries at once in the many-query attention variant
 
 struct TickLds {
   union {
@@ -72,7 +81,7 @@ __device__ __forceinline__ uint64_t fail_tag(const TickArgs& a) { return a.epoch
 __device__ __forceinline__ bool wave_wait(const uint64_t* flags, int n, uint64_t target, const TickArgs& a,
                                           int inner = 1 << 30, int stride = 0) {
   constexpr int GR = 4;  // groups of 64 flags per round trip
-  const int lane = threadIdx.x & 63;
+  const int lane = tix() & 63;
   const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
   for (int base = 0; base < n; base += GR * WAVE) {
     int64_t fi[GR];
@@ -107,9 +116,9 @@ __device__ __forceinline__ bool wave_wait(const uint64_t* flags, int n, uint64_t
 
 __device__ __forceinline__ bool wg_wait(const uint64_t* flags, int n, uint64_t target, const TickArgs& a, TickLds& L,
                                         int inner = 1 << 30, int stride = 0) {
-  if (threadIdx.x < WAVE) {
+  if (tix() < WAVE) {
     const bool ok = wave_wait(flags, n, target, a, inner, stride);
-    if (threadIdx.x == 0) L.ok = ok;
+    if (tix() == 0) L.ok = ok;
   }
   __syncthreads();
   const bool ok = L.ok;
@@ -118,7 +127,7 @@ __device__ __forceinline__ bool wg_wait(const uint64_t* flags, int n, uint64_t t
 }
 
 __device__ __forceinline__ void trace_mark(const TickArgs& a, int ev, int n_layers) {
-  if (a.trace && threadIdx.x == 0)
+  if (a.trace && tix() == 0)
     a.trace[(int64_t)blockIdx.x * trace_events(n_layers) + ev] = __builtin_amdgcn_s_memrealtime();
 }
 
@@ -136,7 +145,7 @@ __device__ __forceinline__ void trace_mark(const TickArgs& a, int ev, int n_laye
 template <int TW>
 __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int rows, int K, const float* ssq, int Ms,
                                       int Kn, float eps, TickLds& L, const float* rope = nullptr) {
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = tix(), wave = tid >> 6, lane = tid & 63;
   const int cpr = K / 8;  // chunks per row
   if (lane < cpr) {
     int64_t off;  // element offset of lane's chunk in row 0 of the chunk
@@ -186,7 +195,7 @@ __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int r
 // i = w, w+4, w+8, w+12 (a range is at most 512 columns = 16 blocks), whose 1 KiB weight blocks it holds
 // in registers.
 __device__ __forceinline__ void load_unit_w(const uint4* __restrict__ wtile, int kb0, int nkb, uint4 w[4]) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = tix() >> 6, lane = tix() & 63;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int i = wave + 4 * j;
@@ -198,7 +207,7 @@ __device__ __forceinline__ void load_unit_w(const uint4* __restrict__ wtile, int
 // over the 4 waves through LDS and handed to epi(mt, C-layout values, c, grp) by wave mt % 4.
 template <typename Epi>
 __device__ __forceinline__ void unit_gemm(const uint4 w[4], int nkb, int mt_n, TickLds& L, Epi epi) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = tix() >> 6, lane = tix() & 63;
   const int c = lane & 15, grp = lane >> 4;
   // every row tile of the chunk buffer is multiplied (straight-line code); tiles past mt_n are not used
   f32x4 acc[MTMAX];
@@ -233,7 +242,7 @@ __device__ __forceinline__ void reduce_tile(const TickArgs& a, const TickParams&
                                             uint32_t* cnt, uint64_t* flag, uint64_t st) {
   const int M = tp.M, d = dm.d, total = M * 16;
   constexpr int BATCH = 2;
-  for (int i0 = threadIdx.x; i0 < total; i0 += BATCH * NTHR) {
+  for (int i0 = tix(); i0 < total; i0 += BATCH * NTHR) {
     float p[BATCH][8], hv[BATCH];
 #pragma unroll
     for (int k = 0; k < BATCH; ++k) {
@@ -264,10 +273,10 @@ __device__ __forceinline__ void reduce_tile(const TickArgs& a, const TickParams&
       if (c == 0 && idx < total) st_dev_f(ssq_dst + (int64_t)nt * tp.Ms + m, sq);
     }
   }
-  if (threadIdx.x == 0) st_dev(cnt + nt, 0u);
+  if (tix() == 0) st_dev(cnt + nt, 0u);
   stores_done();
   __syncthreads();
-  if (threadIdx.x == 0) st_dev(flag + nt, st);
+  if (tix() == 0) st_dev(flag + nt, st);
 }
 
 // ------------------------------------------------------------------------------------------ embed
@@ -280,7 +289,7 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
   for (int u = blockIdx.x; u < n_units; u += G) {
     if (u < nt) {
       // thread: row m = i / 8, column pair 2 * (i % 8)
-      for (int i = threadIdx.x; i < M * 8; i += NTHR) {
+      for (int i = tix(); i < M * 8; i += NTHR) {
         const int m = i >> 3, cp = (i & 7) * 2, n = u * 16 + cp;
         const int64_t idx = (int64_t)m * d + n;
         float v0, v1;
@@ -302,7 +311,7 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
       }
     } else {
       const int m = u - nt, b = m / tp.S, t = m % tp.S;
-      for (int j = threadIdx.x; j < half; j += NTHR) {
+      for (int j = tix(); j < half; j += NTHR) {
         double cs = 1.0, sn = 0.0;
         if (dm.rope_base > 0.f) {
           const double ang = (double)(tp.pos[b] + t) * pow((double)dm.rope_base, -2.0 * (double)j / (double)dm.Dh);
@@ -314,16 +323,16 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
       }
     }
     // return the counters to zero (robust to an earlier launch that stopped midway)
-    for (int i = u * NTHR + threadIdx.x; i < a.n_att_cnt; i += n_units * NTHR) st_dev(a.att_cnt + i, 0u);
-    for (int i = u * NTHR + threadIdx.x; i < dm.n_layers; i += n_units * NTHR) st_dev(a.sched + i, 0u);
+    for (int i = u * NTHR + tix(); i < a.n_att_cnt; i += n_units * NTHR) st_dev(a.att_cnt + i, 0u);
+    for (int i = u * NTHR + tix(); i < dm.n_layers; i += n_units * NTHR) st_dev(a.sched + i, 0u);
     if (u == 0)
-      for (int i = threadIdx.x; i < nt; i += NTHR) {
+      for (int i = tix(); i < nt; i += NTHR) {
         st_dev(a.o_cnt + i, 0u);
         st_dev(a.d_cnt + i, 0u);
       }
     stores_done();
     __syncthreads();
-    if (threadIdx.x == 0) st_dev(a.f_embed + u, st);
+    if (tix() == 0) st_dev(a.f_embed + u, st);
   }
 }
 
@@ -332,14 +341,14 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
 // registers and multiplies all staged row tiles, so the units of a workgroup run side by side with no
 // cross-wave reduction.
 __device__ __forceinline__ void load_unit_w_full(const uint4* __restrict__ wtile, int nkb, uint4 w[16]) {
-  const int lane = threadIdx.x & 63;
+  const int lane = tix() & 63;
 #pragma unroll
   for (int i = 0; i < 16; ++i) w[i] = i < nkb ? ld_global(wtile + (int64_t)i * WAVE + lane) : make_uint4(0, 0, 0, 0);
 }
 
 template <typename Epi>
 __device__ __forceinline__ void wave_gemm(const uint4 w[16], int nkb, int mt_n, TickLds& L, Epi epi) {
-  const int lane = threadIdx.x & 63, c = lane & 15, grp = lane >> 4;
+  const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
 #pragma unroll
   for (int mt = 0; mt < MTMAX; ++mt) {
     if (mt < mt_n) {
@@ -354,7 +363,7 @@ __device__ __forceinline__ void wave_gemm(const uint4 w[16], int nkb, int mt_n, 
 
 __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   const int G = gridDim.x, d = dm.d, M = tp.M, A = dm.A, Dh = dm.Dh, half = Dh / 2;
-  const int wave = threadIdx.x >> 6;
+  const int wave = tix() >> 6;
   const int n_units = 3 * A / 16;
   const TickLayer& W = a.layers[l];
   const int KB = d / 32;
@@ -425,7 +434,7 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
   stores_done();
   __syncthreads();
   TICK_SUB(l, 4);
-  if (threadIdx.x == 0) {
+  if (tix() == 0) {
     const uint64_t st = stamp_of(a, l, dm.n_layers);
     for (int u = blockIdx.x; u < n_units; u += G) st_dev(a.f_qkv + u, st);
   }
@@ -458,7 +467,7 @@ __device__ __forceinline__ void load_cache_tile(const char* kb, const char* vb, 
                                                 int r0, int i1, RawTile<KT>& t) {
   constexpr int ES = KT == 0 ? 2 : 1;
   constexpr int64_t RB = DH * ES;
-  const int lane = threadIdx.x & 63, c = lane & 15, grp = lane >> 4;
+  const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
   auto roff = [&](int i) -> int64_t {
     int64_t slot = start + (i < i1 ? i : i0);
     if (slot >= cap) slot -= cap;
@@ -489,7 +498,7 @@ __device__ __forceinline__ void load_cache_tile(const char* kb, const char* vb, 
 // Own-row tile (the expert's rows [r0, r0+32) of S, bf16, produced in this launch): device-coherent loads.
 __device__ __forceinline__ void load_own_tile(const char* ks, const char* vs, int64_t srow, int r0, int S,
                                               RawTile<0>& t) {
-  const int lane = threadIdx.x & 63, c = lane & 15, grp = lane >> 4;
+  const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
     const int i = r0 + 16 * rt + c;
@@ -509,7 +518,7 @@ __device__ __forceinline__ void load_own_tile(const char* ks, const char* vs, in
 template <int NQ, bool F16>
 __device__ __forceinline__ void load_q(const TickArgs& a, const TickParams& tp, const Dims& dm, int b, int h, int tt0,
                                        int nq, uint4 (&q)[NQ][4]) {
-  const int lane = threadIdx.x & 63, grp = lane >> 4;
+  const int lane = tix() & 63, grp = lane >> 4;
 #pragma unroll
   for (int tt = 0; tt < NQ; ++tt) {
     const int t = (tt0 + tt) * 16 + (lane & 15);
@@ -538,7 +547,7 @@ __device__ __forceinline__ void load_q(const TickArgs& a, const TickParams& tp, 
 template <bool F16>
 __device__ __forceinline__ void load_q_lds(const TickArgs& a, const TickParams& tp, const Dims& dm, int b, int h,
                                            int tt0, int nq, TickLds& L) {
-  for (int i = threadIdx.x; i < nq * 16 * (DH / 8); i += NTHR) {
+  for (int i = tix(); i < nq * 16 * (DH / 8); i += NTHR) {
     const int row = i / (DH / 8), c8 = (i % (DH / 8)) * 8;
     const int t = tt0 * 16 + row;
     float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
@@ -567,7 +576,7 @@ template <int KT, int NQ, typename QF>
 __device__ __forceinline__ void tile_compute(const RawTile<KT>& t, QF qf, int nq, int r0, int i1, float kscale,
                                              f32x4 (&o)[NQ][8], float (&m_run)[NQ], float (&l_run)[NQ]) {
   constexpr bool F16 = KT == 1;
-  const int lane = threadIdx.x & 63, grp = lane >> 4;
+  const int lane = tix() & 63, grp = lane >> 4;
   uint4 kf[8], vr[8];
   if constexpr (KT == 0) {
 #pragma unroll
@@ -651,7 +660,7 @@ __device__ __forceinline__ void tile_compute(const RawTile<KT>& t, QF qf, int nq
 
 // write a wave's state (o in the PV C layout, m and the lane-partial l) to LDS slot w
 __device__ __forceinline__ void state_to_lds(float* stw, const f32x4 o[8], float m_run, float l_run) {
-  const int lane = threadIdx.x & 63, c = lane & 15, grp = lane >> 4;
+  const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
   float lt = l_run + shfl_xor(l_run, 16);
   lt += shfl_xor(lt, 32);
 #pragma unroll
@@ -680,7 +689,7 @@ struct AUnit {
 // the attention output; else store the unnormalised partial of slot `item`.
 __device__ __forceinline__ void merge_states(const TickArgs& a, const TickParams& tp, const Dims& dm, int l,
                                              const AUnit& U, int tt, bool final_out, int64_t item, TickLds& L) {
-  const int t = threadIdx.x >> 4, d0 = (threadIdx.x & 15) * 8;
+  const int t = tix() >> 4, d0 = (tix() & 15) * 8;
   float Mx = -INFINITY;
 #pragma unroll
   for (int w = 0; w < 4; ++w) Mx = fmaxf(Mx, L.u.a.st[w][2048 + 2 * t]);
@@ -707,7 +716,7 @@ __device__ __forceinline__ void merge_states(const TickArgs& a, const TickParams
     float* po = a.att_o + (item * 16 + t) * 128 + d0;
     st_dev_f4(po, make_float4(acc[0], acc[1], acc[2], acc[3]));
     st_dev_f4(po + 4, make_float4(acc[4], acc[5], acc[6], acc[7]));
-    if ((threadIdx.x & 15) == 0) {
+    if ((tix() & 15) == 0) {
       st_dev_f(a.att_ml + item * 32 + 2 * t, Mx);
       st_dev_f(a.att_ml + item * 32 + 2 * t + 1, Ls);
     }
@@ -717,7 +726,7 @@ __device__ __forceinline__ void merge_states(const TickArgs& a, const TickParams
 // the last range of an agent to finish merges the partials of all its ranges (fixed order)
 __device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickParams& tp, const Dims& dm, int l,
                                                const AUnit& U) {
-  const int t = threadIdx.x >> 4, d0 = (threadIdx.x & 15) * 8;
+  const int t = tix() >> 4, d0 = (tix() & 15) * 8;
   const int H = dm.H;
   for (int tt = 0; tt < tp.n_tt; ++tt) {
     float Mx = -INFINITY, Ls = 0.f, acc[8];
@@ -755,7 +764,7 @@ __device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickPara
 template <int KT, int NQ, int PD>
 __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& tp, const Dims& dm, int l,
                                           const AUnit& U, int tt0, int nq, TickLds& L) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, c16 = lane & 15, grp = lane >> 4;
+  const int wave = tix() >> 6, lane = tix() & 63, c16 = lane & 15, grp = lane >> 4;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
   // this wave's cache tiles: j = wave + 4 i, i < nc
   const int nc = U.nct > wave ? (U.nct - wave + 3) / 4 : 0;
@@ -864,7 +873,7 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
   while (u < n_units) {
     // take the next unit now; the answer is needed only at the end of this one
     uint32_t nxt = 0;
-    if (threadIdx.x == 0) nxt = atomic_add_dev(a.sched + l, 1u);
+    if (tix() == 0) nxt = atomic_add_dev(a.sched + l, 1u);
     AUnit U;
     int k = 0;
     while (k + 1 < tp.B && tp.unit_prefix[k + 1] <= u) ++k;
@@ -890,24 +899,29 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
       U.vsc = a.cv.v_scale[si];
     }
     bool ok = true;
-    for (int tt0 = 0; tt0 < n_tt && ok; ++tt0) ok = attn_unit<KT, 1, KT == 0 ? 2 : 3>(a, tp, dm, l, U, tt0, 1, L);
+    if (n_tt == 1) {
+      ok = attn_unit<KT, 1, KT == 0 ? 3 : 4>(a, tp, dm, l, U, 0, 1, L);
+    } else {
+      for (int tt0 = 0; tt0 < n_tt && ok; tt0 += NQW)
+        ok = attn_unit<KT, NQW, 2>(a, tp, dm, l, U, tt0, min(NQW, n_tt - tt0), L);
+    }
     if (!ok) return false;
     if (first) TICK_SUB(l, 5);
-    if (threadIdx.x == 0) L.next = G + (int)nxt;
+    if (tix() == 0) L.next = G + (int)nxt;
     stores_done();
     __syncthreads();
     if (first) TICK_SUB(l, 6);
     const int ci = b * H + U.h;
     // an (agent, head) is complete when all its ranges are written
     const uint32_t need = (uint32_t)U.nr;
-    if (threadIdx.x == 0) L.last = need == 1 ? 1 : atomic_add_dev(a.att_cnt + ci, 1u) == need - 1;
+    if (tix() == 0) L.last = need == 1 ? 1 : atomic_add_dev(a.att_cnt + ci, 1u) == need - 1;
     __syncthreads();
     if (L.last) {
       if (need > 1) combine_ranges(a, tp, dm, l, U);
-      if (threadIdx.x == 0 && need > 1) st_dev(a.att_cnt + ci, 0u);
+      if (tix() == 0 && need > 1) st_dev(a.att_cnt + ci, 0u);
       stores_done();
       __syncthreads();
-      if (threadIdx.x == 0) st_dev(a.f_attn + ci, st);
+      if (tix() == 0) st_dev(a.f_attn + ci, st);
     }
     u = L.next;
     first = false;
@@ -945,7 +959,7 @@ __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams&
     stores_done();
     __syncthreads();
     if (u == (int)blockIdx.x) TICK_SUB(l, 8);
-    if (threadIdx.x == 0) L.last = atomic_add_dev(a.o_cnt + nt, 1u) == (uint32_t)(a.ks_o - 1);
+    if (tix() == 0) L.last = atomic_add_dev(a.o_cnt + nt, 1u) == (uint32_t)(a.ks_o - 1);
     __syncthreads();
     if (u == (int)blockIdx.x) TICK_SUB(l, 9);
     if (L.last)
@@ -1003,7 +1017,7 @@ __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams
   }
   stores_done();
   __syncthreads();
-  if (threadIdx.x == 0)
+  if (tix() == 0)
     for (int u = blockIdx.x; u < n_units; u += G) st_dev(a.f_z + u, st);
   return true;
 }
@@ -1034,7 +1048,7 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
     }
     stores_done();
     __syncthreads();
-    if (threadIdx.x == 0) L.last = atomic_add_dev(a.d_cnt + nt, 1u) == (uint32_t)(a.ks_d - 1);
+    if (tix() == 0) L.last = atomic_add_dev(a.d_cnt + nt, 1u) == (uint32_t)(a.ks_d - 1);
     __syncthreads();
     if (L.last)
       reduce_tile(a, tp, dm, nt, a.ks_d, hmid, a.hout + (int64_t)l * M * d, a.hbout + (int64_t)l * tp.Mp * d,
@@ -1049,7 +1063,7 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
 // tid + 256 and holds the pooled rows in registers (16 rows per pass).
 __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& tp, const Dims& dm, bool ok, TickLds& L) {
   const int G = gridDim.x, d = dm.d, M = tp.M, nl = dm.n_layers, T = tp.T;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = tix(), wave = tid >> 6, lane = tid & 63;
   for (int b = blockIdx.x; b < tp.B; b += G) {
     if (ok) ok = wg_wait(a.f_hout, d / 16, stamp_of(a, nl - 1, nl), a, L);
     if (!ok) {
@@ -1115,7 +1129,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_tick(TickArgs a, TickParams tp, Dim
   __shared__ TickLds L;
   const int nl = dm.n_layers;
   trace_mark(a, 0, nl);
-  if (threadIdx.x == 0) L.ok = 1;
+  if (tix() == 0) L.ok = 1;
   __syncthreads();
   phase_embed(a, tp, dm, L);
   trace_mark(a, 1, nl);

@@ -184,6 +184,23 @@ def test_small_fp8_cache_matches_oracle():
         assert e <= FP8_WP_TOL and ed <= BF16_WP_TOL
 
 
+def test_small_fp8_cache_with_frame_tokens_matches_oracle():
+    """fp8 cache rows with several query tiles per agent (10 expert + 30 frame tokens)."""
+    wl = small(62, lengths=(290, 64), capacity=300, cache_dtype="fp8").replace(n_frame_tokens=30)
+    say("case small fp8 with frame tokens")
+    model = Model(wl)
+    ex = model.create()
+    cache = Cache(wl, starts=(250, 7))
+    host_tok, tok = tokens_for(wl)
+    wp, _ = run_forward(ex, cache, tok, wl.batch, wl.n_frame_tokens)
+    for b in range(wl.batch):
+        ref, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        refd, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b, decoded=True), cache.desc.pos[b])
+        e, ed = rel_err(wp[b], ref), rel_err(wp[b], refd)
+        say(f"  agent {b} err vs source {e:.3e}, vs decoded {ed:.3e}")
+        assert e <= FP8_WP_TOL and ed <= BF16_WP_TOL
+
+
 @pytest.mark.slow
 def test_ragged_fp8_agents_match_oracle():
     """8 agents with ragged histories (256..16384 rows) in an fp8 cache; sampled agents vs the oracle."""
