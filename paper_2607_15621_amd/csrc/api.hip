@@ -30,20 +30,7 @@ int esize(int dtype) { return dtype == FSX_F32 ? 4 : (dtype == FSX_BF16 ? 2 : 1)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-constexpr int KSPLIT_MAX = 8;
-
-// split factor of the output projection: a divisor of H whose head group is at most 512 columns wide
-int pick_ks_o(int H, int Dh) {
-  for (int ks = 1; ks <= H; ++ks)
-    if (H % ks == 0 && (H / ks) * Dh <= 512 && ks >= std::min(H, KSPLIT_MAX)) return ks <= KSPLIT_MAX ? ks : -1;
-  return -1;
-}
-// split factor of the down projection: ranges of F/ks columns, a multiple of 32, at most 512
-int pick_ks_d(int F) {
-  for (int ks = KSPLIT_MAX; ks >= 1; --ks)
-    if ((F / 32) % ks == 0 && F / ks <= 512) return ks;
-  return -1;
-}
+constexpr int KSPLIT_MAX = 8;  // split factor bound of the per-phase path's split-K projections
 
 }  // namespace
 
@@ -64,9 +51,8 @@ struct fsx_expert {
   const float* final_norm = nullptr;
   // persistent tick kernel
   bool tick = false;
-  int ks_o = 8, ks_d = 8, n_att_cnt = 0, cu_count = 0;
+  int cu_count = 0, nx = 0;
   TickArgs ta{};            // workspace pointers; per-forward fields are filled in forward
-  TickLayer* dlayers = nullptr;
   uint64_t* trace = nullptr;
   uint64_t epoch = 0;
   uint64_t status_seen = 0;
@@ -78,7 +64,6 @@ static void free_expert(fsx_expert* ex) {
   if (ex->fbuf) (void)hipFree(ex->fbuf);
   if (ex->head_w) (void)hipFree(ex->head_w);
   if (ex->wsbuf) (void)hipFree(ex->wsbuf);
-  if (ex->dlayers) (void)hipFree(ex->dlayers);
   if (ex->trace) (void)hipFree(ex->trace);
   delete ex;
 }
@@ -239,44 +224,67 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
              {(void**)&ex->gws.g, (size_t)M * F * 4},   {(void**)&ex->gws.u, (size_t)M * F * 4},
              {(void**)&ex->gws.rope, (size_t)M * Dh * 4}};
   }
-  const int L = c.n_layers;
   const int nflag_attn = c.max_batch * H;
   if (ex->path == 0 && !(c.flags & FSX_FLAG_MULTI_LAUNCH)) {
-    ex->ks_o = pick_ks_o(H, Dh);
-    ex->ks_d = pick_ks_d(F);
-    auto pow2 = [](int v) { return v > 0 && (v & (v - 1)) == 0; };
-    ex->tick = d <= 512 && pow2(d) && ex->ks_o > 0 && ex->ks_d > 0 && pow2(A / ex->ks_o) && pow2(F / ex->ks_d) &&
+    // The tick kernel splits heads and FFN columns over the XCDs; find how many there are and check that
+    // every XCD's share fits the kernel (at most 4 heads of width 128 and 512 FFN columns per XCD).
+    hipDeviceProp_t prop;
+    if (!ok(hipGetDeviceProperties(&prop, ex->device), "hipGetDeviceProperties")) return cleanup(FSX_E_HIP);
+    ex->cu_count = prop.multiProcessorCount;
+    int nx = 0;
+    if (ex->cu_count <= 512) {
+      uint32_t* dev_ids = nullptr;
+      std::vector<uint32_t> ids(ex->cu_count);
+      if (!ok(hipMalloc((void**)&dev_ids, sizeof(uint32_t) * ex->cu_count), "hipMalloc(xcd probe)")) return cleanup(FSX_E_OOM);
+      const bool good = ok(probe_xcds(dev_ids, ex->cu_count, s), "probe_xcds") &&
+                        ok(hipMemcpyAsync(ids.data(), dev_ids, sizeof(uint32_t) * ex->cu_count, hipMemcpyDeviceToHost, s),
+                           "copy xcd probe") &&
+                        ok(hipStreamSynchronize(s), "hipStreamSynchronize(xcd probe)");
+      (void)hipFree(dev_ids);
+      if (!good) return cleanup(FSX_E_HIP);
+      bool seen[16] = {false};
+      for (uint32_t id : ids) seen[id & 15] = true;
+      for (bool b : seen) nx += b;
+    }
+    ex->nx = nx;
+    const int nh_max = nx > 0 ? (H + nx - 1) / nx : 1 << 30;
+    const int fr_max = nx > 0 ? 32 * ((F / 32 + nx - 1) / nx) : 1 << 30;
+    ex->tick = nx > 0 && nx <= NXMAX && ex->cu_count <= XFLAGS && d <= 512 && d % 32 == 0 && F % 32 == 0 && nh_max <= 4 && fr_max <= 512 &&
                c.n_expert_tokens <= 64;
   }
   if (ex->tick) {
     TickArgs& t = ex->ta;
     const size_t dt = (size_t)d / 16;
     const size_t Mp = ((size_t)M + 7) / 8 * 8, Ms = ((size_t)M + 31) / 32 * 32;
+    auto r256 = [](size_t b) { return (b + 255) & ~(size_t)255; };
+    const size_t rep_f = r256(Mp * d * 4), rep_b = r256(Mp * d * 2), rep_s = r256(dt * Ms * 4),
+                 rep_r = r256((size_t)M * Dh * 4);
+    t.x_stride_f = (int64_t)(rep_f / 4);
+    t.x_stride_b = (int64_t)(rep_b / 2);
+    t.x_stride_s = (int64_t)(rep_s / 4);
+    t.x_stride_r = (int64_t)(rep_r / 4);
+    const size_t G = (size_t)ex->cu_count;
+    // data first, then everything that must start at zero (flags, stamped words, registration, status)
     std::vector<std::pair<void**, size_t>> tp = {
-        {(void**)&t.h0, (size_t)M * d * 4},
-        {(void**)&t.hb0, Mp * d * 2},
-        {(void**)&t.hbmid, (size_t)L * Mp * d * 2},
-        {(void**)&t.hbout, (size_t)L * Mp * d * 2},
-        {(void**)&t.ssq0, dt * Ms * 4},
-        {(void**)&t.hmid, (size_t)L * M * d * 4},
-        {(void**)&t.hout, (size_t)L * M * d * 4},
-        {(void**)&t.ssq_mid, (size_t)L * dt * Ms * 4},
-        {(void**)&t.ssq_out, (size_t)L * dt * Ms * 4},
-        {(void**)&t.attn, (size_t)L * M * A * 2},
-        {(void**)&t.z, (size_t)L * Mp * F * 2},
-        {(void**)&t.f_embed, (dt + (size_t)M) * 8},
-        {(void**)&t.f_qkv, (size_t)3 * A / 16 * 8},
-        {(void**)&t.f_attn, (size_t)nflag_attn * 8},
-        {(void**)&t.f_hmid, dt * 8},
-        {(void**)&t.f_z, (size_t)2 * F / 16 * 8},
-        {(void**)&t.f_hout, dt * 8},
-        {(void**)&t.status, 256},
-        {(void**)&t.att_cnt, (size_t)nflag_attn * 4},
-        {(void**)&t.o_cnt, dt * 4},
-        {(void**)&t.d_cnt, dt * 4},
-        {(void**)&t.sched, (size_t)L * 4}};
+        {(void**)&t.hres, NXMAX * rep_f},
+        {(void**)&t.xb_mid, NXMAX * rep_b},
+        {(void**)&t.xb_out, NXMAX * rep_b},
+        {(void**)&t.ssq_mid, NXMAX * rep_s},
+        {(void**)&t.ssq_out, NXMAX * rep_s},
+        {(void**)&t.rope, NXMAX * rep_r},
+        {(void**)&t.z, Mp * F * 2},
+        {(void**)&t.po, NXMAX * dt * Mp * 16 * 8},
+        {(void**)&t.pd, NXMAX * dt * Mp * 16 * 8},
+        {(void**)&t.reg, G * 8},
+        {(void**)&t.f_rope, (size_t)NXMAX * XFLAGS * FPAD * 8},
+        {(void**)&t.f_out, (size_t)NXMAX * XFLAGS * FPAD * 8},
+        {(void**)&t.f_mid, (size_t)NXMAX * XFLAGS * FPAD * 8},
+        {(void**)&t.f_q, (size_t)3 * A / 16 * FPAD * 8},
+        {(void**)&t.f_attn, (size_t)nflag_attn * FPAD * 8},
+        {(void**)&t.f_rng, (size_t)ex->items_max * FPAD * 8},
+        {(void**)&t.f_z, (size_t)F / 8 * FPAD * 8},
+        {(void**)&t.status, 256}};
     parts.insert(parts.end(), tp.begin(), tp.end());
-    ex->n_att_cnt = nflag_attn;
   }
   size_t total = 0;
   for (auto& p : parts) total += (p.second + 255) & ~(size_t)255;
@@ -288,37 +296,22 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
     q += (p.second + 255) & ~(size_t)255;
   }
   if (ex->tick) {
-    // flags, counters and status start at zero; stamps only grow, counters return to zero
+    // stamped words, flags, registration and status start at zero; stamps only grow
     TickArgs& t = ex->ta;
-    const size_t zbytes = (size_t)((char*)q - (char*)t.f_embed);
-    if (!ok(hipMemsetAsync(t.f_embed, 0, zbytes, s), "hipMemsetAsync(flags)")) return cleanup(FSX_E_HIP);
-    std::vector<TickLayer> tl(c.n_layers);
-    for (int l = 0; l < c.n_layers; ++l)
-      tl[l] = TickLayer{ex->fw[l].wqkv, ex->fw[l].wo, ex->fw[l].wgu, ex->fw[l].wd, ex->fw[l].attn_norm,
-                        ex->fw[l].ffn_norm};
-    if (!ok(hipMalloc((void**)&ex->dlayers, sizeof(TickLayer) * c.n_layers), "hipMalloc(layer table)") ||
-        !ok(hipMemcpyAsync(ex->dlayers, tl.data(), sizeof(TickLayer) * c.n_layers, hipMemcpyHostToDevice, s),
-            "copy layer table"))
-      return cleanup(FSX_E_HIP);
-    t.layers = ex->dlayers;
+    const size_t zbytes = (size_t)((char*)q - (char*)t.po);
+    if (!ok(hipMemsetAsync(t.po, 0, zbytes, s), "hipMemsetAsync(flags)")) return cleanup(FSX_E_HIP);
+    t.wbase = (const char*)ex->wbuf;
     t.final_norm = ex->final_norm;
     t.head_w = ex->head_w;
     t.head_dtype = c.dtype;
     t.q = ex->ws.q;
     t.kself = ex->ws.kself;
     t.vself = ex->ws.vself;
+    t.attn = ex->ws.attn;
     t.att_o = ex->ws.att_o;
     t.att_ml = ex->ws.att_ml;
-    t.part = ex->ws.part;
-    t.rope = ex->ws.rope;
-    t.n_att_cnt = ex->n_att_cnt;
-    t.ks_o = ex->ks_o;
-    t.ks_d = ex->ks_d;
     const uint64_t us = c.tick_timeout_us > 0 ? (uint64_t)c.tick_timeout_us : 2000000ull;
     t.timeout_ticks = us * 100;  // the real-time counter runs at 100 MHz
-    hipDeviceProp_t prop;
-    if (!ok(hipGetDeviceProperties(&prop, ex->device), "hipGetDeviceProperties")) return cleanup(FSX_E_HIP);
-    ex->cu_count = prop.multiProcessorCount;
     if (c.flags & FSX_FLAG_TRACE) {
       const size_t nt = (size_t)ex->cu_count * trace_events(c.n_layers);
       if (!ok(hipMalloc((void**)&ex->trace, nt * 8), "hipMalloc(trace)") ||
@@ -432,12 +425,13 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
     tp.Mp = (tp.M + 7) / 8 * 8;
     tp.Ms = (tp.M + 31) / 32 * 32;
     // Attention units: (agent, range of rows, head).  Rows per unit (one head) aim at about one unit per
-    // workgroup for small work and 2 or 4 for larger work (units are handed out dynamically, so several
-    // per workgroup even out), never below 512 rows; an agent's ranges are equal, multiples of 32 rows.
+    // workgroup for small work, so that every CU streams a share of the cache, and 2 or 4 for larger work;
+    // an agent's ranges are equal, multiples of 32 rows.
     const int64_t total_rh = rows * dm.H;
     const int64_t per_wg = total_rh / G;
     const int k_units = per_wg >= 4096 ? 4 : (per_wg >= 512 ? 2 : 1);
-    int64_t unit_rows = std::max<int64_t>(512, (total_rh + (int64_t)k_units * G - 1) / ((int64_t)k_units * G));
+    int64_t unit_rows = std::max<int64_t>(32, (total_rh + (int64_t)k_units * G - 1) / ((int64_t)k_units * G));
+    unit_rows = (unit_rows + 31) / 32 * 32;
     for (;;) {
       int64_t slots = 0;
       for (int b = 0; b < batch; ++b) slots += std::max<int64_t>(1, (tp.len[b] + unit_rows - 1) / unit_rows);
@@ -462,12 +456,17 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
       tp.unit_prefix[k + 1] = tp.unit_prefix[k] + (tp.range_prefix[b + 1] - tp.range_prefix[b]) * dm.H;
     }
     tp.n_units = tp.unit_prefix[batch];
+    tp.nf_prefix[0] = 0;
+    for (int k = 0; k < batch; ++k) {
+      const int b = ord[k];
+      tp.nf_prefix[k + 1] = tp.nf_prefix[k] + (tp.range_prefix[b + 1] - tp.range_prefix[b]) - 1;
+    }
     TickArgs a = ex->ta;
     a.tok_dtype = c.dtype;
     a.tokens = tokens;
     a.cv = cv;
     a.waypoints = waypoints;
-    if (hidden) a.hout = hidden;
+    a.hidden = hidden;
     a.epoch = ++ex->epoch;
     HIP_TRY(launch_tick(a, tp, dm, ex->cu_count, s));
     g_err.clear();

@@ -20,17 +20,15 @@ constexpr float LOG2E = 1.4426950408889634f;
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
-// round-to-nearest-even float -> bf16 bits (finite inputs; NaN stays NaN)
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
+
+// round-to-nearest-even float -> bf16 bits (NaN stays NaN): one v_cvt_pk_bf16_f32 on gfx950
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 // two floats -> packed bf16x2 (RNE), low half = a
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+  const bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
@@ -137,6 +135,15 @@ __device__ __forceinline__ void vm_wait_all() {
 }
 __device__ __forceinline__ void stores_done() { vm_wait_all(); }
 
+// Stores of data exchanged between workgroups of ONE XCD: plain stores, which stay in the XCD's L2 (the
+// vector L1 is write-through); readers use device-scope loads, which are served by that L2 and never by a
+// stale L1 line.  A producer waits for the stores (stores_done) before it publishes a flag.
+__device__ __forceinline__ void st_loc(uint32_t* p, uint32_t v) { *p = v; }
+__device__ __forceinline__ void st_loc(uint64_t* p, uint64_t v) { *p = v; }
+__device__ __forceinline__ void st_loc_f(float* p, float v) { st_loc(reinterpret_cast<uint32_t*>(p), __float_as_uint(v)); }
+__device__ __forceinline__ void st_loc16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
+__device__ __forceinline__ void st_loc_f4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+
 // Load through a pointer that addresses global memory.  A pointer the compiler cannot prove global (one
 // read from memory, such as a table of weight pointers) would otherwise give a flat load, which also counts
 // in the LDS counter, so every later LDS wait would wait for it too.
@@ -149,10 +156,12 @@ __device__ __forceinline__ uint4 ld_global(const uint4* p) {
 
 // Direct load global -> LDS of 16 bytes per lane: lane l's 16 bytes at src land at lds_base + 16 l
 // (lds_base is wave-uniform).  No registers hold the data; completion is counted by vmcnt.
+// COH: device-scope (sc1) load, for data produced inside the same launch.
+template <bool COH = false>
 __device__ __forceinline__ void load_lds16(const void* src, void* lds_base) {
   typedef __attribute__((address_space(3))) void lds_void_t;
   typedef const __attribute__((address_space(1))) void g_void_t;
-  __builtin_amdgcn_global_load_lds((g_void_t*)src, (lds_void_t*)lds_base, 16, 0, 0);
+  __builtin_amdgcn_global_load_lds((g_void_t*)src, (lds_void_t*)lds_base, 16, 0, COH ? 16 : 0);
 }
 
 // Plain or device-coherent access, chosen at compile time.

@@ -28,6 +28,8 @@ struct TickParams {
   int32_t range_rows[FSX_MAX_BATCH];
   int32_t unit_prefix[FSX_MAX_BATCH + 1];
   int32_t order[FSX_MAX_BATCH];
+  // tick kernel: ranges other than an agent's last, counted over agents in `order`; nf_prefix[B] in total
+  int32_t nf_prefix[FSX_MAX_BATCH + 1];
 };
 
 // Cache view of one layer.
@@ -95,17 +97,16 @@ hipError_t launch_head(const TickParams& tp, const Dims& dm, const Workspace& ws
                        const void* head_w, int head_dtype, float* waypoints, hipStream_t s);
 
 // ------------------------------------------------------------------ persistent tick kernel
-struct TickLayer {
-  const uint4* wqkv;
-  const uint4* wo;
-  const uint4* wgu;
-  const uint4* wd;
-  const float* attn_norm;
-  const float* ffn_norm;
-};
+// The tick kernel splits every layer over the chip's XCDs the way a tensor-parallel layer is split over
+// devices: XCD X owns a contiguous range of heads and of FFN columns.  Buffers marked "per XCD" hold one
+// replica per XCD rank (at most NXMAX); the others are indexed by head or FFN unit, so each of their
+// cache lines is written and read by one XCD only.
+constexpr int NXMAX = 16;
+constexpr int FPAD = 16;     // flags are 64-bit stamps, one per 128-byte line (index * FPAD)
+constexpr int XFLAGS = 512;  // flag slots per XCD of the per-XCD flag arrays
 
 struct TickArgs {
-  const TickLayer* layers;  // device [n_layers]
+  const char* wbase;   // packed weights of layer 0; layers follow back to back (see layer_w)
   const float* final_norm;
   const void* head_w;
   int head_dtype;
@@ -113,42 +114,41 @@ struct TickArgs {
   const void* tokens;
   CacheView cv;
   float* waypoints;
-  // exchanged inside the launch, device-coherent accesses
-  float* q;
-  uint16_t* kself;
-  uint16_t* vself;
-  float* att_o;
-  float* att_ml;
-  uint32_t* att_cnt;
-  int n_att_cnt;
-  float* part;
-  uint32_t* o_cnt;
-  uint32_t* d_cnt;
-  uint32_t* sched;   // [n_layers] attention units taken beyond the first G
-  // written once per launch (per layer); "tile-major" = [column tile][Mp rows][16 columns]
-  float* h0;
-  uint16_t* hb0;     // [d/16][Mp][16] bf16 copy of h0, tile-major
-  uint16_t* hbmid;   // [L][d/16][Mp][16] bf16 copy of hmid, tile-major
-  uint16_t* hbout;   // [L][d/16][Mp][16] bf16 copy of hout, tile-major
-  float* ssq0;     // [d/16][Ms] per-tile sums of squares of h0
-  float* rope;     // [M][Dh/2][2] cos, sin
-  float* hmid;     // [L][M][d]
-  float* hout;     // [L][M][d] (the caller's hidden buffer when given)
-  float* ssq_mid;  // [L][d/16][Ms]
-  float* ssq_out;  // [L][d/16][Ms]
-  uint16_t* attn;  // [L][M][A]
-  uint16_t* z;     // [L][F/8][Mp][8] SwiGLU output, tile-major
-  // flags (stamps) and status
-  uint64_t* f_embed;
-  uint64_t* f_qkv;
-  uint64_t* f_attn;
-  uint64_t* f_hmid;
-  uint64_t* f_z;
-  uint64_t* f_hout;
+  float* hidden;       // optional caller buffer [n_layers][M][d]
+  uint64_t* reg;       // [grid] registration words: epoch << 8 | hardware XCD id
+  // per XCD, tile-major = [d/16 column tiles][Mp rows][16 columns]
+  float* hres;         // residual stream, each tile touched only by its owner workgroup
+  uint16_t* xb_mid;    // bf16 copy of the residual after attention (input of the FFN)
+  uint16_t* xb_out;    // bf16 copy of the residual after the FFN (input of the next layer)
+  float* ssq_mid;      // [d/16][Ms] per-tile sums of squares
+  float* ssq_out;
+  float* rope;         // [M][Dh/2][2] cos, sin
+  int64_t x_stride_f;  // floats between replicas of hres
+  int64_t x_stride_b;  // bf16 elements between replicas of xb_mid / xb_out
+  int64_t x_stride_s;  // floats between replicas of ssq_mid / ssq_out
+  int64_t x_stride_r;  // floats between replicas of rope
+  // by head / FFN unit
+  float* q;            // [M][A] rotated, pre-scaled queries
+  uint16_t* kself;     // [M][A]
+  uint16_t* vself;     // [M][A]
+  uint16_t* attn;      // [M][A]
+  uint16_t* z;         // [F/8][Mp][8] SwiGLU output
+  float* att_o;        // [items][16][Dh] range partials
+  float* att_ml;       // [items][16][2]
+  // crossing XCDs: stamped 8-byte words (payload in the low half, stamp in the high half)
+  uint64_t* po;        // [NXMAX][d/16][Mp][16] output-projection partials
+  uint64_t* pd;        // [NXMAX][d/16][Mp][16] down-projection partials
+  // flags (stamps), each in its own 128-byte line: element [i] lives at f[i * FPAD]
+  uint64_t* f_rope;    // [NXMAX][XFLAGS] by workgroup slot
+  uint64_t* f_out;     // [NXMAX][XFLAGS] by column tile
+  uint64_t* f_mid;     // [NXMAX][XFLAGS] by column tile
+  uint64_t* f_q;       // [3A/16]
+  uint64_t* f_attn;    // [B*H]
+  uint64_t* f_rng;     // [range pairs]
+  uint64_t* f_z;       // [F/8]
   uint64_t* status;
   uint64_t epoch;
   uint64_t timeout_ticks;  // real-time counter ticks (100 MHz)
-  int ks_o, ks_d;
   uint64_t* trace;         // optional: [grid][trace_events(n_layers)] real-time stamps per workgroup
 };
 
@@ -157,6 +157,8 @@ __host__ __device__ inline int trace_events(int n_layers) { return 2 + 16 * n_la
 
 hipError_t tick_occupancy(int kt, int* blocks_per_cu);
 hipError_t launch_tick(const TickArgs& a, const TickParams& tp, const Dims& dm, int grid, hipStream_t s);
+// Hardware XCD id of every workgroup of a one-workgroup-per-CU launch (create-time placement check).
+hipError_t probe_xcds(uint32_t* dev_out, int grid, hipStream_t s);
 
 // ------------------------------------------------------------------ cache append
 hipError_t launch_append(const fsx_cache_desc& c, const void* k_rows, const void* v_rows, int n_rows,

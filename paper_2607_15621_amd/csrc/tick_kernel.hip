@@ -1,32 +1,35 @@
-// The whole expert tick (Sec. 3.1, Eq. (1)) as ONE persistent cooperative launch.
+// The whole expert tick (Sec. 3.1, Eq. (1)) as ONE persistent cooperative launch, with every layer split
+// over the chip's XCDs the way a tensor-parallel transformer layer is split over devices.
 //
-// Every workgroup (one per CU) walks the same phase sequence; within a layer
-//   Q  : RMSNorm + q/k/v projection (+ rotary, q pre-scale) per 16-column tile
-//   A  : joint attention per (agent, range of cached rows, head): the 4 waves split the 32-row tiles and
-//        merge in LDS; each wave keeps a ring of raw tiles in flight; the expert's own rows are tiles of
-//        the agent's last range; when an agent's rows were split over several ranges, the last range to
-//        finish merges them (log-sum-exp).  Units after the first are taken from a per-layer counter.
-//   O  : output projection, split-K by head group; the last split of each column tile adds the
-//        residual and writes h_mid plus per-tile sums of squares for the next RMSNorm
-//   F1 : RMSNorm + gate/up projection with SwiGLU
-//   D  : down projection, split-K; the last split adds the residual and writes h_out
-// and the head pools the first T tokens at the end.  Phases are connected by per-producer flags, not
-// grid barriers: a producer writes its outputs with device-coherent stores, waits for them to
-// complete, and stores a flag holding a stamp that grows with (launch, layer); a consumer polls only
-// the flags of the tiles it reads.
+// MI355X has 8 XCDs of 32 CUs; each XCD has its own L2.  A hand-off between two workgroups of one XCD
+// goes through that L2 (a flag written with a plain store and polled with a device-scope load is seen
+// after ~0.3 us); a hand-off between XCDs has to go through memory (~0.55 us one way).  So XCD X owns a
+// contiguous range of heads and a contiguous range of FFN columns, and a layer runs as
+//   Q  : RMSNorm + q/k/v projection (+ rotary, q pre-scale) of X's heads, per 16-column tile
+//   A  : joint attention of X's heads (agent, range of cached rows, head); an agent's last range merges the
+//        others (log-sum-exp)
+//   O  : output projection restricted to X's heads: a partial sum over X's attention columns for each
+//        16-column tile of the residual
+//   R1 : reduction across XCDs: the owner of column tile i in EVERY XCD reads the 8 partials of tile i
+//        (stamped words, polled directly), adds them in a fixed order to its copy of the residual and
+//        publishes the bf16 tile and its sums of squares inside its XCD
+//   F1 : RMSNorm + gate/up projection with SwiGLU for X's FFN columns
+//   D  : down projection restricted to X's FFN columns (partials)
+//   R2 : reduction across XCDs as R1, giving the layer output
+// All exchanges except R1 and R2 stay inside an XCD.  Every XCD keeps a bit-identical replica of the
+// residual stream (same values, same summation order).  The head pools the first T tokens at the end.
 //
-// Coherence.  Each XCD has its own L2, and a cache line written in parts by workgroups on different
-// XCDs can sit in a reader's L2 with parts missing.  Buffers that many workgroups read (the bf16
-// projection inputs, their sums of squares, the SwiGLU output, the attention output) are therefore laid
-// out so that every 128-byte line has exactly one producer (tile-major: [column tile][row][16 or 8
-// columns], rows padded), are written once per launch, and are read with ordinary loads after the
-// producer's flag, so they are served from L2 after the first reader of an XCD.  Everything else
-// produced inside the launch (queries, the expert's own keys/values, split-K partials, the residual
-// stream, attention partial states) is read with device-coherent loads.  Weights and cache rows are
-// read-only.  Every wait is bounded in real time; on timeout the launch records a failure and the head
-// writes NaN waypoints.
+// Placement.  Each workgroup reads its hardware XCD id at the start of the tick and publishes it; from the
+// published ids every workgroup derives its XCD rank X, its slot s among that XCD's n workgroups, and the
+// number NX of XCDs, so the split is right whatever the hardware placement is.
+//
+// Coherence.  Inside an XCD: plain stores, a wait for them (stores_done), then a flag; readers poll flags
+// and read data with device-scope loads, which are served by the XCD's L2 and never by a stale L1 line.
+// Across XCDs: 8-byte words holding a 32-bit payload and a 32-bit stamp, written with device-scope stores
+// and read with device-scope loads; a word is valid when its stamp is the expected one, so no flag is
+// needed.  Weights and cache rows are read-only and use ordinary loads.  Every wait is bounded in real time;
+// on timeout the launch records a failure and the head writes NaN waypoints.
 
-#include "attn_device.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -43,11 +46,13 @@ __device__ __forceinline__ int tix() {
 
 constexpr int XSTR = 520;  // LDS row stride (bf16 elements) of staged activations: 512 + 8 padding
 constexpr int NTHR = 256;
-constexpr int UMAX = 4;    // projection units whose weights a wave holds in registers at once
 constexpr int MTMAX = 5;   // 16-row tiles per staged chunk (80 rows)
 constexpr int DH = 128;    // head width of the fused path
 constexpr int STW = 16 * DH + 32;  // LDS floats of one wave's attention state: O[16][128], (m, l)[16]
 constexpr int NQW = 3;     // query tiles a wave carries at once in the many-query attention variant
+
+// A value read from LDS that is the same in every lane, moved to a scalar register.
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 struct TickLds {
   union {
@@ -66,8 +71,7 @@ struct TickLds {
   float red2[16][16];   // head: per-wave partial sums
   float hr[64];         // head: row scales of the pooled tokens (at most 64)
   int ok;
-  int last;
-  int next;
+  int X, s, n, NX, n0;  // XCD rank, slot in the XCD, workgroups of the XCD, XCDs, workgroups of XCD 0
 };
 
 __device__ __forceinline__ uint64_t stamp_of(const TickArgs& a, int layer, int n_layers) {
@@ -75,9 +79,17 @@ __device__ __forceinline__ uint64_t stamp_of(const TickArgs& a, int layer, int n
 }
 __device__ __forceinline__ uint64_t fail_tag(const TickArgs& a) { return a.epoch + 1; }
 
-// Wave-level wait until flags[(i / inner) * stride + i % inner] >= target for i < n.  Up to 256 flags are
-// polled per round trip.  False on timeout or when another workgroup has already recorded a failure for
-// this launch.
+// Checked inside wait loops every few spins: the elapsed real time every 4 spins, the launch's failure word (a
+// device-scope vector load) every 64.
+__device__ __forceinline__ bool timed_out(const TickArgs& a, uint64_t t0, uint32_t spin) {
+  if ((spin & 3) != 3) return false;
+  if (__builtin_amdgcn_s_memrealtime() - t0 > a.timeout_ticks) return true;
+  return (spin & 63) == 63 && ld_dev(a.status) == fail_tag(a);
+}
+
+// Wave-level wait until flags[((i / inner) * stride + i % inner) * FPAD] >= target for i < n, with device-scope
+// vector loads (served by the XCD's L2 for flags written inside the XCD); up to 256 flags per round trip.  False
+// on timeout or when another workgroup has already recorded a failure for this launch.
 __device__ __forceinline__ bool wave_wait(const uint64_t* flags, int n, uint64_t target, const TickArgs& a,
                                           int inner = 1 << 30, int stride = 0) {
   constexpr int GR = 4;  // groups of 64 flags per round trip
@@ -88,7 +100,7 @@ __device__ __forceinline__ bool wave_wait(const uint64_t* flags, int n, uint64_t
 #pragma unroll
     for (int g = 0; g < GR; ++g) {
       const int i = base + g * WAVE + lane;
-      fi[g] = i < n ? (int64_t)(i / inner) * stride + i % inner : -1;
+      fi[g] = i < n ? ((int64_t)(i / inner) * stride + i % inner) * FPAD : -1;
     }
     for (uint32_t spin = 0;; ++spin) {
       uint64_t v[GR];
@@ -98,22 +110,17 @@ __device__ __forceinline__ bool wave_wait(const uint64_t* flags, int n, uint64_t
 #pragma unroll
       for (int g = 0; g < GR; ++g) ok = ok && v[g] >= target;
       if (__all(ok)) break;
-      // back off after the first polls: many workgroups poll the same flag lines
-      if (spin < 8)
-        __builtin_amdgcn_s_sleep(1);
-      else
-        __builtin_amdgcn_s_sleep(6);
-      if ((spin & 31) == 31) {
-        if (__builtin_amdgcn_s_memrealtime() - t0 > a.timeout_ticks || ld_dev(a.status) == fail_tag(a)) {
-          if (lane == 0) st_dev(a.status, fail_tag(a));
-          return false;
-        }
+      __builtin_amdgcn_s_sleep(1);
+      if (timed_out(a, t0, spin)) {
+        if (lane == 0) st_dev(a.status, fail_tag(a));
+        return false;
       }
     }
   }
   return true;
 }
 
+// Workgroup-level wait: wave 0 polls, the others wait at a barrier.
 __device__ __forceinline__ bool wg_wait(const uint64_t* flags, int n, uint64_t target, const TickArgs& a, TickLds& L,
                                         int inner = 1 << 30, int stride = 0) {
   if (tix() < WAVE) {
@@ -134,14 +141,124 @@ __device__ __forceinline__ void trace_mark(const TickArgs& a, int ev, int n_laye
 // sub-phase mark k (0..10) of layer l
 #define TICK_SUB(l, k) trace_mark(a, 2 + 16 * (l) + 5 + (k), dm.n_layers)
 
+// ------------------------------------------------------------------------------------------ weights
+// Packed weights of layer l: [W_q; W_k; W_v] (3A x d), W_o (d x A), [W_gate; W_up] (2F x d), W_down (d x F), stored
+// back to back for every layer, so their addresses follow from the layer index without a memory access.
+struct LayerW {
+  const uint4* wqkv;
+  const uint4* wo;
+  const uint4* wgu;
+  const uint4* wd;
+};
+__device__ __forceinline__ LayerW layer_w(const TickArgs& a, const Dims& dm, int l) {
+  const int64_t ad = (int64_t)dm.A * dm.d * 2, fd = (int64_t)dm.F * dm.d * 2;  // bytes of one A x d / F x d matrix
+  const char* base = a.wbase + (int64_t)l * (4 * ad + 3 * fd);
+  LayerW w;
+  w.wqkv = reinterpret_cast<const uint4*>(base);
+  w.wo = reinterpret_cast<const uint4*>(base + 3 * ad);
+  w.wgu = reinterpret_cast<const uint4*>(base + 4 * ad);
+  w.wd = reinterpret_cast<const uint4*>(base + 4 * ad + 2 * fd);
+  return w;
+}
+
+// ------------------------------------------------------------------------------------------ work split
+// Heads [h0, h1) and FFN columns [f0, f1) (multiples of 32) of XCD rank X.
+__device__ __forceinline__ int head_lo(int X, int NX, int H) { return X * H / NX; }
+__device__ __forceinline__ int ffn_lo(int X, int NX, int F) { return 32 * (X * (F / 32) / NX); }
+
+// ------------------------------------------------------------------------------------------ registration
+__device__ __forceinline__ uint32_t hw_xcc_id() {
+  uint32_t v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return v & 15u;
+}
+
+// Every workgroup publishes (epoch, hardware XCD id); wave 0 of each then reads all G words and derives
+// the XCD rank X (rank of its id among the ids present), its slot s (workgroups of the same id with a
+// smaller index), n (workgroups of its XCD), NX and n0 (workgroups of rank 0).  G <= 512.
+__device__ __forceinline__ bool xcd_register(const TickArgs& a, TickLds& L) {
+  constexpr int EPL = 8;
+  const int G = gridDim.x;
+  if (tix() == 0) st_dev(a.reg + blockIdx.x, (a.epoch << 8) | (uint64_t)hw_xcc_id());
+  if (tix() < WAVE) {
+    const int lane = tix();
+    uint32_t xc[EPL];
+    bool have[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      have[e] = e * WAVE + lane >= G;
+      xc[e] = 0xffu;
+    }
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    bool ok = true;
+    for (uint32_t spin = 0;; ++spin) {
+      bool all = true;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        if (!have[e]) {
+          const uint64_t v = ld_dev(a.reg + e * WAVE + lane);
+          if ((v >> 8) == a.epoch) {
+            have[e] = true;
+            xc[e] = (uint32_t)(v & 0xffu);
+          } else {
+            all = false;
+          }
+        }
+      }
+      if (__all(all)) break;
+      __builtin_amdgcn_s_sleep(1);
+      if (timed_out(a, t0, spin)) {
+        if (lane == 0) st_dev(a.status, fail_tag(a));
+        ok = false;
+        break;
+      }
+    }
+    if (ok) {
+      const int w = blockIdx.x;
+      uint32_t sel = 0;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e)
+        if (e == w / WAVE) sel = xc[e];
+      const uint32_t mine = (uint32_t)__shfl((int)sel, w % WAVE, WAVE);
+      int X = 0, NX = 0, n = 0, s = 0, n0 = 0;
+      for (uint32_t x = 0; x < 16; ++x) {
+        int cnt = 0;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) cnt += __popcll(__ballot(xc[e] == x));
+        if (cnt > 0) {
+          if (NX == 0) n0 = cnt;
+          if (x < mine) ++X;
+          ++NX;
+        }
+        if (x == mine) n = cnt;
+      }
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) s += __popcll(__ballot(xc[e] == mine && e * WAVE + lane < w));
+      if (lane == 0) {
+        L.X = X;
+        L.s = s;
+        L.n = n;
+        L.NX = NX;
+        L.n0 = n0;
+        if (NX > NXMAX) ok = false;
+      }
+    }
+    if (lane == 0) L.ok = ok;
+  }
+  __syncthreads();
+  const bool ok = L.ok;
+  __syncthreads();
+  return ok;
+}
+
 // ------------------------------------------------------------------------------------------ staging
-// Stage rows [m0, m0+rows) x K columns (K/8 <= 64 chunks of 16 bytes) of a bf16 activation into L.x with
-// direct global->LDS loads (one instruction per row: lane l brings columns 8l..8l+7), the rotary rows into
-// L.rope when given, and, when ssq is given, the RMSNorm row scales r[row] = 1/sqrt(mean(h^2) + eps) from the
-// per-16-column sums of squares ssq[tile][Ms] into L.r.  TW = 0: row-major source [M][ld]; TW = 16 or 8:
-// tile-major source [K/TW][ld = Mp][TW].  Every load is issued before any is waited for; ends with a
-// barrier.  Rows past `rows` are left as they are: an MFMA output row depends only on its input row, and
-// those rows are never stored.
+// Stage rows [m0, m0+rows) x K columns (K/8 <= 64 chunks of 16 bytes) of a bf16 activation produced in this
+// launch into L.x with direct global->LDS loads (device scope; one instruction per row: lane l brings
+// columns 8l..8l+7), the rotary rows into L.rope when given, and, when ssq is given, the RMSNorm row scales
+// r[row] = 1/sqrt(mean(h^2) + eps) from the per-16-column sums of squares ssq[tile][Ms] into L.r.  TW = 0:
+// row-major source [M][ld]; TW = 16 or 8: tile-major source [K/TW][ld = Mp][TW].  Every load is issued
+// before any is waited for; ends with a barrier.  Rows past `rows` are left as they are: an MFMA output row
+// depends only on its input row, and those rows are never stored.
 template <int TW>
 __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int rows, int K, const float* ssq, int Ms,
                                       int Kn, float eps, TickLds& L, const float* rope = nullptr) {
@@ -156,11 +273,11 @@ __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int r
     else
       off = ((int64_t)lane * ld + m0) * 8;
     const int64_t row_step = TW == 0 ? ld : TW;  // elements between consecutive rows
-    for (int m = wave; m < rows; m += 4) load_lds16(src + off + (int64_t)m * row_step, &L.u.p.x[m][0]);
+    for (int m = wave; m < rows; m += 4) load_lds16<true>(src + off + (int64_t)m * row_step, &L.u.p.x[m][0]);
   }
   if (rope) {  // rows [M][DH/2][2] floats, 512 bytes: one instruction per 2 rows
     for (int m = 2 * wave; m < rows; m += 8)
-      if (m + (lane >> 5) < rows) load_lds16(rope + ((int64_t)(m0 + m) * DH + lane * 4), &L.rope[m][0][0]);
+      if (m + (lane >> 5) < rows) load_lds16<true>(rope + ((int64_t)(m0 + m) * DH + lane * 4), &L.rope[m][0][0]);
   }
   float part[MTMAX];
   const int g = tid & 15, rw = tid >> 4, ntn = Kn / 16;  // ntn <= 32
@@ -170,8 +287,8 @@ __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int r
       const int i = rw + 16 * p;
       float s0 = 0.f, s1 = 0.f;
       if (i < rows) {
-        if (g < ntn) s0 = ssq[(int64_t)g * Ms + m0 + i];
-        if (g + 16 < ntn) s1 = ssq[(int64_t)(g + 16) * Ms + m0 + i];
+        if (g < ntn) s0 = ld_dev_f(ssq + (int64_t)g * Ms + m0 + i);
+        if (g + 16 < ntn) s1 = ld_dev_f(ssq + (int64_t)(g + 16) * Ms + m0 + i);
       }
       part[p] = s0 + s1;
     }
@@ -191,9 +308,8 @@ __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int r
 }
 
 // ------------------------------------------------------------------------------------------ projections
-// A projection unit is one 16-column tile over a range of nkb k-blocks; wave w owns the unit's k-blocks
-// i = w, w+4, w+8, w+12 (a range is at most 512 columns = 16 blocks), whose 1 KiB weight blocks it holds
-// in registers.
+// A projection unit is one 16-column tile over a range of nkb <= 16 k-blocks; wave w owns the unit's
+// k-blocks i = w, w+4, w+8, w+12, whose 1 KiB weight blocks it holds in registers.
 __device__ __forceinline__ void load_unit_w(const uint4* __restrict__ wtile, int kb0, int nkb, uint4 w[4]) {
   const int wave = tix() >> 6, lane = tix() & 63;
 #pragma unroll
@@ -203,225 +319,294 @@ __device__ __forceinline__ void load_unit_w(const uint4* __restrict__ wtile, int
   }
 }
 
-// acc = staged x (mt_n row tiles, k-blocks 0..nkb-1 of the unit's range) times the unit's weights, summed
-// over the 4 waves through LDS and handed to epi(mt, C-layout values, c, grp) by wave mt % 4.
-template <typename Epi>
-__device__ __forceinline__ void unit_gemm(const uint4 w[4], int nkb, int mt_n, TickLds& L, Epi epi) {
+// acc = staged x (MT row tiles, k-blocks 0..nkb-1 of the unit's range) times the unit's weights, summed over
+// the 4 waves through LDS and handed to epi(mt, C-layout values, c, grp) by wave mt % 4.  Every LDS operand is
+// read before the first MFMA, so the reads overlap instead of each MFMA waiting for its own.
+template <int MT, typename Epi>
+__device__ __forceinline__ void unit_gemm_t(const uint4 w[4], int nkb, TickLds& L, Epi epi) {
   const int wave = tix() >> 6, lane = tix() & 63;
   const int c = lane & 15, grp = lane >> 4;
-  // every row tile of the chunk buffer is multiplied (straight-line code); tiles past mt_n are not used
-  f32x4 acc[MTMAX];
+  uint4 xa[4][MT];
 #pragma unroll
-  for (int mt = 0; mt < MTMAX; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < 4; ++j)
+    if (wave + 4 * j < nkb)
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int i = wave + 4 * j;
-    if (i < nkb) {
-      uint4 xa[MTMAX];
+      for (int mt = 0; mt < MT; ++mt)
+        xa[j][mt] = *reinterpret_cast<const uint4*>(&L.u.p.x[mt * 16 + c][(wave + 4 * j) * 32 + 8 * grp]);
+  f32x4 acc[MT];
 #pragma unroll
-      for (int mt = 0; mt < MTMAX; ++mt) xa[mt] = *reinterpret_cast<const uint4*>(&L.u.p.x[mt * 16 + c][i * 32 + 8 * grp]);
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int mt = 0; mt < MTMAX; ++mt) acc[mt] = mfma_bf16(xa[mt], w[j], acc[mt]);
-    }
-  }
+  for (int j = 0; j < 4; ++j)
+    if (wave + 4 * j < nkb)
 #pragma unroll
-  for (int mt = 0; mt < MTMAX; ++mt) L.u.p.red[wave][mt][lane] = acc[mt];
+      for (int mt = 0; mt < MT; ++mt) acc[mt] = mfma_bf16(xa[j][mt], w[j], acc[mt]);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) L.u.p.red[wave][mt][lane] = acc[mt];
   __syncthreads();
-  for (int mt = wave; mt < mt_n; mt += 4) {
+  for (int mt = wave; mt < MT; mt += 4) {
     const f32x4 s = L.u.p.red[0][mt][lane] + L.u.p.red[1][mt][lane] + L.u.p.red[2][mt][lane] + L.u.p.red[3][mt][lane];
     epi(mt, s, c, grp);
   }
   __syncthreads();
 }
 
-// Last split of a column tile: h_dst[m][tile] = h_src[m][tile] + sum_s part[s][m][tile] (fixed order); the
-// tile also goes to hb_dst (bf16, tile-major [tile][Mp][16]) and ssq_dst[tile][m] = sum over the tile of
-// h_dst^2.  Resets the tile's counter and publishes its flag.
-__device__ __forceinline__ void reduce_tile(const TickArgs& a, const TickParams& tp, const Dims& dm, int nt, int nsplit,
-                                            const float* h_src, float* h_dst, uint16_t* hb_dst, float* ssq_dst,
-                                            uint32_t* cnt, uint64_t* flag, uint64_t st) {
-  const int M = tp.M, d = dm.d, total = M * 16;
-  constexpr int BATCH = 2;
-  for (int i0 = tix(); i0 < total; i0 += BATCH * NTHR) {
-    float p[BATCH][8], hv[BATCH];
-#pragma unroll
-    for (int k = 0; k < BATCH; ++k) {
-      const int idx = i0 + k * NTHR;
-      const int m = idx >> 4, n = nt * 16 + (idx & 15);
-      const bool in = idx < total;
-      hv[k] = in ? ld_dev_f(h_src + (int64_t)m * d + n) : 0.f;
-#pragma unroll
-      for (int s = 0; s < 8; ++s) p[k][s] = in && s < nsplit ? ld_dev_f(a.part + ((int64_t)s * M + m) * d + n) : 0.f;
-    }
-#pragma unroll
-    for (int k = 0; k < BATCH; ++k) {
-      const int idx = i0 + k * NTHR;
-      const int m = idx >> 4, c = idx & 15, n = nt * 16 + c;
-      float acc = 0.f;
-#pragma unroll
-      for (int s = 0; s < 8; ++s) acc += p[k][s];
-      const float v = hv[k] + acc;
-      if (idx < total) st_dev_f(h_dst + (int64_t)m * d + n, v);
-      const float vn = shfl_xor(v, 1);
-      if (idx < total && (c & 1) == 0)
-        st_dev(reinterpret_cast<uint32_t*>(hb_dst + ((int64_t)nt * tp.Mp + m) * 16 + c), pack_bf16x2(v, vn));
-      float sq = v * v;
-      sq += shfl_xor(sq, 8);
-      sq += shfl_xor(sq, 4);
-      sq += shfl_xor(sq, 2);
-      sq += shfl_xor(sq, 1);
-      if (c == 0 && idx < total) st_dev_f(ssq_dst + (int64_t)nt * tp.Ms + m, sq);
-    }
-  }
-  if (tix() == 0) st_dev(cnt + nt, 0u);
-  stores_done();
-  __syncthreads();
-  if (tix() == 0) st_dev(flag + nt, st);
-}
-
-// ------------------------------------------------------------------------------------------ embed
-// Units 0 .. d/16-1: column tile u of every row (h0, its bf16 tile and sums of squares); units d/16 .. d/16+M-1:
-// the rotary table of row m = u - d/16 (fp64 angle).  The units also return every counter to zero.
-__device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams& tp, const Dims& dm, TickLds& L) {
-  const int G = gridDim.x, d = dm.d, M = tp.M, half = dm.Dh / 2, nt = d / 16;
-  const uint64_t st = stamp_of(a, -1, dm.n_layers);
-  const int n_units = nt + M;
-  for (int u = blockIdx.x; u < n_units; u += G) {
-    if (u < nt) {
-      // thread: row m = i / 8, column pair 2 * (i % 8)
-      for (int i = tix(); i < M * 8; i += NTHR) {
-        const int m = i >> 3, cp = (i & 7) * 2, n = u * 16 + cp;
-        const int64_t idx = (int64_t)m * d + n;
-        float v0, v1;
-        if (a.tok_dtype == FSX_BF16) {
-          const uint32_t pr = *reinterpret_cast<const uint32_t*>((const uint16_t*)a.tokens + idx);
-          v0 = bf16_to_f32((uint16_t)(pr & 0xffffu));
-          v1 = bf16_to_f32((uint16_t)(pr >> 16));
-        } else {
-          v0 = ((const float*)a.tokens)[idx];
-          v1 = ((const float*)a.tokens)[idx + 1];
-        }
-        st_dev(reinterpret_cast<uint64_t*>(a.h0 + idx), (uint64_t)__float_as_uint(v0) | ((uint64_t)__float_as_uint(v1) << 32));
-        st_dev(reinterpret_cast<uint32_t*>(a.hb0 + ((int64_t)u * tp.Mp + m) * 16 + cp), pack_bf16x2(v0, v1));
-        float sq = v0 * v0 + v1 * v1;  // the 8 threads of a row are adjacent lanes
-        sq += shfl_xor(sq, 4);
-        sq += shfl_xor(sq, 2);
-        sq += shfl_xor(sq, 1);
-        if ((i & 7) == 0) st_dev_f(a.ssq0 + (int64_t)u * tp.Ms + m, sq);
-      }
-    } else {
-      const int m = u - nt, b = m / tp.S, t = m % tp.S;
-      for (int j = tix(); j < half; j += NTHR) {
-        double cs = 1.0, sn = 0.0;
-        if (dm.rope_base > 0.f) {
-          const double ang = (double)(tp.pos[b] + t) * pow((double)dm.rope_base, -2.0 * (double)j / (double)dm.Dh);
-          cs = cos(ang);
-          sn = sin(ang);
-        }
-        st_dev_f(a.rope + ((int64_t)m * half + j) * 2, (float)cs);
-        st_dev_f(a.rope + ((int64_t)m * half + j) * 2 + 1, (float)sn);
-      }
-    }
-    // return the counters to zero (robust to an earlier launch that stopped midway)
-    for (int i = u * NTHR + tix(); i < a.n_att_cnt; i += n_units * NTHR) st_dev(a.att_cnt + i, 0u);
-    for (int i = u * NTHR + tix(); i < dm.n_layers; i += n_units * NTHR) st_dev(a.sched + i, 0u);
-    if (u == 0)
-      for (int i = tix(); i < nt; i += NTHR) {
-        st_dev(a.o_cnt + i, 0u);
-        st_dev(a.d_cnt + i, 0u);
-      }
-    stores_done();
-    __syncthreads();
-    if (tix() == 0) st_dev(a.f_embed + u, st);
+template <typename Epi>
+__device__ __forceinline__ void unit_gemm(const uint4 w[4], int nkb, int mt_n, TickLds& L, Epi epi) {
+  switch (mt_n) {
+    case 1: unit_gemm_t<1>(w, nkb, L, epi); break;
+    case 2: unit_gemm_t<2>(w, nkb, L, epi); break;
+    case 3: unit_gemm_t<3>(w, nkb, L, epi); break;
+    case 4: unit_gemm_t<4>(w, nkb, L, epi); break;
+    default: unit_gemm_t<5>(w, nkb, L, epi); break;
   }
 }
 
-// ------------------------------------------------------------------------------------------ Q
 // One wave per projection unit: the wave holds the unit's 16-column tile for every k-block (K <= 512) in
-// registers and multiplies all staged row tiles, so the units of a workgroup run side by side with no
-// cross-wave reduction.
+// registers and multiplies all staged row tiles.
 __device__ __forceinline__ void load_unit_w_full(const uint4* __restrict__ wtile, int nkb, uint4 w[16]) {
   const int lane = tix() & 63;
 #pragma unroll
   for (int i = 0; i < 16; ++i) w[i] = i < nkb ? ld_global(wtile + (int64_t)i * WAVE + lane) : make_uint4(0, 0, 0, 0);
 }
 
-template <typename Epi>
-__device__ __forceinline__ void wave_gemm(const uint4 w[16], int nkb, int mt_n, TickLds& L, Epi epi) {
+// Per row tile: the 16 LDS operands are read first, then the MFMAs run on two accumulators (even and odd
+// k-blocks) so that consecutive MFMAs do not depend on each other.
+template <int MT, typename Epi>
+__device__ __forceinline__ void wave_gemm_t(const uint4 w[16], int nkb, TickLds& L, Epi epi) {
   const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
 #pragma unroll
-  for (int mt = 0; mt < MTMAX; ++mt) {
-    if (mt < mt_n) {
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int mt = 0; mt < MT; ++mt) {
+    uint4 xa[16];
 #pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if (i < nkb) acc = mfma_bf16(*reinterpret_cast<const uint4*>(&L.u.p.x[mt * 16 + c][i * 32 + 8 * grp]), w[i], acc);
-      epi(mt, acc, c, grp);
+    for (int i = 0; i < 16; ++i)
+      if (i < nkb) xa[i] = *reinterpret_cast<const uint4*>(&L.u.p.x[mt * 16 + c][i * 32 + 8 * grp]);
+    f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
+#pragma unroll
+    for (int i = 0; i < 16; i += 2) {
+      if (i < nkb) acc0 = mfma_bf16(xa[i], w[i], acc0);
+      if (i + 1 < nkb) acc1 = mfma_bf16(xa[i + 1], w[i + 1], acc1);
     }
+    epi(mt, acc0 + acc1, c, grp);
   }
 }
 
+template <typename Epi>
+__device__ __forceinline__ void wave_gemm(const uint4 w[16], int nkb, int mt_n, TickLds& L, Epi epi) {
+  switch (mt_n) {
+    case 1: wave_gemm_t<1>(w, nkb, L, epi); break;
+    case 2: wave_gemm_t<2>(w, nkb, L, epi); break;
+    case 3: wave_gemm_t<3>(w, nkb, L, epi); break;
+    case 4: wave_gemm_t<4>(w, nkb, L, epi); break;
+    default: wave_gemm_t<5>(w, nkb, L, epi); break;
+  }
+}
+
+// ------------------------------------------------------------------------------------------ reductions
+// Column tile i of the residual, in the owner workgroup of XCD X: h[m][i] += sum over XCDs x (fixed order)
+// of part[x][i][m][:], where part holds stamped words.  Thread t owns the elements e = t + 256 k (e = m*16 + c,
+// k < EB); all of its words are loaded before any is checked, then it polls its own stale words until their
+// stamps are right.  The new tile goes to hres (owner-private), to the bf16 tile-major copy xb and the per-row
+// sums of squares ssq (read by the whole XCD), and, if given, to hidden; then the tile's flag is published.
+constexpr int EB = 2;  // element batches per pass: M <= 32 rows in one pass
+__device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, int i,
+                                            const uint64_t* part, uint16_t* xb, float* ssq, uint64_t* flag,
+                                            float* hidden_l, TickLds& L) {
+  const int M = tp.M, X = uni(L.X), NX = uni(L.NX), nt = dm.d / 16;
+  const uint64_t st = stamp_of(a, l, dm.n_layers);
+  const uint32_t st32 = (uint32_t)st;
+  float* hres = a.hres + (int64_t)X * a.x_stride_f + (int64_t)i * tp.Mp * 16;
+  const int64_t xs = (int64_t)nt * tp.Mp * 16;  // words between the partials of two XCDs
+  bool ok = true;
+  for (int e0 = 0; e0 < M * 16 && ok; e0 += EB * NTHR) {
+    uint64_t v[EB][NXMAX];
+    float hold[EB];
+#pragma unroll
+    for (int k = 0; k < EB; ++k) {
+      const int e = e0 + k * NTHR + tix();
+      const bool in = e < M * 16;
+      const uint64_t* src = part + (int64_t)i * tp.Mp * 16 + e;
+#pragma unroll
+      for (int x = 0; x < NXMAX; ++x) v[k][x] = (x < NX && in) ? ld_dev(src + x * xs) : ((uint64_t)st32 << 32);
+      hold[k] = in ? hres[e] : 0.f;
+    }
+    uint32_t pending = 0;
+#pragma unroll
+    for (int k = 0; k < EB; ++k)
+#pragma unroll
+      for (int x = 0; x < NXMAX; ++x)
+        if ((uint32_t)(v[k][x] >> 32) != st32) pending |= 1u << (k * NXMAX + x);
+    if (pending) {
+      const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+      for (uint32_t spin = 0; pending; ++spin) {
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int k = 0; k < EB; ++k) {
+          const uint64_t* src = part + (int64_t)i * tp.Mp * 16 + e0 + k * NTHR + tix();
+#pragma unroll
+          for (int x = 0; x < NXMAX; ++x)
+            if (pending & (1u << (k * NXMAX + x))) v[k][x] = ld_dev(src + x * xs);
+        }
+#pragma unroll
+        for (int k = 0; k < EB; ++k)
+#pragma unroll
+          for (int x = 0; x < NXMAX; ++x)
+            if ((uint32_t)(v[k][x] >> 32) == st32) pending &= ~(1u << (k * NXMAX + x));
+        if (pending && timed_out(a, t0, spin)) {
+          st_dev(a.status, fail_tag(a));
+          ok = false;
+          break;
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < EB; ++k) {
+      const int e = e0 + k * NTHR + tix();
+      const bool in = e < M * 16;
+      const int m = e >> 4, c = e & 15;
+      float acc = 0.f;
+#pragma unroll
+      for (int x = 0; x < NXMAX; ++x)
+        if (x < NX) acc += __uint_as_float((uint32_t)v[k][x]);
+      const float hv = hold[k] + acc;
+      if (in) {
+        hres[e] = hv;
+        if (hidden_l) hidden_l[(int64_t)m * dm.d + i * 16 + c] = hv;
+      }
+      const float vn = shfl_xor(hv, 1);
+      if (in && (c & 1) == 0)
+        st_loc(reinterpret_cast<uint32_t*>(xb + ((int64_t)i * tp.Mp + m) * 16 + c), pack_bf16x2(hv, vn));
+      float sq = hv * hv;
+      sq += shfl_xor(sq, 8);
+      sq += shfl_xor(sq, 4);
+      sq += shfl_xor(sq, 2);
+      sq += shfl_xor(sq, 1);
+      if (in && c == 0) st_loc_f(ssq + (int64_t)i * tp.Ms + m, sq);
+    }
+  }
+  stores_done();
+  __syncthreads();
+  if (tix() == 0) st_loc(flag + (int64_t)i * FPAD, st);
+  return __syncthreads_and(ok);
+}
+
+// ------------------------------------------------------------------------------------------ embed
+// In every XCD: the owner of column tile i copies the tokens' tile into the residual, its bf16 copy and sums of
+// squares (the input of layer 0) and publishes it; rotary rows m = s, s + n, ... (fp64 angles) are written for
+// the XCD's own use.
+__device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams& tp, const Dims& dm, TickLds& L) {
+  const int X = uni(L.X), s = uni(L.s), n = uni(L.n), d = dm.d, M = tp.M, half = dm.Dh / 2, nt = d / 16;
+  const uint64_t st = stamp_of(a, -1, dm.n_layers);
+  float* hres = a.hres + (int64_t)X * a.x_stride_f;
+  uint16_t* xb = a.xb_out + (int64_t)X * a.x_stride_b;
+  float* ssq = a.ssq_out + (int64_t)X * a.x_stride_s;
+  float* rope = a.rope + (int64_t)X * a.x_stride_r;
+  for (int i = s; i < nt; i += n) {
+    for (int e = tix(); e < M * 16; e += NTHR) {
+      const int m = e >> 4, c = e & 15;
+      const int64_t idx = (int64_t)m * d + i * 16 + c;
+      const float v = a.tok_dtype == FSX_BF16 ? bf16_to_f32(((const uint16_t*)a.tokens)[idx]) : ((const float*)a.tokens)[idx];
+      hres[(int64_t)i * tp.Mp * 16 + e] = v;
+      const float vn = shfl_xor(v, 1);
+      if ((c & 1) == 0) st_loc(reinterpret_cast<uint32_t*>(xb + ((int64_t)i * tp.Mp + m) * 16 + c), pack_bf16x2(v, vn));
+      float sq = v * v;
+      sq += shfl_xor(sq, 8);
+      sq += shfl_xor(sq, 4);
+      sq += shfl_xor(sq, 2);
+      sq += shfl_xor(sq, 1);
+      if (c == 0) st_loc_f(ssq + (int64_t)i * tp.Ms + m, sq);
+    }
+    stores_done();
+    __syncthreads();
+    if (tix() == 0) st_loc(a.f_out + ((int64_t)X * XFLAGS + i) * FPAD, st);
+  }
+  for (int m = s; m < M; m += n) {
+    const int b = m / tp.S, t = m % tp.S;
+    for (int j = tix(); j < half; j += NTHR) {
+      double cs = 1.0, sn = 0.0;
+      if (dm.rope_base > 0.f) {
+        const double ang = (double)(tp.pos[b] + t) * pow((double)dm.rope_base, -2.0 * (double)j / (double)dm.Dh);
+        cs = cos(ang);
+        sn = sin(ang);
+      }
+      st_loc_f(rope + ((int64_t)m * half + j) * 2, (float)cs);
+      st_loc_f(rope + ((int64_t)m * half + j) * 2 + 1, (float)sn);
+    }
+  }
+  stores_done();
+  __syncthreads();
+  if (tix() == 0) st_loc(a.f_rope + ((int64_t)X * XFLAGS + s) * FPAD, st);
+}
+
+// ------------------------------------------------------------------------------------------ Q
+// Units of XCD X: u = (local head hl, section sec (q, k, v), 16-column tile t), 24 per head of width 128.
+// Workgroup s takes units s, s + n, ...; its k-th unit goes to wave k % 4, which holds the unit's weights in
+// registers (loaded before the wait).  Each unit publishes a flag once its columns are written.
 __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
-  const int G = gridDim.x, d = dm.d, M = tp.M, A = dm.A, Dh = dm.Dh, half = Dh / 2;
+  const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
+  const int d = dm.d, M = tp.M, A = dm.A, H = dm.H, half = DH / 2, nt = d / 16;
   const int wave = tix() >> 6;
-  const int n_units = 3 * A / 16;
-  const TickLayer& W = a.layers[l];
+  const int h0 = head_lo(X, NX, H), nh = head_lo(X + 1, NX, H) - h0;
+  const int n_units = 24 * nh;
+  const LayerW W = layer_w(a, dm, l);
   const int KB = d / 32;
-  const float qs = LOG2E / sqrtf((float)Dh);
-  const uint16_t* hbsrc = l == 0 ? a.hb0 : a.hbout + (int64_t)(l - 1) * tp.Mp * d;
-  const float* ssq = l == 0 ? a.ssq0 : a.ssq_out + (int64_t)(l - 1) * (d / 16) * tp.Ms;
+  const float qs = LOG2E / sqrtf((float)DH);
+  const uint16_t* xb = a.xb_out + (int64_t)X * a.x_stride_b;
+  const float* ssq = a.ssq_out + (int64_t)X * a.x_stride_s;
+  const float* rope = a.rope + (int64_t)X * a.x_stride_r;
+  const uint64_t st = stamp_of(a, l, dm.n_layers);
   bool waited = false;
-  for (int u0 = blockIdx.x; u0 < n_units; u0 += 4 * G) {
-    const int u = u0 + wave * G;  // this wave's unit in this round
+  for (int u0 = s; u0 < n_units; u0 += 4 * n) {
+    const int u = u0 + wave * n;  // this wave's unit in this round
     const bool mine = u < n_units;
+    const int hl = u / 24, sec = (u % 24) / 8, t = u % 8;
+    const int h = h0 + hl;
+    const int tile = sec * (A / 16) + h * (DH / 16) + t;  // 16-row tile of packed [q; k; v]
     uint4 w[16];
-    if (mine) load_unit_w_full(W.wqkv + (int64_t)u * KB * WAVE, KB, w);
+    if (mine) load_unit_w_full(W.wqkv + (int64_t)tile * KB * WAVE, KB, w);
     if (!waited) {
       TICK_SUB(l, 0);
-      const bool ok = l == 0 ? wg_wait(a.f_embed, d / 16 + M, stamp_of(a, -1, dm.n_layers), a, L)
-                             : wg_wait(a.f_hout, d / 16, stamp_of(a, l - 1, dm.n_layers), a, L);
+      bool ok = wg_wait(a.f_out + (int64_t)X * XFLAGS * FPAD, nt, stamp_of(a, l - 1, dm.n_layers), a, L);
+      if (ok && l == 0) ok = wg_wait(a.f_rope + (int64_t)X * XFLAGS * FPAD, n, stamp_of(a, -1, dm.n_layers), a, L);
       if (!ok) return false;
       waited = true;
       TICK_SUB(l, 1);
     }
-    const int sec = (u * 16) / A;  // 0 q, 1 k, 2 v
-    const int nl0 = u * 16 - sec * A;
+    const int nl0 = h * DH + t * 16;  // first column of the unit inside its section
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      // rotary rows ([M][Dh/2][2], 512 bytes each, one producer per row, complete before any projection
-      // starts) are read with ordinary loads
-      stage<16>(hbsrc, tp.Mp, m0, rows, d, ssq, tp.Ms, d, dm.eps, L, a.rope);
+      stage<16>(xb, tp.Mp, m0, rows, d, ssq, tp.Ms, d, dm.eps, L, rope);
       TICK_SUB(l, 2);
       if (mine) {
-        wave_gemm(w, KB, mt_n, L, [&](int mt, f32x4 s, int c, int grp) {
+        wave_gemm(w, KB, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
           const int nl = nl0 + c;
           if (sec == 2) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int row = m0 + mt * 16 + 4 * grp + i;
-              s[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
-              const float other = shfl_xor(s[i], 1);
+              sacc[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
+              const float other = shfl_xor(sacc[i], 1);
               if ((c & 1) == 0 && row < M)
-                st_dev(reinterpret_cast<uint32_t*>(a.vself + (int64_t)row * A + nl), pack_bf16x2(s[i], other));
+                st_loc(reinterpret_cast<uint32_t*>(a.vself + (int64_t)row * A + nl), pack_bf16x2(sacc[i], other));
             }
           } else {
-            const int head = nl / Dh, p = nl % Dh;
+            const int p = nl % DH;
             const int j = 8 * (p / 16) + (c & 7);
             const int dch = c < 8 ? j : half + j;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              s[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
-              const float partner = shfl_xor(s[i], 8);
+              sacc[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
+              const float partner = shfl_xor(sacc[i], 8);
               const int row = m0 + mt * 16 + 4 * grp + i;
               const float cs = L.rope[mt * 16 + 4 * grp + i][j][0];
               const float sn = L.rope[mt * 16 + 4 * grp + i][j][1];
-              const float r = c < 8 ? s[i] * cs - partner * sn : s[i] * cs + partner * sn;
-              const int64_t o = (int64_t)row * A + head * Dh + dch;
+              const float r = c < 8 ? sacc[i] * cs - partner * sn : sacc[i] * cs + partner * sn;
+              const int64_t o = (int64_t)row * A + h * DH + dch;
               if (sec == 0) {
-                if (row < M) st_dev_f(a.q + o, r * qs);
+                if (row < M) st_loc_f(a.q + o, r * qs);
               } else {
                 const float nb = shfl_xor(r, 1);  // neighbouring channel dch+1 sits in lane c+1
-                if ((c & 1) == 0 && row < M) st_dev(reinterpret_cast<uint32_t*>(a.kself + o), pack_bf16x2(r, nb));
+                if ((c & 1) == 0 && row < M) st_loc(reinterpret_cast<uint32_t*>(a.kself + o), pack_bf16x2(r, nb));
               }
             }
           }
@@ -429,15 +614,11 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
       }
       __syncthreads();  // the next chunk overwrites the staged rows
     }
+    // publish this wave's unit
+    stores_done();
+    if (mine && (tix() & 63) == 0) st_loc(a.f_q + (int64_t)tile * FPAD, st);
   }
   TICK_SUB(l, 3);
-  stores_done();
-  __syncthreads();
-  TICK_SUB(l, 4);
-  if (tix() == 0) {
-    const uint64_t st = stamp_of(a, l, dm.n_layers);
-    for (int u = blockIdx.x; u < n_units; u += G) st_dev(a.f_qkv + u, st);
-  }
   return true;
 }
 
@@ -495,7 +676,7 @@ __device__ __forceinline__ void load_cache_tile(const char* kb, const char* vb, 
   }
 }
 
-// Own-row tile (the expert's rows [r0, r0+32) of S, bf16, produced in this launch): device-coherent loads.
+// Own-row tile (the expert's rows [r0, r0+32) of S, bf16, produced in this launch): device-scope loads.
 __device__ __forceinline__ void load_own_tile(const char* ks, const char* vs, int64_t srow, int r0, int S,
                                               RawTile<0>& t) {
   const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
@@ -524,20 +705,23 @@ __device__ __forceinline__ void load_q(const TickArgs& a, const TickParams& tp, 
     const int t = (tt0 + tt) * 16 + (lane & 15);
     const bool tv = tt < nq && t < tp.S;
     const float* row = a.q + ((int64_t)b * tp.S + (tv ? t : 0)) * dm.A + (int64_t)h * DH;
+    // every load first, then the conversions
+    float4 lo[4], hi[4];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
       const int ch = F16 ? 64 * (kb >> 1) + 16 * grp + 8 * (kb & 1) : 32 * kb + 8 * grp;
-      if (tv) {
-        lo = ld_dev_f4(row + ch);
-        hi = ld_dev_f4(row + ch + 4);
-      }
+      lo[kb] = ld_dev_f4(row + ch);
+      hi[kb] = ld_dev_f4(row + ch + 4);
+    }
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      if (!tv) lo[kb] = hi[kb] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (F16)
-        q[tt][kb] = make_uint4(pack_f16x2(lo.x, lo.y), pack_f16x2(lo.z, lo.w), pack_f16x2(hi.x, hi.y),
-                               pack_f16x2(hi.z, hi.w));
+        q[tt][kb] = make_uint4(pack_f16x2(lo[kb].x, lo[kb].y), pack_f16x2(lo[kb].z, lo[kb].w),
+                               pack_f16x2(hi[kb].x, hi[kb].y), pack_f16x2(hi[kb].z, hi[kb].w));
       else
-        q[tt][kb] = make_uint4(pack_bf16x2(lo.x, lo.y), pack_bf16x2(lo.z, lo.w), pack_bf16x2(hi.x, hi.y),
-                               pack_bf16x2(hi.z, hi.w));
+        q[tt][kb] = make_uint4(pack_bf16x2(lo[kb].x, lo[kb].y), pack_bf16x2(lo[kb].z, lo[kb].w),
+                               pack_bf16x2(hi[kb].x, hi[kb].y), pack_bf16x2(hi[kb].z, hi[kb].w));
     }
   }
 }
@@ -687,7 +871,7 @@ struct AUnit {
 
 // Merge the 4 waves' LDS states of query tile tt: each thread owns (t, 8 channels).  If final, normalise into
 // the attention output; else store the unnormalised partial of slot `item`.
-__device__ __forceinline__ void merge_states(const TickArgs& a, const TickParams& tp, const Dims& dm, int l,
+__device__ __forceinline__ void merge_states(const TickArgs& a, const TickParams& tp, const Dims& dm,
                                              const AUnit& U, int tt, bool final_out, int64_t item, TickLds& L) {
   const int t = tix() >> 4, d0 = (tix() & 15) * 8;
   float Mx = -INFINITY;
@@ -708,50 +892,67 @@ __device__ __forceinline__ void merge_states(const TickArgs& a, const TickParams
     const int tok = tt * 16 + t;
     if (tok < tp.S) {
       const float inv = 1.0f / Ls;
-      uint16_t* dst = a.attn + (int64_t)l * tp.M * dm.A + ((int64_t)U.b * tp.S + tok) * dm.A + (int64_t)U.h * DH + d0;
-      st_dev16(dst, make_uint4(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
+      uint16_t* dst = a.attn + ((int64_t)U.b * tp.S + tok) * dm.A + (int64_t)U.h * DH + d0;
+      st_loc16(dst, make_uint4(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
                                pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv)));
     }
   } else {
     float* po = a.att_o + (item * 16 + t) * 128 + d0;
-    st_dev_f4(po, make_float4(acc[0], acc[1], acc[2], acc[3]));
-    st_dev_f4(po + 4, make_float4(acc[4], acc[5], acc[6], acc[7]));
+    st_loc_f4(po, make_float4(acc[0], acc[1], acc[2], acc[3]));
+    st_loc_f4(po + 4, make_float4(acc[4], acc[5], acc[6], acc[7]));
     if ((tix() & 15) == 0) {
-      st_dev_f(a.att_ml + item * 32 + 2 * t, Mx);
-      st_dev_f(a.att_ml + item * 32 + 2 * t + 1, Ls);
+      st_loc_f(a.att_ml + item * 32 + 2 * t, Mx);
+      st_loc_f(a.att_ml + item * 32 + 2 * t + 1, Ls);
     }
   }
 }
 
-// the last range of an agent to finish merges the partials of all its ranges (fixed order)
-__device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickParams& tp, const Dims& dm, int l,
-                                               const AUnit& U) {
+// an agent's last range merges the partials of all its ranges (fixed order) into the attention output; the
+// partials are loaded 8 ranges at a time, every load issued before any is used
+__device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickParams& tp, const Dims& dm, const AUnit& U) {
+  constexpr int RB = 8;
   const int t = tix() >> 4, d0 = (tix() & 15) * 8;
   const int H = dm.H;
   for (int tt = 0; tt < tp.n_tt; ++tt) {
     float Mx = -INFINITY, Ls = 0.f, acc[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[k] = 0.f;
-#pragma unroll 2
-    for (int r = 0; r < U.nr; ++r) {
-      const int64_t item = ((int64_t)(tp.range_prefix[U.b] + r) * H + U.h) * tp.n_tt + tt;  // pair * n_tt + tt
-      const float ms = ld_dev_f(a.att_ml + item * 32 + 2 * t), ls = ld_dev_f(a.att_ml + item * 32 + 2 * t + 1);
-      const float* po = a.att_o + (item * 16 + t) * 128 + d0;
-      const float4 v0 = ld_dev_f4(po), v1 = ld_dev_f4(po + 4);
-      const float mn = fmaxf(Mx, ms);
-      const float fa = Mx == -INFINITY ? 0.f : exp2f(Mx - mn), fb = ms == -INFINITY ? 0.f : exp2f(ms - mn);
-      Ls = Ls * fa + ls * fb;
-      acc[0] = acc[0] * fa + v0.x * fb; acc[1] = acc[1] * fa + v0.y * fb;
-      acc[2] = acc[2] * fa + v0.z * fb; acc[3] = acc[3] * fa + v0.w * fb;
-      acc[4] = acc[4] * fa + v1.x * fb; acc[5] = acc[5] * fa + v1.y * fb;
-      acc[6] = acc[6] * fa + v1.z * fb; acc[7] = acc[7] * fa + v1.w * fb;
-      Mx = mn;
+    for (int r0 = 0; r0 < U.nr; r0 += RB) {
+      float ms[RB], ls[RB];
+      float4 v0[RB], v1[RB];
+#pragma unroll
+      for (int j = 0; j < RB; ++j) {
+        ms[j] = -INFINITY;
+        ls[j] = 0.f;
+        v0[j] = v1[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (r0 + j < U.nr) {
+          const int64_t item = ((int64_t)(tp.range_prefix[U.b] + r0 + j) * H + U.h) * tp.n_tt + tt;  // pair * n_tt + tt
+          ms[j] = ld_dev_f(a.att_ml + item * 32 + 2 * t);
+          ls[j] = ld_dev_f(a.att_ml + item * 32 + 2 * t + 1);
+          const float* po = a.att_o + (item * 16 + t) * 128 + d0;
+          v0[j] = ld_dev_f4(po);
+          v1[j] = ld_dev_f4(po + 4);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < RB; ++j) {
+        if (r0 + j < U.nr) {
+          const float mn = fmaxf(Mx, ms[j]);
+          const float fa = Mx == -INFINITY ? 0.f : exp2f(Mx - mn), fb = ms[j] == -INFINITY ? 0.f : exp2f(ms[j] - mn);
+          Ls = Ls * fa + ls[j] * fb;
+          acc[0] = acc[0] * fa + v0[j].x * fb; acc[1] = acc[1] * fa + v0[j].y * fb;
+          acc[2] = acc[2] * fa + v0[j].z * fb; acc[3] = acc[3] * fa + v0[j].w * fb;
+          acc[4] = acc[4] * fa + v1[j].x * fb; acc[5] = acc[5] * fa + v1[j].y * fb;
+          acc[6] = acc[6] * fa + v1[j].z * fb; acc[7] = acc[7] * fa + v1[j].w * fb;
+          Mx = mn;
+        }
+      }
     }
     const int tok = tt * 16 + t;
     if (tok < tp.S) {
       const float inv = 1.0f / Ls;
-      uint16_t* dst = a.attn + (int64_t)l * tp.M * dm.A + ((int64_t)U.b * tp.S + tok) * dm.A + (int64_t)U.h * DH + d0;
-      st_dev16(dst, make_uint4(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
+      uint16_t* dst = a.attn + ((int64_t)U.b * tp.S + tok) * dm.A + (int64_t)U.h * DH + d0;
+      st_loc16(dst, make_uint4(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
                                pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv)));
     }
   }
@@ -759,8 +960,8 @@ __device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickPara
 
 // The tiles of one unit for query tiles tt0 .. tt0+nq-1 (nq <= NQ): wave w takes cache tiles w, w+4, ..., kept
 // PD deep in registers, then the own-row tiles that continue the same round robin; the states are merged
-// through LDS and written out.  One query tile is held in registers; several are read from LDS.  Returns
-// false if a wait failed.
+// through LDS and written out (normalised if the agent has one range, else as the partial of this range).
+// Returns false if a wait failed.
 template <int KT, int NQ, int PD>
 __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& tp, const Dims& dm, int l,
                                           const AUnit& U, int tt0, int nq, TickLds& L) {
@@ -770,21 +971,14 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
   const int nc = U.nct > wave ? (U.nct - wave + 3) / 4 : 0;
   RawTile<KT> ring[PD];
   auto cache_tile = [&](int i, RawTile<KT>& t) {
-    const int ii = i < nc ? i : nc - 1;
-    load_cache_tile<KT>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * (wave + 4 * ii), U.i1, t);
+    load_cache_tile<KT>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * (wave + 4 * i), U.i1, t);
   };
   // the first tiles do not depend on this layer's projections: issue them before waiting
-  if (nc > 0) {
 #pragma unroll
-    for (int dd = 0; dd < PD; ++dd) cache_tile(dd, ring[dd]);
-  }
-  {
-    // the q, k and v column tiles of this head
-    const bool ok = wave_wait(a.f_qkv + U.h * (DH / 16), 3 * (DH / 16), st, a, DH / 16, dm.A / 16);
-    if (!ok && lane == 0) L.ok = 0;
-    __syncthreads();
-    if (!L.ok) return false;
-  }
+  for (int dd = 0; dd < PD; ++dd)
+    if (dd < nc) cache_tile(dd, ring[dd]);
+  // the q, k and v column tiles of this head
+  if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16)) return false;
   f32x4 o[NQ][8];
   float m_run[NQ], l_run[NQ];
 #pragma unroll
@@ -814,7 +1008,7 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
 #pragma unroll
     for (int dd = 0; dd < PD; ++dd) {
       tile_compute<KT, NQ>(ring[dd], qf, nq, U.i0 + 32 * (wave + 4 * (i + dd)), U.i1, U.ksc, o, m_run, l_run);
-      cache_tile(i + dd + PD, ring[dd]);
+      if (i + dd + PD < nc) cache_tile(i + dd + PD, ring[dd]);
     }
   }
 #pragma unroll
@@ -852,49 +1046,55 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
     if (tt < nq) {
       state_to_lds(L.u.a.st[wave], o[tt], m_run[tt], l_run[tt]);
       __syncthreads();
-      merge_states(a, tp, dm, l, U, tt0 + tt, final_out, pair * tp.n_tt + tt0 + tt, L);
+      merge_states(a, tp, dm, U, tt0 + tt, final_out, pair * tp.n_tt + tt0 + tt, L);
       __syncthreads();
     }
   }
   return true;
 }
 
-// Attention units are (agent, range, head), numbered agent by agent in the planner's order (largest ranges
-// first), heads fastest.  Workgroup w starts with unit w; further units come from a per-layer counter.
+// Attention units of XCD X: (pair q, local head j) numbered u = q * nh + j, where the pairs (agent, range) list
+// every agent's ranges but its last (agents in the planner's order) and then every agent's last range.  Workgroup
+// s takes units s, s + n, ....  A last range of an agent with several ranges waits for the others and merges
+// them; since all such units come after all the others in every workgroup's list, the waits cannot form a cycle.
 template <int KT>
 __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   constexpr int ES = KT == 0 ? 2 : 1;
-  const int G = gridDim.x;
-  const int H = dm.H, A = dm.A, n_tt = tp.n_tt;
+  const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
+  const int H = dm.H, A = dm.A, n_tt = tp.n_tt, B = tp.B;
+  const int h0 = head_lo(X, NX, H), nh = head_lo(X + 1, NX, H) - h0;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
-  const int n_units = tp.n_units;
-  int u = blockIdx.x;
+  const int NF = tp.nf_prefix[B];
+  const int n_units = nh * (NF + B);
   bool first = true;
-  while (u < n_units) {
-    // take the next unit now; the answer is needed only at the end of this one
-    uint32_t nxt = 0;
-    if (tix() == 0) nxt = atomic_add_dev(a.sched + l, 1u);
-    AUnit U;
-    int k = 0;
-    while (k + 1 < tp.B && tp.unit_prefix[k + 1] <= u) ++k;
+  for (int u = s; u < n_units; u += n) {
+    const int q = u / nh, h = h0 + u % nh;
+    int k = 0, r;
+    if (q < NF) {
+      while (k + 1 < B && tp.nf_prefix[k + 1] <= q) ++k;
+      r = q - tp.nf_prefix[k];
+    } else {
+      k = q - NF;
+      r = -1;
+    }
     const int b = tp.order[k];
-    const int rem = u - tp.unit_prefix[k];
+    AUnit U;
     U.b = b;
-    U.r = rem / H;
-    U.h = rem - U.r * H;
+    U.h = h;
     U.nr = tp.range_prefix[b + 1] - tp.range_prefix[b];
+    U.r = r < 0 ? U.nr - 1 : r;
     U.i0 = U.r * tp.range_rows[b];
     U.i1 = min(U.i0 + tp.range_rows[b], tp.len[b]);
     U.nct = U.i1 > U.i0 ? (U.i1 - U.i0 + 31) / 32 : 0;
     U.nst = U.r == U.nr - 1 ? (tp.S + 31) / 32 : 0;
-    const int64_t slab = (((int64_t)b * a.cv.n_layers + l) * H + U.h) * a.cv.cap;  // head-major (b, l, h) ring
+    const int64_t slab = (((int64_t)b * a.cv.n_layers + l) * H + h) * a.cv.cap;  // head-major (b, l, h) ring
     U.kc = (const char*)a.cv.k + slab * DH * ES;
     U.vc = (const char*)a.cv.v + slab * DH * ES;
-    U.ks = (const char*)a.kself + ((int64_t)b * tp.S * A + (int64_t)U.h * DH) * 2;
-    U.vs = (const char*)a.vself + ((int64_t)b * tp.S * A + (int64_t)U.h * DH) * 2;
+    U.ks = (const char*)a.kself + ((int64_t)b * tp.S * A + (int64_t)h * DH) * 2;
+    U.vs = (const char*)a.vself + ((int64_t)b * tp.S * A + (int64_t)h * DH) * 2;
     U.ksc = U.vsc = 1.f;
     if (KT == 1) {
-      const int64_t si = ((int64_t)b * a.cv.n_layers + l) * H + U.h;
+      const int64_t si = ((int64_t)b * a.cv.n_layers + l) * H + h;
       U.ksc = a.cv.k_scale[si];
       U.vsc = a.cv.v_scale[si];
     }
@@ -907,192 +1107,191 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
     }
     if (!ok) return false;
     if (first) TICK_SUB(l, 5);
-    if (tix() == 0) L.next = G + (int)nxt;
-    stores_done();
-    __syncthreads();
-    if (first) TICK_SUB(l, 6);
-    const int ci = b * H + U.h;
-    // an (agent, head) is complete when all its ranges are written
-    const uint32_t need = (uint32_t)U.nr;
-    if (tix() == 0) L.last = need == 1 ? 1 : atomic_add_dev(a.att_cnt + ci, 1u) == need - 1;
-    __syncthreads();
-    if (L.last) {
-      if (need > 1) combine_ranges(a, tp, dm, l, U);
-      if (tix() == 0 && need > 1) st_dev(a.att_cnt + ci, 0u);
+    const int64_t pair0 = (int64_t)tp.range_prefix[b] * H;
+    if (U.nr > 1) {
       stores_done();
       __syncthreads();
-      if (tix() == 0) st_dev(a.f_attn + ci, st);
+      if (U.r < U.nr - 1) {
+        if (tix() == 0) st_loc(a.f_rng + (pair0 + (int64_t)U.r * H + h) * FPAD, st);
+      } else {
+        // the other ranges of (b, h): pairs pair0 + r * H + h, r < nr - 1
+        if (!wg_wait(a.f_rng + (pair0 + h) * FPAD, U.nr - 1, st, a, L, 1, H)) return false;
+        combine_ranges(a, tp, dm, U);
+      }
     }
-    u = L.next;
+    if (U.r == U.nr - 1) {
+      stores_done();
+      __syncthreads();
+      if (tix() == 0) st_loc(a.f_attn + ((int64_t)b * H + h) * FPAD, st);
+    }
+    if (first) TICK_SUB(l, 6);
     first = false;
     __syncthreads();
   }
   return true;
 }
 
-// ------------------------------------------------------------------------------------------ O
+// ------------------------------------------------------------------------------------------ O (+ R1)
+// Column tile i (owner: slot i mod n) of the output projection over X's attention columns, as stamped partial
+// words; then the reduction of tile i over the XCDs into h_mid.
 __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
-  const int G = gridDim.x, d = dm.d, M = tp.M, A = dm.A, H = dm.H;
-  const int ntiles = d / 16, n_units = ntiles * a.ks_o;
-  const int hps = H / a.ks_o, nk = A / a.ks_o, nkb = nk / 32;
+  const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
+  const int d = dm.d, M = tp.M, A = dm.A, H = dm.H, nt = d / 16;
+  const int h0 = head_lo(X, NX, H), nh = head_lo(X + 1, NX, H) - h0;
+  const int kb0 = h0 * (DH / 32), nkb = nh * (DH / 32);  // <= 16
   const uint64_t st = stamp_of(a, l, dm.n_layers);
-  const TickLayer& W = a.layers[l];
-  const uint16_t* attn = a.attn + (int64_t)l * M * A;
-  const float* hin = l == 0 ? a.h0 : a.hout + (int64_t)(l - 1) * M * d;
-  for (int u = blockIdx.x; u < n_units; u += G) {
-    const int nt = u % ntiles, ks = u / ntiles;
+  const uint32_t st32 = (uint32_t)st;
+  const LayerW W = layer_w(a, dm, l);
+  uint64_t* po = a.po + (int64_t)X * nt * tp.Mp * 16;
+  bool first = true;
+  for (int i = s; i < nt; i += n) {
     uint4 w[4];
-    load_unit_w(W.wo + (int64_t)nt * (A / 32) * WAVE, ks * nkb, nkb, w);
-    if (!wg_wait(a.f_attn + ks * hps, tp.B * hps, st, a, L, hps, H)) return false;
-    if (u == (int)blockIdx.x) TICK_SUB(l, 7);
+    load_unit_w(W.wo + (int64_t)i * (A / 32) * WAVE, kb0, nkb, w);
+    if (nh > 0 && !wg_wait(a.f_attn + (int64_t)h0 * FPAD, tp.B * nh, st, a, L, nh, H)) return false;
+    if (first) TICK_SUB(l, 7);
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      stage<0>(attn + ks * nk, A, m0, rows, nk, nullptr, 0, 0, 0.f, L);
-      unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 s, int c, int grp) {
+      if (nh > 0) stage<0>(a.attn + h0 * DH, A, m0, rows, nh * DH, nullptr, 0, 0, 0.f, L);
+      unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = m0 + mt * 16 + 4 * grp + i;
-          if (row < M) st_dev_f(a.part + ((int64_t)ks * M + row) * d + nt * 16 + c, s[i]);
+        for (int r = 0; r < 4; ++r) {
+          const int row = m0 + mt * 16 + 4 * grp + r;
+          if (row < M)
+            st_dev(po + ((int64_t)i * tp.Mp + row) * 16 + c, ((uint64_t)st32 << 32) | __float_as_uint(sacc[r]));
         }
       });
     }
-    stores_done();
-    __syncthreads();
-    if (u == (int)blockIdx.x) TICK_SUB(l, 8);
-    if (tix() == 0) L.last = atomic_add_dev(a.o_cnt + nt, 1u) == (uint32_t)(a.ks_o - 1);
-    __syncthreads();
-    if (u == (int)blockIdx.x) TICK_SUB(l, 9);
-    if (L.last)
-      reduce_tile(a, tp, dm, nt, a.ks_o, hin, a.hmid + (int64_t)l * M * d, a.hbmid + (int64_t)l * tp.Mp * d,
-                  a.ssq_mid + (int64_t)l * (d / 16) * tp.Ms, a.o_cnt, a.f_hmid, st);
-    __syncthreads();
+    if (first) TICK_SUB(l, 8);
+    if (!reduce_tile(a, tp, dm, l, i, a.po, a.xb_mid + (int64_t)X * a.x_stride_b, a.ssq_mid + (int64_t)X * a.x_stride_s,
+                     a.f_mid + (int64_t)X * XFLAGS * FPAD, nullptr, L))
+      return false;
+    if (first) TICK_SUB(l, 9);
+    first = false;
   }
   return true;
 }
 
 // ------------------------------------------------------------------------------------------ F1
+// Units u of X's FFN columns (8 gate + 8 up rows of the packed matrix -> 8 SwiGLU outputs each); workgroup s takes
+// units s, s + n, ...; the 4 waves split K and reduce through LDS.
 __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
-  const int G = gridDim.x, d = dm.d, M = tp.M;
-  const int n_units = 2 * dm.F / 16;
+  const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
+  const int d = dm.d, M = tp.M, F = dm.F, nt = d / 16;
+  const int f0 = ffn_lo(X, NX, F), f1 = ffn_lo(X + 1, NX, F);
+  const int u0 = f0 / 8, nu = (f1 - f0) / 8;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
-  const TickLayer& W = a.layers[l];
-  const uint16_t* hbmid = a.hbmid + (int64_t)l * tp.Mp * d;
-  const float* ssq = a.ssq_mid + (int64_t)l * (d / 16) * tp.Ms;
-  uint16_t* z = a.z + (int64_t)l * tp.Mp * dm.F;  // tile-major [F/8][Mp][8]
+  const LayerW W = layer_w(a, dm, l);
+  const uint16_t* xb = a.xb_mid + (int64_t)X * a.x_stride_b;
+  const float* ssq = a.ssq_mid + (int64_t)X * a.x_stride_s;
   const int KB = d / 32;
   bool waited = false;
-  for (int u0 = blockIdx.x; u0 < n_units; u0 += UMAX * G) {
-    uint4 w[UMAX][4];
-#pragma unroll
-    for (int k = 0; k < UMAX; ++k) {
-      const int u = u0 + k * G;
-      if (u < n_units) load_unit_w(W.wgu + (int64_t)u * KB * WAVE, 0, KB, w[k]);
-    }
+  for (int k = s; k < nu; k += n) {
+    const int u = u0 + k;
+    uint4 w[4];
+    load_unit_w(W.wgu + (int64_t)u * KB * WAVE, 0, KB, w);
     if (!waited) {
-      if (!wg_wait(a.f_hmid, d / 16, st, a, L)) return false;
+      if (!wg_wait(a.f_mid + (int64_t)X * XFLAGS * FPAD, nt, st, a, L)) return false;
       waited = true;
     }
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      stage<16>(hbmid, tp.Mp, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
+      stage<16>(xb, tp.Mp, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
+      unit_gemm(w, KB, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
-      for (int k = 0; k < UMAX; ++k) {
-        const int u = u0 + k * G;
-        if (u >= n_units) break;
-        unit_gemm(w[k], KB, mt_n, L, [&](int mt, f32x4 s, int c, int grp) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            s[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
-            const float up = shfl_xor(s[i], 8);
-            const float gt = s[i];
-            const float zz = gt / (1.0f + expf(-gt)) * up;
-            const float zn = shfl_xor(zz, 1);
-            const int row = m0 + mt * 16 + 4 * grp + i;
-            if (c < 8 && (c & 1) == 0 && row < M)
-              st_dev(reinterpret_cast<uint32_t*>(z + ((int64_t)u * tp.Mp + row) * 8 + c), pack_bf16x2(zz, zn));
-          }
-        });
-      }
-    }
-  }
-  stores_done();
-  __syncthreads();
-  if (tix() == 0)
-    for (int u = blockIdx.x; u < n_units; u += G) st_dev(a.f_z + u, st);
-  return true;
-}
-
-// ------------------------------------------------------------------------------------------ D
-__device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
-  const int G = gridDim.x, d = dm.d, M = tp.M, F = dm.F;
-  const int ntiles = d / 16, n_units = ntiles * a.ks_d, nk = F / a.ks_d, nkb = nk / 32;
-  const uint64_t st = stamp_of(a, l, dm.n_layers);
-  const TickLayer& W = a.layers[l];
-  const uint16_t* z = a.z + (int64_t)l * tp.Mp * F;
-  const float* hmid = a.hmid + (int64_t)l * M * d;
-  for (int u = blockIdx.x; u < n_units; u += G) {
-    const int nt = u % ntiles, ks = u / ntiles;
-    uint4 w[4];
-    load_unit_w(W.wd + (int64_t)nt * (F / 32) * WAVE, ks * nkb, nkb, w);
-    if (!wg_wait(a.f_z + ks * nk / 8, nk / 8, st, a, L)) return false;
-    for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
-      const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      stage<8>(z + (int64_t)(ks * nk / 8) * tp.Mp * 8, tp.Mp, m0, rows, nk, nullptr, 0, 0, 0.f, L);
-      unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 s, int c, int grp) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = m0 + mt * 16 + 4 * grp + i;
-          if (row < M) st_dev_f(a.part + ((int64_t)ks * M + row) * d + nt * 16 + c, s[i]);
+        for (int r = 0; r < 4; ++r) {
+          sacc[r] *= L.r[mt * 16 + 4 * grp + r];  // RMSNorm row scale
+          const float up = shfl_xor(sacc[r], 8);
+          const float gt = sacc[r];
+          const float zz = gt / (1.0f + expf(-gt)) * up;
+          const float zn = shfl_xor(zz, 1);
+          const int row = m0 + mt * 16 + 4 * grp + r;
+          if (c < 8 && (c & 1) == 0 && row < M)
+            st_loc(reinterpret_cast<uint32_t*>(a.z + ((int64_t)u * tp.Mp + row) * 8 + c), pack_bf16x2(zz, zn));
         }
       });
     }
     stores_done();
     __syncthreads();
-    if (tix() == 0) L.last = atomic_add_dev(a.d_cnt + nt, 1u) == (uint32_t)(a.ks_d - 1);
-    __syncthreads();
-    if (L.last)
-      reduce_tile(a, tp, dm, nt, a.ks_d, hmid, a.hout + (int64_t)l * M * d, a.hbout + (int64_t)l * tp.Mp * d,
-                  a.ssq_out + (int64_t)l * (d / 16) * tp.Ms, a.d_cnt, a.f_hout, st);
-    __syncthreads();
+    if (tix() == 0) st_loc(a.f_z + (int64_t)u * FPAD, st);
+  }
+  return true;
+}
+
+// ------------------------------------------------------------------------------------------ D (+ R2)
+__device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
+  const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
+  const int d = dm.d, M = tp.M, F = dm.F, nt = d / 16;
+  const int f0 = ffn_lo(X, NX, F), f1 = ffn_lo(X + 1, NX, F);
+  const int kb0 = f0 / 32, nkb = (f1 - f0) / 32;  // <= 16
+  const uint64_t st = stamp_of(a, l, dm.n_layers);
+  const uint32_t st32 = (uint32_t)st;
+  const LayerW W = layer_w(a, dm, l);
+  uint64_t* pd = a.pd + (int64_t)X * nt * tp.Mp * 16;
+  float* hidden_l = (a.hidden && X == 0) ? a.hidden + (int64_t)l * M * d : nullptr;
+  for (int i = s; i < nt; i += n) {
+    uint4 w[4];
+    load_unit_w(W.wd + (int64_t)i * (F / 32) * WAVE, kb0, nkb, w);
+    if (nkb > 0 && !wg_wait(a.f_z + (int64_t)(f0 / 8) * FPAD, (f1 - f0) / 8, st, a, L)) return false;
+    for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
+      const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
+      if (nkb > 0) stage<8>(a.z + (int64_t)(f0 / 8) * tp.Mp * 8, tp.Mp, m0, rows, f1 - f0, nullptr, 0, 0, 0.f, L);
+      unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = m0 + mt * 16 + 4 * grp + r;
+          if (row < M)
+            st_dev(pd + ((int64_t)i * tp.Mp + row) * 16 + c, ((uint64_t)st32 << 32) | __float_as_uint(sacc[r]));
+        }
+      });
+    }
+    if (!reduce_tile(a, tp, dm, l, i, a.pd, a.xb_out + (int64_t)X * a.x_stride_b, a.ssq_out + (int64_t)X * a.x_stride_s,
+                     a.f_out + (int64_t)X * XFLAGS * FPAD, hidden_l, L))
+      return false;
   }
   return true;
 }
 
 // ------------------------------------------------------------------------------------------ head
-// wp[b] = mean over t < T of RMSNorm(h[b][t]) * g_final, times W_head^T.  Thread tid owns columns tid and
+// wp[b] = mean over t < T of RMSNorm(h[b][t]) * g_final, times W_head^T, on the workgroups of XCD rank 0
+// (agent b on slot b mod n0), from that XCD's replica of the residual.  Thread tid owns columns tid and
 // tid + 256 and holds the pooled rows in registers (16 rows per pass).
 __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& tp, const Dims& dm, bool ok, TickLds& L) {
-  const int G = gridDim.x, d = dm.d, M = tp.M, nl = dm.n_layers, T = tp.T;
+  const int d = dm.d, nl = dm.n_layers, T = tp.T;
   const int tid = tix(), wave = tid >> 6, lane = tid & 63;
-  for (int b = blockIdx.x; b < tp.B; b += G) {
-    if (ok) ok = wg_wait(a.f_hout, d / 16, stamp_of(a, nl - 1, nl), a, L);
+  if (uni(L.X) != 0 && ok) return;
+  // after a failure every workgroup of XCD 0 (or, if registration failed, workgroup b) writes NaN for its agents
+  const int s = ok ? uni(L.s) : (int)blockIdx.x, n = ok ? uni(L.n0) : (int)gridDim.x;
+  for (int b = s; b < tp.B; b += n) {
+    if (ok) ok = wg_wait(a.f_out, d / 16, stamp_of(a, nl - 1, nl), a, L);  // XCD rank 0's flags
     if (!ok) {
       for (int o = tid; o < dm.n_out; o += NTHR) a.waypoints[(int64_t)b * dm.n_out + o] = __builtin_nanf("");
       continue;
     }
-    const float* h = a.hout + (int64_t)(nl - 1) * M * d + (int64_t)b * tp.S * d;
+    const float* h = a.hres;  // replica of XCD rank 0, tile-major [d/16][Mp][16]
     const int n0 = tid, n1 = tid + NTHR;
+    auto hv = [&](int m, int col) { return ld_dev_f(h + ((int64_t)(col >> 4) * tp.Mp + m) * 16 + (col & 15)); };
     float xm0 = 0.f, xm1 = 0.f;
     for (int t0 = 0; t0 < T; t0 += 16) {
       float v0[16], v1[16];
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
         const bool in = t0 + t < T;
-        v0[t] = in && n0 < d ? ld_dev_f(h + (int64_t)(t0 + t) * d + n0) : 0.f;
-        v1[t] = in && n1 < d ? ld_dev_f(h + (int64_t)(t0 + t) * d + n1) : 0.f;
+        const int m = b * tp.S + t0 + t;
+        v0[t] = in && n0 < d ? hv(m, n0) : 0.f;
+        v1[t] = in && n1 < d ? hv(m, n1) : 0.f;
       }
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
-        float s = v0[t] * v0[t] + v1[t] * v1[t];
+        float sq = v0[t] * v0[t] + v1[t] * v1[t];
 #pragma unroll
-        for (int m = 32; m >= 1; m >>= 1) s += shfl_xor(s, m);
-        if (lane == 0) L.red2[wave][t] = s;
+        for (int m = 32; m >= 1; m >>= 1) sq += shfl_xor(sq, m);
+        if (lane == 0) L.red2[wave][t] = sq;
       }
       __syncthreads();
       if (tid < 16) {
-        float s = 0.f;
-        for (int w = 0; w < NTHR / WAVE; ++w) s += L.red2[w][tid];
-        L.hr[tid] = 1.0f / sqrtf(s / (float)d + dm.eps);
+        float sq = 0.f;
+        for (int w = 0; w < NTHR / WAVE; ++w) sq += L.red2[w][tid];
+        L.hr[tid] = 1.0f / sqrtf(sq / (float)d + dm.eps);
       }
       __syncthreads();
 #pragma unroll
@@ -1110,10 +1309,10 @@ __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& 
     __syncthreads();
     for (int o = wave; o < dm.n_out; o += NTHR / WAVE) {
       float acc = 0.f;
-      for (int n = lane; n < d; n += WAVE) {
-        const float wv = a.head_dtype == FSX_BF16 ? bf16_to_f32(((const uint16_t*)a.head_w)[(int64_t)o * d + n])
-                                                 : ((const float*)a.head_w)[(int64_t)o * d + n];
-        acc += xm[n] * wv;
+      for (int c = lane; c < d; c += WAVE) {
+        const float wv = a.head_dtype == FSX_BF16 ? bf16_to_f32(((const uint16_t*)a.head_w)[(int64_t)o * d + c])
+                                                 : ((const float*)a.head_w)[(int64_t)o * d + c];
+        acc += xm[c] * wv;
       }
 #pragma unroll
       for (int m = 32; m >= 1; m >>= 1) acc += shfl_xor(acc, m);
@@ -1129,11 +1328,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_tick(TickArgs a, TickParams tp, Dim
   __shared__ TickLds L;
   const int nl = dm.n_layers;
   trace_mark(a, 0, nl);
-  if (tix() == 0) L.ok = 1;
-  __syncthreads();
-  phase_embed(a, tp, dm, L);
+  bool ok = xcd_register(a, L);
+  if (ok) phase_embed(a, tp, dm, L);
   trace_mark(a, 1, nl);
-  bool ok = true;
   for (int l = 0; l < nl && ok; ++l) {
     ok = phase_qkv(a, tp, dm, l, L);
     trace_mark(a, 2 + 16 * l, nl);
@@ -1159,6 +1356,15 @@ hipError_t launch_tick(const TickArgs& a, const TickParams& tp, const Dims& dm, 
   void* args[] = {(void*)&a, (void*)&tp, (void*)&dm};
   const void* f = a.cv.dtype == FSX_FP8_E4M3 ? (const void*)k_tick<1> : (const void*)k_tick<0>;
   return hipLaunchCooperativeKernel(f, dim3(grid), dim3(NTHR), args, 0, s);
+}
+
+__global__ void k_probe_xcds(uint32_t* out) {
+  if (threadIdx.x == 0) out[blockIdx.x] = hw_xcc_id();
+}
+
+hipError_t probe_xcds(uint32_t* dev_out, int grid, hipStream_t s) {
+  void* args[] = {(void*)&dev_out};
+  return hipLaunchCooperativeKernel((const void*)k_probe_xcds, dim3(grid), dim3(64), args, 0, s);
 }
 
 }  // namespace fsx
