@@ -425,12 +425,13 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
     tp.Mp = (tp.M + 7) / 8 * 8;
     tp.Ms = (tp.M + 31) / 32 * 32;
     // Attention units: (agent, range of rows, head).  Rows per unit (one head) aim at about one unit per
-    // workgroup for small work, so that every CU streams a share of the cache, and 2 or 4 for larger work;
-    // an agent's ranges are equal, multiples of 32 rows.
+    // workgroup for small work and 2 or 4 for larger work, never below 256 rows (a range merge costs a few
+    // dependent memory round trips, more than streaming 256 rows); an agent's ranges are equal, multiples
+    // of 32 rows.
     const int64_t total_rh = rows * dm.H;
     const int64_t per_wg = total_rh / G;
     const int k_units = per_wg >= 4096 ? 4 : (per_wg >= 512 ? 2 : 1);
-    int64_t unit_rows = std::max<int64_t>(32, (total_rh + (int64_t)k_units * G - 1) / ((int64_t)k_units * G));
+    int64_t unit_rows = std::max<int64_t>(256, (total_rh + (int64_t)k_units * G - 1) / ((int64_t)k_units * G));
     unit_rows = (unit_rows + 31) / 32 * 32;
     for (;;) {
       int64_t slots = 0;

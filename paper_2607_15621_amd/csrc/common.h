@@ -70,6 +70,42 @@ __device__ __forceinline__ f32x4 mfma_f16(uint4 a, uint4 b, f32x4 c) {
 __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v, m, WAVE); }
 __device__ __forceinline__ float shfl(float v, int src) { return __shfl(v, src, WAVE); }
 
+// Cross-lane moves without the LDS crossbar (DPP and the gfx950 permlane swaps):
+//   xor1(v)      value of lane l ^ 1 (quad_perm [1,0,3,2])
+//   xor8(v)      value of lane l ^ 8 (row_ror:8 inside each 16-lane row)
+//   row_sum16(v) sum over the 16 lanes of l's row, in every lane (rotations by 8, 4, 2, 1)
+//   rows_max/rows_sum(v): max / sum over lanes l, l ^ 16, l ^ 32, l ^ 48 (permlane16_swap then permlane32_swap;
+//   each swap of v with itself returns the two halves of the exchange, combined by the operation)
+__device__ __forceinline__ float xor1(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float xor8(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row_sum16(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xF, 0xF, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x124, 0xF, 0xF, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x122, 0xF, 0xF, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x121, 0xF, 0xF, false));
+  return v;
+}
+__device__ __forceinline__ float rows_max(float v) {
+  const unsigned u = __builtin_bit_cast(unsigned, v);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float m = fmaxf(__builtin_bit_cast(float, (unsigned)a[0]), __builtin_bit_cast(float, (unsigned)a[1]));
+  const unsigned mu = __builtin_bit_cast(unsigned, m);
+  const auto b = __builtin_amdgcn_permlane32_swap(mu, mu, false, false);
+  return fmaxf(__builtin_bit_cast(float, (unsigned)b[0]), __builtin_bit_cast(float, (unsigned)b[1]));
+}
+__device__ __forceinline__ float rows_sum(float v) {
+  const unsigned u = __builtin_bit_cast(unsigned, v);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float m = __builtin_bit_cast(float, (unsigned)a[0]) + __builtin_bit_cast(float, (unsigned)a[1]);
+  const unsigned mu = __builtin_bit_cast(unsigned, m);
+  const auto b = __builtin_amdgcn_permlane32_swap(mu, mu, false, false);
+  return __builtin_bit_cast(float, (unsigned)b[0]) + __builtin_bit_cast(float, (unsigned)b[1]);
+}
+
 // Transpose an 8x8 block of 16-bit values held as 8 x uint4 (in[j] = row j, 8 columns) into
 // out[k] = column k as 8 values (element j = in[j][k]).
 __device__ __forceinline__ void transpose8x8_b16(const uint4 in[8], uint4 out[8]) {

@@ -294,11 +294,7 @@ __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int r
     }
 #pragma unroll
     for (int p = 0; p < MTMAX; ++p) {
-      float s = part[p];
-      s += shfl_xor(s, 8);
-      s += shfl_xor(s, 4);
-      s += shfl_xor(s, 2);
-      s += shfl_xor(s, 1);
+      const float s = row_sum16(part[p]);
       const int i = rw + 16 * p;
       if (g == 0) L.r[i] = i < rows ? 1.0f / sqrtf(s / (float)Kn + eps) : 0.f;
     }
@@ -473,14 +469,10 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
         hres[e] = hv;
         if (hidden_l) hidden_l[(int64_t)m * dm.d + i * 16 + c] = hv;
       }
-      const float vn = shfl_xor(hv, 1);
+      const float vn = xor1(hv);
       if (in && (c & 1) == 0)
         st_loc(reinterpret_cast<uint32_t*>(xb + ((int64_t)i * tp.Mp + m) * 16 + c), pack_bf16x2(hv, vn));
-      float sq = hv * hv;
-      sq += shfl_xor(sq, 8);
-      sq += shfl_xor(sq, 4);
-      sq += shfl_xor(sq, 2);
-      sq += shfl_xor(sq, 1);
+      const float sq = row_sum16(hv * hv);
       if (in && c == 0) st_loc_f(ssq + (int64_t)i * tp.Ms + m, sq);
     }
   }
@@ -507,13 +499,9 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
       const int64_t idx = (int64_t)m * d + i * 16 + c;
       const float v = a.tok_dtype == FSX_BF16 ? bf16_to_f32(((const uint16_t*)a.tokens)[idx]) : ((const float*)a.tokens)[idx];
       hres[(int64_t)i * tp.Mp * 16 + e] = v;
-      const float vn = shfl_xor(v, 1);
+      const float vn = xor1(v);
       if ((c & 1) == 0) st_loc(reinterpret_cast<uint32_t*>(xb + ((int64_t)i * tp.Mp + m) * 16 + c), pack_bf16x2(v, vn));
-      float sq = v * v;
-      sq += shfl_xor(sq, 8);
-      sq += shfl_xor(sq, 4);
-      sq += shfl_xor(sq, 2);
-      sq += shfl_xor(sq, 1);
+      const float sq = row_sum16(v * v);
       if (c == 0) st_loc_f(ssq + (int64_t)i * tp.Ms + m, sq);
     }
     stores_done();
@@ -585,7 +573,7 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
             for (int i = 0; i < 4; ++i) {
               const int row = m0 + mt * 16 + 4 * grp + i;
               sacc[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
-              const float other = shfl_xor(sacc[i], 1);
+              const float other = xor1(sacc[i]);
               if ((c & 1) == 0 && row < M)
                 st_loc(reinterpret_cast<uint32_t*>(a.vself + (int64_t)row * A + nl), pack_bf16x2(sacc[i], other));
             }
@@ -596,7 +584,7 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               sacc[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
-              const float partner = shfl_xor(sacc[i], 8);
+              const float partner = xor8(sacc[i]);
               const int row = m0 + mt * 16 + 4 * grp + i;
               const float cs = L.rope[mt * 16 + 4 * grp + i][j][0];
               const float sn = L.rope[mt * 16 + 4 * grp + i][j][1];
@@ -605,7 +593,7 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
               if (sec == 0) {
                 if (row < M) st_loc_f(a.q + o, r * qs);
               } else {
-                const float nb = shfl_xor(r, 1);  // neighbouring channel dch+1 sits in lane c+1
+                const float nb = xor1(r);  // neighbouring channel dch+1 sits in lane c+1
                 if ((c & 1) == 0 && row < M) st_loc(reinterpret_cast<uint32_t*>(a.kself + o), pack_bf16x2(r, nb));
               }
             }
@@ -806,8 +794,7 @@ __device__ __forceinline__ void tile_compute(const RawTile<KT>& t, QF qf, int nq
           s[rt][i] = v;
           mx = fmaxf(mx, v);
         }
-      mx = fmaxf(mx, shfl_xor(mx, 16));
-      mx = fmaxf(mx, shfl_xor(mx, 32));
+      mx = rows_max(mx);
       const bool grow = mx > m_run[tt] + RESCALE_LOG2;
       if (__any(grow)) {
         const float m_new = grow ? mx : m_run[tt];
@@ -845,8 +832,7 @@ __device__ __forceinline__ void tile_compute(const RawTile<KT>& t, QF qf, int nq
 // write a wave's state (o in the PV C layout, m and the lane-partial l) to LDS slot w
 __device__ __forceinline__ void state_to_lds(float* stw, const f32x4 o[8], float m_run, float l_run) {
   const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
-  float lt = l_run + shfl_xor(l_run, 16);
-  lt += shfl_xor(lt, 32);
+  const float lt = rows_sum(l_run);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -1200,10 +1186,10 @@ __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           sacc[r] *= L.r[mt * 16 + 4 * grp + r];  // RMSNorm row scale
-          const float up = shfl_xor(sacc[r], 8);
+          const float up = xor8(sacc[r]);
           const float gt = sacc[r];
           const float zz = gt / (1.0f + expf(-gt)) * up;
-          const float zn = shfl_xor(zz, 1);
+          const float zn = xor1(zz);
           const int row = m0 + mt * 16 + 4 * grp + r;
           if (c < 8 && (c & 1) == 0 && row < M)
             st_loc(reinterpret_cast<uint32_t*>(a.z + ((int64_t)u * tp.Mp + row) * 8 + c), pack_bf16x2(zz, zn));
