@@ -255,6 +255,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   if (ex->tick) {
     TickArgs& t = ex->ta;
     const size_t dt = (size_t)d / 16;
+    const size_t n_tt_max = ((size_t)ex->S_max + 15) / 16;
     const size_t Mp = ((size_t)M + 7) / 8 * 8, Ms = ((size_t)M + 31) / 32 * 32;
     auto r256 = [](size_t b) { return (b + 255) & ~(size_t)255; };
     const size_t rep_f = r256(Mp * d * 4), rep_b = r256(Mp * d * 2), rep_s = r256(dt * Ms * 4),
@@ -280,7 +281,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
         {(void**)&t.f_out, (size_t)NXMAX * XFLAGS * FPAD * 8},
         {(void**)&t.f_mid, (size_t)NXMAX * XFLAGS * FPAD * 8},
         {(void**)&t.f_q, (size_t)3 * A / 16 * FPAD * 8},
-        {(void**)&t.f_attn, (size_t)nflag_attn * FPAD * 8},
+        {(void**)&t.f_attn, (size_t)nflag_attn * n_tt_max * FPAD * 8},
         {(void**)&t.f_rng, (size_t)ex->items_max * FPAD * 8},
         {(void**)&t.f_z, (size_t)F / 8 * FPAD * 8},
         {(void**)&t.status, 256}};

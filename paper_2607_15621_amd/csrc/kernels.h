@@ -143,7 +143,7 @@ struct TickArgs {
   uint64_t* f_out;     // [NXMAX][XFLAGS] by column tile
   uint64_t* f_mid;     // [NXMAX][XFLAGS] by column tile
   uint64_t* f_q;       // [3A/16]
-  uint64_t* f_attn;    // [B*H]
+  uint64_t* f_attn;    // [B*H][n_tt] per query tile
   uint64_t* f_rng;     // [range pairs]
   uint64_t* f_z;       // [F/8]
   uint64_t* status;

@@ -65,7 +65,6 @@ struct TickLds {
       uint16_t qs[NQW * 16][DH + 8];  // many-query attention: the unit's query tiles (bf16 or fp16)
     } a;
   } u;
-  float rope[MTMAX * 16][DH / 2][2];  // rotary cos, sin of the chunk's rows
   float r[MTMAX * 16];  // RMSNorm row scales of the chunk
   float tmp[512];       // head scratch
   float red2[16][16];   // head: per-wave partial sums
@@ -254,14 +253,14 @@ __device__ __forceinline__ bool xcd_register(const TickArgs& a, TickLds& L) {
 // ------------------------------------------------------------------------------------------ staging
 // Stage rows [m0, m0+rows) x K columns (K/8 <= 64 chunks of 16 bytes) of a bf16 activation produced in this
 // launch into L.x with direct global->LDS loads (device scope; one instruction per row: lane l brings
-// columns 8l..8l+7), the rotary rows into L.rope when given, and, when ssq is given, the RMSNorm row scales
+// columns 8l..8l+7) and, when ssq is given, the RMSNorm row scales
 // r[row] = 1/sqrt(mean(h^2) + eps) from the per-16-column sums of squares ssq[tile][Ms] into L.r.  TW = 0:
 // row-major source [M][ld]; TW = 16 or 8: tile-major source [K/TW][ld = Mp][TW].  Every load is issued
 // before any is waited for; ends with a barrier.  Rows past `rows` are left as they are: an MFMA output row
 // depends only on its input row, and those rows are never stored.
 template <int TW>
 __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int rows, int K, const float* ssq, int Ms,
-                                      int Kn, float eps, TickLds& L, const float* rope = nullptr) {
+                                      int Kn, float eps, TickLds& L) {
   const int tid = tix(), wave = tid >> 6, lane = tid & 63;
   const int cpr = K / 8;  // chunks per row
   if (lane < cpr) {
@@ -274,10 +273,6 @@ __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int r
       off = ((int64_t)lane * ld + m0) * 8;
     const int64_t row_step = TW == 0 ? ld : TW;  // elements between consecutive rows
     for (int m = wave; m < rows; m += 4) load_lds16<true>(src + off + (int64_t)m * row_step, &L.u.p.x[m][0]);
-  }
-  if (rope) {  // rows [M][DH/2][2] floats, 512 bytes: one instruction per 2 rows
-    for (int m = 2 * wave; m < rows; m += 8)
-      if (m + (lane >> 5) < rows) load_lds16<true>(rope + ((int64_t)(m0 + m) * DH + lane * 4), &L.rope[m][0][0]);
   }
   float part[MTMAX];
   const int g = tid & 15, rw = tid >> 4, ntn = Kn / 16;  // ntn <= 32
@@ -315,47 +310,33 @@ __device__ __forceinline__ void load_unit_w(const uint4* __restrict__ wtile, int
   }
 }
 
-// acc = staged x (MT row tiles, k-blocks 0..nkb-1 of the unit's range) times the unit's weights, summed over
-// the 4 waves through LDS and handed to epi(mt, C-layout values, c, grp) by wave mt % 4.  Every LDS operand is
-// read before the first MFMA, so the reads overlap instead of each MFMA waiting for its own.
-template <int MT, typename Epi>
-__device__ __forceinline__ void unit_gemm_t(const uint4 w[4], int nkb, TickLds& L, Epi epi) {
+// acc = staged x (mt_n row tiles, k-blocks 0..nkb-1 of the unit's range) times the unit's weights, summed over
+// the 4 waves through LDS and handed to epi(mt, C-layout values, c, grp) by wave mt % 4.  The row tiles are a
+// run-time loop (one copy of the code and of the epilogue, which keeps the kernel small enough for the
+// instruction cache); inside a row tile every LDS operand is read before the MFMAs.
+template <typename Epi>
+__device__ __forceinline__ void unit_gemm(const uint4 w[4], int nkb, int mt_n, TickLds& L, Epi epi) {
   const int wave = tix() >> 6, lane = tix() & 63;
   const int c = lane & 15, grp = lane >> 4;
-  uint4 xa[4][MT];
+#pragma unroll 1
+  for (int mt = 0; mt < mt_n; ++mt) {
+    uint4 xa[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if (wave + 4 * j < nkb)
+    for (int j = 0; j < 4; ++j)
+      if (wave + 4 * j < nkb) xa[j] = *reinterpret_cast<const uint4*>(&L.u.p.x[mt * 16 + c][(wave + 4 * j) * 32 + 8 * grp]);
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-        xa[j][mt] = *reinterpret_cast<const uint4*>(&L.u.p.x[mt * 16 + c][(wave + 4 * j) * 32 + 8 * grp]);
-  f32x4 acc[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if (wave + 4 * j < nkb)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[mt] = mfma_bf16(xa[j][mt], w[j], acc[mt]);
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) L.u.p.red[wave][mt][lane] = acc[mt];
+    for (int j = 0; j < 4; ++j)
+      if (wave + 4 * j < nkb) acc = mfma_bf16(xa[j], w[j], acc);
+    L.u.p.red[wave][mt][lane] = acc;
+  }
   __syncthreads();
-  for (int mt = wave; mt < MT; mt += 4) {
+#pragma unroll 1
+  for (int mt = wave; mt < mt_n; mt += 4) {
     const f32x4 s = L.u.p.red[0][mt][lane] + L.u.p.red[1][mt][lane] + L.u.p.red[2][mt][lane] + L.u.p.red[3][mt][lane];
     epi(mt, s, c, grp);
   }
   __syncthreads();
-}
-
-template <typename Epi>
-__device__ __forceinline__ void unit_gemm(const uint4 w[4], int nkb, int mt_n, TickLds& L, Epi epi) {
-  switch (mt_n) {
-    case 1: unit_gemm_t<1>(w, nkb, L, epi); break;
-    case 2: unit_gemm_t<2>(w, nkb, L, epi); break;
-    case 3: unit_gemm_t<3>(w, nkb, L, epi); break;
-    case 4: unit_gemm_t<4>(w, nkb, L, epi); break;
-    default: unit_gemm_t<5>(w, nkb, L, epi); break;
-  }
 }
 
 // One wave per projection unit: the wave holds the unit's 16-column tile for every k-block (K <= 512) in
@@ -366,13 +347,13 @@ __device__ __forceinline__ void load_unit_w_full(const uint4* __restrict__ wtile
   for (int i = 0; i < 16; ++i) w[i] = i < nkb ? ld_global(wtile + (int64_t)i * WAVE + lane) : make_uint4(0, 0, 0, 0);
 }
 
-// Per row tile: the 16 LDS operands are read first, then the MFMAs run on two accumulators (even and odd
-// k-blocks) so that consecutive MFMAs do not depend on each other.
-template <int MT, typename Epi>
-__device__ __forceinline__ void wave_gemm_t(const uint4 w[16], int nkb, TickLds& L, Epi epi) {
+// Per row tile (a run-time loop): the 16 LDS operands are read first, then the MFMAs run on two accumulators
+// (even and odd k-blocks) so that consecutive MFMAs do not depend on each other.
+template <typename Epi>
+__device__ __forceinline__ void wave_gemm(const uint4 w[16], int nkb, int mt_n, TickLds& L, Epi epi) {
   const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll 1
+  for (int mt = 0; mt < mt_n; ++mt) {
     uint4 xa[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i)
@@ -384,17 +365,6 @@ __device__ __forceinline__ void wave_gemm_t(const uint4 w[16], int nkb, TickLds&
       if (i + 1 < nkb) acc1 = mfma_bf16(xa[i + 1], w[i + 1], acc1);
     }
     epi(mt, acc0 + acc1, c, grp);
-  }
-}
-
-template <typename Epi>
-__device__ __forceinline__ void wave_gemm(const uint4 w[16], int nkb, int mt_n, TickLds& L, Epi epi) {
-  switch (mt_n) {
-    case 1: wave_gemm_t<1>(w, nkb, L, epi); break;
-    case 2: wave_gemm_t<2>(w, nkb, L, epi); break;
-    case 3: wave_gemm_t<3>(w, nkb, L, epi); break;
-    case 4: wave_gemm_t<4>(w, nkb, L, epi); break;
-    default: wave_gemm_t<5>(w, nkb, L, epi); break;
   }
 }
 
@@ -563,7 +533,7 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
     const int nl0 = h * DH + t * 16;  // first column of the unit inside its section
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      stage<16>(xb, tp.Mp, m0, rows, d, ssq, tp.Ms, d, dm.eps, L, rope);
+      stage<16>(xb, tp.Mp, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
       TICK_SUB(l, 2);
       if (mine) {
         wave_gemm(w, KB, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
@@ -581,13 +551,21 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
             const int p = nl % DH;
             const int j = 8 * (p / 16) + (c & 7);
             const int dch = c < 8 ? j : half + j;
+            // cos, sin of the 4 rows of this lane (rotary table [M][Dh/2][2]), all loaded before use
+            float2 rp[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int row = min(m0 + mt * 16 + 4 * grp + i, M - 1);
+              const uint64_t v = ld_dev(reinterpret_cast<const uint64_t*>(rope + ((int64_t)row * half + j) * 2));
+              rp[i] = make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+            }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               sacc[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
               const float partner = xor8(sacc[i]);
               const int row = m0 + mt * 16 + 4 * grp + i;
-              const float cs = L.rope[mt * 16 + 4 * grp + i][j][0];
-              const float sn = L.rope[mt * 16 + 4 * grp + i][j][1];
+              const float cs = rp[i].x;
+              const float sn = rp[i].y;
               const float r = c < 8 ? sacc[i] * cs - partner * sn : sacc[i] * cs + partner * sn;
               const int64_t o = (int64_t)row * A + h * DH + dch;
               if (sec == 0) {
@@ -893,54 +871,53 @@ __device__ __forceinline__ void merge_states(const TickArgs& a, const TickParams
   }
 }
 
-// an agent's last range merges the partials of all its ranges (fixed order) into the attention output; the
-// partials are loaded 8 ranges at a time, every load issued before any is used
-__device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickParams& tp, const Dims& dm, const AUnit& U) {
+// Query tile tt of (agent b, head h): merge the partials of its nr ranges (fixed order) into the attention output;
+// the partials are loaded 8 ranges at a time, every load issued before any is used.
+__device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickParams& tp, const Dims& dm, int b, int h,
+                                               int nr, int tt) {
   constexpr int RB = 8;
   const int t = tix() >> 4, d0 = (tix() & 15) * 8;
   const int H = dm.H;
-  for (int tt = 0; tt < tp.n_tt; ++tt) {
-    float Mx = -INFINITY, Ls = 0.f, acc[8];
+  float Mx = -INFINITY, Ls = 0.f, acc[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) acc[k] = 0.f;
-    for (int r0 = 0; r0 < U.nr; r0 += RB) {
-      float ms[RB], ls[RB];
-      float4 v0[RB], v1[RB];
+  for (int k = 0; k < 8; ++k) acc[k] = 0.f;
+  for (int r0 = 0; r0 < nr; r0 += RB) {
+    float ms[RB], ls[RB];
+    float4 v0[RB], v1[RB];
 #pragma unroll
-      for (int j = 0; j < RB; ++j) {
-        ms[j] = -INFINITY;
-        ls[j] = 0.f;
-        v0[j] = v1[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (r0 + j < U.nr) {
-          const int64_t item = ((int64_t)(tp.range_prefix[U.b] + r0 + j) * H + U.h) * tp.n_tt + tt;  // pair * n_tt + tt
-          ms[j] = ld_dev_f(a.att_ml + item * 32 + 2 * t);
-          ls[j] = ld_dev_f(a.att_ml + item * 32 + 2 * t + 1);
-          const float* po = a.att_o + (item * 16 + t) * 128 + d0;
-          v0[j] = ld_dev_f4(po);
-          v1[j] = ld_dev_f4(po + 4);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < RB; ++j) {
-        if (r0 + j < U.nr) {
-          const float mn = fmaxf(Mx, ms[j]);
-          const float fa = Mx == -INFINITY ? 0.f : exp2f(Mx - mn), fb = ms[j] == -INFINITY ? 0.f : exp2f(ms[j] - mn);
-          Ls = Ls * fa + ls[j] * fb;
-          acc[0] = acc[0] * fa + v0[j].x * fb; acc[1] = acc[1] * fa + v0[j].y * fb;
-          acc[2] = acc[2] * fa + v0[j].z * fb; acc[3] = acc[3] * fa + v0[j].w * fb;
-          acc[4] = acc[4] * fa + v1[j].x * fb; acc[5] = acc[5] * fa + v1[j].y * fb;
-          acc[6] = acc[6] * fa + v1[j].z * fb; acc[7] = acc[7] * fa + v1[j].w * fb;
-          Mx = mn;
-        }
+    for (int j = 0; j < RB; ++j) {
+      ms[j] = -INFINITY;
+      ls[j] = 0.f;
+      v0[j] = v1[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (r0 + j < nr) {
+        const int64_t item = ((int64_t)(tp.range_prefix[b] + r0 + j) * H + h) * tp.n_tt + tt;  // pair * n_tt + tt
+        ms[j] = ld_dev_f(a.att_ml + item * 32 + 2 * t);
+        ls[j] = ld_dev_f(a.att_ml + item * 32 + 2 * t + 1);
+        const float* po = a.att_o + (item * 16 + t) * 128 + d0;
+        v0[j] = ld_dev_f4(po);
+        v1[j] = ld_dev_f4(po + 4);
       }
     }
-    const int tok = tt * 16 + t;
-    if (tok < tp.S) {
-      const float inv = 1.0f / Ls;
-      uint16_t* dst = a.attn + ((int64_t)U.b * tp.S + tok) * dm.A + (int64_t)U.h * DH + d0;
-      st_loc16(dst, make_uint4(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
-                               pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv)));
+#pragma unroll
+    for (int j = 0; j < RB; ++j) {
+      if (r0 + j < nr) {
+        const float mn = fmaxf(Mx, ms[j]);
+        const float fa = Mx == -INFINITY ? 0.f : exp2f(Mx - mn), fb = ms[j] == -INFINITY ? 0.f : exp2f(ms[j] - mn);
+        Ls = Ls * fa + ls[j] * fb;
+        acc[0] = acc[0] * fa + v0[j].x * fb; acc[1] = acc[1] * fa + v0[j].y * fb;
+        acc[2] = acc[2] * fa + v0[j].z * fb; acc[3] = acc[3] * fa + v0[j].w * fb;
+        acc[4] = acc[4] * fa + v1[j].x * fb; acc[5] = acc[5] * fa + v1[j].y * fb;
+        acc[6] = acc[6] * fa + v1[j].z * fb; acc[7] = acc[7] * fa + v1[j].w * fb;
+        Mx = mn;
+      }
     }
+  }
+  const int tok = tt * 16 + t;
+  if (tok < tp.S) {
+    const float inv = 1.0f / Ls;
+    uint16_t* dst = a.attn + ((int64_t)b * tp.S + tok) * dm.A + (int64_t)h * DH + d0;
+    st_loc16(dst, make_uint4(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
+                             pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv)));
   }
 }
 
@@ -989,18 +966,16 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
     if (NQ == 1) return qr[k];
     return *reinterpret_cast<const uint4*>(&L.u.a.qs[tt * 16 + c16][32 * k + 8 * grp]);
   };
-  int i = 0;
-  for (; i + PD <= nc; i += PD) {
+#pragma unroll 1
+  for (int i = 0; i < nc; i += PD) {
 #pragma unroll
     for (int dd = 0; dd < PD; ++dd) {
-      tile_compute<KT, NQ>(ring[dd], qf, nq, U.i0 + 32 * (wave + 4 * (i + dd)), U.i1, U.ksc, o, m_run, l_run);
-      if (i + dd + PD < nc) cache_tile(i + dd + PD, ring[dd]);
+      if (i + dd < nc) {
+        tile_compute<KT, NQ>(ring[dd], qf, nq, U.i0 + 32 * (wave + 4 * (i + dd)), U.i1, U.ksc, o, m_run, l_run);
+        if (i + dd + PD < nc) cache_tile(i + dd + PD, ring[dd]);
+      }
     }
   }
-#pragma unroll
-  for (int dd = 0; dd < PD; ++dd)
-    if (i + dd < nc)
-      tile_compute<KT, NQ>(ring[dd], qf, nq, U.i0 + 32 * (wave + 4 * (i + dd)), U.i1, U.ksc, o, m_run, l_run);
   if (KT == 1) {
     // fp8 values carry their scale: apply it to the cache part of the output before the own rows join
 #pragma unroll
@@ -1040,9 +1015,9 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
 }
 
 // Attention units of XCD X: (pair q, local head j) numbered u = q * nh + j, where the pairs (agent, range) list
-// every agent's ranges but its last (agents in the planner's order) and then every agent's last range.  Workgroup
-// s takes units s, s + n, ....  A last range of an agent with several ranges waits for the others and merges
-// them; since all such units come after all the others in every workgroup's list, the waits cannot form a cycle.
+// every agent's ranges but its last (agents in the planner's order) and then every agent's last range (which also
+// covers the expert's own rows).  Workgroup s takes units s, s + n, ....  An agent with one range gets its
+// normalised output directly; otherwise every range writes a partial and separate merge items combine them.
 template <int KT>
 __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   constexpr int ES = KT == 0 ? 2 : 1;
@@ -1086,32 +1061,38 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
     }
     bool ok = true;
     if (n_tt == 1) {
-      ok = attn_unit<KT, 1, KT == 0 ? 3 : 4>(a, tp, dm, l, U, 0, 1, L);
+      ok = attn_unit<KT, 1, KT == 0 ? 2 : 4>(a, tp, dm, l, U, 0, 1, L);
     } else {
       for (int tt0 = 0; tt0 < n_tt && ok; tt0 += NQW)
         ok = attn_unit<KT, NQW, 2>(a, tp, dm, l, U, tt0, min(NQW, n_tt - tt0), L);
     }
     if (!ok) return false;
     if (first) TICK_SUB(l, 5);
-    const int64_t pair0 = (int64_t)tp.range_prefix[b] * H;
-    if (U.nr > 1) {
-      stores_done();
-      __syncthreads();
-      if (U.r < U.nr - 1) {
-        if (tix() == 0) st_loc(a.f_rng + (pair0 + (int64_t)U.r * H + h) * FPAD, st);
-      } else {
-        // the other ranges of (b, h): pairs pair0 + r * H + h, r < nr - 1
-        if (!wg_wait(a.f_rng + (pair0 + h) * FPAD, U.nr - 1, st, a, L, 1, H)) return false;
-        combine_ranges(a, tp, dm, U);
-      }
-    }
-    if (U.r == U.nr - 1) {
-      stores_done();
-      __syncthreads();
-      if (tix() == 0) st_loc(a.f_attn + ((int64_t)b * H + h) * FPAD, st);
+    stores_done();
+    __syncthreads();
+    if (tix() == 0) {
+      if (U.nr > 1)
+        st_loc(a.f_rng + ((int64_t)(tp.range_prefix[b] + U.r) * H + h) * FPAD, st);
+      else
+        for (int tt = 0; tt < n_tt; ++tt) st_loc(a.f_attn + (((int64_t)b * H + h) * n_tt + tt) * FPAD, st);
     }
     if (first) TICK_SUB(l, 6);
     first = false;
+    __syncthreads();
+  }
+  // Merges of agents with several ranges: one item per (agent, head, query tile), after every range unit of this
+  // workgroup (range units never wait for merges, so these waits cannot form a cycle).
+  const int n_items = B * nh * n_tt;
+  for (int it = s; it < n_items; it += n) {
+    const int tt = it % n_tt, j = (it / n_tt) % nh, k = it / (n_tt * nh);
+    const int b = tp.order[k], h = h0 + j;
+    const int nr = tp.range_prefix[b + 1] - tp.range_prefix[b];
+    if (nr == 1) continue;
+    if (!wg_wait(a.f_rng + ((int64_t)tp.range_prefix[b] * H + h) * FPAD, nr, st, a, L, 1, H)) return false;
+    combine_ranges(a, tp, dm, b, h, nr, tt);
+    stores_done();
+    __syncthreads();
+    if (tix() == 0) st_loc(a.f_attn + (((int64_t)b * H + h) * n_tt + tt) * FPAD, st);
     __syncthreads();
   }
   return true;
@@ -1133,7 +1114,9 @@ __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams&
   for (int i = s; i < nt; i += n) {
     uint4 w[4];
     load_unit_w(W.wo + (int64_t)i * (A / 32) * WAVE, kb0, nkb, w);
-    if (nh > 0 && !wg_wait(a.f_attn + (int64_t)h0 * FPAD, tp.B * nh, st, a, L, nh, H)) return false;
+    if (nh > 0 && !wg_wait(a.f_attn + (int64_t)h0 * tp.n_tt * FPAD, tp.B * nh * tp.n_tt, st, a, L, nh * tp.n_tt,
+                           H * tp.n_tt))
+      return false;
     if (first) TICK_SUB(l, 7);
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
