@@ -249,7 +249,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
     ex->nx = nx;
     const int nh_max = nx > 0 ? (H + nx - 1) / nx : 1 << 30;
     const int fr_max = nx > 0 ? 32 * ((F / 32 + nx - 1) / nx) : 1 << 30;
-    ex->tick = nx > 0 && nx <= NXMAX && ex->cu_count <= XFLAGS && d <= 512 && d % 32 == 0 && F % 32 == 0 && nh_max <= 4 && fr_max <= 512 &&
+    ex->tick = nx > 0 && nx <= NXR && c.n_layers <= SCHED_STRIDE && ex->cu_count <= XFLAGS && d <= 512 && d % 32 == 0 && F % 32 == 0 && nh_max <= 4 && fr_max <= 512 &&
                c.n_expert_tokens <= 64;
   }
   if (ex->tick) {
@@ -284,6 +284,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
         {(void**)&t.f_attn, (size_t)nflag_attn * n_tt_max * FPAD * 8},
         {(void**)&t.f_rng, (size_t)ex->items_max * FPAD * 8},
         {(void**)&t.f_z, (size_t)F / 8 * FPAD * 8},
+        {(void**)&t.sched, (size_t)NXMAX * SCHED_STRIDE * 4},
         {(void**)&t.status, 256}};
     parts.insert(parts.end(), tp.begin(), tp.end());
   }

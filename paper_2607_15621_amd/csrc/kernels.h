@@ -102,8 +102,10 @@ hipError_t launch_head(const TickParams& tp, const Dims& dm, const Workspace& ws
 // replica per XCD rank (at most NXMAX); the others are indexed by head or FFN unit, so each of their
 // cache lines is written and read by one XCD only.
 constexpr int NXMAX = 16;
+constexpr int NXR = 8;      // XCDs the cross-XCD reductions read at most (the XCD count of gfx950 parts)
 constexpr int FPAD = 16;     // flags are 64-bit stamps, one per 128-byte line (index * FPAD)
 constexpr int XFLAGS = 512;  // flag slots per XCD of the per-XCD flag arrays
+constexpr int SCHED_STRIDE = 256;  // per-XCD attention unit counters: [NXMAX][SCHED_STRIDE] (n_layers <= 256)
 
 struct TickArgs {
   const char* wbase;   // packed weights of layer 0; layers follow back to back (see layer_w)
@@ -146,6 +148,7 @@ struct TickArgs {
   uint64_t* f_attn;    // [B*H][n_tt] per query tile
   uint64_t* f_rng;     // [range pairs]
   uint64_t* f_z;       // [F/8]
+  uint32_t* sched;     // [NXMAX][SCHED_STRIDE] attention unit counters per XCD and layer
   uint64_t* status;
   uint64_t epoch;
   uint64_t timeout_ticks;  // real-time counter ticks (100 MHz)

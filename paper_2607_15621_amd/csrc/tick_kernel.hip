@@ -65,12 +65,14 @@ struct TickLds {
       uint16_t qs[NQW * 16][DH + 8];  // many-query attention: the unit's query tiles (bf16 or fp16)
     } a;
   } u;
+  float rq[4][MTMAX * 16][8][2];  // q/k projection: each wave's rotary slice (cos, sin of its 8 pairs) per row
   float r[MTMAX * 16];  // RMSNorm row scales of the chunk
   float tmp[512];       // head scratch
   float red2[16][16];   // head: per-wave partial sums
   float hr[64];         // head: row scales of the pooled tokens (at most 64)
   int ok;
   int X, s, n, NX, n0;  // XCD rank, slot in the XCD, workgroups of the XCD, XCDs, workgroups of XCD 0
+  int next;             // attention: the workgroup's next unit
 };
 
 __device__ __forceinline__ uint64_t stamp_of(const TickArgs& a, int layer, int n_layers) {
@@ -119,12 +121,13 @@ __device__ __forceinline__ bool wave_wait(const uint64_t* flags, int n, uint64_t
   return true;
 }
 
-// Workgroup-level wait: wave 0 polls, the others wait at a barrier.
+// Workgroup-level wait: wave `pw` polls, the others wait at a barrier.  Loads return in issue order, so the polling
+// wave should have no long loads in flight.
 __device__ __forceinline__ bool wg_wait(const uint64_t* flags, int n, uint64_t target, const TickArgs& a, TickLds& L,
-                                        int inner = 1 << 30, int stride = 0) {
-  if (tix() < WAVE) {
+                                        int inner = 1 << 30, int stride = 0, int pw = 0) {
+  if ((tix() >> 6) == pw) {
     const bool ok = wave_wait(flags, n, target, a, inner, stride);
-    if (tix() == 0) L.ok = ok;
+    if ((tix() & 63) == 0) L.ok = ok;
   }
   __syncthreads();
   const bool ok = L.ok;
@@ -239,7 +242,7 @@ __device__ __forceinline__ bool xcd_register(const TickArgs& a, TickLds& L) {
         L.n = n;
         L.NX = NX;
         L.n0 = n0;
-        if (NX > NXMAX) ok = false;
+        if (NX > NXR) ok = false;
       }
     }
     if (lane == 0) L.ok = ok;
@@ -374,7 +377,7 @@ __device__ __forceinline__ void wave_gemm(const uint4 w[16], int nkb, int mt_n, 
 // k < EB); all of its words are loaded before any is checked, then it polls its own stale words until their
 // stamps are right.  The new tile goes to hres (owner-private), to the bf16 tile-major copy xb and the per-row
 // sums of squares ssq (read by the whole XCD), and, if given, to hidden; then the tile's flag is published.
-constexpr int EB = 2;  // element batches per pass: M <= 32 rows in one pass
+constexpr int EB = 4;  // element batches per pass: M <= 64 rows in one pass
 __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, int i,
                                             const uint64_t* part, uint16_t* xb, float* ssq, uint64_t* flag,
                                             float* hidden_l, TickLds& L) {
@@ -385,7 +388,7 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
   const int64_t xs = (int64_t)nt * tp.Mp * 16;  // words between the partials of two XCDs
   bool ok = true;
   for (int e0 = 0; e0 < M * 16 && ok; e0 += EB * NTHR) {
-    uint64_t v[EB][NXMAX];
+    uint64_t v[EB][NXR];
     float hold[EB];
 #pragma unroll
     for (int k = 0; k < EB; ++k) {
@@ -393,15 +396,15 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
       const bool in = e < M * 16;
       const uint64_t* src = part + (int64_t)i * tp.Mp * 16 + e;
 #pragma unroll
-      for (int x = 0; x < NXMAX; ++x) v[k][x] = (x < NX && in) ? ld_dev(src + x * xs) : ((uint64_t)st32 << 32);
+      for (int x = 0; x < NXR; ++x) v[k][x] = (x < NX && in) ? ld_dev(src + x * xs) : ((uint64_t)st32 << 32);
       hold[k] = in ? hres[e] : 0.f;
     }
     uint32_t pending = 0;
 #pragma unroll
     for (int k = 0; k < EB; ++k)
 #pragma unroll
-      for (int x = 0; x < NXMAX; ++x)
-        if ((uint32_t)(v[k][x] >> 32) != st32) pending |= 1u << (k * NXMAX + x);
+      for (int x = 0; x < NXR; ++x)
+        if ((uint32_t)(v[k][x] >> 32) != st32) pending |= 1u << (k * NXR + x);
     if (pending) {
       const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
       for (uint32_t spin = 0; pending; ++spin) {
@@ -410,14 +413,14 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
         for (int k = 0; k < EB; ++k) {
           const uint64_t* src = part + (int64_t)i * tp.Mp * 16 + e0 + k * NTHR + tix();
 #pragma unroll
-          for (int x = 0; x < NXMAX; ++x)
-            if (pending & (1u << (k * NXMAX + x))) v[k][x] = ld_dev(src + x * xs);
+          for (int x = 0; x < NXR; ++x)
+            if (pending & (1u << (k * NXR + x))) v[k][x] = ld_dev(src + x * xs);
         }
 #pragma unroll
         for (int k = 0; k < EB; ++k)
 #pragma unroll
-          for (int x = 0; x < NXMAX; ++x)
-            if ((uint32_t)(v[k][x] >> 32) == st32) pending &= ~(1u << (k * NXMAX + x));
+          for (int x = 0; x < NXR; ++x)
+            if ((uint32_t)(v[k][x] >> 32) == st32) pending &= ~(1u << (k * NXR + x));
         if (pending && timed_out(a, t0, spin)) {
           st_dev(a.status, fail_tag(a));
           ok = false;
@@ -432,7 +435,7 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
       const int m = e >> 4, c = e & 15;
       float acc = 0.f;
 #pragma unroll
-      for (int x = 0; x < NXMAX; ++x)
+      for (int x = 0; x < NXR; ++x)
         if (x < NX) acc += __uint_as_float((uint32_t)v[k][x]);
       const float hv = hold[k] + acc;
       if (in) {
@@ -491,6 +494,10 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
       st_loc_f(rope + ((int64_t)m * half + j) * 2 + 1, (float)sn);
     }
   }
+  // the XCD's per-layer attention unit counters start at zero (read only after layer 0's projections, which wait
+  // for this flag)
+  if (s == 0)
+    for (int i = tix(); i < dm.n_layers; i += NTHR) st_loc(a.sched + (int64_t)X * SCHED_STRIDE + i, 0u);
   stores_done();
   __syncthreads();
   if (tix() == 0) st_loc(a.f_rope + ((int64_t)X * XFLAGS + s) * FPAD, st);
@@ -533,6 +540,14 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
     const int nl0 = h * DH + t * 16;  // first column of the unit inside its section
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
+      // this wave's rotary slice: rope[row][8t .. 8t+7][2] (64 bytes per row), 16 rows per direct load
+      if (mine && sec < 2) {
+        const int ln = tix() & 63;
+        for (int r0 = 0; r0 < rows; r0 += 16) {
+          const int row = min(m0 + r0 + (ln >> 2), M - 1);
+          load_lds16<true>(rope + ((int64_t)row * half + 8 * t) * 2 + (ln & 3) * 4, &L.rq[wave][r0][0][0]);
+        }
+      }
       stage<16>(xb, tp.Mp, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
       TICK_SUB(l, 2);
       if (mine) {
@@ -551,21 +566,13 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
             const int p = nl % DH;
             const int j = 8 * (p / 16) + (c & 7);
             const int dch = c < 8 ? j : half + j;
-            // cos, sin of the 4 rows of this lane (rotary table [M][Dh/2][2]), all loaded before use
-            float2 rp[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int row = min(m0 + mt * 16 + 4 * grp + i, M - 1);
-              const uint64_t v = ld_dev(reinterpret_cast<const uint64_t*>(rope + ((int64_t)row * half + j) * 2));
-              rp[i] = make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
-            }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               sacc[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
               const float partner = xor8(sacc[i]);
               const int row = m0 + mt * 16 + 4 * grp + i;
-              const float cs = rp[i].x;
-              const float sn = rp[i].y;
+              const float cs = L.rq[wave][mt * 16 + 4 * grp + i][c & 7][0];
+              const float sn = L.rq[wave][mt * 16 + 4 * grp + i][c & 7][1];
               const float r = c < 8 ? sacc[i] * cs - partner * sn : sacc[i] * cs + partner * sn;
               const int64_t o = (int64_t)row * A + h * DH + dch;
               if (sec == 0) {
@@ -807,6 +814,105 @@ __device__ __forceinline__ void tile_compute(const RawTile<KT>& t, QF qf, int nq
   }
 }
 
+// MFMA operands of one raw tile: K fragments kf (A operand of S^T = K Q^T) and V transposed to per-channel
+// vectors vt (B operand of O += P V); fp8 codes are decoded to fp16 (exact).
+template <int KT>
+__device__ __forceinline__ void tile_operands(const RawTile<KT>& t, uint4 (&kf)[8], uint4 (&vt)[8]) {
+  uint4 vr[8];
+  if constexpr (KT == 0) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      kf[i] = t.k[i];
+      vr[i] = t.v[i];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      kf[2 * i] = make_uint4(e4m3x2_to_f16x2(t.k[i].x, false), e4m3x2_to_f16x2(t.k[i].x, true),
+                             e4m3x2_to_f16x2(t.k[i].y, false), e4m3x2_to_f16x2(t.k[i].y, true));
+      kf[2 * i + 1] = make_uint4(e4m3x2_to_f16x2(t.k[i].z, false), e4m3x2_to_f16x2(t.k[i].z, true),
+                                 e4m3x2_to_f16x2(t.k[i].w, false), e4m3x2_to_f16x2(t.k[i].w, true));
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      vr[i] = make_uint4(e4m3x2_to_f16x2(t.v[i].x, false), e4m3x2_to_f16x2(t.v[i].x, true),
+                         e4m3x2_to_f16x2(t.v[i].y, false), e4m3x2_to_f16x2(t.v[i].y, true));
+  }
+  transpose8x8_b16(vr, vt);
+}
+
+// One query tile, two cache tiles at once (64 rows): the score MFMAs of both tiles are independent, one running-max
+// update covers both, and both P V products accumulate into the same output.  Twice the data per dependent chain
+// of the single-tile update (the wave is the only one on its SIMD, so nothing else hides that chain).
+template <int KT>
+__device__ __forceinline__ void tile_pair_compute(const RawTile<KT>& ta, const RawTile<KT>& tb, const uint4 (&q)[4],
+                                                  int ra, int rb, int i1, float kscale, f32x4 (&o)[8], float& m_run,
+                                                  float& l_run) {
+  constexpr bool F16 = KT == 1;
+  const int lane = tix() & 63, grp = lane >> 4;
+  uint4 kfa[8], vta[8], kfb[8], vtb[8];
+  tile_operands<KT>(ta, kfa, vta);
+  tile_operands<KT>(tb, kfb, vtb);
+  f32x4 s[4];  // rt 0, 1 of tile a; rt 0, 1 of tile b
+#pragma unroll
+  for (int j = 0; j < 4; ++j) s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      s[rt] = F16 ? mfma_f16(kfa[rt * 4 + k], q[k], s[rt]) : mfma_bf16(kfa[rt * 4 + k], q[k], s[rt]);
+      s[2 + rt] = F16 ? mfma_f16(kfb[rt * 4 + k], q[k], s[2 + rt]) : mfma_bf16(kfb[rt * 4 + k], q[k], s[2 + rt]);
+    }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rr = (j < 2 ? ra : rb) + 16 * (j & 1) + 4 * grp + i;
+      const float v = rr < i1 ? (KT == 1 ? s[j][i] * kscale : s[j][i]) : -INFINITY;
+      s[j][i] = v;
+      mx = fmaxf(mx, v);
+    }
+  mx = rows_max(mx);
+  const bool grow = mx > m_run + RESCALE_LOG2;
+  if (__any(grow)) {
+    const float m_new = grow ? mx : m_run;
+    const float alpha = exp2f(m_run - m_new);
+    l_run *= alpha;
+    m_run = m_new;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float a_i = shfl(alpha, 4 * grp + i);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) o[k][i] *= a_i;
+    }
+  }
+  float p[16], ps = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      p[j * 4 + i] = exp2f(s[j][i] - m_run);
+      ps += p[j * 4 + i];
+    }
+  l_run += ps;
+  uint4 pa, pb;
+  if (F16) {
+    pa = make_uint4(pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3]), pack_f16x2(p[4], p[5]), pack_f16x2(p[6], p[7]));
+    pb = make_uint4(pack_f16x2(p[8], p[9]), pack_f16x2(p[10], p[11]), pack_f16x2(p[12], p[13]), pack_f16x2(p[14], p[15]));
+  } else {
+    pa = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+    pb = make_uint4(pack_bf16x2(p[8], p[9]), pack_bf16x2(p[10], p[11]), pack_bf16x2(p[12], p[13]),
+                    pack_bf16x2(p[14], p[15]));
+  }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    o[k] = F16 ? mfma_f16(pa, vta[k], o[k]) : mfma_bf16(pa, vta[k], o[k]);
+    o[k] = F16 ? mfma_f16(pb, vtb[k], o[k]) : mfma_bf16(pb, vtb[k], o[k]);
+  }
+}
+
 // write a wave's state (o in the PV C layout, m and the lane-partial l) to LDS slot w
 __device__ __forceinline__ void state_to_lds(float* stw, const f32x4 o[8], float m_run, float l_run) {
   const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
@@ -936,12 +1042,20 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
   auto cache_tile = [&](int i, RawTile<KT>& t) {
     load_cache_tile<KT>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * (wave + 4 * i), U.i1, t);
   };
-  // the first tiles do not depend on this layer's projections: issue them before waiting
+  // The first tiles do not depend on this layer's projections: waves 0-2 issue them before waiting; wave 3 polls
+  // the q, k and v column tiles of this head (its poll would otherwise return only after its own prefetch) and
+  // issues its tiles afterwards.
+  if (wave < 3) {
 #pragma unroll
-  for (int dd = 0; dd < PD; ++dd)
-    if (dd < nc) cache_tile(dd, ring[dd]);
-  // the q, k and v column tiles of this head
-  if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16)) return false;
+    for (int dd = 0; dd < PD; ++dd)
+      if (dd < nc) cache_tile(dd, ring[dd]);
+  }
+  if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16, 3)) return false;
+  if (wave == 3) {
+#pragma unroll
+    for (int dd = 0; dd < PD; ++dd)
+      if (dd < nc) cache_tile(dd, ring[dd]);
+  }
   f32x4 o[NQ][8];
   float m_run[NQ], l_run[NQ];
 #pragma unroll
@@ -966,13 +1080,31 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
     if (NQ == 1) return qr[k];
     return *reinterpret_cast<const uint4*>(&L.u.a.qs[tt * 16 + c16][32 * k + 8 * grp]);
   };
+  if constexpr (NQ == 1 && PD % 2 == 0) {
+    // pairs of ring slots (dd, dd + 1); an odd last tile goes through the single-tile update
 #pragma unroll 1
-  for (int i = 0; i < nc; i += PD) {
+    for (int i = 0; i < nc; i += PD) {
 #pragma unroll
-    for (int dd = 0; dd < PD; ++dd) {
-      if (i + dd < nc) {
-        tile_compute<KT, NQ>(ring[dd], qf, nq, U.i0 + 32 * (wave + 4 * (i + dd)), U.i1, U.ksc, o, m_run, l_run);
-        if (i + dd + PD < nc) cache_tile(i + dd + PD, ring[dd]);
+      for (int dd = 0; dd < PD; dd += 2) {
+        if (i + dd + 1 < nc) {
+          tile_pair_compute<KT>(ring[dd], ring[dd + 1], qr, U.i0 + 32 * (wave + 4 * (i + dd)),
+                                U.i0 + 32 * (wave + 4 * (i + dd + 1)), U.i1, U.ksc, o[0], m_run[0], l_run[0]);
+          if (i + dd + PD < nc) cache_tile(i + dd + PD, ring[dd]);
+          if (i + dd + 1 + PD < nc) cache_tile(i + dd + 1 + PD, ring[dd + 1]);
+        } else if (i + dd < nc) {
+          tile_compute<KT, NQ>(ring[dd], qf, nq, U.i0 + 32 * (wave + 4 * (i + dd)), U.i1, U.ksc, o, m_run, l_run);
+        }
+      }
+    }
+  } else {
+#pragma unroll 1
+    for (int i = 0; i < nc; i += PD) {
+#pragma unroll
+      for (int dd = 0; dd < PD; ++dd) {
+        if (i + dd < nc) {
+          tile_compute<KT, NQ>(ring[dd], qf, nq, U.i0 + 32 * (wave + 4 * (i + dd)), U.i1, U.ksc, o, m_run, l_run);
+          if (i + dd + PD < nc) cache_tile(i + dd + PD, ring[dd]);
+        }
       }
     }
   }
@@ -1015,9 +1147,11 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
 }
 
 // Attention units of XCD X: (pair q, local head j) numbered u = q * nh + j, where the pairs (agent, range) list
-// every agent's ranges but its last (agents in the planner's order) and then every agent's last range (which also
-// covers the expert's own rows).  Workgroup s takes units s, s + n, ....  An agent with one range gets its
-// normalised output directly; otherwise every range writes a partial and separate merge items combine them.
+// every agent's ranges but its last (agents in the planner's order, longest ranges first) and then every agent's
+// last range (which also covers the expert's own rows).  Workgroup s starts with unit s; further units come from a
+// counter per XCD and layer (an atomic in the XCD's L2), so workgroups that finish early take more.  An agent with
+// one range gets its normalised output directly; otherwise every range writes a partial and separate merge items
+// combine them.
 template <int KT>
 __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   constexpr int ES = KT == 0 ? 2 : 1;
@@ -1028,7 +1162,11 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
   const int NF = tp.nf_prefix[B];
   const int n_units = nh * (NF + B);
   bool first = true;
-  for (int u = s; u < n_units; u += n) {
+  uint32_t* ctr = a.sched + (int64_t)X * SCHED_STRIDE + l;  // units taken beyond the first n (in this XCD's L2)
+  for (int u = s; u < n_units;) {
+    // the next unit, fetched while this one runs
+    uint32_t nxt = 0;
+    if (tix() == 0) nxt = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     const int q = u / nh, h = h0 + u % nh;
     int k = 0, r;
     if (q < NF) {
@@ -1078,6 +1216,9 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
     }
     if (first) TICK_SUB(l, 6);
     first = false;
+    if (tix() == 0) L.next = n + (int)nxt;
+    __syncthreads();
+    u = L.next;
     __syncthreads();
   }
   // Merges of agents with several ranges: one item per (agent, head, query tile), after every range unit of this
