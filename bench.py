@@ -2,6 +2,14 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
+Measurement helpers (used by the commands recorded in profiles/):
+    python bench.py --copy-calibration BYTES      plain device copies of BYTES (counter calibration)
+    python bench.py --summarize-trace DIR --workload NAME --bench-line FILE
+        writes profiles/tick_kernel_<NAME>.md from a rocprofv3 --kernel-trace --stats output directory
+    python bench.py --summarize-traffic FETCH_DIR WRITE_DIR CFETCH_DIR CWRITE_DIR --workload NAME --copy-bytes B
+        writes profiles/traffic_<NAME>.json/.md from four rocprofv3 --pmc output directories (FETCH_SIZE and
+        WRITE_SIZE of the tick, then of the calibration copy)
+
 Default workload: the full-size expert (32 layers, width 512, 32 heads x 128, SwiGLU 2048) on one agent
 with a 224-row cache per layer (a 40-frame history at 4 rows per frame plus 64 instruction rows), bf16.
 Inputs are seeded synthetic arrays, resident in HBM before the timed region.  Prints ONE JSON line.
@@ -79,6 +87,76 @@ def cpu_baseline(wl, budget_s: float = 15.0):
                       f"S={one.seq}) in {el:.1f} s"}
 
 
+def _csv_rows(d: str, suffix: str):
+    import csv
+    import glob
+    files = sorted(glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True))
+    if not files:
+        raise SystemExit(f"no *{suffix} under {d}")
+    return list(csv.DictReader(open(files[0])))
+
+
+def copy_calibration(nbytes: int, reps: int = 5):
+    """Plain device-to-device copies of nbytes (the kernel whose byte counters calibrate FETCH_SIZE/WRITE_SIZE)."""
+    import torch
+
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
+
+
+def summarize_trace(d: str, workload: str, bench_line: str, command: str):
+    """profiles/tick_kernel_<workload>.md from a rocprofv3 --kernel-trace --stats directory."""
+    rows = _csv_rows(d, "kernel_stats.csv")
+    line = json.loads(open(bench_line).read().strip().splitlines()[-1])
+    out = [f"# Kernel trace: tick kernel, workload `{workload}`", "", "Command (from the repository root, on one MI355X):",
+           "", "```", command, "```", "", "| kernel | calls | total ms | avg µs | min µs | max µs |",
+           "|---|---|---|---|---|---|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        out.append(f"| `{r['Name'][:70]}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
+                   f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    out += ["", f"bench.py line of the same run: {line['us_per_tick']} µs/tick (HIP events over {line['steps']} "
+                f"back-to-back ticks), {line['value']} agent-ticks/s, algorithmic bytes "
+                f"{line['roofline']['algorithmic_bytes_per_launch']:,} per launch, achieved "
+                f"{line['roofline']['achieved']} GB/s = {line['roofline']['frac']} of 8000 GB/s.", ""]
+    path = os.path.join(ROOT, "profiles", f"tick_kernel_{workload}.md")
+    open(path, "w").write("\n".join(out))
+    print(path)
+
+
+def summarize_traffic(dirs, workload: str, copy_bytes: int, commands):
+    """profiles/traffic_<workload>.json/.md: HBM bytes per tick-kernel launch from FETCH_SIZE / WRITE_SIZE, each
+    scaled by what the same counter reads for a plain copy of copy_bytes."""
+    def mean_counter(d, counter, pick):
+        vals = [float(r["Counter_Value"]) for r in _csv_rows(d, "counter_collection.csv")
+                if r["Counter_Name"] == counter and pick(r["Kernel_Name"])]
+        if not vals:
+            raise SystemExit(f"no {counter} rows in {d}")
+        return vals
+
+    tick = lambda n: "k_tick" in n
+    copyk = lambda n: "copy" in n.lower() or "elementwise" in n.lower()
+    f_tick = mean_counter(dirs[0], "FETCH_SIZE", tick)
+    w_tick = mean_counter(dirs[1], "WRITE_SIZE", tick)
+    f_copy = max(mean_counter(dirs[2], "FETCH_SIZE", copyk))
+    w_copy = max(mean_counter(dirs[3], "WRITE_SIZE", copyk))
+    kf, kw = copy_bytes / f_copy, copy_bytes / w_copy  # bytes per counter unit
+    fetch = sum(f_tick) / len(f_tick) * kf
+    write = sum(w_tick) / len(w_tick) * kw
+    d = {"workload": workload, "source_hash": source_hash(), "fetch_bytes_per_launch": int(fetch),
+         "write_bytes_per_launch": int(write), "bytes_per_launch": int(fetch + write),
+         "calibration": {"copy_bytes": copy_bytes, "fetch_counter": f_copy, "write_counter": w_copy,
+                         "bytes_per_fetch_unit": kf, "bytes_per_write_unit": kw},
+         "dispatches": {"fetch": len(f_tick), "write": len(w_tick)}, "commands": commands}
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    json.dump(d, open(path, "w"), indent=1)
+    print(path, json.dumps({k: d[k] for k in ("fetch_bytes_per_launch", "write_bytes_per_launch")}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -87,7 +165,22 @@ def main():
     ap.add_argument("--workload", default="single_bf16_L224")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--multi-launch", action="store_true", help="one launch per phase instead of the tick kernel")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--summarize-trace", metavar="DIR")
+    ap.add_argument("--bench-line", metavar="FILE")
+    ap.add_argument("--summarize-traffic", nargs=4, metavar="DIR")
+    ap.add_argument("--copy-bytes", type=int, default=0)
+    ap.add_argument("--command", action="append", default=[], help="command recorded in a summary")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, args.workload, args.bench_line, " && ".join(args.command))
+        return
+    if args.summarize_traffic:
+        summarize_traffic(args.summarize_traffic, args.workload, args.copy_bytes, args.command)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
