@@ -118,10 +118,11 @@ struct TickArgs {
   float* waypoints;
   float* hidden;       // optional caller buffer [n_layers][M][d]
   uint64_t* reg;       // [grid] registration words: epoch << 8 | hardware XCD id
-  // per XCD, tile-major = [d/16 column tiles][Mp rows][16 columns]
-  float* hres;         // residual stream, each tile touched only by its owner workgroup
-  uint16_t* xb_mid;    // bf16 copy of the residual after attention (input of the FFN)
-  uint16_t* xb_out;    // bf16 copy of the residual after the FFN (input of the next layer)
+  // per XCD
+  float* hres;         // residual stream, tile-major [d/16 column tiles][Mp rows][16 columns], each tile touched
+                       // only by its owner workgroup
+  uint16_t* xb_mid;    // [Mp][d] bf16 copy of the residual after attention (input of the FFN)
+  uint16_t* xb_out;    // [Mp][d] bf16 copy of the residual after the FFN (input of the next layer)
   float* ssq_mid;      // [d/16][Ms] per-tile sums of squares
   float* ssq_out;
   float* rope;         // [M][Dh/2][2] cos, sin
@@ -134,7 +135,7 @@ struct TickArgs {
   uint16_t* kself;     // [M][A]
   uint16_t* vself;     // [M][A]
   uint16_t* attn;      // [M][A]
-  uint16_t* z;         // [F/8][Mp][8] SwiGLU output
+  uint16_t* z;         // [Mp][F] SwiGLU output
   float* att_o;        // [items][16][Dh] range partials
   float* att_ml;       // [items][16][2]
   // crossing XCDs: stamped 8-byte words (payload in the low half, stamp in the high half)

@@ -254,28 +254,19 @@ __device__ __forceinline__ bool xcd_register(const TickArgs& a, TickLds& L) {
 }
 
 // ------------------------------------------------------------------------------------------ staging
-// Stage rows [m0, m0+rows) x K columns (K/8 <= 64 chunks of 16 bytes) of a bf16 activation produced in this
-// launch into L.x with direct global->LDS loads (device scope; one instruction per row: lane l brings
-// columns 8l..8l+7) and, when ssq is given, the RMSNorm row scales
-// r[row] = 1/sqrt(mean(h^2) + eps) from the per-16-column sums of squares ssq[tile][Ms] into L.r.  TW = 0:
-// row-major source [M][ld]; TW = 16 or 8: tile-major source [K/TW][ld = Mp][TW].  Every load is issued
-// before any is waited for; ends with a barrier.  Rows past `rows` are left as they are: an MFMA output row
-// depends only on its input row, and those rows are never stored.
-template <int TW>
+// Stage rows [m0, m0+rows) x K columns (K/8 <= 64 chunks of 16 bytes) of a row-major bf16 activation [M][ld]
+// produced in this launch into L.x with direct global->LDS loads (device scope; one instruction per row: lane l
+// brings columns 8l..8l+7, so an instruction reads whole 128-byte lines) and, when ssq is given, the RMSNorm row
+// scales r[row] = 1/sqrt(mean(h^2) + eps) from the per-16-column sums of squares ssq[tile][Ms] into L.r.  Every
+// load is issued before any is waited for; ends with a barrier.  Rows past `rows` are left as they are: an MFMA
+// output row depends only on its input row, and those rows are never stored.
 __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int rows, int K, const float* ssq, int Ms,
                                       int Kn, float eps, TickLds& L) {
   const int tid = tix(), wave = tid >> 6, lane = tid & 63;
   const int cpr = K / 8;  // chunks per row
   if (lane < cpr) {
-    int64_t off;  // element offset of lane's chunk in row 0 of the chunk
-    if (TW == 0)
-      off = (int64_t)m0 * ld + lane * 8;
-    else if (TW == 16)
-      off = ((int64_t)(lane >> 1) * ld + m0) * 16 + (lane & 1) * 8;
-    else
-      off = ((int64_t)lane * ld + m0) * 8;
-    const int64_t row_step = TW == 0 ? ld : TW;  // elements between consecutive rows
-    for (int m = wave; m < rows; m += 4) load_lds16<true>(src + off + (int64_t)m * row_step, &L.u.p.x[m][0]);
+    const uint16_t* row0 = src + (int64_t)m0 * ld + lane * 8;
+    for (int m = wave; m < rows; m += 4) load_lds16<true>(row0 + (int64_t)m * ld, &L.u.p.x[m][0]);
   }
   float part[MTMAX];
   const int g = tid & 15, rw = tid >> 4, ntn = Kn / 16;  // ntn <= 32
@@ -444,7 +435,7 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
       }
       const float vn = xor1(hv);
       if (in && (c & 1) == 0)
-        st_loc(reinterpret_cast<uint32_t*>(xb + ((int64_t)i * tp.Mp + m) * 16 + c), pack_bf16x2(hv, vn));
+        st_loc(reinterpret_cast<uint32_t*>(xb + (int64_t)m * dm.d + i * 16 + c), pack_bf16x2(hv, vn));
       const float sq = row_sum16(hv * hv);
       if (in && c == 0) st_loc_f(ssq + (int64_t)i * tp.Ms + m, sq);
     }
@@ -473,7 +464,7 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
       const float v = a.tok_dtype == FSX_BF16 ? bf16_to_f32(((const uint16_t*)a.tokens)[idx]) : ((const float*)a.tokens)[idx];
       hres[(int64_t)i * tp.Mp * 16 + e] = v;
       const float vn = xor1(v);
-      if ((c & 1) == 0) st_loc(reinterpret_cast<uint32_t*>(xb + ((int64_t)i * tp.Mp + m) * 16 + c), pack_bf16x2(v, vn));
+      if ((c & 1) == 0) st_loc(reinterpret_cast<uint32_t*>(xb + (int64_t)m * d + i * 16 + c), pack_bf16x2(v, vn));
       const float sq = row_sum16(v * v);
       if (c == 0) st_loc_f(ssq + (int64_t)i * tp.Ms + m, sq);
     }
@@ -548,7 +539,7 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
           load_lds16<true>(rope + ((int64_t)row * half + 8 * t) * 2 + (ln & 3) * 4, &L.rq[wave][r0][0][0]);
         }
       }
-      stage<16>(xb, tp.Mp, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
+      stage(xb, d, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
       TICK_SUB(l, 2);
       if (mine) {
         wave_gemm(w, KB, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
@@ -1205,7 +1196,7 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
         ok = attn_unit<KT, NQW, 2>(a, tp, dm, l, U, tt0, min(NQW, n_tt - tt0), L);
     }
     if (!ok) return false;
-    if (first) TICK_SUB(l, 5);
+    if (first) TICK_SUB(l, 4);
     stores_done();
     __syncthreads();
     if (tix() == 0) {
@@ -1214,7 +1205,6 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
       else
         for (int tt = 0; tt < n_tt; ++tt) st_loc(a.f_attn + (((int64_t)b * H + h) * n_tt + tt) * FPAD, st);
     }
-    if (first) TICK_SUB(l, 6);
     first = false;
     if (tix() == 0) L.next = n + (int)nxt;
     __syncthreads();
@@ -1258,10 +1248,10 @@ __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams&
     if (nh > 0 && !wg_wait(a.f_attn + (int64_t)h0 * tp.n_tt * FPAD, tp.B * nh * tp.n_tt, st, a, L, nh * tp.n_tt,
                            H * tp.n_tt))
       return false;
-    if (first) TICK_SUB(l, 7);
+    if (first) TICK_SUB(l, 5);
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      if (nh > 0) stage<0>(a.attn + h0 * DH, A, m0, rows, nh * DH, nullptr, 0, 0, 0.f, L);
+      if (nh > 0) stage(a.attn + h0 * DH, A, m0, rows, nh * DH, nullptr, 0, 0, 0.f, L);
       unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -1271,11 +1261,10 @@ __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams&
         }
       });
     }
-    if (first) TICK_SUB(l, 8);
+    if (first) TICK_SUB(l, 6);
     if (!reduce_tile(a, tp, dm, l, i, a.po, a.xb_mid + (int64_t)X * a.x_stride_b, a.ssq_mid + (int64_t)X * a.x_stride_s,
                      a.f_mid + (int64_t)X * XFLAGS * FPAD, nullptr, L))
       return false;
-    if (first) TICK_SUB(l, 9);
     first = false;
   }
   return true;
@@ -1302,10 +1291,11 @@ __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams
     if (!waited) {
       if (!wg_wait(a.f_mid + (int64_t)X * XFLAGS * FPAD, nt, st, a, L)) return false;
       waited = true;
+      TICK_SUB(l, 7);
     }
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      stage<16>(xb, tp.Mp, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
+      stage(xb, d, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
       unit_gemm(w, KB, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -1316,10 +1306,11 @@ __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams
           const float zn = xor1(zz);
           const int row = m0 + mt * 16 + 4 * grp + r;
           if (c < 8 && (c & 1) == 0 && row < M)
-            st_loc(reinterpret_cast<uint32_t*>(a.z + ((int64_t)u * tp.Mp + row) * 8 + c), pack_bf16x2(zz, zn));
+            st_loc(reinterpret_cast<uint32_t*>(a.z + (int64_t)row * F + u * 8 + c), pack_bf16x2(zz, zn));
         }
       });
     }
+    if (k == s) TICK_SUB(l, 8);
     stores_done();
     __syncthreads();
     if (tix() == 0) st_loc(a.f_z + (int64_t)u * FPAD, st);
@@ -1342,9 +1333,10 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
     uint4 w[4];
     load_unit_w(W.wd + (int64_t)i * (F / 32) * WAVE, kb0, nkb, w);
     if (nkb > 0 && !wg_wait(a.f_z + (int64_t)(f0 / 8) * FPAD, (f1 - f0) / 8, st, a, L)) return false;
+    if (i == s) TICK_SUB(l, 9);
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      if (nkb > 0) stage<8>(a.z + (int64_t)(f0 / 8) * tp.Mp * 8, tp.Mp, m0, rows, f1 - f0, nullptr, 0, 0, 0.f, L);
+      if (nkb > 0) stage(a.z + f0, F, m0, rows, f1 - f0, nullptr, 0, 0, 0.f, L);
       unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -1354,6 +1346,7 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
         }
       });
     }
+    if (i == s) TICK_SUB(l, 10);
     if (!reduce_tile(a, tp, dm, l, i, a.pd, a.xb_out + (int64_t)X * a.x_stride_b, a.ssq_out + (int64_t)X * a.x_stride_s,
                      a.f_out + (int64_t)X * XFLAGS * FPAD, hidden_l, L))
       return false;
