@@ -66,7 +66,7 @@ struct TickLds {
     } a;
   } u;
   float rq[4][MTMAX * 16][8][2];  // q/k projection: each wave's rotary slice (cos, sin of its 8 pairs) per row
-  float r[MTMAX * 16];  // RMSNorm row scales of the chunk
+  alignas(16) float r[MTMAX * 16];  // RMSNorm row scales of the chunk
   float tmp[512];       // head scratch
   float red2[16][16];   // head: per-wave partial sums
   float hr[64];         // head: row scales of the pooled tokens (at most 64)
@@ -256,43 +256,95 @@ __device__ __forceinline__ bool xcd_register(const TickArgs& a, TickLds& L) {
 // ------------------------------------------------------------------------------------------ staging
 // Stage rows [m0, m0+rows) x K columns (K/8 <= 64 chunks of 16 bytes) of a row-major bf16 activation [M][ld]
 // produced in this launch into L.x with direct global->LDS loads (device scope; one instruction per row: lane l
-// brings columns 8l..8l+7, so an instruction reads whole 128-byte lines) and, when ssq is given, the RMSNorm row
-// scales r[row] = 1/sqrt(mean(h^2) + eps) from the per-16-column sums of squares ssq[tile][Ms] into L.r.  Every
-// load is issued before any is waited for; ends with a barrier.  Rows past `rows` are left as they are: an MFMA
-// output row depends only on its input row, and those rows are never stored.
+// brings columns 8l..8l+7, so an instruction reads whole 128-byte lines), columns K..511 set to zero, and, when
+// ssq is given, the RMSNorm row scales r[row] = 1/sqrt(mean(h^2) + eps) from the per-16-column sums of squares
+// ssq[tile][Ms] into L.r.  extra() issues the caller's own direct loads after the sums of squares (a register load
+// issued after direct loads made the compiler wait for those first).  Every load is issued before any is waited
+// for; ends with a barrier.  Rows past `rows` are left as they are: an MFMA output row depends only on its input
+// row, and those rows are never stored.
+struct NoLoads {
+  __device__ void operator()() const {}
+};
+template <typename Extra = NoLoads>
 __device__ __forceinline__ void stage(const uint16_t* src, int ld, int m0, int rows, int K, const float* ssq, int Ms,
-                                      int Kn, float eps, TickLds& L) {
+                                      int Kn, float eps, TickLds& L, Extra extra = Extra()) {
   const int tid = tix(), wave = tid >> 6, lane = tid & 63;
   const int cpr = K / 8;  // chunks per row
-  if (lane < cpr) {
-    const uint16_t* row0 = src + (int64_t)m0 * ld + lane * 8;
-    for (int m = wave; m < rows; m += 4) load_lds16<true>(row0 + (int64_t)m * ld, &L.u.p.x[m][0]);
-  }
-  float part[MTMAX];
+  // the sums of squares first: loads complete in issue order, so these arrive while the rows are in flight
   const int g = tid & 15, rw = tid >> 4, ntn = Kn / 16;  // ntn <= 32
+  float s0[MTMAX], s1[MTMAX];
   if (ssq) {
 #pragma unroll
     for (int p = 0; p < MTMAX; ++p) {
       const int i = rw + 16 * p;
-      float s0 = 0.f, s1 = 0.f;
-      if (i < rows) {
-        if (g < ntn) s0 = ld_dev_f(ssq + (int64_t)g * Ms + m0 + i);
-        if (g + 16 < ntn) s1 = ld_dev_f(ssq + (int64_t)(g + 16) * Ms + m0 + i);
-      }
-      part[p] = s0 + s1;
-    }
-#pragma unroll
-    for (int p = 0; p < MTMAX; ++p) {
-      const float s = row_sum16(part[p]);
-      const int i = rw + 16 * p;
-      if (g == 0) L.r[i] = i < rows ? 1.0f / sqrtf(s / (float)Kn + eps) : 0.f;
+      s0[p] = i < rows && g < ntn ? ld_dev_f(ssq + (int64_t)g * Ms + m0 + i) : 0.f;
+      s1[p] = i < rows && g + 16 < ntn ? ld_dev_f(ssq + (int64_t)(g + 16) * Ms + m0 + i) : 0.f;
     }
   }
-  vm_wait_all();  // the direct loads (and any weight loads issued earlier) are complete
+  extra();  // the caller's own direct loads
+  if (lane < cpr) {
+    const uint16_t* row0 = src + (int64_t)m0 * ld + lane * 8;
+    for (int m = wave; m < rows; m += 4) load_lds16<true>(row0 + (int64_t)m * ld, &L.u.p.x[m][0]);
+  } else {
+    for (int m = wave; m < rows; m += 4) *reinterpret_cast<uint4*>(&L.u.p.x[m][lane * 8]) = make_uint4(0, 0, 0, 0);
+  }
+  vm_wait_all();  // every load above (and any weight loads issued earlier) is complete
+  if (ssq) {
+#pragma unroll
+    for (int p = 0; p < MTMAX; ++p) {
+      const float sum = row_sum16(s0[p] + s1[p]);
+      const int i = rw + 16 * p;
+      if (g == 0) L.r[i] = i < rows ? 1.0f / sqrtf(sum / (float)Kn + eps) : 0.f;
+    }
+  }
   __syncthreads();
 }
 
 // ------------------------------------------------------------------------------------------ projections
+// LDS operand reads of a projection row tile: every read is issued before one wait.  Written as one asm block
+// (which waits for its own reads) because the compiler, short of registers in this kernel, otherwise reuses one
+// register quad for all of them and waits after each read, which serialises their latencies.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+// x[i] = 16 bytes at p + 64 i, i < 16
+__device__ __forceinline__ void lds_read_16x64(const void* p, u32x4_t (&x)[16]) {
+  asm volatile(
+      "ds_read_b128 %0, %16 offset:0\n\t"
+      "ds_read_b128 %1, %16 offset:64\n\t"
+      "ds_read_b128 %2, %16 offset:128\n\t"
+      "ds_read_b128 %3, %16 offset:192\n\t"
+      "ds_read_b128 %4, %16 offset:256\n\t"
+      "ds_read_b128 %5, %16 offset:320\n\t"
+      "ds_read_b128 %6, %16 offset:384\n\t"
+      "ds_read_b128 %7, %16 offset:448\n\t"
+      "ds_read_b128 %8, %16 offset:512\n\t"
+      "ds_read_b128 %9, %16 offset:576\n\t"
+      "ds_read_b128 %10, %16 offset:640\n\t"
+      "ds_read_b128 %11, %16 offset:704\n\t"
+      "ds_read_b128 %12, %16 offset:768\n\t"
+      "ds_read_b128 %13, %16 offset:832\n\t"
+      "ds_read_b128 %14, %16 offset:896\n\t"
+      "ds_read_b128 %15, %16 offset:960\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3]), "=&v"(x[4]), "=&v"(x[5]), "=&v"(x[6]), "=&v"(x[7]), "=&v"(x[8]), "=&v"(x[9]), "=&v"(x[10]), "=&v"(x[11]), "=&v"(x[12]), "=&v"(x[13]), "=&v"(x[14]), "=&v"(x[15])
+      : "v"(lds_addr(p))
+      : "memory");
+}
+// x[j] = 16 bytes at p + 256 j, j < 4
+__device__ __forceinline__ void lds_read_4x256(const void* p, u32x4_t (&x)[4]) {
+  asm volatile(
+      "ds_read_b128 %0, %4 offset:0\n\t"
+      "ds_read_b128 %1, %4 offset:256\n\t"
+      "ds_read_b128 %2, %4 offset:512\n\t"
+      "ds_read_b128 %3, %4 offset:768\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3])
+      : "v"(lds_addr(p))
+      : "memory");
+}
+__device__ __forceinline__ uint4 as_u4(u32x4_t v) { return make_uint4(v.x, v.y, v.z, v.w); }
+
 // A projection unit is one 16-column tile over a range of nkb <= 16 k-blocks; wave w owns the unit's
 // k-blocks i = w, w+4, w+8, w+12, whose 1 KiB weight blocks it holds in registers.
 __device__ __forceinline__ void load_unit_w(const uint4* __restrict__ wtile, int kb0, int nkb, uint4 w[4]) {
@@ -307,21 +359,23 @@ __device__ __forceinline__ void load_unit_w(const uint4* __restrict__ wtile, int
 // acc = staged x (mt_n row tiles, k-blocks 0..nkb-1 of the unit's range) times the unit's weights, summed over
 // the 4 waves through LDS and handed to epi(mt, C-layout values, c, grp) by wave mt % 4.  The row tiles are a
 // run-time loop (one copy of the code and of the epilogue, which keeps the kernel small enough for the
-// instruction cache); inside a row tile every LDS operand is read before the MFMAs.
+// instruction cache); inside a row tile every LDS operand is read before the MFMAs.  The k-blocks past nkb
+// multiply zero weights by the zero columns stage() leaves there, so the loop has no branches (a branch per
+// k-block makes the compiler wait for each LDS read before issuing the next).
 template <typename Epi>
 __device__ __forceinline__ void unit_gemm(const uint4 w[4], int nkb, int mt_n, TickLds& L, Epi epi) {
   const int wave = tix() >> 6, lane = tix() & 63;
   const int c = lane & 15, grp = lane >> 4;
+  const bool any = nkb > 0;  // nothing staged otherwise
 #pragma unroll 1
   for (int mt = 0; mt < mt_n; ++mt) {
-    uint4 xa[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (wave + 4 * j < nkb) xa[j] = *reinterpret_cast<const uint4*>(&L.u.p.x[mt * 16 + c][(wave + 4 * j) * 32 + 8 * grp]);
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (any) {
+      u32x4_t xa[4];
+      lds_read_4x256(&L.u.p.x[mt * 16 + c][wave * 32 + 8 * grp], xa);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (wave + 4 * j < nkb) acc = mfma_bf16(xa[j], w[j], acc);
+      for (int j = 0; j < 4; ++j) acc = mfma_bf16(as_u4(xa[j]), w[j], acc);
+    }
     L.u.p.red[wave][mt][lane] = acc;
   }
   __syncthreads();
@@ -342,21 +396,20 @@ __device__ __forceinline__ void load_unit_w_full(const uint4* __restrict__ wtile
 }
 
 // Per row tile (a run-time loop): the 16 LDS operands are read first, then the MFMAs run on two accumulators
-// (even and odd k-blocks) so that consecutive MFMAs do not depend on each other.
+// (even and odd k-blocks) so that consecutive MFMAs do not depend on each other.  As in unit_gemm, k-blocks past
+// the staged width multiply zeros, without branches.
 template <typename Epi>
-__device__ __forceinline__ void wave_gemm(const uint4 w[16], int nkb, int mt_n, TickLds& L, Epi epi) {
+__device__ __forceinline__ void wave_gemm(const uint4 w[16], int mt_n, TickLds& L, Epi epi) {
   const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
 #pragma unroll 1
   for (int mt = 0; mt < mt_n; ++mt) {
-    uint4 xa[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (i < nkb) xa[i] = *reinterpret_cast<const uint4*>(&L.u.p.x[mt * 16 + c][i * 32 + 8 * grp]);
+    u32x4_t xa[16];
+    lds_read_16x64(&L.u.p.x[mt * 16 + c][8 * grp], xa);
     f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
 #pragma unroll
     for (int i = 0; i < 16; i += 2) {
-      if (i < nkb) acc0 = mfma_bf16(xa[i], w[i], acc0);
-      if (i + 1 < nkb) acc1 = mfma_bf16(xa[i + 1], w[i + 1], acc1);
+      acc0 = mfma_bf16(as_u4(xa[i]), w[i], acc0);
+      acc1 = mfma_bf16(as_u4(xa[i + 1]), w[i + 1], acc1);
     }
     epi(mt, acc0 + acc1, c, grp);
   }
@@ -366,7 +419,7 @@ __device__ __forceinline__ void wave_gemm(const uint4 w[16], int nkb, int mt_n, 
 // Column tile i of the residual, in the owner workgroup of XCD X: h[m][i] += sum over XCDs x (fixed order)
 // of part[x][i][m][:], where part holds stamped words.  Thread t owns the elements e = t + 256 k (e = m*16 + c,
 // k < EB); all of its words are loaded before any is checked, then it polls its own stale words until their
-// stamps are right.  The new tile goes to hres (owner-private), to the bf16 tile-major copy xb and the per-row
+// stamps are right.  The new tile goes to hres (owner-private), to the row-major bf16 copy xb and the per-row
 // sums of squares ssq (read by the whole XCD), and, if given, to hidden; then the tile's flag is published.
 constexpr int EB = 4;  // element batches per pass: M <= 64 rows in one pass
 __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, int i,
@@ -501,7 +554,7 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
 __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
   const int d = dm.d, M = tp.M, A = dm.A, H = dm.H, half = DH / 2, nt = d / 16;
-  const int wave = tix() >> 6;
+  const int wave = uni(tix() >> 6);  // scalar, so the unit's section is a uniform branch
   const int h0 = head_lo(X, NX, H), nh = head_lo(X + 1, NX, H) - h0;
   const int n_units = 24 * nh;
   const LayerW W = layer_w(a, dm, l);
@@ -532,39 +585,43 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
     for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
       const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
       // this wave's rotary slice: rope[row][8t .. 8t+7][2] (64 bytes per row), 16 rows per direct load
-      if (mine && sec < 2) {
-        const int ln = tix() & 63;
-        for (int r0 = 0; r0 < rows; r0 += 16) {
-          const int row = min(m0 + r0 + (ln >> 2), M - 1);
-          load_lds16<true>(rope + ((int64_t)row * half + 8 * t) * 2 + (ln & 3) * 4, &L.rq[wave][r0][0][0]);
+      auto rope_loads = [&]() {
+        if (mine && sec < 2) {
+          const int ln = tix() & 63;
+          for (int r0 = 0; r0 < rows; r0 += 16) {
+            const int row = min(m0 + r0 + (ln >> 2), M - 1);
+            load_lds16<true>(rope + ((int64_t)row * half + 8 * t) * 2 + (ln & 3) * 4, &L.rq[wave][r0][0][0]);
+          }
         }
-      }
-      stage(xb, d, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
+      };
+      stage(xb, d, m0, rows, d, ssq, tp.Ms, d, dm.eps, L, rope_loads);
       TICK_SUB(l, 2);
       if (mine) {
-        wave_gemm(w, KB, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
-          const int nl = nl0 + c;
+        wave_gemm(w, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
+          // element i of the C tile is row rb + i of the chunk, column nl0 + c
+          const int rb = mt * 16 + 4 * grp, nl = nl0 + c;
+          const f32x4 rs = *reinterpret_cast<const f32x4*>(&L.r[rb]);  // RMSNorm row scales
           if (sec == 2) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const int row = m0 + mt * 16 + 4 * grp + i;
-              sacc[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
-              const float other = xor1(sacc[i]);
-              if ((c & 1) == 0 && row < M)
-                st_loc(reinterpret_cast<uint32_t*>(a.vself + (int64_t)row * A + nl), pack_bf16x2(sacc[i], other));
+              const float v = sacc[i] * rs[i];
+              const float other = xor1(v);
+              if ((c & 1) == 0 && m0 + rb + i < M)
+                st_loc(reinterpret_cast<uint32_t*>(a.vself + (int64_t)(m0 + rb + i) * A + nl), pack_bf16x2(v, other));
             }
           } else {
+            float2 cs[4];  // (cos, sin) of the pair in this lane's column, per row
+#pragma unroll
+            for (int i = 0; i < 4; ++i) cs[i] = *reinterpret_cast<const float2*>(&L.rq[wave][rb + i][c & 7][0]);
             const int p = nl % DH;
             const int j = 8 * (p / 16) + (c & 7);
             const int dch = c < 8 ? j : half + j;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              sacc[i] *= L.r[mt * 16 + 4 * grp + i];  // RMSNorm row scale
-              const float partner = xor8(sacc[i]);
-              const int row = m0 + mt * 16 + 4 * grp + i;
-              const float cs = L.rq[wave][mt * 16 + 4 * grp + i][c & 7][0];
-              const float sn = L.rq[wave][mt * 16 + 4 * grp + i][c & 7][1];
-              const float r = c < 8 ? sacc[i] * cs - partner * sn : sacc[i] * cs + partner * sn;
+              const float v = sacc[i] * rs[i];
+              const float partner = xor8(v);
+              const float r = c < 8 ? v * cs[i].x - partner * cs[i].y : v * cs[i].x + partner * cs[i].y;
+              const int row = m0 + rb + i;
               const int64_t o = (int64_t)row * A + h * DH + dch;
               if (sec == 0) {
                 if (row < M) st_loc_f(a.q + o, r * qs);
