@@ -203,7 +203,15 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   // workspace
   const int M = ex->M_max;
   const int n_tt_max = (ex->S_max + 15) / 16;
-  ex->items_max = std::max(16384, 2 * c.max_batch * H * n_tt_max + 64);
+  {
+    hipDeviceProp_t prop;
+    if (!ok(hipGetDeviceProperties(&prop, ex->device), "hipGetDeviceProperties")) return cleanup(FSX_E_HIP);
+    ex->cu_count = prop.multiProcessorCount;
+  }
+  // partial attention states: per-phase chunks, or the tick kernel's slots (NXR XCDs x (4 per agent + one per
+  // workgroup)) per query tile
+  ex->items_max =
+      std::max({16384, 2 * c.max_batch * H * n_tt_max + 64, NXR * (4 * c.max_batch + ex->cu_count) * n_tt_max});
   std::vector<std::pair<void**, size_t>> parts;
   if (ex->path == 0) {
     parts = {{(void**)&ex->ws.h, (size_t)M * d * 4},
@@ -228,9 +236,6 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   if (ex->path == 0 && !(c.flags & FSX_FLAG_MULTI_LAUNCH)) {
     // The tick kernel splits heads and FFN columns over the XCDs; find how many there are and check that
     // every XCD's share fits the kernel (at most 4 heads of width 128 and 512 FFN columns per XCD).
-    hipDeviceProp_t prop;
-    if (!ok(hipGetDeviceProperties(&prop, ex->device), "hipGetDeviceProperties")) return cleanup(FSX_E_HIP);
-    ex->cu_count = prop.multiProcessorCount;
     int nx = 0;
     if (ex->cu_count <= 512) {
       uint32_t* dev_ids = nullptr;
@@ -249,7 +254,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
     ex->nx = nx;
     const int nh_max = nx > 0 ? (H + nx - 1) / nx : 1 << 30;
     const int fr_max = nx > 0 ? 32 * ((F / 32 + nx - 1) / nx) : 1 << 30;
-    ex->tick = nx > 0 && nx <= NXR && c.n_layers <= SCHED_STRIDE && ex->cu_count <= XFLAGS && d <= 512 && d % 32 == 0 && F % 32 == 0 && nh_max <= 4 && fr_max <= 512 &&
+    ex->tick = nx > 0 && nx <= NXR && ex->cu_count <= XFLAGS && d <= 512 && d % 32 == 0 && F % 32 == 0 && nh_max <= 4 && fr_max <= 512 &&
                c.n_expert_tokens <= 64;
   }
   if (ex->tick) {
@@ -284,7 +289,6 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
         {(void**)&t.f_attn, (size_t)nflag_attn * n_tt_max * FPAD * 8},
         {(void**)&t.f_rng, (size_t)ex->items_max * FPAD * 8},
         {(void**)&t.f_z, (size_t)F / 8 * FPAD * 8},
-        {(void**)&t.sched, (size_t)NXMAX * SCHED_STRIDE * 4},
         {(void**)&t.status, 256}};
     parts.insert(parts.end(), tp.begin(), tp.end());
   }
@@ -426,44 +430,22 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
     const int G = ex->cu_count;
     tp.Mp = (tp.M + 7) / 8 * 8;
     tp.Ms = (tp.M + 31) / 32 * 32;
-    // Attention units: (agent, range of rows, head).  Rows per unit (one head) aim at about one unit per
-    // workgroup for small work and 2 or 4 for larger work, never below 256 rows (a range merge costs a few
-    // dependent memory round trips, more than streaming 256 rows); an agent's ranges are equal, multiples
-    // of 32 rows.
-    const int64_t total_rh = rows * dm.H;
-    const int64_t per_wg = total_rh / G;
-    const int k_units = per_wg >= 4096 ? 4 : (per_wg >= 512 ? 2 : 1);
-    int64_t unit_rows = std::max<int64_t>(256, (total_rh + (int64_t)k_units * G - 1) / ((int64_t)k_units * G));
-    unit_rows = (unit_rows + 31) / 32 * 32;
-    for (;;) {
-      int64_t slots = 0;
-      for (int b = 0; b < batch; ++b) slots += std::max<int64_t>(1, (tp.len[b] + unit_rows - 1) / unit_rows);
-      if (slots * dm.H * tp.n_tt <= ex->items_max) break;
-      unit_rows *= 2;
-    }
-    tp.range_prefix[0] = 0;
-    for (int b = 0; b < batch; ++b) {
-      const int64_t nr = std::max<int64_t>(1, (tp.len[b] + unit_rows - 1) / unit_rows);
-      const int64_t rr = std::max<int64_t>(32, ((tp.len[b] + nr - 1) / nr + 31) / 32 * 32);
-      tp.range_rows[b] = (int)std::min<int64_t>(rr, INT32_MAX / 2);
-      tp.range_prefix[b + 1] = tp.range_prefix[b] + (int)nr;
-    }
-    // agents with the largest ranges first
+    // Attention work (the kernel slices it): agents longest first; per head, agent b weighs its 32-row cache
+    // tiles (at least one, for the expert's own rows)
     std::vector<int> ord(batch);
     for (int b = 0; b < batch; ++b) ord[b] = b;
-    std::stable_sort(ord.begin(), ord.end(), [&](int x, int y) { return tp.range_rows[x] > tp.range_rows[y]; });
-    tp.unit_prefix[0] = 0;
+    std::stable_sort(ord.begin(), ord.end(), [&](int x, int y) { return tp.len[x] > tp.len[y]; });
+    tp.seg_p[0] = 0;
     for (int k = 0; k < batch; ++k) {
       const int b = ord[k];
       tp.order[k] = b;
-      tp.unit_prefix[k + 1] = tp.unit_prefix[k] + (tp.range_prefix[b + 1] - tp.range_prefix[b]) * dm.H;
+      tp.seg_w[k] = std::max<int>(1, (int)((tp.len[b] + 31) / 32));
+      tp.seg_p[k + 1] = tp.seg_p[k] + tp.seg_w[k];
     }
-    tp.n_units = tp.unit_prefix[batch];
-    tp.nf_prefix[0] = 0;
-    for (int k = 0; k < batch; ++k) {
-      const int b = ord[k];
-      tp.nf_prefix[k + 1] = tp.nf_prefix[k] + (tp.range_prefix[b + 1] - tp.range_prefix[b]) - 1;
-    }
+    // partial-state slots per XCD: at most one per segment plus one per slice boundary
+    tp.slot_x = batch * 4 + G;
+    if ((int64_t)NXR * tp.slot_x * tp.n_tt > ex->items_max)
+      return fail(FSX_E_UNSUPPORTED, "attention partial-state slots exceed the workspace");
     TickArgs a = ex->ta;
     a.tok_dtype = c.dtype;
     a.tokens = tokens;

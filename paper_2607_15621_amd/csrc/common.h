@@ -170,6 +170,15 @@ __device__ __forceinline__ void vm_wait_all() {
   asm volatile("" ::: "memory");
 }
 __device__ __forceinline__ void stores_done() { vm_wait_all(); }
+// Wait until at most N (< 64) of this thread's vector memory operations are pending: they complete in issue order,
+// so everything issued before the last N has completed.
+template <int N>
+__device__ __forceinline__ void vm_wait_below_c() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
 
 // Stores of data exchanged between workgroups of ONE XCD: plain stores, which stay in the XCD's L2 (the
 // vector L1 is write-through); readers use device-scope loads, which are served by that L2 and never by a

@@ -16,20 +16,17 @@ struct TickParams {
   int32_t n_items;                            // per-phase path: attention work items
   int32_t Mp;                                 // M rounded up to 8: rows of tile-major activations
   int32_t Ms;                                 // M rounded up to 32: rows of the sums of squares
-  int32_t n_units;                            // tick kernel: attention units
   int64_t pos[FSX_MAX_BATCH];                 // rotary position of token 0
   int64_t start[FSX_MAX_BATCH];               // ring slot of the oldest valid row
   int32_t len[FSX_MAX_BATCH];                 // valid cache rows
   int32_t chunk_prefix[FSX_MAX_BATCH + 1];    // per-phase path: chunk slots before agent b (ceil(len/chunk_rows) + 1 each)
-  // tick kernel: attention units are (agent, range of range_rows[b] rows, head); agent b owns range slots
-  // range_prefix[b] .. range_prefix[b+1]-1 (at least one, the last also holds the expert's own rows).  Units are
-  // numbered agent by agent in the order order[0..B-1]; the k-th agent's units start at unit_prefix[k].
-  int32_t range_prefix[FSX_MAX_BATCH + 1];
-  int32_t range_rows[FSX_MAX_BATCH];
-  int32_t unit_prefix[FSX_MAX_BATCH + 1];
+  // tick kernel attention: agents in the order order[0..B-1]; the k-th weighs seg_w[k] work tiles per head
+  // (its 32-row cache tiles, at least 1), seg_p[k] = seg_w[0] + ... + seg_w[k-1]; partial-state slots of XCD X
+  // are X * slot_x .. X * slot_x + slot_x - 1
   int32_t order[FSX_MAX_BATCH];
-  // tick kernel: ranges other than an agent's last, counted over agents in `order`; nf_prefix[B] in total
-  int32_t nf_prefix[FSX_MAX_BATCH + 1];
+  int32_t seg_w[FSX_MAX_BATCH];
+  int32_t seg_p[FSX_MAX_BATCH + 1];
+  int32_t slot_x;
 };
 
 // Cache view of one layer.
@@ -105,7 +102,6 @@ constexpr int NXMAX = 16;
 constexpr int NXR = 8;      // XCDs the cross-XCD reductions read at most (the XCD count of gfx950 parts)
 constexpr int FPAD = 16;     // flags are 64-bit stamps, one per 128-byte line (index * FPAD)
 constexpr int XFLAGS = 512;  // flag slots per XCD of the per-XCD flag arrays
-constexpr int SCHED_STRIDE = 256;  // per-XCD attention unit counters: [NXMAX][SCHED_STRIDE] (n_layers <= 256)
 
 struct TickArgs {
   const char* wbase;   // packed weights of layer 0; layers follow back to back (see layer_w)
@@ -136,8 +132,8 @@ struct TickArgs {
   uint16_t* vself;     // [M][A]
   uint16_t* attn;      // [M][A]
   uint16_t* z;         // [Mp][F] SwiGLU output
-  float* att_o;        // [items][16][Dh] range partials
-  float* att_ml;       // [items][16][2]
+  float* att_o;        // [slot * n_tt + query tile][16][Dh] partial attention states
+  float* att_ml;       // [slot * n_tt + query tile][16][2]
   // crossing XCDs: stamped 8-byte words (payload in the low half, stamp in the high half)
   uint64_t* po;        // [NXMAX][d/16][Mp][16] output-projection partials
   uint64_t* pd;        // [NXMAX][d/16][Mp][16] down-projection partials
@@ -147,9 +143,8 @@ struct TickArgs {
   uint64_t* f_mid;     // [NXMAX][XFLAGS] by column tile
   uint64_t* f_q;       // [3A/16]
   uint64_t* f_attn;    // [B*H][n_tt] per query tile
-  uint64_t* f_rng;     // [range pairs]
+  uint64_t* f_rng;     // [slot] partial states written
   uint64_t* f_z;       // [F/8]
-  uint32_t* sched;     // [NXMAX][SCHED_STRIDE] attention unit counters per XCD and layer
   uint64_t* status;
   uint64_t epoch;
   uint64_t timeout_ticks;  // real-time counter ticks (100 MHz)

@@ -50,6 +50,9 @@ constexpr int MTMAX = 5;   // 16-row tiles per staged chunk (80 rows)
 constexpr int DH = 128;    // head width of the fused path
 constexpr int STW = 16 * DH + 32;  // LDS floats of one wave's attention state: O[16][128], (m, l)[16]
 constexpr int NQW = 3;     // query tiles a wave carries at once in the many-query attention variant
+constexpr int FP8_PD = 4;  // fp8 single-query attention: LDS ring slots per wave (tiles staged ahead)
+constexpr int FP8_SLOT = 2 * 32 * DH;  // bytes of one staged fp8 tile: K rows then V rows (32 x 128 each)
+constexpr int NSEG = FSX_MAX_BATCH * 4;  // attention segments (agent, local head) of one XCD, at most
 
 // A value read from LDS that is the same in every lane, moved to a scalar register.
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -57,22 +60,35 @@ __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlan
 struct TickLds {
   union {
     struct {
-      uint16_t x[MTMAX * 16][XSTR];  // staged activation rows (bf16) of the current chunk
-      f32x4 red[4][MTMAX][WAVE];     // cross-wave reduction of projection accumulators
+      uint16_t x[MTMAX * 16][XSTR];    // staged activation rows (bf16) of the current chunk
+      f32x4 red[4][MTMAX][WAVE];       // cross-wave reduction of projection accumulators
+      float rq[4][MTMAX * 16][8][2];   // q/k projection: each wave's rotary slice (cos, sin of its 8 pairs) per row
     } p;
-    struct {
-      float st[4][STW];                // per-wave attention states
-      uint16_t qs[NQW * 16][DH + 8];  // many-query attention: the unit's query tiles (bf16 or fp16)
+    union {
+      struct {
+        float st[4][STW];               // per-wave attention states
+        uint16_t qs[NQW * 16][DH + 8];  // many-query attention: the unit's query tiles (bf16 or fp16)
+      };
+      // fp8 single-query attention: each wave's tiles, staged by direct loads; after its last tile a wave's state
+      // goes to the start of its own slots (STW floats)
+      uint8_t ring[4][FP8_PD][FP8_SLOT];
     } a;
   } u;
-  float rq[4][MTMAX * 16][8][2];  // q/k projection: each wave's rotary slice (cos, sin of its 8 pairs) per row
   alignas(16) float r[MTMAX * 16];  // RMSNorm row scales of the chunk
   float tmp[512];       // head scratch
   float red2[16][16];   // head: per-wave partial sums
   float hr[64];         // head: row scales of the pooled tokens (at most 64)
   int ok;
   int X, s, n, NX, n0;  // XCD rank, slot in the XCD, workgroups of the XCD, XCDs, workgroups of XCD 0
-  int next;             // attention: the workgroup's next unit
+  // attention plan of the workgroup's XCD, made once per launch: segment g = j * B + k (local head j, agent
+  // order[k]) has its tiles at work units [seg0[g], seg0[g] + segw[g]); they meet np[g] slices, the first being slice
+  // sf[g], and when np[g] > 1 its partial states occupy slots pb[g] .. pb[g] + np[g] - 1 of the XCD.  amode: 1 =
+  // slice s is segment s, 0 = slices of equal work; ant: work units in total
+  int seg0[NSEG];
+  int segw[NSEG];
+  int pb[NSEG];
+  int16_t sf[NSEG], np[NSEG];
+  int amode, ant;
 };
 
 __device__ __forceinline__ uint64_t stamp_of(const TickArgs& a, int layer, int n_layers) {
@@ -538,10 +554,6 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
       st_loc_f(rope + ((int64_t)m * half + j) * 2 + 1, (float)sn);
     }
   }
-  // the XCD's per-layer attention unit counters start at zero (read only after layer 0's projections, which wait
-  // for this flag)
-  if (s == 0)
-    for (int i = tix(); i < dm.n_layers; i += NTHR) st_loc(a.sched + (int64_t)X * SCHED_STRIDE + i, 0u);
   stores_done();
   __syncthreads();
   if (tix() == 0) st_loc(a.f_rope + ((int64_t)X * XFLAGS + s) * FPAD, st);
@@ -590,7 +602,7 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
           const int ln = tix() & 63;
           for (int r0 = 0; r0 < rows; r0 += 16) {
             const int row = min(m0 + r0 + (ln >> 2), M - 1);
-            load_lds16<true>(rope + ((int64_t)row * half + 8 * t) * 2 + (ln & 3) * 4, &L.rq[wave][r0][0][0]);
+            load_lds16<true>(rope + ((int64_t)row * half + 8 * t) * 2 + (ln & 3) * 4, &L.u.p.rq[wave][r0][0][0]);
           }
         }
       };
@@ -612,7 +624,7 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
           } else {
             float2 cs[4];  // (cos, sin) of the pair in this lane's column, per row
 #pragma unroll
-            for (int i = 0; i < 4; ++i) cs[i] = *reinterpret_cast<const float2*>(&L.rq[wave][rb + i][c & 7][0]);
+            for (int i = 0; i < 4; ++i) cs[i] = *reinterpret_cast<const float2*>(&L.u.p.rq[wave][rb + i][c & 7][0]);
             const int p = nl % DH;
             const int j = 8 * (p / 16) + (c & 7);
             const int dch = c < 8 ? j : half + j;
@@ -977,7 +989,9 @@ __device__ __forceinline__ void state_to_lds(float* stw, const f32x4 o[8], float
 
 // Describes the tiles of one attention unit: cache rows [i0, i1) then (last range only) the S own rows.
 struct AUnit {
-  int b, h, r, nr;
+  int b, h;
+  bool final_out;   // the whole (agent, head): normalised output, else the partial state of slot `slot`
+  int slot;
   int i0, i1;       // cache rows of this range
   int nct, nst;     // cache tiles, own-row tiles
   const char* kc;   // cache K/V base of (b, layer, head) (slot 0)
@@ -989,18 +1003,24 @@ struct AUnit {
 
 // Merge the 4 waves' LDS states of query tile tt: each thread owns (t, 8 channels).  If final, normalise into
 // the attention output; else store the unnormalised partial of slot `item`.
+// Where wave w's attention state goes: its slots of the LDS tile ring (RING) or the state array.
+template <bool RING>
+__device__ __forceinline__ float* state_of(TickLds& L, int w) {
+  return RING ? reinterpret_cast<float*>(&L.u.a.ring[w][0][0]) : L.u.a.st[w];
+}
+template <bool RING = false>
 __device__ __forceinline__ void merge_states(const TickArgs& a, const TickParams& tp, const Dims& dm,
                                              const AUnit& U, int tt, bool final_out, int64_t item, TickLds& L) {
   const int t = tix() >> 4, d0 = (tix() & 15) * 8;
   float Mx = -INFINITY;
 #pragma unroll
-  for (int w = 0; w < 4; ++w) Mx = fmaxf(Mx, L.u.a.st[w][2048 + 2 * t]);
+  for (int w = 0; w < 4; ++w) Mx = fmaxf(Mx, state_of<RING>(L, w)[2048 + 2 * t]);
   float Ls = 0.f, acc[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) acc[k] = 0.f;
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    const float* stw = L.u.a.st[w];
+    const float* stw = state_of<RING>(L, w);
     const float f = Mx == -INFINITY ? 0.f : exp2f(stw[2048 + 2 * t] - Mx);
     Ls += stw[2048 + 2 * t + 1] * f;
 #pragma unroll
@@ -1028,7 +1048,7 @@ __device__ __forceinline__ void merge_states(const TickArgs& a, const TickParams
 // Query tile tt of (agent b, head h): merge the partials of its nr ranges (fixed order) into the attention output;
 // the partials are loaded 8 ranges at a time, every load issued before any is used.
 __device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickParams& tp, const Dims& dm, int b, int h,
-                                               int nr, int tt) {
+                                               int slot0, int nr, int tt) {
   constexpr int RB = 8;
   const int t = tix() >> 4, d0 = (tix() & 15) * 8;
   const int H = dm.H;
@@ -1044,7 +1064,7 @@ __device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickPara
       ls[j] = 0.f;
       v0[j] = v1[j] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (r0 + j < nr) {
-        const int64_t item = ((int64_t)(tp.range_prefix[b] + r0 + j) * H + h) * tp.n_tt + tt;  // pair * n_tt + tt
+        const int64_t item = (int64_t)(slot0 + r0 + j) * tp.n_tt + tt;
         ms[j] = ld_dev_f(a.att_ml + item * 32 + 2 * t);
         ls[j] = ld_dev_f(a.att_ml + item * 32 + 2 * t + 1);
         const float* po = a.att_o + (item * 16 + t) * 128 + d0;
@@ -1075,6 +1095,68 @@ __device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickPara
   }
 }
 
+// fp8 tile staged into LDS with direct loads (whole 128-byte rows: every instruction reads 8 full rows, which streams
+// from HBM faster than the 64-byte row pieces of register loads in MFMA operand order).  Slot layout: K rows
+// [32][128 B] then V rows [32][128 B]; the 16-byte chunk k of row r sits at chunk position k ^ ((r >> 1) & 7), so
+// the 16 rows of a K fragment read fall in distinct banks.  Lane l of instruction q brings row 8q + l/8 into chunk
+// position l % 8.  Rows past i1 repeat row i0 (masked in the update).
+__device__ __forceinline__ void stage_tile_fp8(const char* kb, const char* vb, int64_t start, int64_t cap, int i0,
+                                               int r0, int i1, uint8_t* slot) {
+  const int lane = tix() & 63, rl = lane >> 3, pc = lane & 7;
+  asm volatile("" ::: "memory");  // after every read of the slot's previous tile
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int r = 8 * q + rl;
+    int64_t row = start + (r0 + r < i1 ? r0 + r : i0);
+    if (row >= cap) row -= cap;
+    const int64_t off = row * DH + 16 * (pc ^ ((r >> 1) & 7));
+    load_lds16<false>(kb + off, slot + q * 1024);
+    load_lds16<false>(vb + off, slot + 32 * DH + q * 1024);
+  }
+}
+// The RawTile<1> fragments of a staged tile (see RawTile and stage_tile_fp8): K row 16rt + c, chunks 4h + grp; V
+// rows 4grp + j (+16), bytes 8c..8c+7.  One asm block that waits for its own reads: reads the compiler sees after
+// direct loads into the same LDS object make it wait for every pending direct load, the next tile's included.
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void read_tile_fp8(const uint8_t* slot, RawTile<1>& t) {
+  const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
+  const uint32_t s0 = lds_addr(slot);
+  const uint32_t ak0 = s0 + c * DH + 16 * (grp ^ (c >> 1));        // (r >> 1) & 7 == c >> 1 for r = 16 rt + c
+  const uint32_t ak1 = s0 + c * DH + 16 * ((4 + grp) ^ (c >> 1));
+  const uint32_t vb = s0 + 32 * DH + 4 * grp * DH + 8 * (c & 1);
+  const uint32_t av0 = vb + 0 * DH + 16 * ((c >> 1) ^ (2 * grp));      // rows 4grp + jj: (r >> 1) & 7 == 2grp + jj/2
+  const uint32_t av1 = vb + 1 * DH + 16 * ((c >> 1) ^ (2 * grp));
+  const uint32_t av2 = vb + 2 * DH + 16 * ((c >> 1) ^ (2 * grp + 1));
+  const uint32_t av3 = vb + 3 * DH + 16 * ((c >> 1) ^ (2 * grp + 1));
+  u32x4_t k0, k1, k2, k3;
+  u32x2_t v0, v1, v2, v3, v4, v5, v6, v7;
+  asm volatile(
+      "ds_read_b128 %0, %12\n\t"
+      "ds_read_b128 %1, %13\n\t"
+      "ds_read_b128 %2, %12 offset:2048\n\t"
+      "ds_read_b128 %3, %13 offset:2048\n\t"
+      "ds_read_b64 %4, %14\n\t"
+      "ds_read_b64 %5, %15\n\t"
+      "ds_read_b64 %6, %16\n\t"
+      "ds_read_b64 %7, %17\n\t"
+      "ds_read_b64 %8, %14 offset:2048\n\t"
+      "ds_read_b64 %9, %15 offset:2048\n\t"
+      "ds_read_b64 %10, %16 offset:2048\n\t"
+      "ds_read_b64 %11, %17 offset:2048\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(k0), "=&v"(k1), "=&v"(k2), "=&v"(k3), "=&v"(v0), "=&v"(v1), "=&v"(v2), "=&v"(v3), "=&v"(v4), "=&v"(v5),
+        "=&v"(v6), "=&v"(v7)
+      : "v"(ak0), "v"(ak1), "v"(av0), "v"(av1), "v"(av2), "v"(av3)
+      : "memory");
+  t.k[0] = as_u4(k0);
+  t.k[1] = as_u4(k1);
+  t.k[2] = as_u4(k2);
+  t.k[3] = as_u4(k3);
+  const u32x2_t vv[8] = {v0, v1, v2, v3, v4, v5, v6, v7};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) t.v[j] = make_uint2(vv[j].x, vv[j].y);
+}
+
 // The tiles of one unit for query tiles tt0 .. tt0+nq-1 (nq <= NQ): wave w takes cache tiles w, w+4, ..., kept
 // PD deep in registers, then the own-row tiles that continue the same round robin; the states are merged
 // through LDS and written out (normalised if the agent has one range, else as the partial of this range).
@@ -1086,24 +1168,33 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
   const uint64_t st = stamp_of(a, l, dm.n_layers);
   // this wave's cache tiles: j = wave + 4 i, i < nc
   const int nc = U.nct > wave ? (U.nct - wave + 3) / 4 : 0;
-  RawTile<KT> ring[PD];
+  constexpr bool LDS_RING = KT == 1 && NQ == 1;  // fp8, one query tile: tiles staged in LDS by direct loads
+  uint8_t* lring = L.u.a.ring[wave][0];
+  auto stage_tile = [&](int i) {
+    stage_tile_fp8(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * (wave + 4 * i), U.i1,
+                   lring + (i % FP8_PD) * FP8_SLOT);
+  };
+  RawTile<KT> ring[LDS_RING ? 1 : PD];
   auto cache_tile = [&](int i, RawTile<KT>& t) {
     load_cache_tile<KT>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * (wave + 4 * i), U.i1, t);
   };
   // The first tiles do not depend on this layer's projections: waves 0-2 issue them before waiting; wave 3 polls
   // the q, k and v column tiles of this head (its poll would otherwise return only after its own prefetch) and
   // issues its tiles afterwards.
-  if (wave < 3) {
+  auto prefetch = [&]() {
+    if constexpr (LDS_RING) {
 #pragma unroll
-    for (int dd = 0; dd < PD; ++dd)
-      if (dd < nc) cache_tile(dd, ring[dd]);
-  }
+      for (int dd = 0; dd < FP8_PD; ++dd)
+        if (dd < nc) stage_tile(dd);
+    } else {
+#pragma unroll
+      for (int dd = 0; dd < PD; ++dd)
+        if (dd < nc) cache_tile(dd, ring[dd]);
+    }
+  };
+  if (wave < 3) prefetch();
   if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16, 3)) return false;
-  if (wave == 3) {
-#pragma unroll
-    for (int dd = 0; dd < PD; ++dd)
-      if (dd < nc) cache_tile(dd, ring[dd]);
-  }
+  if (wave == 3) prefetch();
   f32x4 o[NQ][8];
   float m_run[NQ], l_run[NQ];
 #pragma unroll
@@ -1128,7 +1219,34 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
     if (NQ == 1) return qr[k];
     return *reinterpret_cast<const uint4*>(&L.u.a.qs[tt * 16 + c16][32 * k + 8 * grp]);
   };
-  if constexpr (NQ == 1 && PD % 2 == 0) {
+  if constexpr (LDS_RING) {
+    // Pairs of tiles (i, i + 1) in slots i % 4, i % 4 + 1.  The memory operations issued after tile i + 1 are the
+    // direct loads (8 per tile) of tiles i + 2 and i + 3, so at most 8 per such tile pending means the pair has
+    // landed; once both are read into registers their slots take tiles i + 4 and i + 5, which stream in while
+    // the pair is computed.
+    static_assert(FP8_PD == 4, "the pair loop uses four slots");
+#pragma unroll 1
+    for (int i = 0; i < nc; i += 2) {
+      const bool two = i + 1 < nc;
+      const int after = min(nc - 2 - i, 2);  // tiles in flight behind the pair (when two)
+      if (two && after == 2)
+        vm_wait_below_c<16>();
+      else if (two && after == 1)
+        vm_wait_below_c<8>();
+      else
+        vm_wait_all();
+      RawTile<KT> ta, tb;
+      read_tile_fp8(lring + (i % FP8_PD) * FP8_SLOT, reinterpret_cast<RawTile<1>&>(ta));
+      if (two) read_tile_fp8(lring + (i % FP8_PD + 1) * FP8_SLOT, reinterpret_cast<RawTile<1>&>(tb));
+      if (i + 4 < nc) stage_tile(i + 4);
+      if (i + 5 < nc) stage_tile(i + 5);
+      if (two)
+        tile_pair_compute<KT>(ta, tb, qr, U.i0 + 32 * (wave + 4 * i), U.i0 + 32 * (wave + 4 * (i + 1)), U.i1, U.ksc,
+                              o[0], m_run[0], l_run[0]);
+      else
+        tile_compute<KT, 1>(ta, qf, 1, U.i0 + 32 * (wave + 4 * i), U.i1, U.ksc, o, m_run, l_run);
+    }
+  } else if constexpr (NQ == 1 && PD % 2 == 0) {
     // pairs of ring slots (dd, dd + 1); an odd last tile goes through the single-tile update
 #pragma unroll 1
     for (int i = 0; i < nc; i += PD) {
@@ -1180,26 +1298,71 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
       tile_compute<0, NQ>(t, qf_own, nq, 32 * j, tp.S, 1.f, o, m_run, l_run);
     }
   }
-  const bool final_out = U.nr == 1;
-  const int64_t pair = (int64_t)(tp.range_prefix[U.b] + U.r) * dm.H + U.h;
+  const bool final_out = U.final_out;
 #pragma unroll
   for (int tt = 0; tt < NQ; ++tt) {
     if (tt < nq) {
-      state_to_lds(L.u.a.st[wave], o[tt], m_run[tt], l_run[tt]);
+      state_to_lds(state_of<LDS_RING>(L, wave), o[tt], m_run[tt], l_run[tt]);
       __syncthreads();
-      merge_states(a, tp, dm, U, tt0 + tt, final_out, pair * tp.n_tt + tt0 + tt, L);
+      merge_states<LDS_RING>(a, tp, dm, U, tt0 + tt, final_out, (int64_t)U.slot * tp.n_tt + tt0 + tt, L);
       __syncthreads();
     }
   }
   return true;
 }
 
-// Attention units of XCD X: (pair q, local head j) numbered u = q * nh + j, where the pairs (agent, range) list
-// every agent's ranges but its last (agents in the planner's order, longest ranges first) and then every agent's
-// last range (which also covers the expert's own rows).  Workgroup s starts with unit s; further units come from a
-// counter per XCD and layer (an atomic in the XCD's L2), so workgroups that finish early take more.  An agent with
-// one range gets its normalised output directly; otherwise every range writes a partial and separate merge items
-// combine them.
+// Attention work of XCD X: the segments (local head, agent) laid end to end, head-major (the short segments of
+// ragged agents then fall into different slices), each weighing SEG_COST work units for its start-up (loading the
+// queries and the first tiles, merging the waves' states) followed by one unit per 32-row cache tile (an agent with
+// no cached rows has one tile, for the expert's own rows).  With enough work every workgroup takes an equal run of
+// work units (slice); a segment whose tiles fall into several slices leaves one partial state per slice, merged
+// afterwards by separate items (agent, head, query tile) in a fixed order.  With little work (fewer than 16 tiles per
+// workgroup) and few segments, workgroup s takes segment s whole.  Equal slices keep every workgroup streaming until
+// the phase ends.
+constexpr int SEG_COST = 16;
+__device__ __forceinline__ void attn_plan(const TickParams& tp, const Dims& dm, TickLds& L) {
+  const int X = uni(L.X), NX = uni(L.NX), n = uni(L.n);
+  const int nh = head_lo(X + 1, NX, dm.H) - head_lo(X, NX, dm.H);
+  const int nseg = tp.B * nh;  // <= NSEG = NTHR
+  const int NT = nh * tp.seg_p[tp.B];  // cache (work) tiles
+  const int mode = NT < 16 * n && nseg <= n ? 1 : 0;
+  const int NC = NT + nseg * SEG_COST;  // work units
+  const int g = tix();
+  int np = 0;
+  if (g < nseg) {
+    const int j = g / tp.B, k = g % tp.B, w = tp.seg_w[k];
+    const int g0 = j * (tp.seg_p[tp.B] + tp.B * SEG_COST) + tp.seg_p[k] + k * SEG_COST + SEG_COST;  // first tile's unit
+    int sf = g;
+    np = 1;
+    if (mode == 0) {
+      // slice of work unit c: the s with floor(s NC / n) <= c < floor((s + 1) NC / n)
+      auto slice = [&](int c) { return (int)(((int64_t)(c + 1) * n - 1) / NC); };
+      sf = slice(g0);
+      np = slice(g0 + w - 1) - sf + 1;
+    }
+    L.seg0[g] = g0;
+    L.segw[g] = w;
+    L.sf[g] = (int16_t)sf;
+    L.np[g] = (int16_t)np;
+  }
+  if (g == 0) {
+    L.amode = mode;
+    L.ant = NC;
+  }
+  // slots: exclusive prefix over segments of np where np > 1 (inclusive scan in LDS, then minus own)
+  const int own = np > 1 ? np : 0;
+  L.pb[g] = own;
+  __syncthreads();
+  for (int off = 1; off < NSEG; off <<= 1) {
+    const int v = g >= off ? L.pb[g - off] : 0;
+    __syncthreads();
+    L.pb[g] += v;
+    __syncthreads();
+  }
+  L.pb[g] -= own;
+  __syncthreads();
+}
+
 template <int KT>
 __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   constexpr int ES = KT == 0 ? 2 : 1;
@@ -1207,33 +1370,33 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
   const int H = dm.H, A = dm.A, n_tt = tp.n_tt, B = tp.B;
   const int h0 = head_lo(X, NX, H), nh = head_lo(X + 1, NX, H) - h0;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
-  const int NF = tp.nf_prefix[B];
-  const int n_units = nh * (NF + B);
+  const int nseg = B * nh, NC = uni(L.ant), mode = uni(L.amode);
+  // this workgroup's work units [w0, w1)
+  int w0, w1, g = 0;
+  if (mode == 1) {
+    w0 = s < nseg ? uni(L.seg0[s]) : 0;
+    w1 = s < nseg ? w0 + uni(L.segw[s]) : 0;
+    g = s;
+  } else {
+    w0 = (int)((int64_t)s * NC / n);
+    w1 = (int)((int64_t)(s + 1) * NC / n);
+    while (g < nseg && uni(L.seg0[g]) + uni(L.segw[g]) <= w0) ++g;
+  }
   bool first = true;
-  uint32_t* ctr = a.sched + (int64_t)X * SCHED_STRIDE + l;  // units taken beyond the first n (in this XCD's L2)
-  for (int u = s; u < n_units;) {
-    // the next unit, fetched while this one runs
-    uint32_t nxt = 0;
-    if (tix() == 0) nxt = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    const int q = u / nh, h = h0 + u % nh;
-    int k = 0, r;
-    if (q < NF) {
-      while (k + 1 < B && tp.nf_prefix[k + 1] <= q) ++k;
-      r = q - tp.nf_prefix[k];
-    } else {
-      k = q - NF;
-      r = -1;
-    }
-    const int b = tp.order[k];
+  for (; w0 < w1 && g < nseg && uni(L.seg0[g]) < w1; ++g) {
+    const int g0 = uni(L.seg0[g]), g1 = g0 + uni(L.segw[g]);
+    const int t0 = max(w0, g0) - g0, t1 = min(w1, g1) - g0;  // the segment's tiles in this slice
+    const int b = tp.order[g % B], h = h0 + g / B;
+    const int npart = uni(L.np[g]);
     AUnit U;
     U.b = b;
     U.h = h;
-    U.nr = tp.range_prefix[b + 1] - tp.range_prefix[b];
-    U.r = r < 0 ? U.nr - 1 : r;
-    U.i0 = U.r * tp.range_rows[b];
-    U.i1 = min(U.i0 + tp.range_rows[b], tp.len[b]);
+    U.final_out = npart == 1;
+    U.slot = X * tp.slot_x + uni(L.pb[g]) + (mode == 1 ? 0 : s - uni(L.sf[g]));
+    U.i0 = 32 * t0;
+    U.i1 = min(32 * t1, tp.len[b]);
     U.nct = U.i1 > U.i0 ? (U.i1 - U.i0 + 31) / 32 : 0;
-    U.nst = U.r == U.nr - 1 ? (tp.S + 31) / 32 : 0;
+    U.nst = t1 == g1 - g0 ? (tp.S + 31) / 32 : 0;  // the segment's last slice also takes the expert's own rows
     const int64_t slab = (((int64_t)b * a.cv.n_layers + l) * H + h) * a.cv.cap;  // head-major (b, l, h) ring
     U.kc = (const char*)a.cv.k + slab * DH * ES;
     U.vc = (const char*)a.cv.v + slab * DH * ES;
@@ -1254,30 +1417,27 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
     }
     if (!ok) return false;
     if (first) TICK_SUB(l, 4);
+    first = false;
     stores_done();
     __syncthreads();
     if (tix() == 0) {
-      if (U.nr > 1)
-        st_loc(a.f_rng + ((int64_t)(tp.range_prefix[b] + U.r) * H + h) * FPAD, st);
+      if (!U.final_out)
+        st_loc(a.f_rng + (int64_t)U.slot * FPAD, st);
       else
         for (int tt = 0; tt < n_tt; ++tt) st_loc(a.f_attn + (((int64_t)b * H + h) * n_tt + tt) * FPAD, st);
     }
-    first = false;
-    if (tix() == 0) L.next = n + (int)nxt;
-    __syncthreads();
-    u = L.next;
     __syncthreads();
   }
-  // Merges of agents with several ranges: one item per (agent, head, query tile), after every range unit of this
-  // workgroup (range units never wait for merges, so these waits cannot form a cycle).
-  const int n_items = B * nh * n_tt;
-  for (int it = s; it < n_items; it += n) {
-    const int tt = it % n_tt, j = (it / n_tt) % nh, k = it / (n_tt * nh);
-    const int b = tp.order[k], h = h0 + j;
-    const int nr = tp.range_prefix[b + 1] - tp.range_prefix[b];
-    if (nr == 1) continue;
-    if (!wg_wait(a.f_rng + ((int64_t)tp.range_prefix[b] * H + h) * FPAD, nr, st, a, L, 1, H)) return false;
-    combine_ranges(a, tp, dm, b, h, nr, tt);
+  // Merges of segments cut into several partials: item (segment, query tile) m on workgroup m mod n, after this
+  // workgroup's own slice (slices never wait for merges, so these waits cannot form a cycle).
+  for (int m = s; m < nseg * n_tt; m += n) {
+    const int gm = m / n_tt, tt = m % n_tt;
+    const int npart = uni(L.np[gm]);
+    if (npart == 1) continue;
+    const int b = tp.order[gm % B], h = h0 + gm / B;
+    const int slot0 = X * tp.slot_x + uni(L.pb[gm]);
+    if (!wg_wait(a.f_rng + (int64_t)slot0 * FPAD, npart, st, a, L)) return false;
+    combine_ranges(a, tp, dm, b, h, slot0, npart, tt);
     stores_done();
     __syncthreads();
     if (tix() == 0) st_loc(a.f_attn + (((int64_t)b * H + h) * n_tt + tt) * FPAD, st);
@@ -1489,6 +1649,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_tick(TickArgs a, TickParams tp, Dim
   const int nl = dm.n_layers;
   trace_mark(a, 0, nl);
   bool ok = xcd_register(a, L);
+  if (ok) attn_plan(tp, dm, L);
   if (ok) phase_embed(a, tp, dm, L);
   trace_mark(a, 1, nl);
   for (int l = 0; l < nl && ok; ++l) {
