@@ -50,8 +50,8 @@ constexpr int MTMAX = 5;   // 16-row tiles per staged chunk (80 rows)
 constexpr int DH = 128;    // head width of the fused path
 constexpr int STW = 16 * DH + 32;  // LDS floats of one wave's attention state: O[16][128], (m, l)[16]
 constexpr int NQW = 3;     // query tiles a wave carries at once in the many-query attention variant
-constexpr int FP8_PD = 4;  // fp8 single-query attention: LDS ring slots per wave (tiles staged ahead)
-constexpr int FP8_SLOT = 2 * 32 * DH;  // bytes of one staged fp8 tile: K rows then V rows (32 x 128 each)
+constexpr int RSLOTS = 4;     // single-query attention: LDS ring slots per wave
+constexpr int RSLOT = 8192;   // bytes of one slot: an fp8 tile (32 rows) or half a bf16 tile (16 rows), K then V
 constexpr int NSEG = FSX_MAX_BATCH * 4;  // attention segments (agent, local head) of one XCD, at most
 
 // A value read from LDS that is the same in every lane, moved to a scalar register.
@@ -71,7 +71,7 @@ struct TickLds {
       };
       // fp8 single-query attention: each wave's tiles, staged by direct loads; after its last tile a wave's state
       // goes to the start of its own slots (STW floats)
-      uint8_t ring[4][FP8_PD][FP8_SLOT];
+      uint8_t ring[4][RSLOTS][RSLOT];
     } a;
   } u;
   alignas(16) float r[MTMAX * 16];  // RMSNorm row scales of the chunk
@@ -1157,6 +1157,88 @@ __device__ __forceinline__ void read_tile_fp8(const uint8_t* slot, RawTile<1>& t
   for (int j = 0; j < 8; ++j) t.v[j] = make_uint2(vv[j].x, vv[j].y);
 }
 
+// bf16 tile staged into two LDS slots with direct loads of whole 256-byte rows (4 rows per instruction): slot h holds
+// rows 16h .. 16h+15, K rows [16][256 B] then V rows [16][256 B]; the 16-byte chunk k of row r sits at chunk position
+// k ^ (r & 15) (the 16 rows of a K fragment read, and the 4 rows of a V fragment read, fall in distinct banks).  Lane
+// l of instruction q brings row 4q + l/16 into chunk position l % 16.  Rows past i1 repeat row i0.
+__device__ __forceinline__ void stage_tile_bf16(const char* kb, const char* vb, int64_t start, int64_t cap, int i0,
+                                                int r0, int i1, uint8_t* slot) {
+  const int lane = tix() & 63, rl = lane >> 4, pc = lane & 15;
+  asm volatile("" ::: "memory");  // after every read of the slots' previous tile
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int r = 4 * q + rl;  // row of the tile, 0..31
+    int64_t row = start + (r0 + r < i1 ? r0 + r : i0);
+    if (row >= cap) row -= cap;
+    const int64_t off = row * DH * 2 + 16 * (pc ^ (r & 15));
+    uint8_t* dst = slot + (q >> 2) * RSLOT + (q & 3) * 1024;
+    load_lds16<false>(kb + off, dst);
+    load_lds16<false>(vb + off, dst + 16 * DH * 2);
+  }
+}
+// The RawTile<0> fragments of a staged bf16 tile: K row 16rt + c (slot rt, row c), channels 32k + 8grp (chunk 4k +
+// grp); V rows 4grp + j (slot j / 4), channels 8c .. 8c+7 (chunk c).  One asm block that waits for its own reads.
+__device__ __forceinline__ void read_tile_bf16(const uint8_t* slot, RawTile<0>& t) {
+  const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
+  const uint32_t s0 = lds_addr(slot);
+  uint32_t ak[4], av[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) ak[k] = s0 + c * 256 + 16 * ((4 * k + grp) ^ c);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) av[j] = s0 + 16 * 256 + (4 * grp + j) * 256 + 16 * (c ^ (4 * grp + j));
+  u32x4_t k0, k1, k2, k3, k4, k5, k6, k7, v0, v1, v2, v3, v4, v5, v6, v7;
+  asm volatile(
+      "ds_read_b128 %0, %16\n\t"
+      "ds_read_b128 %1, %17\n\t"
+      "ds_read_b128 %2, %18\n\t"
+      "ds_read_b128 %3, %19\n\t"
+      "ds_read_b128 %4, %16 offset:8192\n\t"
+      "ds_read_b128 %5, %17 offset:8192\n\t"
+      "ds_read_b128 %6, %18 offset:8192\n\t"
+      "ds_read_b128 %7, %19 offset:8192\n\t"
+      "ds_read_b128 %8, %20\n\t"
+      "ds_read_b128 %9, %21\n\t"
+      "ds_read_b128 %10, %22\n\t"
+      "ds_read_b128 %11, %23\n\t"
+      "ds_read_b128 %12, %20 offset:8192\n\t"
+      "ds_read_b128 %13, %21 offset:8192\n\t"
+      "ds_read_b128 %14, %22 offset:8192\n\t"
+      "ds_read_b128 %15, %23 offset:8192\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(k0), "=&v"(k1), "=&v"(k2), "=&v"(k3), "=&v"(k4), "=&v"(k5), "=&v"(k6), "=&v"(k7), "=&v"(v0), "=&v"(v1),
+        "=&v"(v2), "=&v"(v3), "=&v"(v4), "=&v"(v5), "=&v"(v6), "=&v"(v7)
+      : "v"(ak[0]), "v"(ak[1]), "v"(ak[2]), "v"(ak[3]), "v"(av[0]), "v"(av[1]), "v"(av[2]), "v"(av[3])
+      : "memory");
+  const u32x4_t kk[8] = {k0, k1, k2, k3, k4, k5, k6, k7}, vv[8] = {v0, v1, v2, v3, v4, v5, v6, v7};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    t.k[i] = as_u4(kk[i]);
+    t.v[i] = as_u4(vv[i]);
+  }
+}
+template <int KT>
+__device__ __forceinline__ void stage_tile(const char* kb, const char* vb, int64_t start, int64_t cap, int i0, int r0,
+                                           int i1, uint8_t* slot) {
+  if constexpr (KT == 0)
+    stage_tile_bf16(kb, vb, start, cap, i0, r0, i1, slot);
+  else
+    stage_tile_fp8(kb, vb, start, cap, i0, r0, i1, slot);
+}
+template <int KT>
+__device__ __forceinline__ void read_tile(const uint8_t* slot, RawTile<KT>& t) {
+  if constexpr (KT == 0)
+    read_tile_bf16(slot, t);
+  else
+    read_tile_fp8(slot, t);
+}
+// Ring geometry: slots per tile, tiles the ring holds, direct-load instructions per tile.
+template <int KT>
+struct RingOf {
+  static constexpr int spt = KT == 0 ? 2 : 1;
+  static constexpr int tiles = RSLOTS / spt;
+  static constexpr int loads = KT == 0 ? 16 : 8;
+};
+
 // The tiles of one unit for query tiles tt0 .. tt0+nq-1 (nq <= NQ): wave w takes cache tiles w, w+4, ..., kept
 // PD deep in registers, then the own-row tiles that continue the same round robin; the states are merged
 // through LDS and written out (normalised if the agent has one range, else as the partial of this range).
@@ -1168,11 +1250,12 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
   const uint64_t st = stamp_of(a, l, dm.n_layers);
   // this wave's cache tiles: j = wave + 4 i, i < nc
   const int nc = U.nct > wave ? (U.nct - wave + 3) / 4 : 0;
-  constexpr bool LDS_RING = KT == 1 && NQ == 1;  // fp8, one query tile: tiles staged in LDS by direct loads
+  constexpr bool LDS_RING = NQ == 1;  // one query tile: tiles staged in LDS by direct loads
+  using RG = RingOf<KT>;
   uint8_t* lring = L.u.a.ring[wave][0];
-  auto stage_tile = [&](int i) {
-    stage_tile_fp8(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * (wave + 4 * i), U.i1,
-                   lring + (i % FP8_PD) * FP8_SLOT);
+  auto slot_of = [&](int i) { return lring + (i % RG::tiles) * RG::spt * RSLOT; };
+  auto ring_tile = [&](int i) {
+    stage_tile<KT>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * (wave + 4 * i), U.i1, slot_of(i));
   };
   RawTile<KT> ring[LDS_RING ? 1 : PD];
   auto cache_tile = [&](int i, RawTile<KT>& t) {
@@ -1184,8 +1267,8 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
   auto prefetch = [&]() {
     if constexpr (LDS_RING) {
 #pragma unroll
-      for (int dd = 0; dd < FP8_PD; ++dd)
-        if (dd < nc) stage_tile(dd);
+      for (int dd = 0; dd < RG::tiles; ++dd)
+        if (dd < nc) ring_tile(dd);
     } else {
 #pragma unroll
       for (int dd = 0; dd < PD; ++dd)
@@ -1220,26 +1303,26 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
     return *reinterpret_cast<const uint4*>(&L.u.a.qs[tt * 16 + c16][32 * k + 8 * grp]);
   };
   if constexpr (LDS_RING) {
-    // Pairs of tiles (i, i + 1) in slots i % 4, i % 4 + 1.  The memory operations issued after tile i + 1 are the
-    // direct loads (8 per tile) of tiles i + 2 and i + 3, so at most 8 per such tile pending means the pair has
-    // landed; once both are read into registers their slots take tiles i + 4 and i + 5, which stream in while
-    // the pair is computed.
-    static_assert(FP8_PD == 4, "the pair loop uses four slots");
+    // Pairs of tiles (i, i + 1) at ring places i % T, i % T + 1 (T = tiles the ring holds).  The memory operations
+    // issued after tile i + 1 are the direct loads of tiles i + 2 .. i + T - 1, so once at most that many loads are
+    // pending the pair has landed; once both are read into registers their places take tiles i + T and i + T + 1,
+    // which stream in while the pair is computed.
+    static_assert(RG::tiles == 2 || RG::tiles == 4, "the waits below cover rings of two or four tiles");
 #pragma unroll 1
     for (int i = 0; i < nc; i += 2) {
       const bool two = i + 1 < nc;
-      const int after = min(nc - 2 - i, 2);  // tiles in flight behind the pair (when two)
+      const int after = RG::tiles == 4 ? min(nc - 2 - i, 2) : 0;  // tiles in flight behind the pair (when two)
       if (two && after == 2)
-        vm_wait_below_c<16>();
+        vm_wait_below_c<2 * RG::loads>();
       else if (two && after == 1)
-        vm_wait_below_c<8>();
+        vm_wait_below_c<RG::loads>();
       else
         vm_wait_all();
       RawTile<KT> ta, tb;
-      read_tile_fp8(lring + (i % FP8_PD) * FP8_SLOT, reinterpret_cast<RawTile<1>&>(ta));
-      if (two) read_tile_fp8(lring + (i % FP8_PD + 1) * FP8_SLOT, reinterpret_cast<RawTile<1>&>(tb));
-      if (i + 4 < nc) stage_tile(i + 4);
-      if (i + 5 < nc) stage_tile(i + 5);
+      read_tile<KT>(slot_of(i), ta);
+      if (two) read_tile<KT>(slot_of(i + 1), tb);
+      if (i + RG::tiles < nc) ring_tile(i + RG::tiles);
+      if (i + RG::tiles + 1 < nc) ring_tile(i + RG::tiles + 1);
       if (two)
         tile_pair_compute<KT>(ta, tb, qr, U.i0 + 32 * (wave + 4 * i), U.i0 + 32 * (wave + 4 * (i + 1)), U.i1, U.ksc,
                               o[0], m_run[0], l_run[0]);
