@@ -288,7 +288,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
         {(void**)&t.f_q, (size_t)3 * A / 16 * FPAD * 8},
         {(void**)&t.f_attn, (size_t)nflag_attn * n_tt_max * FPAD * 8},
         {(void**)&t.f_rng, (size_t)ex->items_max * FPAD * 8},
-        {(void**)&t.f_z, (size_t)F / 8 * FPAD * 8},
+        {(void**)&t.f_z, (size_t)F / 8 * ((M + 79) / 80) * FPAD * 8},
         {(void**)&t.status, 256}};
     parts.insert(parts.end(), tp.begin(), tp.end());
   }

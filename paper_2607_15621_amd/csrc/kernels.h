@@ -144,7 +144,7 @@ struct TickArgs {
   uint64_t* f_q;       // [3A/16]
   uint64_t* f_attn;    // [B*H][n_tt] per query tile
   uint64_t* f_rng;     // [slot] partial states written
-  uint64_t* f_z;       // [F/8]
+  uint64_t* f_z;       // [F/8][row blocks of 80 rows]
   uint64_t* status;
   uint64_t epoch;
   uint64_t timeout_ticks;  // real-time counter ticks (100 MHz)

@@ -1530,11 +1530,17 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
 }
 
 // ------------------------------------------------------------------------------------------ O (+ R1)
-// Column tile i (owner: slot i mod n) of the output projection over X's attention columns, as stamped partial
-// words; then the reduction of tile i over the XCDs into h_mid.
+// The row-split projections (O, F1, D) work on items (column tile or unit k, row block r) of MTMAX*16 rows,
+// item = k * R + r with R row blocks; workgroup s takes items s, s + n, ... (when n is a multiple of R, all of one
+// workgroup's items share a row block, which it stages once).  With more than one row block this halves (or more)
+// the rows a workgroup stages and multiplies, against every workgroup taking all rows of fewer tiles.
+__device__ __forceinline__ int row_blocks(int M) { return (M + MTMAX * 16 - 1) / (MTMAX * 16); }
+
+// Column tile k (of the residual) of the output projection over X's attention columns, rows of block r, as stamped
+// partial words; then the reduction of every tile i this workgroup owns (slot i mod n) over the XCDs into h_mid.
 __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
-  const int d = dm.d, M = tp.M, A = dm.A, H = dm.H, nt = d / 16;
+  const int d = dm.d, M = tp.M, A = dm.A, H = dm.H, nt = d / 16, R = row_blocks(M);
   const int h0 = head_lo(X, NX, H), nh = head_lo(X + 1, NX, H) - h0;
   const int kb0 = h0 * (DH / 32), nkb = nh * (DH / 32);  // <= 16
   const uint64_t st = stamp_of(a, l, dm.n_layers);
@@ -1542,40 +1548,42 @@ __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams&
   const LayerW W = layer_w(a, dm, l);
   uint64_t* po = a.po + (int64_t)X * nt * tp.Mp * 16;
   bool first = true;
-  for (int i = s; i < nt; i += n) {
+  int staged = -1;  // row block in L.x
+  for (int item = s; item < nt * R; item += n) {
+    const int k = item / R, r = item % R;
     uint4 w[4];
-    load_unit_w(W.wo + (int64_t)i * (A / 32) * WAVE, kb0, nkb, w);
-    if (nh > 0 && !wg_wait(a.f_attn + (int64_t)h0 * tp.n_tt * FPAD, tp.B * nh * tp.n_tt, st, a, L, nh * tp.n_tt,
-                           H * tp.n_tt))
+    load_unit_w(W.wo + (int64_t)k * (A / 32) * WAVE, kb0, nkb, w);
+    if (first && nh > 0 &&
+        !wg_wait(a.f_attn + (int64_t)h0 * tp.n_tt * FPAD, tp.B * nh * tp.n_tt, st, a, L, nh * tp.n_tt, H * tp.n_tt))
       return false;
     if (first) TICK_SUB(l, 5);
-    for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
-      const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      if (nh > 0) stage(a.attn + h0 * DH, A, m0, rows, nh * DH, nullptr, 0, 0, 0.f, L);
-      unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
+    const int m0 = r * MTMAX * 16, rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
+    if (nh > 0 && staged != r) stage(a.attn + h0 * DH, A, m0, rows, nh * DH, nullptr, 0, 0, 0.f, L);
+    staged = r;
+    unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = m0 + mt * 16 + 4 * grp + r;
-          if (row < M)
-            st_dev(po + ((int64_t)i * tp.Mp + row) * 16 + c, ((uint64_t)st32 << 32) | __float_as_uint(sacc[r]));
-        }
-      });
-    }
+      for (int q = 0; q < 4; ++q) {
+        const int row = m0 + mt * 16 + 4 * grp + q;
+        if (row < M)
+          st_dev(po + ((int64_t)k * tp.Mp + row) * 16 + c, ((uint64_t)st32 << 32) | __float_as_uint(sacc[q]));
+      }
+    });
     if (first) TICK_SUB(l, 6);
+    first = false;
+  }
+  for (int i = s; i < nt; i += n)
     if (!reduce_tile(a, tp, dm, l, i, a.po, a.xb_mid + (int64_t)X * a.x_stride_b, a.ssq_mid + (int64_t)X * a.x_stride_s,
                      a.f_mid + (int64_t)X * XFLAGS * FPAD, nullptr, L))
       return false;
-    first = false;
-  }
   return true;
 }
 
 // ------------------------------------------------------------------------------------------ F1
-// Units u of X's FFN columns (8 gate + 8 up rows of the packed matrix -> 8 SwiGLU outputs each); workgroup s takes
-// units s, s + n, ...; the 4 waves split K and reduce through LDS.
+// Items (unit k of X's FFN columns: 8 gate + 8 up rows of the packed matrix -> 8 SwiGLU outputs, row block r); the 4
+// waves split K and reduce through LDS.  Each item publishes the flag f_z[unit * R + r].
 __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
-  const int d = dm.d, M = tp.M, F = dm.F, nt = d / 16;
+  const int d = dm.d, M = tp.M, F = dm.F, nt = d / 16, R = row_blocks(M);
   const int f0 = ffn_lo(X, NX, F), f1 = ffn_lo(X + 1, NX, F);
   const int u0 = f0 / 8, nu = (f1 - f0) / 8;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
@@ -1584,8 +1592,9 @@ __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams
   const float* ssq = a.ssq_mid + (int64_t)X * a.x_stride_s;
   const int KB = d / 32;
   bool waited = false;
-  for (int k = s; k < nu; k += n) {
-    const int u = u0 + k;
+  int staged = -1;
+  for (int item = s; item < nu * R; item += n) {
+    const int u = u0 + item / R, r = item % R;
     uint4 w[4];
     load_unit_w(W.wgu + (int64_t)u * KB * WAVE, 0, KB, w);
     if (!waited) {
@@ -1593,35 +1602,36 @@ __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams
       waited = true;
       TICK_SUB(l, 7);
     }
-    for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
-      const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      stage(xb, d, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
-      unit_gemm(w, KB, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
+    const int m0 = r * MTMAX * 16, rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
+    if (staged != r) stage(xb, d, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
+    staged = r;
+    unit_gemm(w, KB, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          sacc[r] *= L.r[mt * 16 + 4 * grp + r];  // RMSNorm row scale
-          const float up = xor8(sacc[r]);
-          const float gt = sacc[r];
-          const float zz = gt / (1.0f + expf(-gt)) * up;
-          const float zn = xor1(zz);
-          const int row = m0 + mt * 16 + 4 * grp + r;
-          if (c < 8 && (c & 1) == 0 && row < M)
-            st_loc(reinterpret_cast<uint32_t*>(a.z + (int64_t)row * F + u * 8 + c), pack_bf16x2(zz, zn));
-        }
-      });
-    }
-    if (k == s) TICK_SUB(l, 8);
+      for (int q = 0; q < 4; ++q) {
+        sacc[q] *= L.r[mt * 16 + 4 * grp + q];  // RMSNorm row scale
+        const float up = xor8(sacc[q]);
+        const float gt = sacc[q];
+        const float zz = gt / (1.0f + expf(-gt)) * up;
+        const float zn = xor1(zz);
+        const int row = m0 + mt * 16 + 4 * grp + q;
+        if (c < 8 && (c & 1) == 0 && row < M)
+          st_loc(reinterpret_cast<uint32_t*>(a.z + (int64_t)row * F + u * 8 + c), pack_bf16x2(zz, zn));
+      }
+    });
+    if (item == s) TICK_SUB(l, 8);
     stores_done();
     __syncthreads();
-    if (tix() == 0) st_loc(a.f_z + (int64_t)u * FPAD, st);
+    if (tix() == 0) st_loc(a.f_z + ((int64_t)u * R + r) * FPAD, st);
   }
   return true;
 }
 
 // ------------------------------------------------------------------------------------------ D (+ R2)
+// Items (column tile k, row block r) of the down projection over X's FFN columns, as stamped partial words; then the
+// reduction of every tile this workgroup owns into the layer output.
 __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
-  const int d = dm.d, M = tp.M, F = dm.F, nt = d / 16;
+  const int d = dm.d, M = tp.M, F = dm.F, nt = d / 16, R = row_blocks(M);
   const int f0 = ffn_lo(X, NX, F), f1 = ffn_lo(X + 1, NX, F);
   const int kb0 = f0 / 32, nkb = (f1 - f0) / 32;  // <= 16
   const uint64_t st = stamp_of(a, l, dm.n_layers);
@@ -1629,28 +1639,33 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
   const LayerW W = layer_w(a, dm, l);
   uint64_t* pd = a.pd + (int64_t)X * nt * tp.Mp * 16;
   float* hidden_l = (a.hidden && X == 0) ? a.hidden + (int64_t)l * M * d : nullptr;
-  for (int i = s; i < nt; i += n) {
+  bool waited = false;
+  int staged = -1;
+  for (int item = s; item < nt * R; item += n) {
+    const int k = item / R, r = item % R;
     uint4 w[4];
-    load_unit_w(W.wd + (int64_t)i * (F / 32) * WAVE, kb0, nkb, w);
-    if (nkb > 0 && !wg_wait(a.f_z + (int64_t)(f0 / 8) * FPAD, (f1 - f0) / 8, st, a, L)) return false;
-    if (i == s) TICK_SUB(l, 9);
-    for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
-      const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-      if (nkb > 0) stage(a.z + f0, F, m0, rows, f1 - f0, nullptr, 0, 0, 0.f, L);
-      unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
+    load_unit_w(W.wd + (int64_t)k * (F / 32) * WAVE, kb0, nkb, w);
+    if (!waited && nkb > 0 && !wg_wait(a.f_z + (int64_t)(f0 / 8) * R * FPAD, (f1 - f0) / 8 * R, st, a, L))
+      return false;
+    if (!waited) TICK_SUB(l, 9);
+    waited = true;
+    const int m0 = r * MTMAX * 16, rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
+    if (nkb > 0 && staged != r) stage(a.z + f0, F, m0, rows, f1 - f0, nullptr, 0, 0, 0.f, L);
+    staged = r;
+    unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = m0 + mt * 16 + 4 * grp + r;
-          if (row < M)
-            st_dev(pd + ((int64_t)i * tp.Mp + row) * 16 + c, ((uint64_t)st32 << 32) | __float_as_uint(sacc[r]));
-        }
-      });
-    }
-    if (i == s) TICK_SUB(l, 10);
+      for (int q = 0; q < 4; ++q) {
+        const int row = m0 + mt * 16 + 4 * grp + q;
+        if (row < M)
+          st_dev(pd + ((int64_t)k * tp.Mp + row) * 16 + c, ((uint64_t)st32 << 32) | __float_as_uint(sacc[q]));
+      }
+    });
+    if (item == s) TICK_SUB(l, 10);
+  }
+  for (int i = s; i < nt; i += n)
     if (!reduce_tile(a, tp, dm, l, i, a.pd, a.xb_out + (int64_t)X * a.x_stride_b, a.ssq_out + (int64_t)X * a.x_stride_s,
                      a.f_out + (int64_t)X * XFLAGS * FPAD, hidden_l, L))
       return false;
-  }
   return true;
 }
 
