@@ -437,7 +437,8 @@ __device__ __forceinline__ void wave_gemm(const uint4 w[16], int mt_n, TickLds& 
 // k < EB); all of its words are loaded before any is checked, then it polls its own stale words until their
 // stamps are right.  The new tile goes to hres (owner-private), to the row-major bf16 copy xb and the per-row
 // sums of squares ssq (read by the whole XCD), and, if given, to hidden; then the tile's flag is published.
-constexpr int EB = 4;  // element batches per pass: M <= 64 rows in one pass
+constexpr int EB = 4;  // element batches per pass: M <= 64 rows in one pass (EB * NXR bits of pending words)
+static_assert(EB * NXR <= 32, "the pending-word mask has 32 bits");
 __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, int i,
                                             const uint64_t* part, uint16_t* xb, float* ssq, uint64_t* flag,
                                             float* hidden_l, TickLds& L) {
@@ -1446,7 +1447,7 @@ __device__ __forceinline__ void attn_plan(const TickParams& tp, const Dims& dm, 
   __syncthreads();
 }
 
-template <int KT>
+template <int KT, bool MQ>
 __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   constexpr int ES = KT == 0 ? 2 : 1;
   const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
@@ -1492,7 +1493,7 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
       U.vsc = a.cv.v_scale[si];
     }
     bool ok = true;
-    if (n_tt == 1) {
+    if constexpr (!MQ) {
       ok = attn_unit<KT, 1, KT == 0 ? 2 : 4>(a, tp, dm, l, U, 0, 1, L);
     } else {
       for (int tt0 = 0; tt0 < n_tt && ok; tt0 += NQW)
@@ -1741,7 +1742,9 @@ __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& 
 }
 
 // ------------------------------------------------------------------------------------------ kernel
-template <int KT>
+// KT: cache element type (0 bf16, 1 fp8); MQ: more than one query tile per agent (S > 16).  Four instances, so that
+// each carries only the attention variant it runs (smaller code for the instruction cache).
+template <int KT, bool MQ>
 __global__ __launch_bounds__(NTHR, 1) void k_tick(TickArgs a, TickParams tp, Dims dm) {
   __shared__ TickLds L;
   const int nl = dm.n_layers;
@@ -1753,7 +1756,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_tick(TickArgs a, TickParams tp, Dim
   for (int l = 0; l < nl && ok; ++l) {
     ok = phase_qkv(a, tp, dm, l, L);
     trace_mark(a, 2 + 16 * l, nl);
-    ok = ok && phase_attn<KT>(a, tp, dm, l, L);
+    ok = ok && phase_attn<KT, MQ>(a, tp, dm, l, L);
     trace_mark(a, 3 + 16 * l, nl);
     ok = ok && phase_oproj(a, tp, dm, l, L);
     trace_mark(a, 4 + 16 * l, nl);
@@ -1766,14 +1769,27 @@ __global__ __launch_bounds__(NTHR, 1) void k_tick(TickArgs a, TickParams tp, Dim
   trace_mark(a, 2 + 16 * nl, nl);
 }
 
+static const void* tick_fn(int kt, bool mq) {
+  if (kt == 0) return mq ? (const void*)k_tick<0, true> : (const void*)k_tick<0, false>;
+  return mq ? (const void*)k_tick<1, true> : (const void*)k_tick<1, false>;
+}
+
 hipError_t tick_occupancy(int kt, int* blocks_per_cu) {
-  const void* f = kt == 0 ? (const void*)k_tick<0> : (const void*)k_tick<1>;
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, f, NTHR, 0);
+  // every instance must fit
+  int lo = 1 << 30;
+  for (int mq = 0; mq < 2; ++mq) {
+    int b = 0;
+    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, tick_fn(kt, mq != 0), NTHR, 0);
+    if (e != hipSuccess) return e;
+    lo = b < lo ? b : lo;
+  }
+  *blocks_per_cu = lo;
+  return hipSuccess;
 }
 
 hipError_t launch_tick(const TickArgs& a, const TickParams& tp, const Dims& dm, int grid, hipStream_t s) {
   void* args[] = {(void*)&a, (void*)&tp, (void*)&dm};
-  const void* f = a.cv.dtype == FSX_FP8_E4M3 ? (const void*)k_tick<1> : (const void*)k_tick<0>;
+  const void* f = tick_fn(a.cv.dtype == FSX_FP8_E4M3 ? 1 : 0, tp.n_tt > 1);
   return hipLaunchCooperativeKernel(f, dim3(grid), dim3(NTHR), args, 0, s);
 }
 
