@@ -1403,7 +1403,7 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
 // afterwards by separate items (agent, head, query tile) in a fixed order.  With little work (fewer than 16 tiles per
 // workgroup) and few segments, workgroup s takes segment s whole.  Equal slices keep every workgroup streaming until
 // the phase ends.
-constexpr int SEG_COST = 16;
+constexpr int SEG_COST = 24;
 __device__ __forceinline__ void attn_plan(const TickParams& tp, const Dims& dm, TickLds& L) {
   const int X = uni(L.X), NX = uni(L.NX), n = uni(L.n);
   const int nh = head_lo(X + 1, NX, dm.H) - head_lo(X, NX, dm.H);
