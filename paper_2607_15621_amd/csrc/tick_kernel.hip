@@ -437,8 +437,7 @@ __device__ __forceinline__ void wave_gemm(const uint4 w[16], int mt_n, TickLds& 
 // k < EB); all of its words are loaded before any is checked, then it polls its own stale words until their
 // stamps are right.  The new tile goes to hres (owner-private), to the row-major bf16 copy xb and the per-row
 // sums of squares ssq (read by the whole XCD), and, if given, to hidden; then the tile's flag is published.
-constexpr int EB = 4;  // element batches per pass: M <= 64 rows in one pass (EB * NXR bits of pending words)
-static_assert(EB * NXR <= 32, "the pending-word mask has 32 bits");
+constexpr int EB = 5;  // element batches per pass: M <= 80 rows in one pass
 __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, int i,
                                             const uint64_t* part, uint16_t* xb, float* ssq, uint64_t* flag,
                                             float* hidden_l, TickLds& L) {
@@ -449,23 +448,37 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
   const int64_t xs = (int64_t)nt * tp.Mp * 16;  // words between the partials of two XCDs
   bool ok = true;
   for (int e0 = 0; e0 < M * 16 && ok; e0 += EB * NTHR) {
+    // Batch k is skipped as a whole when none of its elements exists; in a partial batch the threads past the
+    // end load the last element (in bounds) and ignore it, so no load depends on a per-thread branch.  Words
+    // are used only where use[k] bit x is set (x < NX and the element exists).
     uint64_t v[EB][NXR];
     float hold[EB];
+    uint32_t use[EB], pend[EB];
 #pragma unroll
     for (int k = 0; k < EB; ++k) {
       const int e = e0 + k * NTHR + tix();
-      const bool in = e < M * 16;
-      const uint64_t* src = part + (int64_t)i * tp.Mp * 16 + e;
+      const uint64_t* src = part + (int64_t)i * tp.Mp * 16 + min(e, M * 16 - 1);
+      use[k] = e < M * 16 ? (1u << NX) - 1 : 0u;
+      if (e0 + k * NTHR < M * 16) {
 #pragma unroll
-      for (int x = 0; x < NXR; ++x) v[k][x] = (x < NX && in) ? ld_dev(src + x * xs) : ((uint64_t)st32 << 32);
-      hold[k] = in ? hres[e] : 0.f;
+        for (int x = 0; x < NXR; ++x) v[k][x] = ld_dev(src + (x < NX ? x : 0) * xs);
+        hold[k] = hres[min(e, M * 16 - 1)];
+      } else {
+#pragma unroll
+        for (int x = 0; x < NXR; ++x) v[k][x] = 0;
+        hold[k] = 0.f;
+      }
     }
-    uint32_t pending = 0;
+    bool pending = false;
 #pragma unroll
-    for (int k = 0; k < EB; ++k)
+    for (int k = 0; k < EB; ++k) {
+      pend[k] = 0;
 #pragma unroll
       for (int x = 0; x < NXR; ++x)
-        if ((uint32_t)(v[k][x] >> 32) != st32) pending |= 1u << (k * NXR + x);
+        if ((uint32_t)(v[k][x] >> 32) != st32) pend[k] |= 1u << x;
+      pend[k] &= use[k];
+      pending = pending || pend[k] != 0;
+    }
     if (pending) {
       const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
       for (uint32_t spin = 0; pending; ++spin) {
@@ -475,13 +488,16 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
           const uint64_t* src = part + (int64_t)i * tp.Mp * 16 + e0 + k * NTHR + tix();
 #pragma unroll
           for (int x = 0; x < NXR; ++x)
-            if (pending & (1u << (k * NXR + x))) v[k][x] = ld_dev(src + x * xs);
+            if (pend[k] & (1u << x)) v[k][x] = ld_dev(src + x * xs);
         }
+        pending = false;
 #pragma unroll
-        for (int k = 0; k < EB; ++k)
+        for (int k = 0; k < EB; ++k) {
 #pragma unroll
           for (int x = 0; x < NXR; ++x)
-            if ((uint32_t)(v[k][x] >> 32) == st32) pending &= ~(1u << (k * NXR + x));
+            if ((uint32_t)(v[k][x] >> 32) == st32) pend[k] &= ~(1u << x);
+          pending = pending || pend[k] != 0;
+        }
         if (pending && timed_out(a, t0, spin)) {
           st_dev(a.status, fail_tag(a));
           ok = false;
@@ -492,12 +508,12 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
 #pragma unroll
     for (int k = 0; k < EB; ++k) {
       const int e = e0 + k * NTHR + tix();
-      const bool in = e < M * 16;
+      const bool in = use[k] != 0;
       const int m = e >> 4, c = e & 15;
       float acc = 0.f;
 #pragma unroll
       for (int x = 0; x < NXR; ++x)
-        if (x < NX) acc += __uint_as_float((uint32_t)v[k][x]);
+        if (use[k] & (1u << x)) acc += __uint_as_float((uint32_t)v[k][x]);
       const float hv = hold[k] + acc;
       if (in) {
         hres[e] = hv;
