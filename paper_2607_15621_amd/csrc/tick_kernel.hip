@@ -49,8 +49,8 @@ constexpr int NTHR = 256;
 constexpr int MTMAX = 5;   // 16-row tiles per staged chunk (80 rows)
 constexpr int DH = 128;    // head width of the fused path
 constexpr int STW = 16 * DH + 32;  // LDS floats of one wave's attention state: O[16][128], (m, l)[16]
-constexpr int NQW = 3;     // query tiles a wave carries at once in the many-query attention variant
-constexpr int RSLOTS = 4;     // single-query attention: LDS ring slots per wave
+constexpr int NQW = 6;     // many-query attention: query tiles per pass over the cache (96 queries)
+constexpr int RSLOTS = 4;     // attention: LDS ring slots per wave
 constexpr int RSLOT = 8192;   // bytes of one slot: an fp8 tile (32 rows) or half a bf16 tile (16 rows), K then V
 constexpr int NSEG = FSX_MAX_BATCH * 4;  // attention segments (agent, local head) of one XCD, at most
 
@@ -64,13 +64,9 @@ struct TickLds {
       f32x4 red[4][MTMAX][WAVE];       // cross-wave reduction of projection accumulators
       float rq[4][MTMAX * 16][8][2];   // q/k projection: each wave's rotary slice (cos, sin of its 8 pairs) per row
     } p;
-    union {
-      struct {
-        float st[4][STW];               // per-wave attention states
-        uint16_t qs[NQW * 16][DH + 8];  // many-query attention: the unit's query tiles (bf16 or fp16)
-      };
-      // fp8 single-query attention: each wave's tiles, staged by direct loads; after its last tile a wave's state
-      // goes to the start of its own slots (STW floats)
+    struct {
+      // attention: each wave's cache tiles, staged by direct loads; after its last tile a wave's state goes to the
+      // start of its own slots (STW floats)
       uint8_t ring[4][RSLOTS][RSLOT];
     } a;
   } u;
@@ -673,11 +669,11 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
 }
 
 // ------------------------------------------------------------------------------------------ A
-// Raw registers of one 32-row tile, as loaded.  bf16: k[rt*4 + kb] = K row r0+16rt+c, channels 32kb+8grp..+7;
+// Registers of one 32-row tile, as read from its LDS slots.  bf16: k[rt*4 + kb] = K row r0+16rt+c, channels 32kb+8grp..+7;
 // fp8: k[rt*2 + h] = K row r0+16rt+c, channels 64h+16grp..+15 (16 bytes; the k-blocks of the score MFMA then
 // hold channels 64(kb/2) + 16grp + 8(kb%2) + j, and the fp16 queries use the same order).  v[j] = V row
-// r0 + (j<4 ? 4grp+j : 16+4grp+j-4), channels 8c..8c+7.  fp8 tiles hold the codes and are decoded only when
-// the tile is used, so the loads of the following tiles stay in flight meanwhile.
+// r0 + (j<4 ? 4grp+j : 16+4grp+j-4), channels 8c..8c+7.  fp8 tiles hold the codes, decoded when the tile is
+// used.
 template <int KT>
 struct RawTile;
 template <>
@@ -690,41 +686,6 @@ struct RawTile<1> {
   uint4 k[4];
   uint2 v[8];
 };
-
-// Cache tile at ring rows [r0, r0+32) of a (agent, layer, head) slab; rows at or past i1 load row i0 (they are
-// masked out of the softmax).
-template <int KT>
-__device__ __forceinline__ void load_cache_tile(const char* kb, const char* vb, int64_t start, int64_t cap, int i0,
-                                                int r0, int i1, RawTile<KT>& t) {
-  constexpr int ES = KT == 0 ? 2 : 1;
-  constexpr int64_t RB = DH * ES;
-  const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
-  auto roff = [&](int i) -> int64_t {
-    int64_t slot = start + (i < i1 ? i : i0);
-    if (slot >= cap) slot -= cap;
-    return slot * RB;
-  };
-#pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    const char* p = kb + roff(r0 + 16 * rt + c);
-    if constexpr (KT == 0) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) t.k[rt * 4 + k] = *reinterpret_cast<const uint4*>(p + (32 * k + 8 * grp) * 2);
-    } else {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) t.k[rt * 2 + h] = *reinterpret_cast<const uint4*>(p + 64 * h + 16 * grp);
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int rr = r0 + (j < 4 ? 4 * grp + j : 16 + 4 * grp + (j - 4));
-    const char* p = vb + roff(rr) + 8 * c * ES;
-    if constexpr (KT == 0)
-      t.v[j] = *reinterpret_cast<const uint4*>(p);
-    else
-      t.v[j] = *reinterpret_cast<const uint2*>(p);
-  }
-}
 
 // Own-row tile (the expert's rows [r0, r0+32) of S, bf16, produced in this launch): device-scope loads.
 __device__ __forceinline__ void load_own_tile(const char* ks, const char* vs, int64_t srow, int r0, int S,
@@ -744,15 +705,15 @@ __device__ __forceinline__ void load_own_tile(const char* ks, const char* vs, in
   }
 }
 
-// Query fragments of query tiles tt0 .. tt0+nq-1 of agent b, head h (16 queries x 128 channels each, B operand
+// Query fragments of query tiles tts[j] (j < nq) of agent b, head h (16 queries x 128 channels each, B operand
 // of S^T = K Q^T): bf16 in plain channel order (F16 = false), or fp16 in the channel order of fp8 key tiles.
 template <int NQ, bool F16>
-__device__ __forceinline__ void load_q(const TickArgs& a, const TickParams& tp, const Dims& dm, int b, int h, int tt0,
-                                       int nq, uint4 (&q)[NQ][4]) {
+__device__ __forceinline__ void load_q(const TickArgs& a, const TickParams& tp, const Dims& dm, int b, int h,
+                                       const int (&tts)[NQ], int nq, uint4 (&q)[NQ][4]) {
   const int lane = tix() & 63, grp = lane >> 4;
 #pragma unroll
   for (int tt = 0; tt < NQ; ++tt) {
-    const int t = (tt0 + tt) * 16 + (lane & 15);
+    const int t = tts[tt] * 16 + (lane & 15);
     const bool tv = tt < nq && t < tp.S;
     const float* row = a.q + ((int64_t)b * tp.S + (tv ? t : 0)) * dm.A + (int64_t)h * DH;
     // every load first, then the conversions
@@ -776,120 +737,9 @@ __device__ __forceinline__ void load_q(const TickArgs& a, const TickParams& tp, 
   }
 }
 
-// The unit's query tiles tt0 .. tt0+nq-1 into LDS rows (16 per tile) of 128 channels, bf16 or fp16; ends
-// with a barrier.
-template <bool F16>
-__device__ __forceinline__ void load_q_lds(const TickArgs& a, const TickParams& tp, const Dims& dm, int b, int h,
-                                           int tt0, int nq, TickLds& L) {
-  for (int i = tix(); i < nq * 16 * (DH / 8); i += NTHR) {
-    const int row = i / (DH / 8), c8 = (i % (DH / 8)) * 8;
-    const int t = tt0 * 16 + row;
-    float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
-    if (t < tp.S) {
-      const float* src = a.q + ((int64_t)b * tp.S + t) * dm.A + (int64_t)h * DH + c8;
-      lo = ld_dev_f4(src);
-      hi = ld_dev_f4(src + 4);
-    }
-    uint4 v;
-    if (F16)
-      v = make_uint4(pack_f16x2(lo.x, lo.y), pack_f16x2(lo.z, lo.w), pack_f16x2(hi.x, hi.y), pack_f16x2(hi.z, hi.w));
-    else
-      v = make_uint4(pack_bf16x2(lo.x, lo.y), pack_bf16x2(lo.z, lo.w), pack_bf16x2(hi.x, hi.y), pack_bf16x2(hi.z, hi.w));
-    *reinterpret_cast<uint4*>(&L.u.a.qs[row][c8]) = v;
-  }
-  __syncthreads();
-}
-
-// Online-softmax update of the states of the nq query tiles with one tile whose rows r0.. (valid below i1)
-// are in t; qf(tt, kb) returns the B-operand fragment kb of query tile tt.  fp8 tiles (KT 1) are decoded to
-// fp16 (exact) and use fp16 MFMA; their key scale multiplies the fp32 scores (the value scale is applied to
-// the output once, after the cache tiles).  The running max of a query only moves when a score exceeds it
-// by more than 2^8 (log2 units), so the accumulators are rescaled rarely; probabilities stay below 2^8.
-constexpr float RESCALE_LOG2 = 8.0f;
-template <int KT, int NQ, typename QF>
-__device__ __forceinline__ void tile_compute(const RawTile<KT>& t, QF qf, int nq, int r0, int i1, float kscale,
-                                             f32x4 (&o)[NQ][8], float (&m_run)[NQ], float (&l_run)[NQ]) {
-  constexpr bool F16 = KT == 1;
-  const int lane = tix() & 63, grp = lane >> 4;
-  uint4 kf[8], vr[8];
-  if constexpr (KT == 0) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      kf[i] = t.k[i];
-      vr[i] = t.v[i];
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      kf[2 * i] = make_uint4(e4m3x2_to_f16x2(t.k[i].x, false), e4m3x2_to_f16x2(t.k[i].x, true),
-                             e4m3x2_to_f16x2(t.k[i].y, false), e4m3x2_to_f16x2(t.k[i].y, true));
-      kf[2 * i + 1] = make_uint4(e4m3x2_to_f16x2(t.k[i].z, false), e4m3x2_to_f16x2(t.k[i].z, true),
-                                 e4m3x2_to_f16x2(t.k[i].w, false), e4m3x2_to_f16x2(t.k[i].w, true));
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      vr[i] = make_uint4(e4m3x2_to_f16x2(t.v[i].x, false), e4m3x2_to_f16x2(t.v[i].x, true),
-                         e4m3x2_to_f16x2(t.v[i].y, false), e4m3x2_to_f16x2(t.v[i].y, true));
-  }
-  uint4 vt[8];
-  transpose8x8_b16(vr, vt);
-#pragma unroll
-  for (int tt = 0; tt < NQ; ++tt) {
-    if (tt < nq) {
-      f32x4 s[2];
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        s[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const uint4 qk = qf(tt, k);
-          s[rt] = F16 ? mfma_f16(kf[rt * 4 + k], qk, s[rt]) : mfma_bf16(kf[rt * 4 + k], qk, s[rt]);
-        }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int rr = r0 + 16 * rt + 4 * grp + i;
-          const float v = rr < i1 ? (KT == 1 ? s[rt][i] * kscale : s[rt][i]) : -INFINITY;
-          s[rt][i] = v;
-          mx = fmaxf(mx, v);
-        }
-      mx = rows_max(mx);
-      const bool grow = mx > m_run[tt] + RESCALE_LOG2;
-      if (__any(grow)) {
-        const float m_new = grow ? mx : m_run[tt];
-        const float alpha = exp2f(m_run[tt] - m_new);
-        l_run[tt] *= alpha;
-        m_run[tt] = m_new;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float a_i = shfl(alpha, 4 * grp + i);
-#pragma unroll
-          for (int k = 0; k < 8; ++k) o[tt][k][i] *= a_i;
-        }
-      }
-      float p[8], ps = 0.f;
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          p[rt * 4 + i] = exp2f(s[rt][i] - m_run[tt]);
-          ps += p[rt * 4 + i];
-        }
-      l_run[tt] += ps;
-      uint4 pf;
-      if (F16)
-        pf = make_uint4(pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3]), pack_f16x2(p[4], p[5]), pack_f16x2(p[6], p[7]));
-      else
-        pf = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
-                        pack_bf16x2(p[6], p[7]));
-#pragma unroll
-      for (int k = 0; k < 8; ++k) o[tt][k] = F16 ? mfma_f16(pf, vt[k], o[tt][k]) : mfma_bf16(pf, vt[k], o[tt][k]);
-    }
-  }
-}
+// 2^x by the hardware instruction (about 1 ulp; results below the normal range are flushed to zero, which only
+// drops probabilities under 2^-126).
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // MFMA operands of one raw tile: K fragments kf (A operand of S^T = K Q^T) and V transposed to per-channel
 // vectors vt (B operand of O += P V); fp8 codes are decoded to fp16 (exact).
@@ -918,6 +768,106 @@ __device__ __forceinline__ void tile_operands(const RawTile<KT>& t, uint4 (&kf)[
   transpose8x8_b16(vr, vt);
 }
 
+// Online-softmax update of NJ query-tile states ("jobs") with one tile whose rows r0.. (valid below i1) are in t;
+// job j takes part when bit j of ACT is set, and qf(j, kb) returns the B-operand fragment kb of its queries.  The
+// steps run for all jobs together (scores, then maxima, then one rescale test, then probabilities, then P V), so
+// the independent work of the jobs can overlap.  fp8 tiles (KT 1) are decoded to fp16 (exact) and use fp16 MFMA;
+// their key scale multiplies the fp32 scores (the value scale is applied to the output once, after the cache
+// tiles).  The running max of a query only moves when a score exceeds it by more than 2^8 (log2 units), so the
+// accumulators are rescaled rarely; probabilities stay below 2^8.  Rows at or past i1 are masked only in a tile
+// that reaches past i1.
+constexpr float RESCALE_LOG2 = 8.0f;
+template <int KT, int NJ, int ACT, typename QF>
+__device__ __forceinline__ void tile_jobs(const RawTile<KT>& t, QF qf, int r0, int i1, float kscale,
+                                          f32x4 (&o)[NJ][8], float (&m_run)[NJ], float (&l_run)[NJ]) {
+  constexpr bool F16 = KT == 1;
+  const int lane = tix() & 63, grp = lane >> 4;
+  uint4 kf[8], vt[8];
+  tile_operands<KT>(t, kf, vt);
+  f32x4 s[NJ][2];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) s[j][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (ACT >> j & 1) {
+        const uint4 qk = qf(j, k);
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+          s[j][rt] = F16 ? mfma_f16(kf[rt * 4 + k], qk, s[j][rt]) : mfma_bf16(kf[rt * 4 + k], qk, s[j][rt]);
+      }
+  if (KT == 1)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) s[j][rt] *= kscale;
+  if (r0 + 32 > i1) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (r0 + 16 * rt + 4 * grp + i >= i1) s[j][rt][i] = -INFINITY;
+  }
+  float mx[NJ];
+  bool grow = false;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    mx[j] = -INFINITY;
+    if (ACT >> j & 1) {
+      mx[j] = fmaxf(fmaxf(fmaxf(s[j][0][0], s[j][0][1]), fmaxf(s[j][0][2], s[j][0][3])),
+                    fmaxf(fmaxf(s[j][1][0], s[j][1][1]), fmaxf(s[j][1][2], s[j][1][3])));
+      mx[j] = rows_max(mx[j]);
+      grow = grow || mx[j] > m_run[j] + RESCALE_LOG2;
+    }
+  }
+  if (__any(grow)) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (ACT >> j & 1) {
+        const float m_new = mx[j] > m_run[j] + RESCALE_LOG2 ? mx[j] : m_run[j];
+        const float alpha = exp2_fast(m_run[j] - m_new);
+        l_run[j] *= alpha;
+        m_run[j] = m_new;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float a_i = shfl(alpha, 4 * grp + i);
+#pragma unroll
+          for (int k = 0; k < 8; ++k) o[j][k][i] *= a_i;
+        }
+      }
+  }
+  uint4 pf[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    if (ACT >> j & 1) {
+      float p[8], ps = 0.f;
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          p[rt * 4 + i] = exp2_fast(s[j][rt][i] - m_run[j]);
+          ps += p[rt * 4 + i];
+        }
+      l_run[j] += ps;
+      if (F16)
+        pf[j] = make_uint4(pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3]), pack_f16x2(p[4], p[5]),
+                           pack_f16x2(p[6], p[7]));
+      else
+        pf[j] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                           pack_bf16x2(p[6], p[7]));
+    }
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (ACT >> j & 1) o[j][k] = F16 ? mfma_f16(pf[j], vt[k], o[j][k]) : mfma_bf16(pf[j], vt[k], o[j][k]);
+}
+
 // One query tile, two cache tiles at once (64 rows): the score MFMAs of both tiles are independent, one running-max
 // update covers both, and both P V products accumulate into the same output.  Twice the data per dependent chain
 // of the single-tile update (the wave is the only one on its SIMD, so nothing else hides that chain).
@@ -941,21 +891,25 @@ __device__ __forceinline__ void tile_pair_compute(const RawTile<KT>& ta, const R
       s[2 + rt] = F16 ? mfma_f16(kfb[rt * 4 + k], q[k], s[2 + rt]) : mfma_bf16(kfb[rt * 4 + k], q[k], s[2 + rt]);
     }
   }
-  float mx = -INFINITY;
+  if (KT == 1)
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 4; ++j) s[j] *= kscale;
+  if (rb + 32 > i1) {  // tile b ends past i1 (tile a lies before b)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int rr = (j < 2 ? ra : rb) + 16 * (j & 1) + 4 * grp + i;
-      const float v = rr < i1 ? (KT == 1 ? s[j][i] * kscale : s[j][i]) : -INFINITY;
-      s[j][i] = v;
-      mx = fmaxf(mx, v);
-    }
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if ((j < 2 ? ra : rb) + 16 * (j & 1) + 4 * grp + i >= i1) s[j][i] = -INFINITY;
+  }
+  float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                   fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+  mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(s[2][0], s[2][1]), fmaxf(s[2][2], s[2][3])),
+                       fmaxf(fmaxf(s[3][0], s[3][1]), fmaxf(s[3][2], s[3][3]))));
   mx = rows_max(mx);
   const bool grow = mx > m_run + RESCALE_LOG2;
   if (__any(grow)) {
     const float m_new = grow ? mx : m_run;
-    const float alpha = exp2f(m_run - m_new);
+    const float alpha = exp2_fast(m_run - m_new);
     l_run *= alpha;
     m_run = m_new;
 #pragma unroll
@@ -970,7 +924,7 @@ __device__ __forceinline__ void tile_pair_compute(const RawTile<KT>& ta, const R
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      p[j * 4 + i] = exp2f(s[j][i] - m_run);
+      p[j * 4 + i] = exp2_fast(s[j][i] - m_run);
       ps += p[j * 4 + i];
     }
   l_run += ps;
@@ -1018,26 +972,23 @@ struct AUnit {
   float ksc, vsc;   // fp8 scales
 };
 
+// Where wave w's attention state goes: the start of its slots of the LDS tile ring.
+static_assert(STW * 4 <= RSLOTS * RSLOT, "a wave's state fits in its ring slots");
+__device__ __forceinline__ float* state_of(TickLds& L, int w) { return reinterpret_cast<float*>(&L.u.a.ring[w][0][0]); }
 // Merge the 4 waves' LDS states of query tile tt: each thread owns (t, 8 channels).  If final, normalise into
 // the attention output; else store the unnormalised partial of slot `item`.
-// Where wave w's attention state goes: its slots of the LDS tile ring (RING) or the state array.
-template <bool RING>
-__device__ __forceinline__ float* state_of(TickLds& L, int w) {
-  return RING ? reinterpret_cast<float*>(&L.u.a.ring[w][0][0]) : L.u.a.st[w];
-}
-template <bool RING = false>
 __device__ __forceinline__ void merge_states(const TickArgs& a, const TickParams& tp, const Dims& dm,
                                              const AUnit& U, int tt, bool final_out, int64_t item, TickLds& L) {
   const int t = tix() >> 4, d0 = (tix() & 15) * 8;
   float Mx = -INFINITY;
 #pragma unroll
-  for (int w = 0; w < 4; ++w) Mx = fmaxf(Mx, state_of<RING>(L, w)[2048 + 2 * t]);
+  for (int w = 0; w < 4; ++w) Mx = fmaxf(Mx, state_of(L, w)[2048 + 2 * t]);
   float Ls = 0.f, acc[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) acc[k] = 0.f;
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    const float* stw = state_of<RING>(L, w);
+    const float* stw = state_of(L, w);
     const float f = Mx == -INFINITY ? 0.f : exp2f(stw[2048 + 2 * t] - Mx);
     Ls += stw[2048 + 2 * t + 1] * f;
 #pragma unroll
@@ -1117,13 +1068,14 @@ __device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickPara
 // [32][128 B] then V rows [32][128 B]; the 16-byte chunk k of row r sits at chunk position k ^ ((r >> 1) & 7), so
 // the 16 rows of a K fragment read fall in distinct banks.  Lane l of instruction q brings row 8q + l/8 into chunk
 // position l % 8.  Rows past i1 repeat row i0 (masked in the update).
+template <int NQI = 4>
 __device__ __forceinline__ void stage_tile_fp8(const char* kb, const char* vb, int64_t start, int64_t cap, int i0,
-                                               int r0, int i1, uint8_t* slot) {
+                                               int r0, int i1, uint8_t* slot, int q0 = 0) {
   const int lane = tix() & 63, rl = lane >> 3, pc = lane & 7;
   asm volatile("" ::: "memory");  // after every read of the slot's previous tile
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int r = 8 * q + rl;
+  for (int qq = 0; qq < NQI; ++qq) {
+    const int q = q0 + qq, r = 8 * q + rl;
     int64_t row = start + (r0 + r < i1 ? r0 + r : i0);
     if (row >= cap) row -= cap;
     const int64_t off = row * DH + 16 * (pc ^ ((r >> 1) & 7));
@@ -1178,13 +1130,14 @@ __device__ __forceinline__ void read_tile_fp8(const uint8_t* slot, RawTile<1>& t
 // rows 16h .. 16h+15, K rows [16][256 B] then V rows [16][256 B]; the 16-byte chunk k of row r sits at chunk position
 // k ^ (r & 15) (the 16 rows of a K fragment read, and the 4 rows of a V fragment read, fall in distinct banks).  Lane
 // l of instruction q brings row 4q + l/16 into chunk position l % 16.  Rows past i1 repeat row i0.
+template <int NQI = 8>
 __device__ __forceinline__ void stage_tile_bf16(const char* kb, const char* vb, int64_t start, int64_t cap, int i0,
-                                                int r0, int i1, uint8_t* slot) {
+                                                int r0, int i1, uint8_t* slot, int q0 = 0) {
   const int lane = tix() & 63, rl = lane >> 4, pc = lane & 15;
   asm volatile("" ::: "memory");  // after every read of the slots' previous tile
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int r = 4 * q + rl;  // row of the tile, 0..31
+  for (int qq = 0; qq < NQI; ++qq) {
+    const int q = q0 + qq, r = 4 * q + rl;  // row of the tile, 0..31
     int64_t row = start + (r0 + r < i1 ? r0 + r : i0);
     if (row >= cap) row -= cap;
     const int64_t off = row * DH * 2 + 16 * (pc ^ (r & 15));
@@ -1237,9 +1190,25 @@ template <int KT>
 __device__ __forceinline__ void stage_tile(const char* kb, const char* vb, int64_t start, int64_t cap, int i0, int r0,
                                            int i1, uint8_t* slot) {
   if constexpr (KT == 0)
-    stage_tile_bf16(kb, vb, start, cap, i0, r0, i1, slot);
+    stage_tile_bf16<8>(kb, vb, start, cap, i0, r0, i1, slot);
   else
-    stage_tile_fp8(kb, vb, start, cap, i0, r0, i1, slot);
+    stage_tile_fp8<4>(kb, vb, start, cap, i0, r0, i1, slot);
+}
+// The expert's own rows [r0, r0+32) of (agent, head) (bf16, produced in this launch) staged in the bf16 tile layout
+// by device-scope direct loads; instructions q0 .. q0+NQI-1 of the eight.  Rows at or past S repeat row 0.
+template <int NQI>
+__device__ __forceinline__ void stage_own_tile(const char* ks, const char* vs, int64_t srow, int r0, int S,
+                                               uint8_t* slot, int q0) {
+  const int lane = tix() & 63, rl = lane >> 4, pc = lane & 15;
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int qq = 0; qq < NQI; ++qq) {
+    const int q = q0 + qq, r = 4 * q + rl;
+    const int64_t off = (int64_t)(r0 + r < S ? r0 + r : 0) * srow + 16 * (pc ^ (r & 15));
+    uint8_t* dst = slot + (q >> 2) * RSLOT + (q & 3) * 1024;
+    load_lds16<true>(ks + off, dst);
+    load_lds16<true>(vs + off, dst + 16 * DH * 2);
+  }
 }
 template <int KT>
 __device__ __forceinline__ void read_tile(const uint8_t* slot, RawTile<KT>& t) {
@@ -1256,158 +1225,284 @@ struct RingOf {
   static constexpr int loads = KT == 0 ? 16 : 8;
 };
 
-// The tiles of one unit for query tiles tt0 .. tt0+nq-1 (nq <= NQ): wave w takes cache tiles w, w+4, ..., kept
-// PD deep in registers, then the own-row tiles that continue the same round robin; the states are merged
-// through LDS and written out (normalised if the agent has one range, else as the partial of this range).
-// Returns false if a wait failed.
-template <int KT, int NQ, int PD>
+// The tiles of one unit for the agent's single query tile: wave w takes cache tiles w, w+4, ..., staged through its
+// own LDS ring by direct loads (RingOf<KT>::tiles in flight), then the own-row tiles that continue the same round
+// robin; the waves' states are merged through LDS and written out (normalised if the agent has one range, else as
+// the partial of this range).  Returns false if a wait failed.
+template <int KT>
 __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& tp, const Dims& dm, int l,
-                                          const AUnit& U, int tt0, int nq, TickLds& L) {
-  const int wave = tix() >> 6, lane = tix() & 63, c16 = lane & 15, grp = lane >> 4;
+                                          const AUnit& U, TickLds& L) {
+  const int wave = tix() >> 6;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
   // this wave's cache tiles: j = wave + 4 i, i < nc
   const int nc = U.nct > wave ? (U.nct - wave + 3) / 4 : 0;
-  constexpr bool LDS_RING = NQ == 1;  // one query tile: tiles staged in LDS by direct loads
   using RG = RingOf<KT>;
   uint8_t* lring = L.u.a.ring[wave][0];
   auto slot_of = [&](int i) { return lring + (i % RG::tiles) * RG::spt * RSLOT; };
   auto ring_tile = [&](int i) {
     stage_tile<KT>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * (wave + 4 * i), U.i1, slot_of(i));
   };
-  RawTile<KT> ring[LDS_RING ? 1 : PD];
-  auto cache_tile = [&](int i, RawTile<KT>& t) {
-    load_cache_tile<KT>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * (wave + 4 * i), U.i1, t);
-  };
   // The first tiles do not depend on this layer's projections: waves 0-2 issue them before waiting; wave 3 polls
   // the q, k and v column tiles of this head (its poll would otherwise return only after its own prefetch) and
   // issues its tiles afterwards.
   auto prefetch = [&]() {
-    if constexpr (LDS_RING) {
 #pragma unroll
-      for (int dd = 0; dd < RG::tiles; ++dd)
-        if (dd < nc) ring_tile(dd);
-    } else {
-#pragma unroll
-      for (int dd = 0; dd < PD; ++dd)
-        if (dd < nc) cache_tile(dd, ring[dd]);
-    }
+    for (int dd = 0; dd < RG::tiles; ++dd)
+      if (dd < nc) ring_tile(dd);
   };
   if (wave < 3) prefetch();
   if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16, 3)) return false;
   if (wave == 3) prefetch();
-  f32x4 o[NQ][8];
-  float m_run[NQ], l_run[NQ];
+  f32x4 o[1][8];
+  float m_run[1] = {-INFINITY}, l_run[1] = {0.f};
 #pragma unroll
-  for (int tt = 0; tt < NQ; ++tt) {
-#pragma unroll
-    for (int k = 0; k < 8; ++k) o[tt][k] = f32x4{0.f, 0.f, 0.f, 0.f};
-    m_run[tt] = -INFINITY;
-    l_run[tt] = 0.f;
+  for (int k = 0; k < 8; ++k) o[0][k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint4 qr[1][4];
+  const int tt_one[1] = {0};
+  load_q<1, KT == 1>(a, tp, dm, U.b, U.h, tt_one, 1, qr);
+  auto qf = [&](int, int k) -> uint4 { return qr[0][k]; };
+  // Pairs of tiles (i, i + 1) at ring places i % T, i % T + 1 (T = tiles the ring holds).  The memory operations
+  // issued after tile i + 1 are the direct loads of tiles i + 2 .. i + T - 1, so once at most that many loads are
+  // pending the pair has landed; once both are read into registers their places take tiles i + T and i + T + 1,
+  // which stream in while the pair is computed.
+  static_assert(RG::tiles == 2 || RG::tiles == 4, "the waits below cover rings of two or four tiles");
+#pragma unroll 1
+  for (int i = 0; i < nc; i += 2) {
+    const bool two = i + 1 < nc;
+    const int after = RG::tiles == 4 ? min(nc - 2 - i, 2) : 0;  // tiles in flight behind the pair (when two)
+    if (two && after == 2)
+      vm_wait_below_c<2 * RG::loads>();
+    else if (two && after == 1)
+      vm_wait_below_c<RG::loads>();
+    else
+      vm_wait_all();
+    RawTile<KT> ta, tb;
+    read_tile<KT>(slot_of(i), ta);
+    if (two) read_tile<KT>(slot_of(i + 1), tb);
+    if (i + RG::tiles < nc) ring_tile(i + RG::tiles);
+    if (i + RG::tiles + 1 < nc) ring_tile(i + RG::tiles + 1);
+    if (two)
+      tile_pair_compute<KT>(ta, tb, qr[0], U.i0 + 32 * (wave + 4 * i), U.i0 + 32 * (wave + 4 * (i + 1)), U.i1, U.ksc,
+                            o[0], m_run[0], l_run[0]);
+    else
+      tile_jobs<KT, 1, 1>(ta, qf, U.i0 + 32 * (wave + 4 * i), U.i1, U.ksc, o, m_run, l_run);
   }
-  uint4 qr[4];  // NQ == 1: the query fragments
-  if (NQ == 1)
-    load_q<1, KT == 1>(a, tp, dm, U.b, U.h, tt0, nq, reinterpret_cast<uint4(&)[1][4]>(qr));
-  else
-    load_q_lds<KT == 1>(a, tp, dm, U.b, U.h, tt0, nq, L);
-  // LDS queries are in plain channel order; fp8 key tiles want the permuted order (see RawTile)
-  auto qf = [&](int tt, int k) -> uint4 {
-    if (NQ == 1) return qr[k];
-    const int ch = KT == 1 ? 64 * (k >> 1) + 16 * grp + 8 * (k & 1) : 32 * k + 8 * grp;
-    return *reinterpret_cast<const uint4*>(&L.u.a.qs[tt * 16 + c16][ch]);
-  };
-  auto qf_own = [&](int tt, int k) -> uint4 {
-    if (NQ == 1) return qr[k];
-    return *reinterpret_cast<const uint4*>(&L.u.a.qs[tt * 16 + c16][32 * k + 8 * grp]);
-  };
-  if constexpr (LDS_RING) {
-    // Pairs of tiles (i, i + 1) at ring places i % T, i % T + 1 (T = tiles the ring holds).  The memory operations
-    // issued after tile i + 1 are the direct loads of tiles i + 2 .. i + T - 1, so once at most that many loads are
-    // pending the pair has landed; once both are read into registers their places take tiles i + T and i + T + 1,
-    // which stream in while the pair is computed.
-    static_assert(RG::tiles == 2 || RG::tiles == 4, "the waits below cover rings of two or four tiles");
-#pragma unroll 1
-    for (int i = 0; i < nc; i += 2) {
-      const bool two = i + 1 < nc;
-      const int after = RG::tiles == 4 ? min(nc - 2 - i, 2) : 0;  // tiles in flight behind the pair (when two)
-      if (two && after == 2)
-        vm_wait_below_c<2 * RG::loads>();
-      else if (two && after == 1)
-        vm_wait_below_c<RG::loads>();
-      else
-        vm_wait_all();
-      RawTile<KT> ta, tb;
-      read_tile<KT>(slot_of(i), ta);
-      if (two) read_tile<KT>(slot_of(i + 1), tb);
-      if (i + RG::tiles < nc) ring_tile(i + RG::tiles);
-      if (i + RG::tiles + 1 < nc) ring_tile(i + RG::tiles + 1);
-      if (two)
-        tile_pair_compute<KT>(ta, tb, qr, U.i0 + 32 * (wave + 4 * i), U.i0 + 32 * (wave + 4 * (i + 1)), U.i1, U.ksc,
-                              o[0], m_run[0], l_run[0]);
-      else
-        tile_compute<KT, 1>(ta, qf, 1, U.i0 + 32 * (wave + 4 * i), U.i1, U.ksc, o, m_run, l_run);
-    }
-  } else if constexpr (NQ == 1 && PD % 2 == 0) {
-    // pairs of ring slots (dd, dd + 1); an odd last tile goes through the single-tile update
-#pragma unroll 1
-    for (int i = 0; i < nc; i += PD) {
+  if (KT == 1) {
+    // fp8 values carry their scale: apply it to the cache part of the output before the own rows join
 #pragma unroll
-      for (int dd = 0; dd < PD; dd += 2) {
-        if (i + dd + 1 < nc) {
-          tile_pair_compute<KT>(ring[dd], ring[dd + 1], qr, U.i0 + 32 * (wave + 4 * (i + dd)),
-                                U.i0 + 32 * (wave + 4 * (i + dd + 1)), U.i1, U.ksc, o[0], m_run[0], l_run[0]);
-          if (i + dd + PD < nc) cache_tile(i + dd + PD, ring[dd]);
-          if (i + dd + 1 + PD < nc) cache_tile(i + dd + 1 + PD, ring[dd + 1]);
-        } else if (i + dd < nc) {
-          tile_compute<KT, NQ>(ring[dd], qf, nq, U.i0 + 32 * (wave + 4 * (i + dd)), U.i1, U.ksc, o, m_run, l_run);
-        }
-      }
+    for (int k = 0; k < 8; ++k) o[0][k] *= U.vsc;
+  }
+  // own rows (bf16): tiles U.nct .. U.nct+nst-1 of the round robin
+  if (U.nst > 0) {
+    if (KT == 1) load_q<1, false>(a, tp, dm, U.b, U.h, tt_one, 1, qr);  // the queries again, as bf16
+    const int first_own = (wave - U.nct % 4 + 4) % 4;
+    for (int j = first_own; j < U.nst; j += 4) {
+      RawTile<0> t;
+      load_own_tile(U.ks, U.vs, (int64_t)dm.A * 2, 32 * j, tp.S, t);
+      tile_jobs<0, 1, 1>(t, qf, 32 * j, tp.S, 1.f, o, m_run, l_run);
     }
+  }
+  state_to_lds(state_of(L, wave), o[0], m_run[0], l_run[0]);
+  __syncthreads();
+  merge_states(a, tp, dm, U, 0, U.final_out, (int64_t)U.slot * tp.n_tt, L);
+  __syncthreads();
+  return true;
+}
+
+// Wait until at most `behind` tiles of LOADS direct loads each are pending (behind <= MAXB).
+template <int LOADS, int MAXB>
+__device__ __forceinline__ void vm_wait_tiles(int behind) {
+  if constexpr (MAXB == 0) {
+    vm_wait_all();
   } else {
-#pragma unroll 1
-    for (int i = 0; i < nc; i += PD) {
+    if (behind >= MAXB)
+      vm_wait_below_c<MAXB * LOADS>();
+    else
+      vm_wait_tiles<LOADS, MAXB - 1>(behind);
+  }
+}
+
+// Many-query unit (query tiles tt0 .. tt0+nq-1, nq <= NQW = 6).  Every cache tile of the unit is staged once into a
+// workgroup ring of T tiles by direct loads (each wave issues its share of every tile), in groups of four, and the
+// waves split the arithmetic as jobs (query tile u, key class): a job takes the tiles i with i mod P = p.  The first
+// F = 4 query tiles (when nq >= 4) are one whole job each (wave w: tile w, P = 1); the R = nq - F others are split
+// by keys: one tile over all four waves (P = 4, p = w), or two tiles over two waves each (tile F + w/2, P = 2,
+// p = w mod 2), or, for R = 3 (then F = 0), both.  So a wave has at most two jobs, and within a group of four tiles
+// every wave does the same work.  At group step i a barrier follows this wave's wait for its share of tiles
+// i .. i + 3, so they have landed and every wave is done with the previous group.  The own rows follow through the
+// same ring, under the same key classes (own tile index j).  A whole job's state is written out by its wave; the
+// key-split tiles are merged through LDS, one query tile at a time.  Output: normalised if the agent has one range,
+// else the partial of this range.
+template <int KT>
+struct WRingOf {
+  static constexpr int tb = KT == 0 ? 2 * RSLOT : RSLOT;  // bytes of a staged tile
+  static constexpr int tiles = 4 * RSLOTS * RSLOT / tb;    // 8 (bf16) or 16 (fp8)
+  static constexpr int loads = KT == 0 ? 4 : 2;           // direct loads of a thread per tile
+  static constexpr int own = 4 * RSLOTS * RSLOT / (2 * RSLOT);  // bf16 own-row tiles the ring holds
+};
+template <int KT>
+__device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams& tp, const Dims& dm, int l,
+                                             const AUnit& U, int tt0, int nq, TickLds& L) {
+  using WR = WRingOf<KT>;
+  const int wave = tix() >> 6, lane = tix() & 63, c16 = lane & 15, grp = lane >> 4;
+  const uint64_t st = stamp_of(a, l, dm.n_layers);
+  const int nc = U.nct;
+  // this wave's jobs: query tile ju[j] (relative to tt0), key class (jp[j] = P - 1 as a mask, jk[j] = p)
+  const int F = nq >= 4 ? 4 : 0, R = nq - F;
+  int nj = 0, ju[2] = {0, 0}, jp[2] = {0, 0}, jk[2] = {0, 0};
+  auto add_job = [&](int u, int P, int pk) {
+    ju[nj] = u;
+    jp[nj] = P - 1;
+    jk[nj] = pk;
+    ++nj;
+  };
+  if (F) add_job(wave, 1, 0);
+  if (R == 1) add_job(F, 4, wave);
+  if (R >= 2) add_job(F + (wave >> 1), 2, wave & 1);
+  if (R == 3) add_job(F + 2, 4, wave);
+  auto act_of = [&](int i) { return (nj > 0 && (i & jp[0]) == jk[0] ? 1 : 0) | (nj > 1 && (i & jp[1]) == jk[1] ? 2 : 0); };
+  uint8_t* base = &L.u.a.ring[0][0][0];
+  auto place = [&](int i) { return base + (i % WR::tiles) * WR::tb; };
+  auto stage = [&](int i) {
+    if constexpr (KT == 0)
+      stage_tile_bf16<2>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * i, U.i1, place(i), 2 * wave);
+    else
+      stage_tile_fp8<1>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * i, U.i1, place(i), wave);
+  };
+  constexpr int G = 4;  // tiles per barrier step
+  auto prefetch = [&]() {
+    for (int i = 0; i < WR::tiles - G && i < nc; ++i) stage(i);
+  };
+  if (wave < 3) prefetch();
+  if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16, 3)) return false;
+  if (wave == 3) prefetch();
+  f32x4 o[2][8];
+  float m_run[2], l_run[2];
 #pragma unroll
-      for (int dd = 0; dd < PD; ++dd) {
-        if (i + dd < nc) {
-          tile_compute<KT, NQ>(ring[dd], qf, nq, U.i0 + 32 * (wave + 4 * (i + dd)), U.i1, U.ksc, o, m_run, l_run);
-          if (i + dd + PD < nc) cache_tile(i + dd + PD, ring[dd]);
-        }
+  for (int j = 0; j < 2; ++j) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) o[j][k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m_run[j] = -INFINITY;
+    l_run[j] = 0.f;
+  }
+  const int tts[2] = {tt0 + ju[0], tt0 + ju[1]};
+  uint4 qr[2][4];
+  load_q<2, KT == 1>(a, tp, dm, U.b, U.h, tts, nj, qr);
+  auto qf = [&](int j, int k) -> uint4 { return qr[j][k]; };
+  // one step of the online softmax for the jobs that take tile i (index in its sequence)
+  auto update = [&](const auto& t, int i, int r0, int i1, float ksc) {
+    constexpr int TK = sizeof(t) == sizeof(RawTile<0>) ? 0 : 1;
+    const int act = act_of(i);
+    if (act == 3)
+      tile_jobs<TK, 2, 3>(t, qf, r0, i1, ksc, o, m_run, l_run);
+    else if (act == 1)
+      tile_jobs<TK, 2, 1>(t, qf, r0, i1, ksc, o, m_run, l_run);
+    else if (act == 2)
+      tile_jobs<TK, 2, 2>(t, qf, r0, i1, ksc, o, m_run, l_run);
+  };
+  // Groups of G tiles i .. i + G - 1: once they have landed and every wave is done with the previous group, that
+  // group's places take tiles i + T - G .. i + T - 1.  A barrier per group of four (not per tile) lets the key-split
+  // jobs, which take one tile in four, even out within the group.
+#pragma unroll 1
+  for (int i = 0; i < nc; i += G) {
+    // tiles issued: 0 .. min(i + T - G - 1, nc - 1); those after tile i + G - 1 (or the last) may stay in flight
+    vm_wait_tiles<WR::loads, WR::tiles - 2 * G>(max(0, min(WR::tiles - 2 * G, nc - G - i)));
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < G; ++e)
+      if (i + WR::tiles - G + e < nc) stage(i + WR::tiles - G + e);
+#pragma unroll
+    for (int e = 0; e < G; ++e) {
+      if (i + e < nc && act_of(i + e)) {
+        RawTile<KT> t;
+        read_tile<KT>(place(i + e), t);
+        update(t, i + e, U.i0 + 32 * (i + e), U.i1, U.ksc);
       }
     }
   }
   if (KT == 1) {
     // fp8 values carry their scale: apply it to the cache part of the output before the own rows join
 #pragma unroll
-    for (int tt = 0; tt < NQ; ++tt)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int k = 0; k < 8; ++k) o[tt][k] *= U.vsc;
+      for (int k = 0; k < 8; ++k) o[j][k] *= U.vsc;
   }
-  // own rows (bf16): tiles U.nct .. U.nct+nst-1 of the round robin
-  if (U.nst > 0) {
-    if (KT == 1) {  // the queries again, as bf16
-      if (NQ == 1) {
-        load_q<1, false>(a, tp, dm, U.b, U.h, tt0, nq, reinterpret_cast<uint4(&)[1][4]>(qr));
-      } else {
-        __syncthreads();  // every wave is done with the fp16 queries
-        load_q_lds<false>(a, tp, dm, U.b, U.h, tt0, nq, L);
+  // own rows (bf16), up to WR::own tiles per round through the ring
+  for (int j0 = 0; j0 < U.nst; j0 += WR::own) {
+    const int nown = min(WR::own, U.nst - j0);
+    __syncthreads();  // every wave is done with the ring
+    for (int j = 0; j < nown; ++j)
+      stage_own_tile<2>(U.ks, U.vs, (int64_t)dm.A * 2, 32 * (j0 + j), tp.S, base + j * 2 * RSLOT, 2 * wave);
+    if (KT == 1 && j0 == 0) load_q<2, false>(a, tp, dm, U.b, U.h, tts, nj, qr);  // the queries as bf16
+    vm_wait_all();
+    __syncthreads();
+    for (int j = 0; j < nown; ++j) {
+      if (act_of(j0 + j)) {
+        RawTile<0> t;
+        read_tile<0>(base + j * 2 * RSLOT, t);
+        update(t, j0 + j, 32 * (j0 + j), tp.S, 1.f);
       }
     }
-    const int first_own = (wave - U.nct % 4 + 4) % 4;
-    for (int j = first_own; j < U.nst; j += 4) {
-      RawTile<0> t;
-      load_own_tile(U.ks, U.vs, (int64_t)dm.A * 2, 32 * j, tp.S, t);
-      tile_compute<0, NQ>(t, qf_own, nq, 32 * j, tp.S, 1.f, o, m_run, l_run);
-    }
   }
-  const bool final_out = U.final_out;
+  // whole jobs: lane (c16, grp) holds rows 4 grp + r, channels 8 c16 .. 8 c16 + 7 of o; m and the lane-partial l of
+  // query c16
 #pragma unroll
-  for (int tt = 0; tt < NQ; ++tt) {
-    if (tt < nq) {
-      state_to_lds(state_of<LDS_RING>(L, wave), o[tt], m_run[tt], l_run[tt]);
-      __syncthreads();
-      merge_states<LDS_RING>(a, tp, dm, U, tt0 + tt, final_out, (int64_t)U.slot * tp.n_tt + tt0 + tt, L);
-      __syncthreads();
+  for (int j = 0; j < 2; ++j) {
+    if (j < nj && jp[j] == 0) {
+      const int tt = tt0 + ju[j];
+      const float lt = rows_sum(l_run[j]);
+      if (U.final_out) {
+        const float inv = 1.0f / lt;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float f = shfl(inv, 4 * grp + r);
+          const int tok = tt * 16 + 4 * grp + r;
+          if (tok < tp.S) {
+            uint16_t* dst = a.attn + ((int64_t)U.b * tp.S + tok) * dm.A + (int64_t)U.h * DH + 8 * c16;
+            st_loc16(dst, make_uint4(pack_bf16x2(o[j][0][r] * f, o[j][1][r] * f),
+                                     pack_bf16x2(o[j][2][r] * f, o[j][3][r] * f),
+                                     pack_bf16x2(o[j][4][r] * f, o[j][5][r] * f),
+                                     pack_bf16x2(o[j][6][r] * f, o[j][7][r] * f)));
+          }
+        }
+      } else {
+        const int64_t item = (int64_t)U.slot * tp.n_tt + tt;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float* po = a.att_o + (item * 16 + 4 * grp + r) * 128 + 8 * c16;
+          st_loc_f4(po, make_float4(o[j][0][r], o[j][1][r], o[j][2][r], o[j][3][r]));
+          st_loc_f4(po + 4, make_float4(o[j][4][r], o[j][5][r], o[j][6][r], o[j][7][r]));
+        }
+        if (grp == 0) {
+          st_loc_f(a.att_ml + item * 32 + 2 * c16, m_run[j]);
+          st_loc_f(a.att_ml + item * 32 + 2 * c16 + 1, lt);
+        }
+      }
     }
   }
+  // key-split query tiles F .. nq-1: each wave's state (empty if it has no job on the tile), merged in LDS
+  for (int u = F; u < nq; ++u) {
+    __syncthreads();  // the ring (and the previous merge) is free
+    f32x4 oe[8];
+    float me = -INFINITY, le = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) oe[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (nj > 0 && jp[0] != 0 && ju[0] == u) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) oe[k] = o[0][k];
+      me = m_run[0];
+      le = l_run[0];
+    } else if (nj > 1 && jp[1] != 0 && ju[1] == u) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) oe[k] = o[1][k];
+      me = m_run[1];
+      le = l_run[1];
+    }
+    state_to_lds(state_of(L, wave), oe, me, le);
+    __syncthreads();
+    merge_states(a, tp, dm, U, tt0 + u, U.final_out, (int64_t)U.slot * tp.n_tt + tt0 + u, L);
+  }
+  __syncthreads();  // the ring is free for the next unit
   return true;
 }
 
@@ -1510,10 +1605,10 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
     }
     bool ok = true;
     if constexpr (!MQ) {
-      ok = attn_unit<KT, 1, KT == 0 ? 2 : 4>(a, tp, dm, l, U, 0, 1, L);
+      ok = attn_unit<KT>(a, tp, dm, l, U, L);
     } else {
       for (int tt0 = 0; tt0 < n_tt && ok; tt0 += NQW)
-        ok = attn_unit<KT, NQW, 2>(a, tp, dm, l, U, tt0, min(NQW, n_tt - tt0), L);
+        ok = attn_unit_mq<KT>(a, tp, dm, l, U, tt0, min(NQW, n_tt - tt0), L);
     }
     if (!ok) return false;
     if (first) TICK_SUB(l, 4);

@@ -30,7 +30,8 @@ def small(wid, lengths, n_frame=0, capacity=400, n_layers=3, d_model=128, n_head
                           capacity=capacity)
 
 
-@pytest.mark.parametrize("n_frame", [0, 30])
+# n_frame 30, 50, 90: 3, 4 and 7 query tiles per agent (7: more than one attention pass over the cache)
+@pytest.mark.parametrize("n_frame", [0, 30, 50, 90])
 def test_tick_kernel_and_per_phase_launches_match_oracle(n_frame):
     wl = small(70 + n_frame, lengths=(17, 0, 250, 399), n_frame=n_frame)
     say(f"case tick vs per-phase, n_frame={n_frame}")
