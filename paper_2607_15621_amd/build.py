@@ -16,6 +16,9 @@ FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC",
     # no packed-FP32 VALU instructions (v_pk_{add,mul,fma}_f32) in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs: the attention's online softmax rescales its accumulators with VALU
+    # instructions, and accumulators kept in AGPRs were copied to VGPRs and back on every tile
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall", "-Wno-unused-function", "-Wno-unused-variable",
 ]
 
