@@ -819,8 +819,8 @@ __device__ __forceinline__ void tile_jobs(const RawTile<KT>& t, QF qf, int r0, i
   for (int j = 0; j < NJ; ++j) {
     mx[j] = -INFINITY;
     if (ACT >> j & 1) {
-      mx[j] = fmaxf(fmaxf(fmaxf(s[j][0][0], s[j][0][1]), fmaxf(s[j][0][2], s[j][0][3])),
-                    fmaxf(fmaxf(s[j][1][0], s[j][1][1]), fmaxf(s[j][1][2], s[j][1][3])));
+      mx[j] = vmax3(vmax3(s[j][0][0], s[j][0][1], s[j][0][2]), vmax3(s[j][0][3], s[j][1][0], s[j][1][1]),
+                    vmax(s[j][1][2], s[j][1][3]));
       mx[j] = rows_max(mx[j]);
       grow = grow || mx[j] > m_run[j] + RESCALE_LOG2;
     }
@@ -901,10 +901,8 @@ __device__ __forceinline__ void tile_pair_compute(const RawTile<KT>& ta, const R
       for (int i = 0; i < 4; ++i)
         if ((j < 2 ? ra : rb) + 16 * (j & 1) + 4 * grp + i >= i1) s[j][i] = -INFINITY;
   }
-  float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
-                   fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
-  mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(s[2][0], s[2][1]), fmaxf(s[2][2], s[2][3])),
-                       fmaxf(fmaxf(s[3][0], s[3][1]), fmaxf(s[3][2], s[3][3]))));
+  float mx = vmax3(vmax3(s[0][0], s[0][1], s[0][2]), vmax3(s[0][3], s[1][0], s[1][1]), vmax3(s[1][2], s[1][3], s[2][0]));
+  mx = vmax3(mx, vmax3(s[2][1], s[2][2], s[2][3]), vmax3(s[3][0], s[3][1], vmax3(s[3][2], s[3][3], s[3][3])));
   mx = rows_max(mx);
   const bool grow = mx > m_run + RESCALE_LOG2;
   if (__any(grow)) {
@@ -1087,16 +1085,34 @@ __device__ __forceinline__ void stage_tile_fp8(const char* kb, const char* vb, i
 // rows 4grp + j (+16), bytes 8c..8c+7.  One asm block that waits for its own reads: reads the compiler sees after
 // direct loads into the same LDS object make it wait for every pending direct load, the next tile's included.
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ void read_tile_fp8(const uint8_t* slot, RawTile<1>& t) {
+// This lane's byte offsets (from the tile's first slot) of the reads of a staged tile, computed once per unit.
+template <int KT>
+struct TileLanes {
+  uint32_t k[4], v[4];  // bf16: K chunks k = 0..3, V rows j = 0..3; fp8: K halves k = 0, 1, V rows j = 0..3
+};
+template <int KT>
+__device__ __forceinline__ TileLanes<KT> tile_lanes() {
   const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
+  TileLanes<KT> tl;
+  if constexpr (KT == 0) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) tl.k[k] = c * 256 + 16 * ((4 * k + grp) ^ c);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) tl.v[j] = 16 * 256 + (4 * grp + j) * 256 + 16 * (c ^ (4 * grp + j));
+  } else {
+    tl.k[0] = c * DH + 16 * (grp ^ (c >> 1));  // (r >> 1) & 7 == c >> 1 for r = 16 rt + c
+    tl.k[1] = c * DH + 16 * ((4 + grp) ^ (c >> 1));
+    tl.k[2] = tl.k[3] = 0;
+    const uint32_t vb = 32 * DH + 4 * grp * DH + 8 * (c & 1);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) tl.v[j] = vb + j * DH + 16 * ((c >> 1) ^ (2 * grp + (j >> 1)));  // (r >> 1) & 7 == 2grp + j/2
+  }
+  return tl;
+}
+__device__ __forceinline__ void read_tile_fp8(const uint8_t* slot, const TileLanes<1>& tl, RawTile<1>& t) {
   const uint32_t s0 = lds_addr(slot);
-  const uint32_t ak0 = s0 + c * DH + 16 * (grp ^ (c >> 1));        // (r >> 1) & 7 == c >> 1 for r = 16 rt + c
-  const uint32_t ak1 = s0 + c * DH + 16 * ((4 + grp) ^ (c >> 1));
-  const uint32_t vb = s0 + 32 * DH + 4 * grp * DH + 8 * (c & 1);
-  const uint32_t av0 = vb + 0 * DH + 16 * ((c >> 1) ^ (2 * grp));      // rows 4grp + jj: (r >> 1) & 7 == 2grp + jj/2
-  const uint32_t av1 = vb + 1 * DH + 16 * ((c >> 1) ^ (2 * grp));
-  const uint32_t av2 = vb + 2 * DH + 16 * ((c >> 1) ^ (2 * grp + 1));
-  const uint32_t av3 = vb + 3 * DH + 16 * ((c >> 1) ^ (2 * grp + 1));
+  const uint32_t ak0 = s0 + tl.k[0], ak1 = s0 + tl.k[1];
+  const uint32_t av0 = s0 + tl.v[0], av1 = s0 + tl.v[1], av2 = s0 + tl.v[2], av3 = s0 + tl.v[3];
   u32x4_t k0, k1, k2, k3;
   u32x2_t v0, v1, v2, v3, v4, v5, v6, v7;
   asm volatile(
@@ -1148,14 +1164,13 @@ __device__ __forceinline__ void stage_tile_bf16(const char* kb, const char* vb, 
 }
 // The RawTile<0> fragments of a staged bf16 tile: K row 16rt + c (slot rt, row c), channels 32k + 8grp (chunk 4k +
 // grp); V rows 4grp + j (slot j / 4), channels 8c .. 8c+7 (chunk c).  One asm block that waits for its own reads.
-__device__ __forceinline__ void read_tile_bf16(const uint8_t* slot, RawTile<0>& t) {
-  const int lane = tix() & 63, c = lane & 15, grp = lane >> 4;
+__device__ __forceinline__ void read_tile_bf16(const uint8_t* slot, const TileLanes<0>& tl, RawTile<0>& t) {
   const uint32_t s0 = lds_addr(slot);
   uint32_t ak[4], av[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) ak[k] = s0 + c * 256 + 16 * ((4 * k + grp) ^ c);
+  for (int k = 0; k < 4; ++k) ak[k] = s0 + tl.k[k];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) av[j] = s0 + 16 * 256 + (4 * grp + j) * 256 + 16 * (c ^ (4 * grp + j));
+  for (int j = 0; j < 4; ++j) av[j] = s0 + tl.v[j];
   u32x4_t k0, k1, k2, k3, k4, k5, k6, k7, v0, v1, v2, v3, v4, v5, v6, v7;
   asm volatile(
       "ds_read_b128 %0, %16\n\t"
@@ -1211,11 +1226,11 @@ __device__ __forceinline__ void stage_own_tile(const char* ks, const char* vs, i
   }
 }
 template <int KT>
-__device__ __forceinline__ void read_tile(const uint8_t* slot, RawTile<KT>& t) {
+__device__ __forceinline__ void read_tile(const uint8_t* slot, const TileLanes<KT>& tl, RawTile<KT>& t) {
   if constexpr (KT == 0)
-    read_tile_bf16(slot, t);
+    read_tile_bf16(slot, tl, t);
   else
-    read_tile_fp8(slot, t);
+    read_tile_fp8(slot, tl, t);
 }
 // Ring geometry: slots per tile, tiles the ring holds, direct-load instructions per tile.
 template <int KT>
@@ -1258,6 +1273,7 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
 #pragma unroll
   for (int k = 0; k < 8; ++k) o[0][k] = f32x4{0.f, 0.f, 0.f, 0.f};
   uint4 qr[1][4];
+  const TileLanes<KT> tl = tile_lanes<KT>();
   const int tt_one[1] = {0};
   load_q<1, KT == 1>(a, tp, dm, U.b, U.h, tt_one, 1, qr);
   auto qf = [&](int, int k) -> uint4 { return qr[0][k]; };
@@ -1277,8 +1293,8 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
     else
       vm_wait_all();
     RawTile<KT> ta, tb;
-    read_tile<KT>(slot_of(i), ta);
-    if (two) read_tile<KT>(slot_of(i + 1), tb);
+    read_tile<KT>(slot_of(i), tl, ta);
+    if (two) read_tile<KT>(slot_of(i + 1), tl, tb);
     if (i + RG::tiles < nc) ring_tile(i + RG::tiles);
     if (i + RG::tiles + 1 < nc) ring_tile(i + RG::tiles + 1);
     if (two)
@@ -1387,6 +1403,7 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
   }
   const int tts[2] = {tt0 + ju[0], tt0 + ju[1]};
   uint4 qr[2][4];
+  const TileLanes<KT> tl = tile_lanes<KT>();
   load_q<2, KT == 1>(a, tp, dm, U.b, U.h, tts, nj, qr);
   auto qf = [&](int j, int k) -> uint4 { return qr[j][k]; };
   // one step of the online softmax for the jobs that take tile i (index in its sequence)
@@ -1411,11 +1428,11 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
 #pragma unroll
     for (int e = 0; e < G; ++e)
       if (i + WR::tiles - G + e < nc) stage(i + WR::tiles - G + e);
-#pragma unroll
+#pragma unroll 1
     for (int e = 0; e < G; ++e) {
       if (i + e < nc && act_of(i + e)) {
         RawTile<KT> t;
-        read_tile<KT>(place(i + e), t);
+        read_tile<KT>(place(i + e), tl, t);
         update(t, i + e, U.i0 + 32 * (i + e), U.i1, U.ksc);
       }
     }
@@ -1436,10 +1453,11 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
     if (KT == 1 && j0 == 0) load_q<2, false>(a, tp, dm, U.b, U.h, tts, nj, qr);  // the queries as bf16
     vm_wait_all();
     __syncthreads();
+    const TileLanes<0> tl0 = tile_lanes<0>();
     for (int j = 0; j < nown; ++j) {
       if (act_of(j0 + j)) {
         RawTile<0> t;
-        read_tile<0>(base + j * 2 * RSLOT, t);
+        read_tile<0>(base + j * 2 * RSLOT, tl0, t);
         update(t, j0 + j, 32 * (j0 + j), tp.S, 1.f);
       }
     }
