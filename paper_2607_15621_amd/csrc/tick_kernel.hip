@@ -1627,19 +1627,23 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
 // afterwards by separate items (agent, head, query tile) in a fixed order.  With little work (fewer than 16 tiles per
 // workgroup) and few segments, workgroup s takes segment s whole.  Equal slices keep every workgroup streaming until
 // the phase ends.
+// Many-query units weigh no extra start-up: every slice pays one (its queries, its first group of tiles), and without
+// the padding equal segments split into whole slices when the workgroups divide them evenly.
 constexpr int SEG_COST = 24;
+constexpr int SEG_COST_MQ = 0;
 __device__ __forceinline__ void attn_plan(const TickParams& tp, const Dims& dm, TickLds& L) {
   const int X = uni(L.X), NX = uni(L.NX), n = uni(L.n);
   const int nh = head_lo(X + 1, NX, dm.H) - head_lo(X, NX, dm.H);
   const int nseg = tp.B * nh;  // <= NSEG = NTHR
   const int NT = nh * tp.seg_p[tp.B];  // cache (work) tiles
   const int mode = NT < 16 * n && nseg <= n ? 1 : 0;
-  const int NC = NT + nseg * SEG_COST;  // work units
+  const int SC = tp.n_tt > 1 ? SEG_COST_MQ : SEG_COST;
+  const int NC = NT + nseg * SC;  // work units
   const int g = tix();
   int np = 0;
   if (g < nseg) {
     const int j = g / tp.B, k = g % tp.B, w = tp.seg_w[k];
-    const int g0 = j * (tp.seg_p[tp.B] + tp.B * SEG_COST) + tp.seg_p[k] + k * SEG_COST + SEG_COST;  // first tile's unit
+    const int g0 = j * (tp.seg_p[tp.B] + tp.B * SC) + tp.seg_p[k] + k * SC + SC;  // first tile's unit
     int sf = g;
     np = 1;
     if (mode == 0) {
