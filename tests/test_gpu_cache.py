@@ -184,10 +184,13 @@ def test_small_fp8_cache_matches_oracle():
         assert e <= FP8_WP_TOL and ed <= BF16_WP_TOL
 
 
-def test_small_fp8_cache_with_frame_tokens_matches_oracle():
-    """fp8 cache rows with several query tiles per agent (10 expert + 30 frame tokens)."""
-    wl = small(62, lengths=(290, 64), capacity=300, cache_dtype="fp8").replace(n_frame_tokens=30)
-    say("case small fp8 with frame tokens")
+# 30, 64, 90 frame tokens: 3, 5 and 7 query tiles per agent (key-split jobs only; four whole jobs and one
+# key-split; two passes over the cache)
+@pytest.mark.parametrize("n_frame", [30, 64, 90])
+def test_small_fp8_cache_with_frame_tokens_matches_oracle(n_frame):
+    """fp8 cache rows with several query tiles per agent (10 expert + n_frame frame tokens)."""
+    wl = small(62, lengths=(290, 64), capacity=300, cache_dtype="fp8").replace(n_frame_tokens=n_frame)
+    say(f"case small fp8 with {n_frame} frame tokens")
     model = Model(wl)
     ex = model.create()
     cache = Cache(wl, starts=(250, 7))
