@@ -883,13 +883,14 @@ __device__ __forceinline__ void tile_jobs(const RawTile<KT>& t, QF qf, int r0, i
       if (ACT >> j & 1) o[j][k] = F16 ? mfma_f16(pf[j], vt[k], o[j][k]) : mfma_bf16(pf[j], vt[k], o[j][k]);
 }
 
-// One query tile, two cache tiles at once (64 rows): the score MFMAs of both tiles are independent, one running-max
+// One query tile, two tiles at once (64 rows): the score MFMAs of both tiles are independent, one running-max
 // update covers both, and both P V products accumulate into the same output.  Twice the data per dependent chain
-// of the single-tile update (the wave is the only one on its SIMD, so nothing else hides that chain).
+// of the single-tile update (the wave is the only one on its SIMD, so nothing else hides that chain).  Tile a holds
+// rows ra.. (valid below ia1), tile b rows rb.. (valid below ib1).
 template <int KT>
 __device__ __forceinline__ void tile_pair_compute(const RawTile<KT>& ta, const RawTile<KT>& tb, const uint4 (&q)[4],
-                                                  int ra, int rb, int i1, float kscale, f32x4 (&o)[8], float& m_run,
-                                                  float& l_run) {
+                                                  int ra, int ia1, int rb, int ib1, float kscale, f32x4 (&o)[8],
+                                                  float& m_run, float& l_run) {
   constexpr bool F16 = KT == 1;
   const int lane = tix() & 63, grp = lane >> 4;
   uint4 kfa[8], vta[8], kfb[8], vtb[8];
@@ -909,12 +910,12 @@ __device__ __forceinline__ void tile_pair_compute(const RawTile<KT>& ta, const R
   if (KT == 1)
 #pragma unroll
     for (int j = 0; j < 4; ++j) s[j] *= kscale;
-  if (rb + 32 > i1) {  // tile b ends past i1 (tile a lies before b)
+  if (ra + 32 > ia1 || rb + 32 > ib1) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        if ((j < 2 ? ra : rb) + 16 * (j & 1) + 4 * grp + i >= i1) s[j][i] = -INFINITY;
+        if ((j < 2 ? ra : rb) + 16 * (j & 1) + 4 * grp + i >= (j < 2 ? ia1 : ib1)) s[j][i] = -INFINITY;
   }
   float mx = vmax3(vmax3(s[0][0], s[0][1], s[0][2]), vmax3(s[0][3], s[1][0], s[1][1]), vmax3(s[1][2], s[1][3], s[2][0]));
   mx = vmax3(mx, vmax3(s[2][1], s[2][2], s[2][3]), vmax3(s[3][0], s[3][1], vmax3(s[3][2], s[3][3], s[3][3])));
@@ -1319,27 +1320,39 @@ struct RingOf {
   static constexpr int loads = KT == 0 ? 16 : 8;
 };
 
-// The tiles of one unit for the agent's single query tile: wave w takes cache tiles w, w+4, ..., staged through its
-// own LDS ring by direct loads (RingOf<KT>::tiles in flight), then the own-row tiles that continue the same round
-// robin; the waves' states are merged through LDS and written out (normalised if the agent has one range, else as
-// the partial of this range).  Returns false if a wait failed.
+// The tiles of one unit for the agent's single query tile: wave w takes tiles w, w+4, ... of the unit's sequence,
+// staged through its own LDS ring by direct loads (RingOf<KT>::tiles in flight): the cache tiles, then (last range
+// only) the own-row tiles, which continue the same round robin.  In bf16 units the own-row tiles go through the
+// ring like cache tiles (issued once the queries, keys and values of the head are published); in fp8 units they
+// are bf16 while the cache tiles are not, and are read into registers after the cache tiles.  The waves' states
+// are merged through LDS and written out (normalised if the agent has one range, else as the partial of this
+// range).  Returns false if a wait failed.
 template <int KT>
 __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& tp, const Dims& dm, int l,
                                           const AUnit& U, TickLds& L) {
   constexpr int TK = KT == 0 ? 2 : 1;  // tile kind of the cache tiles (bf16 with V read transposed, or fp8)
   const int wave = tix() >> 6;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
-  // this wave's cache tiles: j = wave + 4 i, i < nc
+  // this wave's cache tiles: j = wave + 4 i, i < nc; then its own-row tiles j = first_own + 4 i, i < no
   const int nc = U.nct > wave ? (U.nct - wave + 3) / 4 : 0;
+  const int first_own = (wave - U.nct % 4 + 4) % 4;
+  const int no = KT == 0 && U.nst > first_own ? (U.nst - first_own + 3) / 4 : 0;
+  const int n = nc + no;
   using RG = RingOf<KT>;
   uint8_t* lring = L.u.a.ring[wave][0];
   auto slot_of = [&](int i) { return lring + (i % RG::tiles) * RG::spt * RSLOT; };
+  auto cache_tile = [&](int i) { return KT == 1 || i < nc; };  // fp8 units have no own-row tiles in the ring
+  auto row0 = [&](int i) { return cache_tile(i) ? U.i0 + 32 * (wave + 4 * i) : 32 * (first_own + 4 * (i - nc)); };
+  auto lim = [&](int i) { return cache_tile(i) ? U.i1 : tp.S; };
   auto ring_tile = [&](int i) {
-    stage_tile<KT>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * (wave + 4 * i), U.i1, slot_of(i));
+    if (cache_tile(i))
+      stage_tile<KT>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, row0(i), U.i1, slot_of(i));
+    else
+      stage_own_tile<8>(U.ks, U.vs, (int64_t)dm.A * 2, row0(i), tp.S, slot_of(i), 0);
   };
   // The first tiles do not depend on this layer's projections: waves 0-2 issue them before waiting; wave 3 polls
   // the q, k and v column tiles of this head (its poll would otherwise return only after its own prefetch) and
-  // issues its tiles afterwards.
+  // issues its tiles afterwards.  Own-row tiles in the first places follow the wait.
   auto prefetch = [&]() {
 #pragma unroll
     for (int dd = 0; dd < RG::tiles; ++dd)
@@ -1348,6 +1361,9 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
   if (wave < 3) prefetch();
   if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16, 3)) return false;
   if (wave == 3) prefetch();
+#pragma unroll
+  for (int dd = 0; dd < RG::tiles; ++dd)
+    if (dd >= nc && dd < n) ring_tile(dd);
   f32x4 o[1][8];
   float m_run[1] = {-INFINITY}, l_run[1] = {0.f};
 #pragma unroll
@@ -1360,12 +1376,12 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
   // Pairs of tiles (i, i + 1) at ring places i % T, i % T + 1 (T = tiles the ring holds).  The memory operations
   // issued after tile i + 1 are the direct loads of tiles i + 2 .. i + T - 1, so once at most that many loads are
   // pending the pair has landed; once both are read into registers their places take tiles i + T and i + T + 1,
-  // which stream in while the pair is computed.
+  // which stream in while the pair is computed.  (An own-row tile has as many direct loads as a bf16 cache tile.)
   static_assert(RG::tiles == 2 || RG::tiles == 4, "the waits below cover rings of two or four tiles");
 #pragma unroll 1
-  for (int i = 0; i < nc; i += 2) {
-    const bool two = i + 1 < nc;
-    const int after = RG::tiles == 4 ? min(nc - 2 - i, 2) : 0;  // tiles in flight behind the pair (when two)
+  for (int i = 0; i < n; i += 2) {
+    const bool two = i + 1 < n;
+    const int after = RG::tiles == 4 ? min(n - 2 - i, 2) : 0;  // tiles in flight behind the pair (when two)
     if (two && after == 2)
       vm_wait_below_c<2 * RG::loads>();
     else if (two && after == 1)
@@ -1375,32 +1391,21 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
     RawTile<TK> ta, tb;
     read_tile<TK>(slot_of(i), tl, ta);
     if (two) read_tile<TK>(slot_of(i + 1), tl, tb);
-    if (i + RG::tiles < nc) ring_tile(i + RG::tiles);
-    if (i + RG::tiles + 1 < nc) ring_tile(i + RG::tiles + 1);
+    if (i + RG::tiles < n) ring_tile(i + RG::tiles);
+    if (i + RG::tiles + 1 < n) ring_tile(i + RG::tiles + 1);
     if (two)
-      tile_pair_compute<TK>(ta, tb, qr[0], U.i0 + 32 * (wave + 4 * i), U.i0 + 32 * (wave + 4 * (i + 1)), U.i1, U.ksc,
-                            o[0], m_run[0], l_run[0]);
+      tile_pair_compute<TK>(ta, tb, qr[0], row0(i), lim(i), row0(i + 1), lim(i + 1), U.ksc, o[0], m_run[0], l_run[0]);
     else
-      tile_jobs<TK, 1, 1>(ta, qf, U.i0 + 32 * (wave + 4 * i), U.i1, U.ksc, o, m_run, l_run);
+      tile_jobs<TK, 1, 1>(ta, qf, row0(i), lim(i), U.ksc, o, m_run, l_run);
   }
-  if (KT == 1) {
+  if constexpr (KT == 1) {
     // fp8 values carry their scale: apply it to the cache part of the output before the own rows join
 #pragma unroll
     for (int k = 0; k < 8; ++k) o[0][k] *= U.vsc;
-  }
-  // own rows (bf16): tiles U.nct .. U.nct+nst-1 of the round robin
-  if (U.nst > 0) {
-    if (KT == 1) load_q<1, false>(a, tp, dm, U.b, U.h, tt_one, 1, qr);  // the queries again, as bf16
-    const int first_own = (wave - U.nct % 4 + 4) % 4;
-    for (int j = first_own; j < U.nst; j += 4) {
-      if constexpr (KT == 0) {
-        // staged like a cache tile (the wave's ring is done) and read transposed, as the cache tiles were
-        stage_own_tile<8>(U.ks, U.vs, (int64_t)dm.A * 2, 32 * j, tp.S, lring, 0);
-        vm_wait_all();
-        RawTile<2> t;
-        read_tile<2>(lring, tl, t);
-        tile_jobs<2, 1, 1>(t, qf, 32 * j, tp.S, 1.f, o, m_run, l_run);
-      } else {
+    // own rows (bf16): tiles U.nct .. U.nct+nst-1 of the round robin
+    if (U.nst > 0) {
+      load_q<1, false>(a, tp, dm, U.b, U.h, tt_one, 1, qr);  // the queries again, as bf16
+      for (int j = first_own; j < U.nst; j += 4) {
         RawTile<0> t;
         load_own_tile(U.ks, U.vs, (int64_t)dm.A * 2, 32 * j, tp.S, t);
         tile_jobs<0, 1, 1>(t, qf, 32 * j, tp.S, 1.f, o, m_run, l_run);
