@@ -55,6 +55,26 @@ def test_tick_kernel_and_per_phase_launches_match_oracle(n_frame):
     assert rel_err(outs["tick"][0], outs["per-phase"][0]) <= 1e-2
 
 
+@pytest.mark.parametrize("lengths", [(150,), (0,), (333,)])
+def test_single_agent_small_matches_oracle(lengths):
+    """One agent, one query tile, 2 heads per XCD (one attention workgroup per head, no partial states), per-layer
+    hidden outputs included; cache lengths 150 (ragged last tile), 0 (own rows only) and 333."""
+    wl = small(96 + lengths[0] % 7, lengths=lengths, capacity=400, n_layers=3, d_model=256, n_heads=16)
+    say(f"case single agent, L={lengths[0]}")
+    model = Model(wl)
+    cache = Cache(wl, starts=(123,))
+    host_tok, tok = tokens_for(wl)
+    ex = model.create()
+    wp, hid = run_forward(ex, cache, tok, 1, 0, with_hidden=True)
+    ref, ref_hid = model.oracle_agent(host_tok[0], cache.oracle_rows(0), cache.desc.pos[0])
+    e = rel_err(wp[0], ref)
+    say(f"  err {e:.3e}")
+    assert e <= TOL
+    for l in range(wl.n_layers):
+        assert rel_err(hid[l, 0], ref_hid[l]) <= TOL, l
+    ex.close()
+
+
 def test_consecutive_ticks_with_new_inputs():
     """Each tick must see its own inputs: forward A, then B (new tokens and cache), then A again."""
     wl_a = small(80, lengths=(64, 120))
