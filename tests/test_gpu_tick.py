@@ -75,6 +75,28 @@ def test_single_agent_small_matches_oracle(lengths):
     ex.close()
 
 
+def test_maximum_batch_of_agents_matches_oracle():
+    """64 agents (the batch limit) of 32 heads: 256 attention segments per XCD (the plan's limit), 640 rows in eight
+    row blocks; ragged cache lengths (0 included) in rings with different starts.  A sample of agents is checked."""
+    rng = np.random.default_rng(7)
+    lengths = tuple(int(x) for x in rng.integers(0, 121, 64))
+    lengths = (0,) + lengths[1:]
+    wl = small(90, lengths=lengths, capacity=128, n_layers=2, d_model=128, n_heads=32)
+    say("case 64 agents")
+    model = Model(wl)
+    cache = Cache(wl, starts=tuple(int(x) for x in rng.integers(0, 128, 64)))
+    host_tok, tok = tokens_for(wl)
+    ex = model.create()
+    wp, _ = run_forward(ex, cache, tok, wl.batch, 0)
+    for b in (0, 1, 17, 40, 63):
+        ref, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        e = rel_err(wp[b], ref)
+        say(f"  agent {b} (L={lengths[b]}) err {e:.3e}")
+        assert e <= TOL, (b, e)
+    assert np.isfinite(wp).all()
+    ex.close()
+
+
 def test_consecutive_ticks_with_new_inputs():
     """Each tick must see its own inputs: forward A, then B (new tokens and cache), then A again."""
     wl_a = small(80, lengths=(64, 120))
