@@ -97,6 +97,26 @@ def test_maximum_batch_of_agents_matches_oracle():
     ex.close()
 
 
+@pytest.mark.parametrize("n_frame", [30, 64])
+def test_many_query_slices_across_agents_match_oracle(n_frame):
+    """Several query tiles per agent with enough cache rows that every workgroup takes an equal slice of the XCD's
+    tiles: slices cut segments of different agents and leave partial states merged per query tile."""
+    wl = small(110 + n_frame, lengths=(3000, 2500, 3100), capacity=3200, n_layers=2, d_model=128, n_heads=16,
+               n_frame=n_frame)
+    say(f"case many-query slices, n_frame={n_frame}")
+    model = Model(wl)
+    cache = Cache(wl, starts=(3000, 17, 900))
+    host_tok, tok = tokens_for(wl)
+    ex = model.create()
+    wp, _ = run_forward(ex, cache, tok, wl.batch, n_frame)
+    for b in range(wl.batch):
+        ref, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        e = rel_err(wp[b], ref)
+        say(f"  agent {b} err {e:.3e}")
+        assert e <= TOL, (b, e)
+    ex.close()
+
+
 def test_consecutive_ticks_with_new_inputs():
     """Each tick must see its own inputs: forward A, then B (new tokens and cache), then A again."""
     wl_a = small(80, lengths=(64, 120))
