@@ -204,6 +204,26 @@ def test_small_fp8_cache_with_frame_tokens_matches_oracle(n_frame):
         assert e <= FP8_WP_TOL and ed <= BF16_WP_TOL
 
 
+def test_fp8_many_query_slices_across_agents_match_oracle():
+    """fp8 cache, 5 query tiles per agent (64 frame tokens) and enough rows that slices cut the segments of several
+    agents: key-split jobs, whole jobs and partial states merged per query tile, with the fp8 output layout."""
+    wl = synth.Workload(name="small_fp8_mq", wid=64, n_layers=2, d_model=128, n_heads=16, head_dim=128, d_ffn=256,
+                        n_expert_tokens=10, n_frame_tokens=64, batch=3, lengths=(3000, 2600, 3100), dtype="bf16",
+                        cache_dtype="fp8", capacity=3200)
+    say("case fp8 many-query slices")
+    model = Model(wl)
+    ex = model.create()
+    cache = Cache(wl, starts=(3100, 5, 700))
+    host_tok, tok = tokens_for(wl)
+    wp, _ = run_forward(ex, cache, tok, wl.batch, wl.n_frame_tokens)
+    for b in range(wl.batch):
+        ref, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        refd, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b, decoded=True), cache.desc.pos[b])
+        e, ed = rel_err(wp[b], ref), rel_err(wp[b], refd)
+        say(f"  agent {b} err vs source {e:.3e}, vs decoded {ed:.3e}")
+        assert e <= FP8_WP_TOL and ed <= BF16_WP_TOL
+
+
 @pytest.mark.slow
 def test_ragged_fp8_agents_match_oracle():
     """8 agents with ragged histories (256..16384 rows) in an fp8 cache; sampled agents vs the oracle."""
