@@ -575,7 +575,9 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
 // ------------------------------------------------------------------------------------------ Q
 // Units of XCD X: u = (local head hl, section sec (q, k, v), 16-column tile t), 24 per head of width 128.
 // Workgroup s takes units s, s + n, ...; its k-th unit goes to wave k % 4, which holds the unit's weights in
-// registers (loaded before the wait).  Each unit publishes a flag once its columns are written.
+// registers (loaded before the wait).  Each unit publishes a flag once its columns are written.  When each
+// attention segment has a workgroup of its own (plan mode 1) and the other workgroups have a wave for every unit,
+// those take all units, so that the attention workgroups start streaming their cache tiles at once.
 __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
   const int d = dm.d, M = tp.M, A = dm.A, H = dm.H, half = DH / 2, nt = d / 16;
@@ -589,9 +591,12 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
   const float* ssq = a.ssq_out + (int64_t)X * a.x_stride_s;
   const float* rope = a.rope + (int64_t)X * a.x_stride_r;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
+  const int nseg = tp.B * nh, nq = n - nseg;  // attention workgroups, and the others
+  const bool spare = uni(L.amode) == 1 && nq > 0 && n_units <= 4 * nq;
+  const int s0 = spare ? s - nseg : s, nw = spare ? nq : n;  // this workgroup's index among the Q workgroups
   bool waited = false;
-  for (int u0 = s; u0 < n_units; u0 += 4 * n) {
-    const int u = u0 + wave * n;  // this wave's unit in this round
+  for (int u0 = s0; s0 >= 0 && u0 < n_units; u0 += 4 * nw) {
+    const int u = u0 + wave * nw;  // this wave's unit in this round
     const bool mine = u < n_units;
     const int hl = u / 24, sec = (u % 24) / 8, t = u % 8;
     const int h = h0 + hl;
