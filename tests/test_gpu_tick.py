@@ -75,6 +75,28 @@ def test_single_agent_small_matches_oracle(lengths):
     ex.close()
 
 
+# 32 heads (4 per XCD, 96 Q units per XCD), one workgroup per attention segment: with 2 agents the 24 other
+# workgroups of an XCD have exactly one wave per Q unit and take them all; with 3 agents the 20 others are too few
+# and every workgroup takes Q units
+@pytest.mark.parametrize("lengths", [(200, 37), (90, 0, 150)])
+def test_attention_workgroups_with_and_without_q_units_match_oracle(lengths):
+    wl = small(120 + len(lengths), lengths=lengths, capacity=256, n_layers=2, d_model=128, n_heads=32)
+    say(f"case {len(lengths)} agents of 32 heads, L={lengths}")
+    model = Model(wl)
+    cache = Cache(wl, starts=tuple(31 * (b + 1) for b in range(len(lengths))))
+    host_tok, tok = tokens_for(wl)
+    ex = model.create()
+    wp, hid = run_forward(ex, cache, tok, wl.batch, 0, with_hidden=True)
+    for b in range(wl.batch):
+        ref, ref_hid = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        e = rel_err(wp[b], ref)
+        say(f"  agent {b} (L={lengths[b]}) err {e:.3e}")
+        assert e <= TOL, (b, e)
+        for l in range(wl.n_layers):
+            assert rel_err(hid[l, b], ref_hid[l]) <= TOL, (b, l)
+    ex.close()
+
+
 def test_maximum_batch_of_agents_matches_oracle():
     """64 agents (the batch limit) of 32 heads: 256 attention segments per XCD (the plan's limit), 640 rows in eight
     row blocks; ragged cache lengths (0 included) in rings with different starts.  A sample of agents is checked."""
