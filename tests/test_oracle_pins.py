@@ -340,6 +340,54 @@ def test_forward_is_composition_of_layers_and_head():
     assert pos[0] == 9
 
 
+def test_forward_with_empty_cache_depends_only_on_relative_positions():
+    # Rotary encoding makes every score depend on the difference of positions only (Sec. 3.1 reading): with no cached
+    # rows, moving token 0 from position 9 to 9 + 1000 leaves the forward unchanged; with cached rows (whose keys keep
+    # the phases they were cached with) the same move changes it.
+    sh, layers, toks, kc, vc, hw = _tiny_forward_inputs(seed=15, L=7)
+    fn = np.ones(sh.d_model)
+    empty = lambda l: (kc[l][:0], vc[l][:0])
+    full = lambda l: (kc[l], vc[l])
+    wp0, hid0 = ox.expert_forward(sh, layers, fn, hw, toks, empty, pos=9)
+    wp1, hid1 = ox.expert_forward(sh, layers, fn, hw, toks, empty, pos=1009)
+    np.testing.assert_allclose(hid1, hid0, rtol=0, atol=1e-10)
+    np.testing.assert_allclose(wp1, wp0, rtol=0, atol=1e-10)
+    wf0, _ = ox.expert_forward(sh, layers, fn, hw, toks, full, pos=9)
+    wf1, _ = ox.expert_forward(sh, layers, fn, hw, toks, full, pos=1009)
+    assert np.abs(wf1 - wf0).max() > 1e-3
+
+
+def test_expert_sequence_attention_is_unmasked():
+    # No mask among the expert-sequence tokens (expert and frame tokens see each other, Sec. 3.1 reading): without the
+    # rotary encoding (rope_base 0, the learned-embedding form) the layers are equivariant to any permutation of the
+    # sequence's rows, and the waypoints, pooled over the first T rows, are invariant to permutations inside the
+    # expert rows and inside the frame rows.  A causal or block mask breaks both.
+    sh, layers, toks, kc, vc, hw = _tiny_forward_inputs(seed=16, L=5, S=7)
+    sh0 = ox.ExpertShape(n_layers=sh.n_layers, d_model=sh.d_model, n_heads=sh.n_heads, head_dim=sh.head_dim,
+                         d_ffn=sh.d_ffn, n_expert_tokens=3, rope_base=0.0)
+    fn = np.ones(sh.d_model)
+    rows = lambda l: (kc[l], vc[l])
+    wp, hid = ox.expert_forward(sh0, layers, fn, hw, toks, rows, pos=5)
+    perm = np.array([6, 2, 4, 0, 5, 1, 3])  # mixes expert rows (0..2) and frame rows (3..6)
+    _, hidp = ox.expert_forward(sh0, layers, fn, hw, toks[perm], rows, pos=5)
+    np.testing.assert_allclose(hidp, hid[:, perm], rtol=0, atol=1e-11)
+    inside = np.array([2, 0, 1, 5, 6, 3, 4])  # permutes inside the expert rows and inside the frame rows
+    wpi, _ = ox.expert_forward(sh0, layers, fn, hw, toks[inside], rows, pos=5)
+    np.testing.assert_allclose(wpi, wp, rtol=0, atol=1e-11)
+    # a causal mask (row t sees the cache and rows <= t) fails the equivariance
+    def causal(q, k_self, v_self, k_cache, v_cache):
+        S = q.shape[0]
+        return np.stack([ox_joint(q[t:t + 1], k_self[:t + 1], v_self[:t + 1], k_cache, v_cache)[0] for t in range(S)])
+    ox_joint = ox.joint_attention
+    try:
+        ox.joint_attention = causal
+        _, hc = ox.expert_forward(sh0, layers, fn, hw, toks, rows, pos=5)
+        _, hcp = ox.expert_forward(sh0, layers, fn, hw, toks[perm], rows, pos=5)
+    finally:
+        ox.joint_attention = ox_joint
+    assert np.abs(hcp - hc[:, perm]).max() > 1e-3
+
+
 def test_append_only_cache_is_exact():
     # Sec. 3.3: with pre-rotated keys, a cache grown by appends equals one built at once; only the
     # set of rows matters.  Appending rows in any split order gives the same forward.
