@@ -10,9 +10,11 @@ Attention", run once per control tick as in Sec. 3.3):
 
 * ``expert.py``  -- RMSNorm, rotary encoding, the joint attention of Eq. (1)
   over [cached backbone K/V ; the expert's own K/V], the output projection, the
-  SwiGLU block, and the mean-pool + linear waypoint head.
-* ``fp8.py``     -- decoding of OCP FP8 E4M3 (e4m3fn) codes, used only to build
-  the diagnostic reference for the fp8-stored cache.
+  SwiGLU block, the mean-pool + linear waypoint head, and the paper's
+  two-layer head over the waypoint-query tokens.
+* ``fp8.py``     -- decoding of OCP FP8 E4M3 (e4m3fn) codes (the diagnostic
+  reference for the fp8-stored cache) and their encoding against a scale
+  (the reference of the quantising append).
 
 Every function is the plain definition evaluated in float64 on the exact values
 the GPU receives (inputs are rounded to the stored dtype first, then upcast).
@@ -32,6 +34,9 @@ from .expert import (  # noqa: F401
     swiglu_ffn,
     expert_layer,
     waypoint_head,
+    gelu,
+    query_head,
+    apply_head,
     expert_forward,
 )
-from .fp8 import e4m3fn_decode  # noqa: F401
+from .fp8 import e4m3fn_decode, e4m3fn_encode  # noqa: F401

@@ -32,15 +32,22 @@ notes; the GPU path implements the same readings):
 * Full multi-head attention: q, k and v all have H heads (the paper gives the
   backbone's 32-head, 128-wide geometry and no grouping).
 * FFN: z = (silu(x W_g^T) * (x W_u^T)) W_d^T with silu(u) = u / (1 + e^-u).
-* Head: final RMSNorm, mean over the first T (expert) tokens, then a linear
-  d -> n_out map without bias; outputs ordered x0, y0, ..., x4, y4.  (The
-  paper's "two-layer head" over the five waypoint queries is not specified
-  further.)
+* Head (workload form, ``head_kind = 0``): final RMSNorm, mean over the first
+  T (expert) tokens, then a linear d -> n_out map without bias; outputs
+  ordered x0, y0, ..., x4, y4.
+* Head (the paper's form, ``head_kind = 1``, Sec. 3.1): the five learnable
+  waypoint queries are decoded to five (x, y) waypoints by a two-layer head.
+  The paper gives neither the width nor the activation; reading: the queries
+  are the LAST n_out/2 of the T expert tokens (the per-frame token list puts
+  the state token and the four visual tokens first), each query row goes
+  through the final RMSNorm, Linear(d -> hidden) with bias, GELU in its exact
+  erf form, Linear(hidden -> 2) with bias; query i gives (x_i, y_i).
 * Precision: no intermediate rounding anywhere -- everything is float64.
 """
 
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass
 from typing import Callable, Sequence
 
@@ -60,6 +67,8 @@ class ExpertShape:
     n_out: int = 10
     rope_base: float = 10000.0
     rms_eps: float = 1e-6
+    head_kind: int = 0  # 0: mean-pool + linear; 1: two-layer head over the waypoint queries
+    head_hidden: int = 0  # width of the two-layer head's hidden layer (head_kind 1)
 
     @property
     def attn_width(self) -> int:
@@ -165,6 +174,35 @@ def waypoint_head(h, final_norm, head_w, n_expert_tokens: int, eps: float) -> np
     return x.mean(axis=0) @ np.asarray(head_w, np.float64).T
 
 
+def gelu(u: np.ndarray) -> np.ndarray:
+    """GELU in its exact form u * Phi(u) = u / 2 * (1 + erf(u / sqrt(2)))."""
+    u = np.asarray(u, dtype=np.float64)
+    erf = np.vectorize(math.erf, otypes=[np.float64])
+    return 0.5 * u * (1.0 + erf(u / math.sqrt(2.0)))
+
+
+def query_head(h, final_norm, w1, b1, w2, b2, n_expert_tokens: int, n_queries: int, eps: float) -> np.ndarray:
+    """The paper's waypoint head (Sec. 3.1): n_queries waypoint-query tokens, each decoded by a two-layer head.
+
+    The queries are rows T - n_queries .. T - 1 of the residual stream (the last expert tokens).  Each row is
+    final-normalised, mapped by Linear(d -> hidden) + b1, GELU, Linear(hidden -> 2) + b2.  Returns
+    [x0, y0, x1, y1, ...] (query i gives waypoint i).
+    """
+    h = np.asarray(h, np.float64)
+    x = rmsnorm(h[n_expert_tokens - n_queries:n_expert_tokens], final_norm, eps)
+    u = gelu(x @ np.asarray(w1, np.float64).T + np.asarray(b1, np.float64))
+    y = u @ np.asarray(w2, np.float64).T + np.asarray(b2, np.float64)
+    return y.reshape(-1)
+
+
+def apply_head(shape: "ExpertShape", h, final_norm, head) -> np.ndarray:
+    """The head of ``shape.head_kind``: head is W_head [n_out][d] (kind 0) or a dict w1, b1, w2, b2 (kind 1)."""
+    if shape.head_kind == 1:
+        return query_head(h, final_norm, head["w1"], head["b1"], head["w2"], head["b2"], shape.n_expert_tokens,
+                          shape.n_out // 2, shape.rms_eps)
+    return waypoint_head(h, final_norm, head, shape.n_expert_tokens, shape.rms_eps)
+
+
 def expert_forward(
     shape: ExpertShape,
     layers: Sequence[dict],
@@ -180,6 +218,7 @@ def expert_forward(
     optional current-frame tokens).  cache_rows(l) -> (K, V), each [L][H][Dh],
     the valid cached rows of layer l in any order (attention is invariant to
     the order of cache rows).  pos: position of token 0.
+    head_w: the head's parameters (see ``apply_head``).
     Returns (waypoints [n_out], hidden [n_layers][S][d]).
     """
     h = np.asarray(tokens, dtype=np.float64)
@@ -190,5 +229,5 @@ def expert_forward(
         kc, vc = cache_rows(layer)
         h = expert_layer(h, lw, kc, vc, positions, shape)
         hidden.append(h)
-    wp = waypoint_head(h, final_norm, head_w, shape.n_expert_tokens, shape.rms_eps)
+    wp = apply_head(shape, h, final_norm, head_w)
     return wp, np.stack(hidden)

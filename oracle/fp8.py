@@ -26,3 +26,31 @@ def e4m3fn_decode(codes) -> np.ndarray:
     sub = sign * np.ldexp(m / 8.0, -6)
     out = np.where(e == 0, sub, normal)
     return np.where((e == 15) & (m == 7), np.nan, out)
+
+
+def e4m3fn_encode(x, scale) -> np.ndarray:
+    """Quantise values to E4M3 codes against one scale: code = RNE(clamp(x / scale, -448, 448)).
+
+    The quotient is taken in float32 (the precision the append kernel divides in), so both sides take the
+    same integer decision from the same float32 value; the rounding to the E4M3 grid is exact here: every
+    finite E4M3 value and every float32 value is a float64 value, so the distances below are exact.  Among
+    the two nearest grid values a tie goes to the one with an even code (even mantissa), as round-to-
+    nearest-even prescribes.  NaN inputs give the NaN code 0x7F (sign kept).
+    """
+    y = np.asarray(x, np.float32) / np.float32(scale)
+    y = np.clip(y, np.float32(-448.0), np.float32(448.0)).astype(np.float64)
+    grid_codes = np.arange(0x7F, dtype=np.uint8)  # 0x00 .. 0x7E: the non-negative finite values, increasing
+    grid = e4m3fn_decode(grid_codes)
+    a = np.abs(y).ravel()
+    hi = np.searchsorted(grid, a, side="left").clip(0, len(grid) - 1)  # first grid value >= a
+    lo = (hi - 1).clip(0, None)
+    d_hi = grid[hi] - a
+    d_lo = a - grid[lo]
+    pick_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (hi % 2 == 0))
+    idx = np.where(pick_hi, hi, lo)
+    idx = np.where(a == grid[hi], hi, idx)
+    code = grid_codes[idx].astype(np.uint8)
+    neg = np.signbit(y.ravel())
+    code = np.where(neg, code | 0x80, code)
+    code = np.where(np.isnan(y.ravel()), np.where(neg, 0xFF, 0x7F), code)
+    return code.astype(np.uint8).reshape(np.shape(x))

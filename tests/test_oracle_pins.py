@@ -211,6 +211,88 @@ def test_waypoint_head_pools_only_expert_tokens():
     np.testing.assert_allclose(b, w @ x0, rtol=1e-13, atol=1e-13)
 
 
+def loop_mean_pool_head(h, g, w, T, eps):
+    """Scalar-loop transcription of the workload head: for each of the first T rows its RMSNorm times the gain,
+    averaged over those rows, then the linear map (no bias)."""
+    d = h.shape[1]
+    pooled = [0.0] * d
+    for t in range(T):
+        ms = sum(h[t][i] * h[t][i] for i in range(d)) / d
+        for i in range(d):
+            pooled[i] += h[t][i] / math.sqrt(ms + eps) * g[i] / T
+    return np.array([sum(w[o][i] * pooled[i] for i in range(d)) for o in range(w.shape[0])])
+
+
+@pytest.mark.parametrize("T,S", [(3, 5), (10, 10), (10, 14)])
+def test_waypoint_head_mean_pool_matches_loop(T, S):
+    # T > 1 with a non-unit final gain: the pooling is a mean (not a sum) of rows normalised one by one (the norm comes
+    # before the pooling), and the rows past T (frame tokens) are not pooled.
+    r = _rng(17, T, S)
+    d = 12
+    h = r.standard_normal((S, d)) * (1 + np.arange(S))[:, None]  # rows of different scales
+    g = 1 + 0.5 * r.standard_normal(d)
+    w = r.standard_normal((10, d))
+    got = ox.waypoint_head(h, g, w, T, 1e-6)
+    np.testing.assert_allclose(got, loop_mean_pool_head(h, g, w, T, 1e-6), rtol=0, atol=1e-12)
+
+
+def loop_query_head(h, g, w1, b1, w2, b2, T, nq, eps):
+    """Scalar-loop transcription of the two-layer query head: rows T-nq .. T-1, each RMSNorm times the gain, then
+    hidden_j = GELU(sum_i w1[j][i] x_i + b1[j]) with GELU(u) = u (1 + erf(u / sqrt 2)) / 2, then out_c = sum_j
+    w2[c][j] hidden_j + b2[c]; query q gives outputs 2q, 2q + 1."""
+    d = h.shape[1]
+    out = []
+    for t in range(T - nq, T):
+        ms = sum(h[t][i] * h[t][i] for i in range(d)) / d
+        x = [h[t][i] / math.sqrt(ms + eps) * g[i] for i in range(d)]
+        hid = []
+        for j in range(w1.shape[0]):
+            u = sum(w1[j][i] * x[i] for i in range(d)) + b1[j]
+            hid.append(u * (1.0 + math.erf(u / math.sqrt(2.0))) / 2.0)
+        for c in range(2):
+            out.append(sum(w2[c][j] * hid[j] for j in range(len(hid))) + b2[c])
+    return np.array(out)
+
+
+def _query_head_inputs(seed=18, T=10, S=12, d=16, hidden=24, nq=5):
+    r = _rng(seed)
+    h = r.standard_normal((S, d)) * 2
+    g = 1 + 0.3 * r.standard_normal(d)
+    w1, b1 = r.standard_normal((hidden, d)) * 0.5, r.standard_normal(hidden)
+    w2, b2 = r.standard_normal((2, hidden)) * 0.5, r.standard_normal(2)
+    return h, g, w1, b1, w2, b2, T, nq
+
+
+def test_query_head_matches_loop():
+    h, g, w1, b1, w2, b2, T, nq = _query_head_inputs()
+    got = ox.query_head(h, g, w1, b1, w2, b2, T, nq, 1e-6)
+    np.testing.assert_allclose(got, loop_query_head(h, g, w1, b1, w2, b2, T, nq, 1e-6), rtol=0, atol=1e-12)
+
+
+def test_query_head_matches_library_and_reads_only_the_query_rows():
+    h, g, w1, b1, w2, b2, T, nq = _query_head_inputs(seed=19)
+    F = torch.nn.functional
+    x = torch.from_numpy(h[T - nq:T])
+    x = F.rms_norm(x, (h.shape[1],), weight=torch.from_numpy(g), eps=1e-6)
+    want = F.linear(F.gelu(F.linear(x, torch.from_numpy(w1), torch.from_numpy(b1))), torch.from_numpy(w2),
+                    torch.from_numpy(b2)).numpy().reshape(-1)
+    got = ox.query_head(h, g, w1, b1, w2, b2, T, nq, 1e-6)
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+    h2 = h.copy()
+    h2[:T - nq] = 50 * _rng(20).standard_normal((T - nq, h.shape[1]))  # state and visual tokens
+    h2[T:] = 50 * _rng(21).standard_normal((h.shape[0] - T, h.shape[1]))  # frame tokens
+    np.testing.assert_array_equal(ox.query_head(h2, g, w1, b1, w2, b2, T, nq, 1e-6), got)
+
+
+def test_gelu_special_values():
+    # GELU(0) = 0; GELU(u) - GELU(-u) = u (Phi(u) + Phi(-u) = 1); Phi(1) from its series closed form
+    u = np.array([0.0, 0.5, 1.0, 3.0])
+    np.testing.assert_allclose(ox.gelu(u) - ox.gelu(-u), u, rtol=0, atol=1e-15)
+    assert ox.gelu(np.array([0.0]))[0] == 0.0
+    phi1 = 0.5 + sum((-1) ** n / (math.factorial(n) * (2 * n + 1) * 2 ** n) for n in range(40)) / math.sqrt(2 * math.pi)
+    np.testing.assert_allclose(ox.gelu(np.array([1.0]))[0], phi1, rtol=1e-15)
+
+
 # ----------------------------------------------------------------------------- one layer, brute force
 
 def _tiny_layer(r, d=8, H=2, Dh=4, F=12):
@@ -412,6 +494,29 @@ def test_e4m3_decode_exhaustive_against_library():
     np.testing.assert_array_equal(got[~nan], lib[~nan])
 
 
+def test_e4m3_encode_against_library():
+    # round-to-nearest-even onto the E4M3 grid after the clamp: torch's float8_e4m3fn cast, on values already
+    # clamped to the finite range (torch itself turns values >= 480 into NaN, hence the clamp), including every
+    # midpoint between neighbouring grid values (ties), the subnormal range and the clamp boundaries
+    r = _rng(22)
+    grid = oracle.e4m3fn_decode(np.arange(0x7F, dtype=np.uint8))
+    mids = ((grid[:-1] + grid[1:]) / 2).astype(np.float32)
+    vals = np.concatenate([r.standard_normal(50000).astype(np.float32) * 40, mids, -mids, grid.astype(np.float32),
+                           np.float32([448, -448, 464, 479.9, 1e6, -1e6, 0.0, -0.0, 2.0 ** -10, 3 * 2.0 ** -11])])
+    for scale in (np.float32(1.0), np.float32(0.0123)):
+        got = oracle.e4m3fn_encode(vals * scale, scale)
+        y = np.clip(vals * scale / scale, -448, 448).astype(np.float32)
+        want = torch.from_numpy(y).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+        np.testing.assert_array_equal(got, want)
+
+
+def test_e4m3_encode_is_inverse_of_decode_on_the_grid():
+    codes = np.array([c for c in range(256) if c not in (0x7F, 0xFF)], np.uint8)
+    vals = oracle.e4m3fn_decode(codes).astype(np.float32)
+    got = oracle.e4m3fn_encode(vals, np.float32(1.0))
+    np.testing.assert_array_equal(got, codes)
+
+
 def test_e4m3_decode_spec_points():
     for line in open(os.path.join(GOLDEN, "e4m3_spec_points.txt")):
         if line.startswith("#") or not line.strip():
@@ -454,6 +559,13 @@ MUTANTS = {
     "self_keys_dropped": ("joint_attention", "noself"),
     "gate_up_swapped": ("swiglu_ffn", "swap"),
     "rms_without_sqrt": ("rmsnorm", "nosqrt"),
+    "head_sum_instead_of_mean": ("waypoint_head", "headsum"),
+    "head_norm_after_pool": ("waypoint_head", "poolnorm"),
+    "query_head_tanh_gelu": ("gelu", "tanhgelu"),
+    "query_head_bias_dropped": ("query_head", "nobias"),
+    "query_head_first_rows": ("query_head", "firstrows"),
+    "e4m3_encode_truncates": ("e4m3fn_encode", "trunc"),
+    "e4m3_encode_ties_toward_zero": ("e4m3fn_encode", "tieslow"),
 }
 
 
@@ -479,10 +591,42 @@ def _mutant(kind):
         def f(x, gain, eps):
             x = np.asarray(x, np.float64)
             return x / (np.mean(x * x, -1, keepdims=True) + eps) * gain
+    elif kind == "headsum":
+        def f(h, g, w, T, eps):
+            return ORIG["waypoint_head"](h, g, w, T, eps) * T
+    elif kind == "poolnorm":
+        def f(h, g, w, T, eps):
+            x = np.asarray(h, np.float64)[:T].mean(axis=0, keepdims=True)
+            return ox.rmsnorm(x, g, eps)[0] @ np.asarray(w, np.float64).T
+    elif kind == "tanhgelu":
+        def f(u):
+            u = np.asarray(u, np.float64)
+            return 0.5 * u * (1 + np.tanh(math.sqrt(2 / math.pi) * (u + 0.044715 * u ** 3)))
+    elif kind == "nobias":
+        def f(h, g, w1, b1, w2, b2, T, nq, eps):
+            return ORIG["query_head"](h, g, w1, np.zeros_like(b1), w2, b2, T, nq, eps)
+    elif kind == "firstrows":
+        def f(h, g, w1, b1, w2, b2, T, nq, eps):
+            return ORIG["query_head"](h, g, w1, b1, w2, b2, nq, nq, eps)
+    elif kind == "trunc":
+        def f(x, scale):
+            y = np.clip(np.asarray(x, np.float32) / np.float32(scale), -448, 448).astype(np.float64)
+            grid = oracle.e4m3fn_decode(np.arange(0x7F, dtype=np.uint8))
+            idx = np.searchsorted(grid, np.abs(y), side="right") - 1
+            return np.where(np.signbit(y), idx | 0x80, idx).astype(np.uint8)
+    elif kind == "tieslow":
+        def f(x, scale):
+            y = np.clip(np.asarray(x, np.float32) / np.float32(scale), -448, 448).astype(np.float64)
+            grid = oracle.e4m3fn_decode(np.arange(0x7F, dtype=np.uint8))
+            a = np.abs(y)
+            idx = np.argmin(np.abs(grid[None, :] - a.reshape(-1, 1)), axis=1)  # first (smaller) of two nearest
+            return np.where(np.signbit(y).reshape(-1), idx | 0x80, idx).astype(np.uint8).reshape(np.shape(x))
     return f
 
 
-ORIG = {n: getattr(ox, n) for n in ("joint_attention", "apply_rope", "swiglu_ffn", "rmsnorm")}
+ORIG = {n: getattr(ox, n) for n in ("joint_attention", "apply_rope", "swiglu_ffn", "rmsnorm", "waypoint_head",
+                                    "query_head", "gelu")}
+ORIG["e4m3fn_encode"] = oracle.fp8.e4m3fn_encode
 PIN_TESTS = [
     lambda: test_attention_matches_brute_force_masked_softmax(5, 3, 2, 4),
     lambda: test_cache_attention_equals_library_attention_over_concatenation(),
@@ -490,13 +634,21 @@ PIN_TESTS = [
     lambda: test_swiglu_matches_library(),
     lambda: test_rmsnorm_matches_library_and_unit_rms(),
     lambda: test_layer_matches_brute_force(6),
+    lambda: test_waypoint_head_mean_pool_matches_loop(3, 5),
+    lambda: test_query_head_matches_loop(),
+    lambda: test_query_head_matches_library_and_reads_only_the_query_rows(),
+    lambda: test_e4m3_encode_against_library(),
 ]
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_planted_mistakes_are_caught(name, monkeypatch):
     fn_name, kind = MUTANTS[name]
-    monkeypatch.setattr(ox, fn_name, _mutant(kind))
+    if fn_name == "e4m3fn_encode":
+        monkeypatch.setattr(oracle.fp8, fn_name, _mutant(kind))
+        monkeypatch.setattr(oracle, fn_name, _mutant(kind))
+    else:
+        monkeypatch.setattr(ox, fn_name, _mutant(kind))
     caught = 0
     for t in PIN_TESTS:
         try:
