@@ -58,6 +58,12 @@ typedef enum {
 
 enum { FSX_APPEND_RING = 0, FSX_APPEND_ERROR = 1 };
 
+/* Layouts of the cache tensors (fsx_cache_desc.layout). */
+enum {
+  FSX_CACHE_HEAD_MAJOR = 0, /* [batch][n_layers][H][capacity][Dh]: one contiguous ring per (agent, layer, head) */
+  FSX_CACHE_TOKEN_MAJOR = 1 /* [batch][n_layers][capacity][H][Dh]: one ring slot holds a cached token for every head */
+};
+
 /* Flags of fsx_expert_cfg.flags. */
 enum {
   FSX_FLAG_GENERIC = 1,     /* force the simple per-op kernels instead of the fused tick kernel */
@@ -99,20 +105,24 @@ typedef struct {
   const float* ffn_norm;   /* [d] RMSNorm gain before the FFN */
 } fsx_layer_weights;
 
-/* The backbone's per-layer KV cache for a batch of agents (Sec. 3.1, Sec. 3.3).
- * Head-major, as a transformer's per-layer cache is usually kept: each (agent, layer, head) owns a
- * contiguous ring of `capacity` rows of Dh elements (one cached token's key, or value, for that head).
- * Keys are stored already rotated.  The valid rows of agent b are ring slots (start[b] + i) mod
- * capacity, i < len[b], the same slots in every layer and head. */
+/* The backbone's per-layer KV cache for a batch of agents (Sec. 3.1: per layer the cache is L tokens of
+ * H heads x Dh; Sec. 3.3: it is standing state that grows by appends).  Each (agent, layer) holds a ring of
+ * `capacity` token slots; a slot holds one cached token's key (or value) for every head.  Two layouts of
+ * the same ring are accepted (`layout`): head-major, where each (agent, layer, head) owns `capacity`
+ * contiguous rows of Dh elements, and token-major, where a slot's H x Dh elements are contiguous (the
+ * L x (H*Dh) rows of a backbone's cache).  Either way one head's row of one token is Dh contiguous
+ * elements.  Keys are stored already rotated.  The valid rows of agent b are ring slots
+ * (start[b] + i) mod capacity, i < len[b], the same slots in every layer and head. */
 typedef struct {
   int32_t dtype;           /* FSX_F32 | FSX_BF16 | FSX_FP8_E4M3 */
   int32_t batch;           /* agents described by this descriptor */
   int32_t n_layers;        /* must equal the expert's */
   int32_t n_heads;         /* must equal the expert's */
   int32_t head_dim;        /* must equal the expert's */
-  int32_t reserved;        /* 0 */
-  int64_t capacity;        /* ring rows per (agent, layer) */
-  void* k;                 /* DEVICE [batch][n_layers][H][capacity][Dh] */
+  int32_t layout;          /* FSX_CACHE_HEAD_MAJOR (0) or FSX_CACHE_TOKEN_MAJOR (1); FSX_E_INVALID otherwise */
+  int64_t capacity;        /* ring slots per (agent, layer) */
+  void* k;                 /* DEVICE [batch][n_layers][H][capacity][Dh] (head-major) or
+                              [batch][n_layers][capacity][H][Dh] (token-major) */
   void* v;                 /* DEVICE, same layout */
   const float* k_scale;    /* FP8 only: DEVICE [batch][n_layers][H], stored value = code * scale */
   const float* v_scale;    /* FP8 only: DEVICE [batch][n_layers][H] */
@@ -152,9 +162,10 @@ int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, const void* 
 
 /* Append n_rows new cached rows to every (agent, layer, head) of the cache (Sec. 3.3: every K ticks
  * the slow system appends the current frame's tokens through an incremental forward).
- *   k_rows, v_rows DEVICE [cache->batch][n_layers][H][n_rows][Dh] in cache->dtype (fp8: codes
- *                  already scaled by the cache's k_scale / v_scale); Dh elements must be a multiple
- *                  of 16 bytes (FSX_E_UNSUPPORTED otherwise)
+ *   k_rows, v_rows DEVICE, in the cache's layout with n_rows slots: [cache->batch][n_layers][H][n_rows][Dh]
+ *                  for a head-major cache, [cache->batch][n_layers][n_rows][H][Dh] for a token-major one;
+ *                  elements of cache->dtype (fp8: codes already scaled by the cache's k_scale / v_scale);
+ *                  Dh elements must be a multiple of 16 bytes (FSX_E_UNSUPPORTED otherwise)
  *   policy         FSX_APPEND_RING: when a ring is full the oldest rows are overwritten (start
  *                  advances); FSX_APPEND_ERROR: FSX_E_CAPACITY if any agent would exceed
  *                  capacity, and nothing is written.
@@ -178,7 +189,8 @@ int fsx_expert_status(fsx_expert* ex, void* stream);
  * if cap is short. */
 int fsx_expert_trace(fsx_expert* ex, uint64_t* host_out, int64_t cap, int32_t* n_wg, int32_t* n_ev, void* stream);
 
-/* Free the packed weights and the workspace (synchronises the device first). NULL is a no-op. */
+/* Wait for the handle's last enqueued tick (not for other work on the device), then free the packed weights
+ * and the workspace.  NULL is a no-op. */
 void fsx_expert_destroy(fsx_expert* ex);
 
 /* Message of the calling thread's last failed call ("" if none). */
@@ -193,6 +205,14 @@ int fsx_expert_info(const fsx_expert* ex, int32_t* path, int64_t* weight_bytes, 
 
 /* Library version, "major.minor.patch". */
 const char* fsx_version(void);
+
+/* Measurement helper, not part of the tick: enqueue one read-only pass over `bytes` of device memory, so the
+ * caller can time (with events on `stream`) the HBM read bandwidth this device reaches with a plain streaming
+ * kernel -- the ceiling next to the published peak that the tick's bandwidth is quoted against.
+ *   buf    DEVICE, 16-byte aligned; bytes a positive multiple of 16 (FSX_E_INVALID otherwise)
+ *   mode   0: 16-byte register loads; 1: 16-byte direct loads into LDS (the attention's access)
+ *   sink   DEVICE [1024] uint32 words the kernel folds a checksum into (contents are meaningless) */
+int fsx_probe_hbm_read(const void* buf, int64_t bytes, int32_t mode, uint32_t* sink, void* stream);
 
 #ifdef __cplusplus
 }

@@ -56,6 +56,7 @@ struct fsx_expert {
   uint64_t* trace = nullptr;
   uint64_t epoch = 0;
   uint64_t status_seen = 0;
+  hipEvent_t done = nullptr;  // recorded after every tick enqueued on the handle (destroy waits for it)
 };
 
 static void free_expert(fsx_expert* ex) {
@@ -65,6 +66,7 @@ static void free_expert(fsx_expert* ex) {
   if (ex->head_w) (void)hipFree(ex->head_w);
   if (ex->wsbuf) (void)hipFree(ex->wsbuf);
   if (ex->trace) (void)hipFree(ex->trace);
+  if (ex->done) (void)hipEventDestroy(ex->done);
   delete ex;
 }
 
@@ -326,6 +328,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
       t.trace = ex->trace;
     }
   }
+  if (!ok(hipEventCreateWithFlags(&ex->done, hipEventDisableTiming), "hipEventCreateWithFlags")) return cleanup(FSX_E_HIP);
   if (!ok(hipStreamSynchronize(s), "hipStreamSynchronize(create)")) return cleanup(FSX_E_HIP);
   *out = ex;
   g_err.clear();
@@ -338,6 +341,8 @@ static int validate_cache(const fsx_expert* ex, const fsx_cache_desc* c, int bat
     return fail(FSX_E_INVALID, "cache dtype must be F32, BF16 or FP8_E4M3");
   if (ex && (c->n_layers != ex->cfg.n_layers || c->n_heads != ex->cfg.n_heads || c->head_dim != ex->cfg.head_dim))
     return fail(FSX_E_INVALID, "cache geometry (n_layers, n_heads, head_dim) differs from the expert's");
+  if (c->layout != FSX_CACHE_HEAD_MAJOR && c->layout != FSX_CACHE_TOKEN_MAJOR)
+    return fail(FSX_E_INVALID, "cache layout must be FSX_CACHE_HEAD_MAJOR or FSX_CACHE_TOKEN_MAJOR");
   if (c->batch <= 0 || c->batch > FSX_MAX_BATCH) return fail(FSX_E_INVALID, "cache batch must be in 1..64");
   if (batch > c->batch) return fail(FSX_E_INVALID, "batch exceeds the cache descriptor's batch");
   if (c->capacity < 0 || c->capacity > (int64_t)INT32_MAX) return fail(FSX_E_INVALID, "capacity out of range");
@@ -395,10 +400,19 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
   CacheView cv{};
   cv.k = cache->k; cv.v = cache->v; cv.k_scale = cache->k_scale; cv.v_scale = cache->v_scale;
   cv.cap = cache->capacity; cv.n_layers = cache->n_layers; cv.layer = 0; cv.dtype = cache->dtype;
+  cv.H = cache->n_heads; cv.Dh = cache->head_dim;
+  if (cache->layout == FSX_CACHE_TOKEN_MAJOR) {
+    cv.hs = cache->head_dim;
+    cv.rs = (int64_t)cache->n_heads * cache->head_dim;
+  } else {
+    cv.hs = cache->capacity * cache->head_dim;
+    cv.rs = cache->head_dim;
+  }
 
   if (ex->path == 1) {
     HIP_TRY(generic_tick(ex->gw.data(), ex->final_norm, ex->head_w, c.dtype, tokens, cv, tp, dm, ex->gws, waypoints,
                          hidden, s));
+    HIP_TRY(hipEventRecord(ex->done, s));
     g_err.clear();
     return FSX_OK;
   }
@@ -454,6 +468,7 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
     a.hidden = hidden;
     a.epoch = ++ex->epoch;
     HIP_TRY(launch_tick(a, tp, dm, ex->cu_count, s));
+    HIP_TRY(hipEventRecord(ex->done, s));
     g_err.clear();
     return FSX_OK;
   }
@@ -476,6 +491,7 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
     HIP_TRY(launch_reduce_norm(tp, dm, ex->ws, ks_d, gnext, hidden ? hidden + (int64_t)l * tp.M * dm.d : nullptr, s));
   }
   HIP_TRY(launch_head(tp, dm, ex->ws, ex->final_norm, ex->head_w, c.dtype, waypoints, s));
+  HIP_TRY(hipEventRecord(ex->done, s));
   g_err.clear();
   return FSX_OK;
 }
@@ -559,7 +575,7 @@ extern "C" int fsx_expert_trace(fsx_expert* ex, uint64_t* host_out, int64_t cap,
 
 extern "C" void fsx_expert_destroy(fsx_expert* ex) {
   if (!ex) return;
-  (void)hipDeviceSynchronize();
+  if (ex->done) (void)hipEventSynchronize(ex->done);  // the handle's last tick, not the whole device
   free_expert(ex);
 }
 
@@ -573,4 +589,13 @@ extern "C" int fsx_expert_info(const fsx_expert* ex, int32_t* path, int64_t* wei
   return FSX_OK;
 }
 
-extern "C" const char* fsx_version(void) { return "0.1.0"; }
+extern "C" const char* fsx_version(void) { return "0.2.0"; }
+
+extern "C" int fsx_probe_hbm_read(const void* buf, int64_t bytes, int32_t mode, uint32_t* sink, void* stream) {
+  if (!buf || !sink) return fail(FSX_E_INVALID, "buf and sink must be non-NULL");
+  if (bytes <= 0 || bytes % 16 || !aligned16(buf)) return fail(FSX_E_INVALID, "bytes must be a positive multiple of 16 and buf 16-byte aligned");
+  if (mode != 0 && mode != 1) return fail(FSX_E_INVALID, "mode must be 0 or 1");
+  HIP_TRY(launch_probe_read(buf, bytes, mode, sink, (hipStream_t)stream));
+  g_err.clear();
+  return FSX_OK;
+}

@@ -334,8 +334,8 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a, TickParams tp) {
     const int i0 = cidx * tp.chunk_rows;
     const int i1 = min(i0 + tp.chunk_rows, tp.len[b]);
     constexpr int ES = KT == 0 ? 2 : 1;
-    // head-major cache: the (agent, layer, head) slab is capacity rows of Dh contiguous elements
-    const int64_t off = ((((int64_t)b * a.cv.n_layers + a.cv.layer) * a.H + h) * a.cv.cap) * a.Dh * ES;
+    // ring slot 0 of (agent, layer, head); slots are a.cv.rs elements apart
+    const int64_t off = cache_head_base(a.cv, b, a.cv.layer, h) * ES;
     float ks = 1.f, vs = 1.f;
     if (KT == 1) {
       const int64_t si = ((int64_t)b * a.cv.n_layers + a.cv.layer) * a.H + h;
@@ -343,7 +343,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a, TickParams tp) {
       vs = a.cv.v_scale[si];
     }
     load_q_frag<KT, false>(a.q, qrow, tv, grp, qf);
-    attn_rows<KT, true, false, false>((const char*)a.cv.k + off, (const char*)a.cv.v + off, (int64_t)a.Dh * ES, tp.start[b],
+    attn_rows<KT, true, false, false>((const char*)a.cv.k + off, (const char*)a.cv.v + off, a.cv.rs * ES, tp.start[b],
                         a.cv.cap, i0, i1, qf, ks, vs, lane, out_o, out_ml, a.Dh);
   }
 }
@@ -481,8 +481,9 @@ hipError_t launch_head(const TickParams& tp, const Dims& dm, const Workspace& ws
 
 // =====================================================================================================
 // Cache append (Sec. 3.3): copy n new rows of every (agent, layer, head) into ring slots
-// (first[b] + j) mod cap, bit-exact, 16 bytes per thread.  Source [B][n_layers][H][n][Dh], destination
-// [B][n_layers][H][cap][Dh].
+// (first[b] + j) mod cap, bit-exact, 16 bytes per thread.  The rows come in the cache's layout with n slots:
+// head-major [B][n_layers][H][n][Dh] into [B][n_layers][H][cap][Dh], or token-major [B][n_layers][n][H][Dh] into
+// [B][n_layers][cap][H][Dh].  Either way thread i copies 16-byte chunk i of the source, so reads are coalesced.
 // =====================================================================================================
 struct AppendArgs {
   const uint4* ks;
@@ -491,7 +492,7 @@ struct AppendArgs {
   uint4* vc;
   int64_t cap;
   int64_t row_chunks;  // 16-byte chunks per head row (Dh elements)
-  int n_layers, n_heads, n_rows, B;
+  int n_layers, n_heads, n_rows, B, token_major;
   int64_t first[FSX_MAX_BATCH];
 };
 
@@ -501,12 +502,24 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a) {
   if (i >= total) return;
   const int64_t ch = i % a.row_chunks;
   int64_t r = i / a.row_chunks;
-  const int j = (int)(r % a.n_rows);
-  r /= a.n_rows;  // (b, l, h) slab index
-  const int b = (int)(r / ((int64_t)a.n_layers * a.n_heads));
-  int64_t slot = a.first[b] + j;
-  if (slot >= a.cap) slot -= a.cap;
-  const int64_t dst = (r * a.cap + slot) * a.row_chunks + ch;
+  int64_t dst;
+  if (a.token_major) {
+    const int h = (int)(r % a.n_heads);
+    r /= a.n_heads;
+    const int j = (int)(r % a.n_rows);
+    r /= a.n_rows;  // (b, l)
+    const int b = (int)(r / a.n_layers);
+    int64_t slot = a.first[b] + j;
+    if (slot >= a.cap) slot -= a.cap;
+    dst = ((r * a.cap + slot) * a.n_heads + h) * a.row_chunks + ch;
+  } else {
+    const int j = (int)(r % a.n_rows);
+    r /= a.n_rows;  // (b, l, h) slab index
+    const int b = (int)(r / ((int64_t)a.n_layers * a.n_heads));
+    int64_t slot = a.first[b] + j;
+    if (slot >= a.cap) slot -= a.cap;
+    dst = (r * a.cap + slot) * a.row_chunks + ch;
+  }
   a.kc[dst] = a.ks[i];
   a.vc[dst] = a.vs[i];
 }
@@ -518,6 +531,7 @@ hipError_t launch_append(const fsx_cache_desc& c, const void* k_rows, const void
   a.ks = (const uint4*)k_rows; a.vs = (const uint4*)v_rows; a.kc = (uint4*)c.k; a.vc = (uint4*)c.v;
   a.cap = c.capacity; a.row_chunks = (int64_t)c.head_dim * es / 16;
   a.n_layers = c.n_layers; a.n_heads = c.n_heads; a.n_rows = n_rows; a.B = c.batch;
+  a.token_major = c.layout == FSX_CACHE_TOKEN_MAJOR;
   for (int b = 0; b < c.batch; ++b) a.first[b] = first[b];
   const int64_t total = (int64_t)a.B * a.n_layers * a.n_heads * a.n_rows * a.row_chunks;
   if (total == 0) return hipSuccess;

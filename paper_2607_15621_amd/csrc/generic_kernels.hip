@@ -82,7 +82,7 @@ __global__ void g_attention(CacheView cv, TickParams tp, const float* q, const f
   const int A = H * Dh;
   const float* qr = q + (int64_t)m * A + (int64_t)h * Dh;
   const int L = tp.len[b];
-  const int64_t slab = (((int64_t)b * cv.n_layers + cv.layer) * H + h) * cv.cap;  // head-major (agent, layer, head) slab
+  const int64_t hb = cache_head_base(cv, b, cv.layer, h);  // ring slot 0 of (agent, layer, head)
   float ks = 1.f, vs = 1.f;
   if (cv.dtype == FSX_FP8_E4M3) {
     ks = cv.k_scale[((int64_t)b * cv.n_layers + cv.layer) * H + h];
@@ -91,7 +91,7 @@ __global__ void g_attention(CacheView cv, TickParams tp, const float* q, const f
   auto cache_off = [&](int r) {
     int64_t slot = tp.start[b] + r;
     if (slot >= cv.cap) slot -= cv.cap;
-    return (slab + slot) * Dh;
+    return hb + slot * cv.rs;
   };
   float mx = -INFINITY;
   for (int r = 0; r < L; ++r) {

@@ -29,17 +29,26 @@ struct TickParams {
   int32_t slot_x;
 };
 
-// Cache view of one layer.
+// Cache view of one layer.  Element offset of (agent b, layer l, head h, ring slot j, channel c):
+// ((b * n_layers + l) * H * cap) * Dh + h * hs + j * rs + c, with (hs, rs) = (cap * Dh, Dh) for a head-major
+// cache and (Dh, H * Dh) for a token-major one.
 struct CacheView {
   const void* k;     // base of the whole cache tensor
   const void* v;
   const float* k_scale;  // fp8 only: [batch][n_layers][H]
   const float* v_scale;
   int64_t cap;           // ring rows
+  int64_t hs;            // elements between the rows of two heads of one slot
+  int64_t rs;            // elements between two ring slots of one head
   int32_t n_layers;
   int32_t layer;
   int32_t dtype;         // fsx_dtype
+  int32_t H, Dh;
 };
+// Element offset of row slot 0 of (agent b, layer l, head h).
+__host__ __device__ inline int64_t cache_head_base(const CacheView& cv, int b, int l, int h) {
+  return ((int64_t)b * cv.n_layers + l) * cv.H * cv.cap * cv.Dh + (int64_t)h * cv.hs;
+}
 
 // ------------------------------------------------------------------ packing (create time)
 enum PackKind { PACK_PLAIN = 0, PACK_ROPE_PAIRS = 1, PACK_SWIGLU_PAIRS = 2 };
@@ -158,6 +167,11 @@ hipError_t tick_occupancy(int kt, int* blocks_per_cu);
 hipError_t launch_tick(const TickArgs& a, const TickParams& tp, const Dims& dm, int grid, hipStream_t s);
 // Hardware XCD id of every workgroup of a one-workgroup-per-CU launch (create-time placement check).
 hipError_t probe_xcds(uint32_t* dev_out, int grid, hipStream_t s);
+
+// ------------------------------------------------------------------ measurement helper
+// One read-only pass over `bytes` (a multiple of 16) of buf; mode 0 register loads, 1 direct loads into LDS;
+// sink: DEVICE [1024] uint32 checksum words.
+hipError_t launch_probe_read(const void* buf, int64_t bytes, int mode, uint32_t* sink, hipStream_t s);
 
 // ------------------------------------------------------------------ cache append
 hipError_t launch_append(const fsx_cache_desc& c, const void* k_rows, const void* v_rows, int n_rows,

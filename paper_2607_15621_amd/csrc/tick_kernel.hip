@@ -988,6 +988,7 @@ struct AUnit {
   int nct, nst;     // cache tiles, own-row tiles
   const char* kc;   // cache K/V base of (b, layer, head) (slot 0)
   const char* vc;
+  int64_t rsb;      // bytes between two ring slots of the head
   const char* ks;   // own rows base of (b, head)
   const char* vs;
   float ksc, vsc;   // fp8 scales
@@ -1090,8 +1091,8 @@ __device__ __forceinline__ void combine_ranges(const TickArgs& a, const TickPara
 // the 16 rows of a K fragment read fall in distinct banks.  Lane l of instruction q brings row 8q + l/8 into chunk
 // position l % 8.  Rows past i1 repeat row i0 (masked in the update).
 template <int NQI = 4>
-__device__ __forceinline__ void stage_tile_fp8(const char* kb, const char* vb, int64_t start, int64_t cap, int i0,
-                                               int r0, int i1, uint8_t* slot, int q0 = 0) {
+__device__ __forceinline__ void stage_tile_fp8(const char* kb, const char* vb, int64_t rsb, int64_t start, int64_t cap,
+                                               int i0, int r0, int i1, uint8_t* slot, int q0 = 0) {
   const int lane = tix() & 63, rl = lane >> 3, pc = lane & 7;
   asm volatile("" ::: "memory");  // after every read of the slot's previous tile
 #pragma unroll
@@ -1099,7 +1100,7 @@ __device__ __forceinline__ void stage_tile_fp8(const char* kb, const char* vb, i
     const int q = q0 + qq, r = 8 * q + rl;
     int64_t row = start + (r0 + r < i1 ? r0 + r : i0);
     if (row >= cap) row -= cap;
-    const int64_t off = row * DH + 16 * (pc ^ ((r >> 1) & 7));
+    const int64_t off = row * rsb + 16 * (pc ^ ((r >> 1) & 7));
     load_lds16<false>(kb + off, slot + q * 1024);
     load_lds16<false>(vb + off, slot + 32 * DH + q * 1024);
   }
@@ -1180,8 +1181,8 @@ __device__ __forceinline__ void read_tile_fp8(const uint8_t* slot, const TileLan
 // k ^ (r & 15) (the 16 rows of a K fragment read, and the 4 rows of a V fragment read, fall in distinct banks).  Lane
 // l of instruction q brings row 4q + l/16 into chunk position l % 16.  Rows past i1 repeat row i0.
 template <int NQI = 8>
-__device__ __forceinline__ void stage_tile_bf16(const char* kb, const char* vb, int64_t start, int64_t cap, int i0,
-                                                int r0, int i1, uint8_t* slot, int q0 = 0) {
+__device__ __forceinline__ void stage_tile_bf16(const char* kb, const char* vb, int64_t rsb, int64_t start, int64_t cap,
+                                                int i0, int r0, int i1, uint8_t* slot, int q0 = 0) {
   const int lane = tix() & 63, rl = lane >> 4, pc = lane & 15;
   asm volatile("" ::: "memory");  // after every read of the slots' previous tile
 #pragma unroll
@@ -1189,7 +1190,7 @@ __device__ __forceinline__ void stage_tile_bf16(const char* kb, const char* vb, 
     const int q = q0 + qq, r = 4 * q + rl;  // row of the tile, 0..31
     int64_t row = start + (r0 + r < i1 ? r0 + r : i0);
     if (row >= cap) row -= cap;
-    const int64_t off = row * DH * 2 + 16 * (pc ^ (r & 15));
+    const int64_t off = row * rsb + 16 * (pc ^ (r & 15));
     uint8_t* dst = slot + (q >> 2) * RSLOT + (q & 3) * 1024;
     load_lds16<false>(kb + off, dst);
     load_lds16<false>(vb + off, dst + 16 * DH * 2);
@@ -1235,12 +1236,12 @@ __device__ __forceinline__ void read_tile_bf16(const uint8_t* slot, const TileLa
   }
 }
 template <int KT>
-__device__ __forceinline__ void stage_tile(const char* kb, const char* vb, int64_t start, int64_t cap, int i0, int r0,
-                                           int i1, uint8_t* slot) {
+__device__ __forceinline__ void stage_tile(const char* kb, const char* vb, int64_t rsb, int64_t start, int64_t cap,
+                                           int i0, int r0, int i1, uint8_t* slot) {
   if constexpr (KT == 0)
-    stage_tile_bf16<8>(kb, vb, start, cap, i0, r0, i1, slot);
+    stage_tile_bf16<8>(kb, vb, rsb, start, cap, i0, r0, i1, slot);
   else
-    stage_tile_fp8<4>(kb, vb, start, cap, i0, r0, i1, slot);
+    stage_tile_fp8<4>(kb, vb, rsb, start, cap, i0, r0, i1, slot);
 }
 // The expert's own rows [r0, r0+32) of (agent, head) (bf16, produced in this launch) staged in the bf16 tile layout
 // by device-scope direct loads; instructions q0 .. q0+NQI-1 of the eight.  Rows at or past S repeat row 0.
@@ -1351,7 +1352,7 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
   auto lim = [&](int i) { return cache_tile(i) ? U.i1 : tp.S; };
   auto ring_tile = [&](int i) {
     if (cache_tile(i))
-      stage_tile<KT>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, row0(i), U.i1, slot_of(i));
+      stage_tile<KT>(U.kc, U.vc, U.rsb, tp.start[U.b], a.cv.cap, U.i0, row0(i), U.i1, slot_of(i));
     else
       stage_own_tile<8>(U.ks, U.vs, (int64_t)dm.A * 2, row0(i), tp.S, slot_of(i), 0);
   };
@@ -1515,9 +1516,9 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
   auto place = [&](int i) { return base + (i % WR::tiles) * WR::tb; };
   auto stage = [&](int i) {
     if constexpr (KT == 0)
-      stage_tile_bf16<2>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * i, U.i1, place(i), 2 * wave);
+      stage_tile_bf16<2>(U.kc, U.vc, U.rsb, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * i, U.i1, place(i), 2 * wave);
     else
-      stage_tile_fp8<1>(U.kc, U.vc, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * i, U.i1, place(i), wave);
+      stage_tile_fp8<1>(U.kc, U.vc, U.rsb, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * i, U.i1, place(i), wave);
   };
   constexpr int G = 4;  // tiles per barrier step
   auto prefetch = [&]() {
@@ -1719,9 +1720,10 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
     U.i1 = min(32 * t1, tp.len[b]);
     U.nct = U.i1 > U.i0 ? (U.i1 - U.i0 + 31) / 32 : 0;
     U.nst = t1 == g1 - g0 ? (tp.S + 31) / 32 : 0;  // the segment's last slice also takes the expert's own rows
-    const int64_t slab = (((int64_t)b * a.cv.n_layers + l) * H + h) * a.cv.cap;  // head-major (b, l, h) ring
-    U.kc = (const char*)a.cv.k + slab * DH * ES;
-    U.vc = (const char*)a.cv.v + slab * DH * ES;
+    const int64_t hb = cache_head_base(a.cv, b, l, h);  // ring slot 0 of (b, l, h)
+    U.kc = (const char*)a.cv.k + hb * ES;
+    U.vc = (const char*)a.cv.v + hb * ES;
+    U.rsb = a.cv.rs * ES;
     U.ks = (const char*)a.kself + ((int64_t)b * tp.S * A + (int64_t)h * DH) * 2;
     U.vs = (const char*)a.vself + ((int64_t)b * tp.S * A + (int64_t)h * DH) * 2;
     U.ksc = U.vsc = 1.f;
@@ -1912,17 +1914,31 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
 // wp[b] = mean over t < T of RMSNorm(h[b][t]) * g_final, times W_head^T, on the workgroups of XCD rank 0
 // (agent b on slot b mod n0), from that XCD's replica of the residual.  Thread tid owns columns tid and
 // tid + 256 and holds the pooled rows in registers (16 rows per pass).
+// Every workgroup that gave up (its failure is in the status word before it gets here) stores NaN into ALL
+// waypoints, after its status store has completed.  The head workgroups store valid waypoints, wait for those
+// stores, then read the status word and store NaN if a failure is recorded.  Either the head sees the failure, or
+// the failing workgroup's status store (and so its NaN stores, which follow it) comes after the head's valid
+// stores: the waypoints of a failed tick end as NaN in both orders.
+__device__ __forceinline__ void poison_waypoints(const TickArgs& a, const TickParams& tp, const Dims& dm) {
+  stores_done();
+  __syncthreads();
+  for (int i = tix(); i < tp.B * dm.n_out; i += NTHR) st_dev_f(a.waypoints + i, __builtin_nanf(""));
+  stores_done();
+}
 __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& tp, const Dims& dm, bool ok, TickLds& L) {
   const int d = dm.d, nl = dm.n_layers, T = tp.T;
   const int tid = tix(), wave = tid >> 6, lane = tid & 63;
-  if (uni(L.X) != 0 && ok) return;
-  // after a failure every workgroup of XCD 0 (or, if registration failed, workgroup b) writes NaN for its agents
-  const int s = ok ? uni(L.s) : (int)blockIdx.x, n = ok ? uni(L.n0) : (int)gridDim.x;
+  if (!ok) {
+    poison_waypoints(a, tp, dm);
+    return;
+  }
+  if (uni(L.X) != 0) return;
+  const int s = uni(L.s), n = uni(L.n0);
   for (int b = s; b < tp.B; b += n) {
-    if (ok) ok = wg_wait(a.f_out, d / 16, stamp_of(a, nl - 1, nl), a, L);  // XCD rank 0's flags
+    ok = wg_wait(a.f_out, d / 16, stamp_of(a, nl - 1, nl), a, L);  // XCD rank 0's flags
     if (!ok) {
-      for (int o = tid; o < dm.n_out; o += NTHR) a.waypoints[(int64_t)b * dm.n_out + o] = __builtin_nanf("");
-      continue;
+      poison_waypoints(a, tp, dm);
+      return;
     }
     const float* h = a.hres;  // replica of XCD rank 0, tile-major [d/16][Mp][16]
     const int n0 = tid, n1 = tid + NTHR;
@@ -1973,10 +1989,16 @@ __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& 
       }
 #pragma unroll
       for (int m = 32; m >= 1; m >>= 1) acc += shfl_xor(acc, m);
-      if (lane == 0) a.waypoints[(int64_t)b * dm.n_out + o] = acc;
+      if (lane == 0) st_dev_f(a.waypoints + (int64_t)b * dm.n_out + o, acc);
     }
     __syncthreads();
   }
+  if (s >= tp.B) return;
+  stores_done();
+  __syncthreads();
+  if (tix() == 0) L.ok = ld_dev(a.status) != fail_tag(a);  // one read, so the branch below is uniform
+  __syncthreads();
+  if (!L.ok) poison_waypoints(a, tp, dm);
 }
 
 // ------------------------------------------------------------------------------------------ kernel

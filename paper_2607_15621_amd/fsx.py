@@ -19,12 +19,14 @@ LIB_PATH = os.path.join(HERE, "libfsx.so")
 
 F32, BF16, FP8_E4M3 = 0, 1, 2
 APPEND_RING, APPEND_ERROR = 0, 1
+CACHE_HEAD_MAJOR, CACHE_TOKEN_MAJOR = 0, 1
 FLAG_GENERIC, FLAG_MULTI_LAUNCH, FLAG_TRACE = 1, 2, 4
 MAX_BATCH = 64
 STATUS = {0: "FSX_OK", 1: "FSX_E_INVALID", 2: "FSX_E_UNSUPPORTED", 3: "FSX_E_CAPACITY", 4: "FSX_E_OOM",
           5: "FSX_E_HIP"}
 SYMBOLS = ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_status",
-           "fsx_expert_trace", "fsx_expert_destroy", "fsx_last_error", "fsx_expert_info", "fsx_version")
+           "fsx_expert_trace", "fsx_expert_destroy", "fsx_last_error", "fsx_expert_info", "fsx_version",
+           "fsx_probe_hbm_read")
 
 
 class FsxError(RuntimeError):
@@ -48,7 +50,7 @@ class LayerWeights(ctypes.Structure):
 
 class CacheDescC(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int32), ("batch", ctypes.c_int32), ("n_layers", ctypes.c_int32),
-                ("n_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("layout", ctypes.c_int32),
                 ("capacity", ctypes.c_int64), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
                 ("k_scale", ctypes.c_void_p), ("v_scale", ctypes.c_void_p),
                 ("start", ctypes.POINTER(ctypes.c_int64)), ("len", ctypes.POINTER(ctypes.c_int64)),
@@ -78,8 +80,9 @@ def lib() -> ctypes.CDLL:
         L.fsx_last_error.restype = ctypes.c_char_p
         L.fsx_expert_info.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i64), ctypes.POINTER(i64)]
         L.fsx_version.restype = ctypes.c_char_p
+        L.fsx_probe_hbm_read.argtypes = [vp, i64, i32, vp, vp]
         for n in ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_info",
-                  "fsx_expert_status", "fsx_expert_trace"):
+                  "fsx_expert_status", "fsx_expert_trace", "fsx_probe_hbm_read"):
             getattr(L, n).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -163,13 +166,14 @@ def expert_info(ex: Expert):
 
 
 class CacheDesc:
-    """fsx_cache_desc: device K/V tensors [batch][n_layers][capacity][H][Dh] plus host ring state.
+    """fsx_cache_desc: device K/V tensors, [batch][n_layers][H][capacity][Dh] (layout CACHE_HEAD_MAJOR) or
+    [batch][n_layers][capacity][H][Dh] (CACHE_TOKEN_MAJOR), plus host ring state.
 
     start / len / pos are numpy int64 arrays that the C side reads, and updates in place on append.
     """
 
     def __init__(self, k, v, dtype: int, n_layers: int, n_heads: int, head_dim: int, capacity: int,
-                 lengths, positions=None, starts=None, k_scale=None, v_scale=None):
+                 lengths, positions=None, starts=None, k_scale=None, v_scale=None, layout: int = CACHE_HEAD_MAJOR):
         self.k, self.v, self.k_scale, self.v_scale = k, v, k_scale, v_scale
         batch = len(lengths)
         self.len = np.ascontiguousarray(np.asarray(lengths, dtype=np.int64))
@@ -177,7 +181,8 @@ class CacheDesc:
         self.start = np.ascontiguousarray(np.zeros(batch, np.int64) if starts is None else
                                           np.asarray(starts, dtype=np.int64))
         P = ctypes.POINTER(ctypes.c_int64)
-        self.c = CacheDescC(dtype, batch, n_layers, n_heads, head_dim, 0, capacity, _ptr(k), _ptr(v),
+        self.layout = layout
+        self.c = CacheDescC(dtype, batch, n_layers, n_heads, head_dim, layout, capacity, _ptr(k), _ptr(v),
                             _ptr(k_scale), _ptr(v_scale), self.start.ctypes.data_as(P),
                             self.len.ctypes.data_as(P), self.pos.ctypes.data_as(P))
 
@@ -209,3 +214,8 @@ def cache_append_rows(cache: CacheDesc, k_rows, v_rows, n_rows: int, policy: int
     """fsx_cache_append_rows: enqueue the row copy; host ring state is updated on return."""
     _check(lib().fsx_cache_append_rows(ctypes.byref(cache.c), _ptr(k_rows), _ptr(v_rows), n_rows, policy,
                                        _stream(stream)))
+
+
+def probe_hbm_read(buf, nbytes: int, mode: int, sink, stream=None):
+    """fsx_probe_hbm_read: enqueue one read-only pass over nbytes of buf (measurement helper)."""
+    _check(lib().fsx_probe_hbm_read(_ptr(buf), nbytes, mode, _ptr(sink), _stream(stream)))

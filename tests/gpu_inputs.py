@@ -55,14 +55,18 @@ class Cache:
     """
 
     def __init__(self, wl: synth.Workload, lengths=None, starts=None, capacity=None, device="cuda",
-                 fill_workers=None):
+                 fill_workers=None, layout=fsx.CACHE_HEAD_MAJOR):
         self.wl = wl
+        self.layout = layout
         self.lengths = list(wl.lengths if lengths is None else lengths)
         B = len(self.lengths)
         cap = wl.capacity if capacity is None else capacity
         self.capacity = cap
         self.starts = [0] * B if starts is None else list(starts)
-        shape = (B, wl.n_layers, wl.n_heads, cap, wl.head_dim)  # head-major rings
+        if layout == fsx.CACHE_TOKEN_MAJOR:
+            shape = (B, wl.n_layers, cap, wl.n_heads, wl.head_dim)  # a slot holds every head of one token
+        else:
+            shape = (B, wl.n_layers, wl.n_heads, cap, wl.head_dim)  # head-major rings
         if wl.cache_dtype == "fp8":
             self.k = torch.zeros(shape, dtype=torch.uint8, device=device)
             self.v = torch.zeros(shape, dtype=torch.uint8, device=device)
@@ -79,7 +83,7 @@ class Cache:
         torch.cuda.synchronize()
         self.desc = fsx.CacheDesc(self.k, self.v, fsx_dtype(wl.cache_dtype), wl.n_layers, wl.n_heads, wl.head_dim,
                                   cap, self.lengths, positions=self.lengths, starts=self.starts,
-                                  k_scale=self.k_scale, v_scale=self.v_scale)
+                                  k_scale=self.k_scale, v_scale=self.v_scale, layout=layout)
 
     def _slots(self, b, n):
         return (self.starts[b] + np.arange(n)) % self.capacity
@@ -97,9 +101,25 @@ class Cache:
                 t = torch.from_numpy(codes)
             else:
                 t = torch.from_numpy(src).to(dst.dtype)
-            # generator slab [L][H][Dh] -> head-major [H][L][Dh] rows of the ring
-            t = t.permute(1, 0, 2).contiguous()
-            dst[b, l].index_copy_(1, idx.to(dst.device), t.to(dst.device, non_blocking=False))
+            if self.layout == fsx.CACHE_TOKEN_MAJOR:  # generator slab [L][H][Dh] = slots of the ring
+                dst[b, l].index_copy_(0, idx.to(dst.device), t.to(dst.device, non_blocking=False))
+            else:  # generator slab [L][H][Dh] -> head-major [H][L][Dh] rows of the ring
+                t = t.permute(1, 0, 2).contiguous()
+                dst[b, l].index_copy_(1, idx.to(dst.device), t.to(dst.device, non_blocking=False))
+
+    def slot_rows(self, b, l, kind, slots):
+        """Device rows [len(slots)][H][Dh] of (agent b, layer l) at the given ring slots, whatever the layout."""
+        t = self.k if kind == "k" else self.v
+        idx = torch.as_tensor(np.asarray(slots), device=t.device)
+        if self.layout == fsx.CACHE_TOKEN_MAJOR:
+            return t[b, l].index_select(0, idx)
+        return t[b, l].index_select(1, idx).permute(1, 0, 2)
+
+    def rows_for_append(self, rows: np.ndarray, dtype):
+        """Generator rows [B][n_layers][n][H][Dh] -> the device layout fsx_cache_append_rows takes for this cache."""
+        if self.layout == fsx.CACHE_TOKEN_MAJOR:
+            return torch.from_numpy(np.ascontiguousarray(rows)).to("cuda", dtype)
+        return head_major_rows(rows, dtype)
 
 
 def head_major_rows(rows: np.ndarray, dtype, device="cuda"):

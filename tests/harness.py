@@ -7,6 +7,10 @@ GPU result into the oracle.
 
 from __future__ import annotations
 
+import json
+import os
+import threading
+
 import numpy as np
 
 import oracle
@@ -45,3 +49,38 @@ class Cache(_Cache):
             return out[0], out[1]
 
         return rows
+
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+ERR_LOG = os.environ.get("FSX_PARITY_LOG") or os.path.join(ROOT, "gpurun_out", "parity_errors.jsonl")
+_log_lock = threading.Lock()
+
+
+def record(agent, err, tol, what="waypoints, max|d| / max|ref|", extra=None):
+    """Print the observed error of one comparison and append it to the parity log (one JSON line per check), then
+    assert it is within tol."""
+    case = os.environ.get("PYTEST_CURRENT_TEST", "?").rsplit(" ", 1)[0]
+    line = {"case": case, "agent": agent, "what": what, "err": float(err), "tol": float(tol),
+            "ok": bool(err <= tol)}
+    if extra:
+        line.update(extra)
+    print(f"  {case} agent {agent} {what}: {err:.3e} (tol {tol})", flush=True)
+    try:
+        with _log_lock:
+            os.makedirs(os.path.dirname(ERR_LOG), exist_ok=True)
+            with open(ERR_LOG, "a") as f:
+                f.write(json.dumps(line) + "\n")
+    except OSError:
+        pass
+    assert err <= tol, line
+
+
+def oracle_agents(model, agents, job, workers=None):
+    """Run job(b) -> oracle result for several agents on a thread pool (NumPy's generators and BLAS release the
+    GIL), BLAS limited to one thread per worker; returns {b: result}."""
+    from threadpoolctl import threadpool_limits
+
+    agents = list(agents)
+    with threadpool_limits(1):
+        res = synth.parallel_map(job, agents, workers)
+    return dict(zip(agents, res))

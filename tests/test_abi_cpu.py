@@ -47,3 +47,14 @@ def test_argument_checks_run_before_any_gpu_work():
     assert L.fsx_expert_forward(None, None, None, 1, 0, None, None, None) == 1
     assert L.fsx_cache_append_rows(None, None, None, 4, 0, None) == 1
     assert fsx.version().count(".") == 2
+
+
+def test_cache_layout_is_validated_before_any_gpu_work():
+    import numpy as np
+
+    lens = np.array([4], np.int64)
+    desc = fsx.CacheDesc(None, None, fsx.BF16, 2, 4, 128, 8, lens)
+    desc.c.layout = 7
+    assert fsx.lib().fsx_cache_append_rows(ctypes.byref(desc.c), None, None, 4, 0, None) == 1
+    assert "layout" in fsx.last_error()
+    assert fsx.lib().fsx_probe_hbm_read(None, 16, 0, None, None) == 1

@@ -18,7 +18,7 @@ import pytest
 import torch
 
 import synth
-from harness import Cache, Model, rel_err, run_forward, tokens_for
+from harness import Cache, Model, record, rel_err, run_forward, tokens_for
 from paper_2607_15621_amd import fsx
 
 pytestmark = pytest.mark.gpu
@@ -46,15 +46,18 @@ def check_agents(model, cache, host_tok, wp, hid, agents, wp_tol, hid_tol=None, 
             err = float(np.abs(wp[b] - ref_wp).max())
         else:
             err = rel_err(wp[b], ref_wp)
-        say(f"  agent {b} L={cache.lengths[b]} waypoint err {err:.3e} (tol {wp_tol})")
-        assert err <= wp_tol, (b, err)
+        record(b, err, wp_tol, what="waypoints, max|d|" if absolute else "waypoints, max|d| / max|ref|",
+               extra={"L": cache.lengths[b]})
         if hid is not None and hid_tol is not None:
+            worst = 0.0
             for l in range(ref_hid.shape[0]):
                 if absolute:
                     e = float(np.abs(hid[l, b] - ref_hid[l]).max())
                 else:
                     e = rel_err(hid[l, b], ref_hid[l])
-                assert e <= hid_tol, (b, l, e)
+                worst = max(worst, e)
+            record(b, worst, hid_tol, what="worst layer hidden, max|d|" if absolute else
+                   "worst layer hidden, max|d| / max|ref|")
 
 
 def test_tiny_fp32_expert_matches_oracle():
