@@ -160,6 +160,21 @@ int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weights* layers
 int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, const void* tokens, int32_t batch,
                        int32_t n_frame_tokens, float* waypoints, float* hidden, void* stream);
 
+/* The same tick as fsx_expert_forward, for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): it allocates nothing, neither in the call nor
+ * through the handle's workspace.  The tick kernel's workspace lives in a static device array of the library of
+ * 48 MiB per device (held until the process ends; its device address is looked up on the first call on a device).
+ * Each call first clears the part of that array that must start at zero, with a kernel on `stream`, so a call does
+ * not depend on what an earlier call left there; calls that overlap on one device (other streams or threads) race
+ * on the array and must be serialised by the caller.  Arguments and results as fsx_expert_forward.
+ *   FSX_E_CAPACITY    the call's sizes need more than the array holds (the message gives the bytes needed;
+ *                     e.g. 16 agents x 10 tokens or one agent x 74 tokens fit, 64 agents do not)
+ *   FSX_E_UNSUPPORTED the handle does not run the persistent tick kernel (fp32 weights, FSX_FLAG_GENERIC,
+ *                     FSX_FLAG_MULTI_LAUNCH, shapes outside the per-XCD split)
+ * A tick that gives up on a wait writes NaN waypoints; fsx_expert_status does not report calls made here. */
+int fsx_expert_forward_noalloc(fsx_expert* ex, const fsx_cache_desc* cache, const void* tokens, int32_t batch,
+                               int32_t n_frame_tokens, float* waypoints, float* hidden, void* stream);
+
 /* Append n_rows new cached rows to every (agent, layer, head) of the cache (Sec. 3.3: every K ticks
  * the slow system appends the current frame's tokens through an incremental forward).
  *   k_rows, v_rows DEVICE, in the cache's layout with n_rows slots: [cache->batch][n_layers][H][n_rows][Dh]

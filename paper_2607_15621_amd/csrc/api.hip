@@ -3,6 +3,7 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <mutex>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -57,6 +58,7 @@ struct fsx_expert {
   uint64_t epoch = 0;
   uint64_t status_seen = 0;
   hipEvent_t done = nullptr;  // recorded after every tick enqueued on the handle (destroy waits for it)
+  int wg_per_xcd_max = 0;     // most workgroups the create-time probe placed on one XCD
 };
 
 static void free_expert(fsx_expert* ex) {
@@ -249,9 +251,12 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
                         ok(hipStreamSynchronize(s), "hipStreamSynchronize(xcd probe)");
       (void)hipFree(dev_ids);
       if (!good) return cleanup(FSX_E_HIP);
-      bool seen[16] = {false};
-      for (uint32_t id : ids) seen[id & 15] = true;
-      for (bool b : seen) nx += b;
+      int cnt[16] = {0};
+      for (uint32_t id : ids) ++cnt[id & 15];
+      for (int x = 0; x < 16; ++x) {
+        nx += cnt[x] > 0;
+        ex->wg_per_xcd_max = std::max(ex->wg_per_xcd_max, cnt[x]);
+      }
     }
     ex->nx = nx;
     const int nh_max = nx > 0 ? (H + nx - 1) / nx : 1 << 30;
@@ -363,8 +368,76 @@ static int validate_cache(const fsx_expert* ex, const fsx_cache_desc* c, int bat
   return FSX_OK;
 }
 
-extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, const void* tokens, int32_t batch,
-                                  int32_t n_frame_tokens, float* waypoints, float* hidden, void* stream) {
+// ------------------------------------------------------------------------------------------------------------
+// The entry point that allocates nothing keeps the tick kernel's workspace in `scratch`, a file-scope device array
+// of STATIC_SCRATCH_BYTES.  In host code `scratch` names a host-side stand-in, never a device address: the device
+// address is looked up once per device (hipGetSymbolAddress, with that device current) and only that pointer is
+// used.  Every call on a device shares its array; a call clears the part that must start at zero (flags, stamped
+// partial words, registration and status words) with a fill kernel on its stream, so calls are independent of the
+// previous contents, but calls that overlap on one device (two streams, two threads) race on the array.
+constexpr size_t STATIC_SCRATCH_BYTES = (size_t)48 << 20;
+constexpr int STATIC_MAX_DEVICES = 64;
+static __device__ __align__(256) uint8_t scratch[STATIC_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_dev[STATIC_MAX_DEVICES] = {};
+
+// Device address of `scratch` on device dev (the current device), looked up on the first call for that device.
+int scratch_of(int dev, void** out) {
+  if (dev < 0 || dev >= STATIC_MAX_DEVICES) return fail(FSX_E_UNSUPPORTED, "device index beyond the static workspace table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return fail(FSX_E_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return FSX_OK;
+}
+
+// Lay the tick kernel's workspace for this call's sizes over `base` (nullptr: only measure).  Data first, then the
+// part that must start at zero, from *zero_off to the returned total.
+size_t static_tick_layout(const fsx_expert* ex, const TickParams& tp, char* base, TickArgs& t, size_t* zero_off) {
+  const fsx_expert_cfg& c = ex->cfg;
+  const size_t d = c.d_model, F = c.d_ffn, Dh = c.head_dim, A = ex->A, M = tp.M, Mp = tp.Mp, Ms = tp.Ms;
+  const size_t dt = d / 16, R = ((size_t)tp.M + 79) / 80, NXS = NXR;  // replicas: the tick path runs on <= NXR XCDs
+  const size_t items = (size_t)NXR * tp.slot_x * tp.n_tt;
+  auto r256 = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  const size_t rep_f = r256(Mp * d * 4), rep_b = r256(Mp * d * 2), rep_s = r256(dt * Ms * 4), rep_r = r256(M * Dh * 4);
+  t.x_stride_f = (int64_t)(rep_f / 4);
+  t.x_stride_b = (int64_t)(rep_b / 2);
+  t.x_stride_s = (int64_t)(rep_s / 4);
+  t.x_stride_r = (int64_t)(rep_r / 4);
+  void* dummy;
+  const std::pair<void**, size_t> parts[] = {
+      {(void**)&t.q, M * A * 4},  {(void**)&t.kself, M * A * 2}, {(void**)&t.vself, M * A * 2},
+      {(void**)&t.attn, M * A * 2}, {(void**)&t.att_o, items * 16 * Dh * 4}, {(void**)&t.att_ml, items * 32 * 4},
+      {(void**)&t.hres, NXS * rep_f}, {(void**)&t.xb_mid, NXS * rep_b}, {(void**)&t.xb_out, NXS * rep_b},
+      {(void**)&t.ssq_mid, NXS * rep_s}, {(void**)&t.ssq_out, NXS * rep_s}, {(void**)&t.rope, NXS * rep_r},
+      {(void**)&t.z, Mp * F * 2},
+      {&dummy, 0},  // start of the part that must start at zero
+      {(void**)&t.po, NXS * dt * Mp * 16 * 8}, {(void**)&t.pd, NXS * dt * Mp * 16 * 8},
+      {(void**)&t.reg, (size_t)ex->cu_count * 8}, {(void**)&t.f_rope, NXS * XFLAGS * FPAD * 8},
+      {(void**)&t.f_out, NXS * XFLAGS * FPAD * 8}, {(void**)&t.f_mid, NXS * XFLAGS * FPAD * 8},
+      {(void**)&t.f_q, 3 * A / 16 * FPAD * 8}, {(void**)&t.f_attn, (size_t)tp.B * c.n_heads * tp.n_tt * FPAD * 8},
+      {(void**)&t.f_rng, items * FPAD * 8}, {(void**)&t.f_z, F / 8 * R * FPAD * 8}, {(void**)&t.status, 256}};
+  size_t off = 0;
+  for (const auto& p : parts) {
+    if (p.first == &dummy) {
+      *zero_off = off;
+      continue;
+    }
+    if (base) *p.first = base + off;
+    off += r256(p.second);
+  }
+  return off;
+}
+}  // namespace
+
+static int forward_impl(fsx_expert* ex, const fsx_cache_desc* cache, const void* tokens, int32_t batch,
+                        int32_t n_frame_tokens, float* waypoints, float* hidden, void* stream, bool use_static) {
   if (!ex) return fail(FSX_E_INVALID, "expert handle is NULL");
   if (!tokens || !waypoints) return fail(FSX_E_INVALID, "tokens and waypoints must be non-NULL");
   const fsx_expert_cfg& c = ex->cfg;
@@ -409,6 +482,9 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
     cv.rs = cache->head_dim;
   }
 
+  if (use_static && !ex->tick)
+    return fail(FSX_E_UNSUPPORTED, "the allocation-free entry point runs the persistent tick kernel only (bf16 expert "
+                                   "whose heads and FFN columns fit the per-XCD split, no FSX_FLAG_MULTI_LAUNCH)");
   if (ex->path == 1) {
     HIP_TRY(generic_tick(ex->gw.data(), ex->final_norm, ex->head_w, c.dtype, tokens, cv, tp, dm, ex->gws, waypoints,
                          hidden, s));
@@ -456,17 +532,33 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
       tp.seg_w[k] = std::max<int>(1, (int)((tp.len[b] + 31) / 32));
       tp.seg_p[k + 1] = tp.seg_p[k] + tp.seg_w[k];
     }
-    // partial-state slots per XCD: at most one per segment plus one per slice boundary
-    tp.slot_x = batch * 4 + G;
-    if ((int64_t)NXR * tp.slot_x * tp.n_tt > ex->items_max)
-      return fail(FSX_E_UNSUPPORTED, "attention partial-state slots exceed the workspace");
+    // partial-state slots per XCD: at most one per segment (<= 4 local heads per agent) plus one per slice boundary
+    // (the kernel checks the bound and fails the tick if the placement breaks it)
+    tp.slot_x = batch * 4 + (use_static ? ex->wg_per_xcd_max : G);
     TickArgs a = ex->ta;
+    if (use_static) {
+      // the workspace for this call's sizes, laid over the static array; epoch 1 on flags cleared by this call
+      size_t zoff = 0;
+      const size_t need = static_tick_layout(ex, tp, nullptr, a, &zoff);
+      if (need > STATIC_SCRATCH_BYTES)
+        return fail(FSX_E_CAPACITY, "this call needs " + std::to_string(need) + " bytes of workspace; the static array "
+                                    "holds " + std::to_string(STATIC_SCRATCH_BYTES));
+      void* base = nullptr;
+      rc = scratch_of(dev, &base);
+      if (rc) return rc;
+      static_tick_layout(ex, tp, (char*)base, a, &zoff);
+      HIP_TRY(launch_fill_zero((char*)base + zoff, need - zoff, s));
+      a.epoch = 1;
+    } else {
+      if ((int64_t)NXR * tp.slot_x * tp.n_tt > ex->items_max)
+        return fail(FSX_E_UNSUPPORTED, "attention partial-state slots exceed the workspace");
+      a.epoch = ++ex->epoch;
+    }
     a.tok_dtype = c.dtype;
     a.tokens = tokens;
     a.cv = cv;
     a.waypoints = waypoints;
     a.hidden = hidden;
-    a.epoch = ++ex->epoch;
     HIP_TRY(launch_tick(a, tp, dm, ex->cu_count, s));
     HIP_TRY(hipEventRecord(ex->done, s));
     g_err.clear();
@@ -494,6 +586,17 @@ extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, c
   HIP_TRY(hipEventRecord(ex->done, s));
   g_err.clear();
   return FSX_OK;
+}
+
+extern "C" int fsx_expert_forward(fsx_expert* ex, const fsx_cache_desc* cache, const void* tokens, int32_t batch,
+                                  int32_t n_frame_tokens, float* waypoints, float* hidden, void* stream) {
+  return forward_impl(ex, cache, tokens, batch, n_frame_tokens, waypoints, hidden, stream, false);
+}
+
+extern "C" int fsx_expert_forward_noalloc(fsx_expert* ex, const fsx_cache_desc* cache, const void* tokens,
+                                          int32_t batch, int32_t n_frame_tokens, float* waypoints, float* hidden,
+                                          void* stream) {
+  return forward_impl(ex, cache, tokens, batch, n_frame_tokens, waypoints, hidden, stream, true);
 }
 
 extern "C" int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, const void* v_rows, int32_t n_rows,

@@ -13,6 +13,8 @@
 //   down  : down projection, split-K partials; then norm again with the next layer's gain.
 // The head pools the first T tokens after a final RMSNorm and applies a d -> n_out map.
 
+#include <algorithm>
+
 #include "attn_device.h"
 #include "common.h"
 #include "kernels.h"
@@ -536,6 +538,27 @@ hipError_t launch_append(const fsx_cache_desc& c, const void* k_rows, const void
   const int64_t total = (int64_t)a.B * a.n_layers * a.n_heads * a.n_rows * a.row_chunks;
   if (total == 0) return hipSuccess;
   hipLaunchKernelGGL(k_append, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace fsx
+
+namespace fsx {
+
+// =====================================================================================================
+// Zero fill of a device range (a kernel, not a memset, so that it is an ordinary kernel node when the caller
+// captures the stream into a graph).  Whole 16-byte chunks; `bytes` is a multiple of 256.
+// =====================================================================================================
+__global__ __launch_bounds__(256) void k_fill_zero(uint4* p, int64_t n16) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = make_uint4(0, 0, 0, 0);
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
+  const int64_t n16 = (int64_t)(bytes / 16);
+  if (n16 == 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n16 + 255) / 256, 2048);
+  hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)blocks), dim3(256), 0, s, (uint4*)p, n16);
   return hipGetLastError();
 }
 

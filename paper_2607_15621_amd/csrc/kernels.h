@@ -168,6 +168,9 @@ hipError_t launch_tick(const TickArgs& a, const TickParams& tp, const Dims& dm, 
 // Hardware XCD id of every workgroup of a one-workgroup-per-CU launch (create-time placement check).
 hipError_t probe_xcds(uint32_t* dev_out, int grid, hipStream_t s);
 
+// Zero `bytes` (a multiple of 256) at p with a kernel.
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+
 // ------------------------------------------------------------------ measurement helper
 // One read-only pass over `bytes` (a multiple of 16) of buf; mode 0 register loads, 1 direct loads into LDS;
 // sink: DEVICE [1024] uint32 checksum words.

@@ -1642,7 +1642,7 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
 // the padding equal segments split into whole slices when the workgroups divide them evenly.
 constexpr int SEG_COST = 24;
 constexpr int SEG_COST_MQ = 0;
-__device__ __forceinline__ void attn_plan(const TickParams& tp, const Dims& dm, TickLds& L) {
+__device__ __forceinline__ bool attn_plan(const TickArgs& a, const TickParams& tp, const Dims& dm, TickLds& L) {
   const int X = uni(L.X), NX = uni(L.NX), n = uni(L.n);
   const int nh = head_lo(X + 1, NX, dm.H) - head_lo(X, NX, dm.H);
   const int nseg = tp.B * nh;  // <= NSEG = NTHR
@@ -1684,6 +1684,17 @@ __device__ __forceinline__ void attn_plan(const TickParams& tp, const Dims& dm, 
   }
   L.pb[g] -= own;
   __syncthreads();
+  // the partial-state slots of this XCD must fit its tp.slot_x; a placement that breaks the host's bound fails the
+  // tick (as a timed-out wait does) instead of writing past the range
+  if (g == 0) {
+    const int used = nseg > 0 ? L.pb[nseg - 1] + (L.np[nseg - 1] > 1 ? L.np[nseg - 1] : 0) : 0;
+    L.ok = used <= tp.slot_x;
+    if (!L.ok) st_dev(a.status, fail_tag(a));
+  }
+  __syncthreads();
+  const bool ok = L.ok;
+  __syncthreads();
+  return ok;
 }
 
 template <int KT, bool MQ>
@@ -2010,7 +2021,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_tick(TickArgs a, TickParams tp, Dim
   const int nl = dm.n_layers;
   trace_mark(a, 0, nl);
   bool ok = xcd_register(a, L);
-  if (ok) attn_plan(tp, dm, L);
+  if (ok) ok = attn_plan(a, tp, dm, L);
   if (ok) phase_embed(a, tp, dm, L);
   trace_mark(a, 1, nl);
   for (int l = 0; l < nl && ok; ++l) {

@@ -26,7 +26,7 @@ STATUS = {0: "FSX_OK", 1: "FSX_E_INVALID", 2: "FSX_E_UNSUPPORTED", 3: "FSX_E_CAP
           5: "FSX_E_HIP"}
 SYMBOLS = ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_status",
            "fsx_expert_trace", "fsx_expert_destroy", "fsx_last_error", "fsx_expert_info", "fsx_version",
-           "fsx_probe_hbm_read")
+           "fsx_probe_hbm_read", "fsx_expert_forward_noalloc")
 
 
 class FsxError(RuntimeError):
@@ -81,6 +81,8 @@ def lib() -> ctypes.CDLL:
         L.fsx_expert_info.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i64), ctypes.POINTER(i64)]
         L.fsx_version.restype = ctypes.c_char_p
         L.fsx_probe_hbm_read.argtypes = [vp, i64, i32, vp, vp]
+        L.fsx_expert_forward_noalloc.argtypes = [vp, ctypes.POINTER(CacheDescC), vp, i32, i32, vp, vp, vp]
+        L.fsx_expert_forward_noalloc.restype = ctypes.c_int
         for n in ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_info",
                   "fsx_expert_status", "fsx_expert_trace", "fsx_probe_hbm_read"):
             getattr(L, n).restype = ctypes.c_int
@@ -192,6 +194,13 @@ def expert_forward(ex: Expert, cache: CacheDesc, tokens, batch: int, n_frame_tok
     """fsx_expert_forward: one tick for `batch` agents (enqueued on `stream`)."""
     _check(lib().fsx_expert_forward(ctypes.c_void_p(ex.handle), ctypes.byref(cache.c), _ptr(tokens), batch,
                                     n_frame_tokens, _ptr(waypoints), _ptr(hidden), _stream(stream)))
+
+
+def expert_forward_noalloc(ex: Expert, cache: CacheDesc, tokens, batch: int, n_frame_tokens: int, waypoints,
+                           hidden=None, stream=None):
+    """fsx_expert_forward_noalloc: the same tick, its workspace in the library's static device array."""
+    _check(lib().fsx_expert_forward_noalloc(ctypes.c_void_p(ex.handle), ctypes.byref(cache.c), _ptr(tokens), batch,
+                                            n_frame_tokens, _ptr(waypoints), _ptr(hidden), _stream(stream)))
 
 
 def expert_status(ex: Expert, stream=None):
