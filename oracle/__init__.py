@@ -11,7 +11,9 @@ Attention", run once per control tick as in Sec. 3.3):
 * ``expert.py``  -- RMSNorm, rotary encoding, the joint attention of Eq. (1)
   over [cached backbone K/V ; the expert's own K/V], the output projection, the
   SwiGLU block, the mean-pool + linear waypoint head, and the paper's
-  two-layer head over the waypoint-query tokens.
+  two-layer head over the waypoint-query tokens; the staleness-augmented training
+  form (Sec. 3.2): every frame's expert block of a clip in one forward, one
+  attention over the whole clip with per-block masks.
 * ``fp8.py``     -- decoding of OCP FP8 E4M3 (e4m3fn) codes (the diagnostic
   reference for the fp8-stored cache) and their encoding against a scale
   (the reference of the quantising append).
@@ -38,5 +40,7 @@ from .expert import (  # noqa: F401
     query_head,
     apply_head,
     expert_forward,
+    staleness_visible_rows,
+    masked_multiblock_forward,
 )
 from .fp8 import e4m3fn_decode, e4m3fn_encode  # noqa: F401

@@ -42,6 +42,9 @@ notes; the GPU path implements the same readings):
   the state token and the four visual tokens first), each query row goes
   through the final RMSNorm, Linear(d -> hidden) with bias, GELU in its exact
   erf form, Linear(hidden -> 2) with bias; query i gives (x_i, y_i).
+* Staleness-augmented training form (Sec. 3.2): frames are numbered from 1;
+  frame j's block sees the prefix up to frame j - delta (text alone when
+  j <= delta); blocks do not see each other (per-block masks).
 * Precision: no intermediate rounding anywhere -- everything is float64.
 """
 
@@ -230,4 +233,58 @@ def expert_forward(
         h = expert_layer(h, lw, kc, vc, positions, shape)
         hidden.append(h)
     wp = apply_head(shape, h, final_norm, head_w)
+    return wp, np.stack(hidden)
+
+
+# ----------------------------------------------------------------------------- staleness-augmented training form
+
+def staleness_visible_rows(n_text: int, rows_per_frame: int, n_frames: int, delta: int) -> np.ndarray:
+    """Backbone prefix rows visible to the expert block of each frame j = 1..n_frames (Sec. 3.2): the prefix ends at
+    frame j - delta, or at the instruction text alone when j < delta (frames are numbered from 1, so j = delta also
+    sees the text alone).  Returns [n_frames] row counts."""
+    j = np.arange(1, n_frames + 1)
+    return n_text + rows_per_frame * np.maximum(0, j - delta)
+
+
+def masked_multiblock_forward(shape: ExpertShape, layers: Sequence[dict], final_norm, head, block_tokens,
+                              prefix_rows: Callable[[int], tuple], visible, positions):
+    """All expert blocks of a training clip in ONE forward (Sec. 3.2): the clip's sequence is [backbone prefix ;
+    block 0 ; block 1 ; ...]; at every layer one attention runs over it with a per-block mask -- a query of block j
+    sees prefix rows < visible[j] and the rows of block j, nothing else (the backbone rows never attend to expert
+    rows, so the prefix is an input).  The MLP acts per token and the head per block.
+
+    block_tokens: [J][S][d]; prefix_rows(l) -> (K, V) [L][H][Dh] (the whole prefix of layer l, rows in order);
+    visible: [J] rows of the prefix block j sees; positions: [J] position of block j's token 0.
+    Returns waypoints [J][n_out] and hidden [n_layers][J][S][d].
+    """
+    blocks = np.asarray(block_tokens, np.float64)
+    J, S, d = blocks.shape
+    H, Dh = shape.n_heads, shape.head_dim
+    h = blocks.reshape(J * S, d)
+    pos = (np.asarray(positions, np.float64)[:, None] + np.arange(S)[None, :]).reshape(J * S)
+    blk = np.repeat(np.arange(J), S)
+    hidden = []
+    for layer, lw in enumerate(layers):
+        kc, vc = (np.asarray(a, np.float64) for a in prefix_rows(layer))
+        L = kc.shape[0]
+        x = rmsnorm(h, lw["attn_norm"], shape.rms_eps)
+        q = apply_rope((x @ np.asarray(lw["wq"], np.float64).T).reshape(J * S, H, Dh), pos, shape.rope_base)
+        k = apply_rope((x @ np.asarray(lw["wk"], np.float64).T).reshape(J * S, H, Dh), pos, shape.rope_base)
+        v = (x @ np.asarray(lw["wv"], np.float64).T).reshape(J * S, H, Dh)
+        keys = np.concatenate([kc, k], axis=0)  # [L + J S][H][Dh]
+        vals = np.concatenate([vc, v], axis=0)
+        # mask [J S][L + J S]: prefix row r visible to block j iff r < visible[j]; expert row visible iff same block
+        allow = np.concatenate([np.arange(L)[None, :] < np.asarray(visible)[blk][:, None],
+                                blk[:, None] == blk[None, :]], axis=1)
+        sc = np.einsum("thc,rhc->htr", q, keys) / np.sqrt(np.float64(Dh))
+        sc = np.where(allow[None], sc, -np.inf)
+        sc = sc - sc.max(axis=-1, keepdims=True)
+        p = np.exp(sc)
+        p = p / p.sum(axis=-1, keepdims=True)
+        a = np.einsum("htr,rhc->thc", p, vals).reshape(J * S, H * Dh)
+        h = h + a @ np.asarray(lw["wo"], np.float64).T
+        x = rmsnorm(h, lw["ffn_norm"], shape.rms_eps)
+        h = h + swiglu_ffn(x, lw["w_gate"], lw["w_up"], lw["w_down"])
+        hidden.append(h.reshape(J, S, d))
+    wp = np.stack([apply_head(shape, h.reshape(J, S, d)[j], final_norm, head) for j in range(J)])
     return wp, np.stack(hidden)

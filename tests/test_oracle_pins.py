@@ -483,6 +483,64 @@ def test_append_only_cache_is_exact():
     np.testing.assert_allclose(inc, mono, rtol=0, atol=1e-12)
 
 
+# ----------------------------------------------------------------------------- staleness-augmented training form
+
+def test_staleness_visible_rows_closed_form():
+    # Sec. 3.2: the prefix visible to frame j's block ends at frame j - delta, or at the text alone when j < delta
+    n_text, per = 64, 4
+    v = ox.staleness_visible_rows(n_text, per, 6, 2)
+    assert list(v) == [64, 64, 68, 72, 76, 80]  # frames 1, 2 (j < delta and j = delta): text only; frame 3 sees frame 1
+    assert list(ox.staleness_visible_rows(n_text, per, 3, 0)) == [68, 72, 76]  # no staleness: up to the frame itself
+    assert list(ox.staleness_visible_rows(10, 4, 2, 5)) == [10, 10]
+
+
+def _multiblock_inputs(seed=23, J=4, S=3, n_text=5, per=2, rope=100.0):
+    r = _rng(seed)
+    layers = []
+    for _ in range(2):
+        lw, sh = _tiny_layer(r)
+        layers.append(lw)
+    sh = ox.ExpertShape(n_layers=2, d_model=sh.d_model, n_heads=sh.n_heads, head_dim=sh.head_dim, d_ffn=sh.d_ffn,
+                        n_expert_tokens=3, rope_base=rope)
+    L = n_text + per * J
+    kc = r.standard_normal((2, L, sh.n_heads, sh.head_dim))
+    vc = r.standard_normal((2, L, sh.n_heads, sh.head_dim))
+    toks = r.standard_normal((J, S, sh.d_model))
+    hw = r.standard_normal((10, sh.d_model))
+    return sh, layers, toks, kc, vc, hw
+
+
+@pytest.mark.parametrize("delta,rope", [(0, 100.0), (2, 100.0), (1, 0.0)])
+def test_multiblock_masked_forward_equals_independent_blocks(delta, rope):
+    # One masked attention over the whole clip equals running each block alone over its truncated prefix -- the
+    # equivalence that lets the blocks run as a batch of agents sharing one cache.
+    sh, layers, toks, kc, vc, hw = _multiblock_inputs(rope=rope)
+    J = toks.shape[0]
+    vis = ox.staleness_visible_rows(5, 2, J, delta)
+    pos = vis + 100
+    fn = 1 + 0.2 * _rng(24).standard_normal(sh.d_model)
+    wp, hid = ox.masked_multiblock_forward(sh, layers, fn, hw, toks, lambda l: (kc[l], vc[l]), vis, pos)
+    for j in range(J):
+        wj, hj = ox.expert_forward(sh, layers, fn, hw, toks[j], lambda l, j=j: (kc[l][:vis[j]], vc[l][:vis[j]]),
+                                   pos=pos[j])
+        np.testing.assert_allclose(wp[j], wj, rtol=0, atol=1e-11)
+        np.testing.assert_allclose(hid[:, j], hj, rtol=0, atol=1e-11)
+
+
+def test_multiblock_masked_forward_matches_brute_force_layer():
+    # one layer of the clip through the scalar-loop layer of each block over its own visible prefix
+    sh, layers, toks, kc, vc, hw = _multiblock_inputs(seed=25, J=3)
+    sh1 = ox.ExpertShape(n_layers=1, d_model=sh.d_model, n_heads=sh.n_heads, head_dim=sh.head_dim, d_ffn=sh.d_ffn,
+                         n_expert_tokens=3, rope_base=sh.rope_base)
+    vis = np.array([5, 7, 9])
+    pos = np.array([9.0, 11.0, 13.0])
+    _, hid = ox.masked_multiblock_forward(sh1, layers[:1], np.ones(sh.d_model), hw, toks,
+                                          lambda l: (kc[l], vc[l]), vis, pos)
+    for j in range(3):
+        want = brute_force_layer(toks[j], layers[0], kc[0][:vis[j]], vc[0][:vis[j]], pos[j], sh1)
+        np.testing.assert_allclose(hid[0, j], want, rtol=0, atol=1e-12)
+
+
 # ----------------------------------------------------------------------------- fp8
 
 def test_e4m3_decode_exhaustive_against_library():
@@ -565,6 +623,8 @@ MUTANTS = {
     "query_head_bias_dropped": ("query_head", "nobias"),
     "query_head_first_rows": ("query_head", "firstrows"),
     "e4m3_encode_truncates": ("e4m3fn_encode", "trunc"),
+    "staleness_off_by_one": ("staleness_visible_rows", "vis_off1"),
+    "multiblock_blocks_see_each_other": ("masked_multiblock_forward", "blockleak"),
     "e4m3_encode_ties_toward_zero": ("e4m3fn_encode", "tieslow"),
 }
 
@@ -608,6 +668,27 @@ def _mutant(kind):
     elif kind == "firstrows":
         def f(h, g, w1, b1, w2, b2, T, nq, eps):
             return ORIG["query_head"](h, g, w1, b1, w2, b2, nq, nq, eps)
+    elif kind == "vis_off1":
+        def f(n_text, per, n_frames, delta):
+            j = np.arange(1, n_frames + 1)
+            return n_text + per * np.maximum(0, j - delta + 1)
+    elif kind == "blockleak":
+        def f(shape, layers, final_norm, head, block_tokens, prefix_rows, visible, positions):
+            # every block also attends to the other blocks' rows: one block holding all the clip's expert tokens
+            # would be the unmasked form; emulate with the first block seeing the second block's tokens
+            bt = np.asarray(block_tokens, np.float64)
+            wp, hid = ORIG["masked_multiblock_forward"](shape, layers, final_norm, head, bt, prefix_rows, visible,
+                                                        positions)
+            if bt.shape[0] > 1:
+                both = np.concatenate([bt[0], bt[1]], axis=0)[None]
+                sh2 = ox.ExpertShape(**{**shape.__dict__})
+                w2, h2 = ORIG["masked_multiblock_forward"](sh2, layers, final_norm, head, both, prefix_rows,
+                                                           np.asarray(visible)[:1], np.asarray(positions)[:1])
+                hid = hid.copy()
+                hid[:, 0] = h2[:, 0, :bt.shape[1]]
+                wp = wp.copy()
+                wp[0] = w2[0]
+            return wp, hid
     elif kind == "trunc":
         def f(x, scale):
             y = np.clip(np.asarray(x, np.float32) / np.float32(scale), -448, 448).astype(np.float64)
@@ -627,6 +708,8 @@ def _mutant(kind):
 ORIG = {n: getattr(ox, n) for n in ("joint_attention", "apply_rope", "swiglu_ffn", "rmsnorm", "waypoint_head",
                                     "query_head", "gelu")}
 ORIG["e4m3fn_encode"] = oracle.fp8.e4m3fn_encode
+ORIG["staleness_visible_rows"] = ox.staleness_visible_rows
+ORIG["masked_multiblock_forward"] = ox.masked_multiblock_forward
 PIN_TESTS = [
     lambda: test_attention_matches_brute_force_masked_softmax(5, 3, 2, 4),
     lambda: test_cache_attention_equals_library_attention_over_concatenation(),
@@ -638,6 +721,8 @@ PIN_TESTS = [
     lambda: test_query_head_matches_loop(),
     lambda: test_query_head_matches_library_and_reads_only_the_query_rows(),
     lambda: test_e4m3_encode_against_library(),
+    lambda: test_staleness_visible_rows_closed_form(),
+    lambda: test_multiblock_masked_forward_equals_independent_blocks(2, 100.0),
 ]
 
 
