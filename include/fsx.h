@@ -58,10 +58,13 @@ typedef enum {
 
 enum { FSX_APPEND_RING = 0, FSX_APPEND_ERROR = 1 };
 
-/* Layouts of the cache tensors (fsx_cache_desc.layout). */
+/* Layouts of the cache tensors (fsx_cache_desc.layout): HEAD_MAJOR or TOKEN_MAJOR, optionally | SHARED. */
 enum {
-  FSX_CACHE_HEAD_MAJOR = 0, /* [batch][n_layers][H][capacity][Dh]: one contiguous ring per (agent, layer, head) */
-  FSX_CACHE_TOKEN_MAJOR = 1 /* [batch][n_layers][capacity][H][Dh]: one ring slot holds a cached token for every head */
+  FSX_CACHE_HEAD_MAJOR = 0,  /* [batch][n_layers][H][capacity][Dh]: one contiguous ring per (agent, layer, head) */
+  FSX_CACHE_TOKEN_MAJOR = 1, /* [batch][n_layers][capacity][H][Dh]: one ring slot holds a cached token for every head */
+  FSX_CACHE_SHARED = 2       /* flag: k, v (and fp8 scales) hold ONE agent's rings, which every agent of the batch
+                                reads through its own start / len / pos -- the expert blocks of one training clip,
+                                each seeing a different (stale) prefix of the same cache (Sec. 3.2) */
 };
 
 /* Flags of fsx_expert_cfg.flags. */
@@ -90,7 +93,25 @@ typedef struct {
   float rms_eps;            /* RMSNorm epsilon */
   int32_t flags;            /* FSX_FLAG_* */
   int32_t tick_timeout_us;  /* bound on any wait inside the tick kernel; 0 = 2 s */
+  int32_t head_kind;        /* FSX_HEAD_MEAN_LINEAR or FSX_HEAD_QUERY_MLP */
+  int32_t head_hidden;      /* FSX_HEAD_QUERY_MLP: width of the head's hidden layer, 1..2048; ignored otherwise */
 } fsx_expert_cfg;
+
+/* Waypoint heads (fsx_expert_cfg.head_kind). */
+enum {
+  FSX_HEAD_MEAN_LINEAR = 0, /* final RMSNorm, mean over the T expert tokens, Linear(d -> n_out) without bias */
+  FSX_HEAD_QUERY_MLP = 1    /* the paper's head (Sec. 3.1): the last n_out / 2 expert tokens are waypoint queries,
+                               each decoded to one (x, y) by final RMSNorm, Linear(d -> head_hidden) + bias, GELU
+                               (erf form), Linear(head_hidden -> 2) + bias; n_out even, n_out / 2 <= min(T, 8) */
+};
+
+/* The head's parameters, DEVICE pointers; matrices in cfg.dtype, biases fp32. */
+typedef struct {
+  const void* w;    /* MEAN_LINEAR: [n_out][d]; QUERY_MLP: first layer [head_hidden][d] */
+  const float* b;   /* QUERY_MLP: [head_hidden]; NULL for MEAN_LINEAR */
+  const void* w2;   /* QUERY_MLP: second layer [2][head_hidden]; NULL for MEAN_LINEAR */
+  const float* b2;  /* QUERY_MLP: [2]; NULL for MEAN_LINEAR */
+} fsx_head_weights;
 
 /* One layer's parameters, DEVICE pointers, elements of cfg.dtype (norm gains always fp32). */
 typedef struct {
@@ -119,13 +140,15 @@ typedef struct {
   int32_t n_layers;        /* must equal the expert's */
   int32_t n_heads;         /* must equal the expert's */
   int32_t head_dim;        /* must equal the expert's */
-  int32_t layout;          /* FSX_CACHE_HEAD_MAJOR (0) or FSX_CACHE_TOKEN_MAJOR (1); FSX_E_INVALID otherwise */
+  int32_t layout;          /* FSX_CACHE_HEAD_MAJOR (0) or FSX_CACHE_TOKEN_MAJOR (1), optionally | FSX_CACHE_SHARED;
+                              FSX_E_INVALID otherwise */
   int64_t capacity;        /* ring slots per (agent, layer) */
   void* k;                 /* DEVICE [batch][n_layers][H][capacity][Dh] (head-major) or
-                              [batch][n_layers][capacity][H][Dh] (token-major) */
+                              [batch][n_layers][capacity][H][Dh] (token-major); batch = 1 in memory when shared */
   void* v;                 /* DEVICE, same layout */
-  const float* k_scale;    /* FP8 only: DEVICE [batch][n_layers][H], stored value = code * scale */
-  const float* v_scale;    /* FP8 only: DEVICE [batch][n_layers][H] */
+  const float* k_scale;    /* FP8 only: DEVICE [batch][n_layers][H] ([1][n_layers][H] when shared), stored value =
+                              code * scale */
+  const float* v_scale;    /* FP8 only: DEVICE, as k_scale */
   int64_t* start;          /* HOST [batch]: ring slot of the oldest valid row */
   int64_t* len;            /* HOST [batch]: valid rows, 0..capacity */
   int64_t* pos;            /* HOST [batch]: position of the agent's expert token 0 (rotary angle) */
@@ -137,14 +160,14 @@ typedef struct fsx_expert fsx_expert;
  *   cfg        sizes and dtype (validated; FSX_E_INVALID / FSX_E_UNSUPPORTED on bad values)
  *   layers     HOST array of cfg.n_layers descriptors (DEVICE weight pointers)
  *   final_norm DEVICE [d] fp32 gain of the RMSNorm before the head
- *   head_w     DEVICE [n_out][d] (cfg.dtype) waypoint head weight, no bias
+ *   head       HOST struct of DEVICE pointers to the head's parameters (cfg.head_kind)
  *   stream     used for the packing copies; the call synchronises it before returning,
  *              so the caller may free its weight buffers afterwards
  *   out        receives the handle (NULL on failure)
  * Allocates the packed weights and a workspace sized for cfg.max_batch agents of
  * T + max_frame_tokens tokens. */
 int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weights* layers, const float* final_norm,
-                      const void* head_w, void* stream, fsx_expert** out);
+                      const fsx_head_weights* head, void* stream, fsx_expert** out);
 
 /* One control tick for `batch` agents (Sec. 3.1, Eq. (1); Sec. 3.3: the expert reads the cache as-is).
  *   cache          descriptor; only rows (start+i) mod capacity, i < len[b], are read.  The
@@ -180,7 +203,8 @@ int fsx_expert_forward_noalloc(fsx_expert* ex, const fsx_cache_desc* cache, cons
  *   k_rows, v_rows DEVICE, in the cache's layout with n_rows slots: [cache->batch][n_layers][H][n_rows][Dh]
  *                  for a head-major cache, [cache->batch][n_layers][n_rows][H][Dh] for a token-major one;
  *                  elements of cache->dtype (fp8: codes already scaled by the cache's k_scale / v_scale);
- *                  Dh elements must be a multiple of 16 bytes (FSX_E_UNSUPPORTED otherwise)
+ *                  Dh elements must be a multiple of 16 bytes (FSX_E_UNSUPPORTED otherwise); a shared cache
+ *                  (FSX_CACHE_SHARED) is refused with FSX_E_UNSUPPORTED
  *   policy         FSX_APPEND_RING: when a ring is full the oldest rows are overwritten (start
  *                  advances); FSX_APPEND_ERROR: FSX_E_CAPACITY if any agent would exceed
  *                  capacity, and nothing is written.

@@ -42,7 +42,9 @@ struct fsx_expert {
   int A = 0, S_max = 0, M_max = 0, items_max = 0;
   void* wbuf = nullptr;    // packed (fused) or copied (per-op) weight matrices
   float* fbuf = nullptr;   // norm gains: [n_layers][2][d] then final [d]
-  void* head_w = nullptr;  // [n_out][d] cfg.dtype
+  void* head_w = nullptr;  // [n_out][d] (mean-pool head) or W1 [hidden][d], then W2 [2][hidden] (query head), cfg.dtype
+  float* head_b = nullptr; // query head: b1 [hidden], then b2 [2]
+  QueryHead qhead{};
   void* wsbuf = nullptr;   // workspace
   int64_t weight_bytes = 0, ws_bytes = 0;
   std::vector<FastWeights> fw;
@@ -66,6 +68,7 @@ static void free_expert(fsx_expert* ex) {
   if (ex->wbuf) (void)hipFree(ex->wbuf);
   if (ex->fbuf) (void)hipFree(ex->fbuf);
   if (ex->head_w) (void)hipFree(ex->head_w);
+  if (ex->head_b) (void)hipFree(ex->head_b);
   if (ex->wsbuf) (void)hipFree(ex->wsbuf);
   if (ex->trace) (void)hipFree(ex->trace);
   if (ex->done) (void)hipEventDestroy(ex->done);
@@ -84,16 +87,27 @@ static int validate_cfg(const fsx_expert_cfg* c) {
   if (!(c->rms_eps >= 0.f) || !(c->rope_base >= 0.f)) return fail(FSX_E_INVALID, "rms_eps and rope_base must be >= 0");
   if ((int64_t)c->n_heads * c->head_dim > (1 << 20) || c->d_model > (1 << 16) || c->d_ffn > (1 << 18))
     return fail(FSX_E_UNSUPPORTED, "sizes beyond the supported range");
+  if (c->head_kind != FSX_HEAD_MEAN_LINEAR && c->head_kind != FSX_HEAD_QUERY_MLP)
+    return fail(FSX_E_INVALID, "head_kind must be FSX_HEAD_MEAN_LINEAR or FSX_HEAD_QUERY_MLP");
+  if (c->head_kind == FSX_HEAD_QUERY_MLP) {
+    if (c->n_out % 2 || c->n_out / 2 > c->n_expert_tokens || c->n_out / 2 > QH_MAX_QUERIES)
+      return fail(FSX_E_INVALID, "the query head needs an even n_out with n_out / 2 <= min(n_expert_tokens, 8)");
+    if (c->head_hidden < 1 || c->head_hidden > 2048) return fail(FSX_E_INVALID, "head_hidden must be in 1..2048");
+    if ((int64_t)(c->n_out / 2) * (c->d_model + c->head_hidden) * 4 > 64 * 1024)
+      return fail(FSX_E_UNSUPPORTED, "query head rows and hidden activations beyond 64 KiB of LDS");
+  }
   return FSX_OK;
 }
 
 extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weights* layers, const float* final_norm,
-                                 const void* head_w, void* stream, fsx_expert** out) {
+                                 const fsx_head_weights* head, void* stream, fsx_expert** out) {
   if (!out) return fail(FSX_E_INVALID, "out is NULL");
   *out = nullptr;
   int rc = validate_cfg(cfg);
   if (rc) return rc;
-  if (!layers || !final_norm || !head_w) return fail(FSX_E_INVALID, "layers, final_norm and head_w must be non-NULL");
+  if (!layers || !final_norm || !head || !head->w) return fail(FSX_E_INVALID, "layers, final_norm and head->w must be non-NULL");
+  if (cfg->head_kind == FSX_HEAD_QUERY_MLP && (!head->b || !head->w2 || !head->b2))
+    return fail(FSX_E_INVALID, "the query head needs w, b, w2 and b2");
   const fsx_expert_cfg& c = *cfg;
   for (int l = 0; l < c.n_layers; ++l) {
     const fsx_layer_weights& w = layers[l];
@@ -116,7 +130,9 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   ex->path = (fused_ok && !(c.flags & FSX_FLAG_GENERIC)) ? 0 : 1;
   const int es = esize(c.dtype);
   const int64_t per_layer = (int64_t)4 * A * d + (int64_t)3 * F * d;  // elements
-  ex->weight_bytes = (per_layer * c.n_layers + (int64_t)c.n_out * d) * es;
+  const bool qh = c.head_kind == FSX_HEAD_QUERY_MLP;
+  const int64_t head_elems = qh ? (int64_t)c.head_hidden * d + 2 * (int64_t)c.head_hidden : (int64_t)c.n_out * d;
+  ex->weight_bytes = (per_layer * c.n_layers + head_elems) * es;
 
   int last = FSX_OK;
   auto cleanup = [&](int code) {
@@ -135,7 +151,9 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   if (!ok(hipMalloc(&ex->wbuf, (size_t)(per_layer * c.n_layers * es)), "hipMalloc(weights)")) return cleanup(FSX_E_OOM);
   if (!ok(hipMalloc((void**)&ex->fbuf, sizeof(float) * ((size_t)2 * c.n_layers * d + d)), "hipMalloc(norms)"))
     return cleanup(FSX_E_OOM);
-  if (!ok(hipMalloc(&ex->head_w, (size_t)c.n_out * d * es), "hipMalloc(head)")) return cleanup(FSX_E_OOM);
+  if (!ok(hipMalloc(&ex->head_w, (size_t)head_elems * es), "hipMalloc(head)")) return cleanup(FSX_E_OOM);
+  if (qh && !ok(hipMalloc((void**)&ex->head_b, sizeof(float) * ((size_t)c.head_hidden + 2)), "hipMalloc(head bias)"))
+    return cleanup(FSX_E_OOM);
 
   // norm gains and head
   for (int l = 0; l < c.n_layers; ++l) {
@@ -148,8 +166,23 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   ex->final_norm = ex->fbuf + (size_t)2 * c.n_layers * d;
   if (!ok(hipMemcpyAsync((void*)ex->final_norm, final_norm, sizeof(float) * d, hipMemcpyDeviceToDevice, s),
           "copy final_norm") ||
-      !ok(hipMemcpyAsync(ex->head_w, head_w, (size_t)c.n_out * d * es, hipMemcpyDeviceToDevice, s), "copy head"))
+      !ok(hipMemcpyAsync(ex->head_w, head->w, (size_t)(qh ? (int64_t)c.head_hidden * d : (int64_t)c.n_out * d) * es,
+                         hipMemcpyDeviceToDevice, s), "copy head"))
     return cleanup(FSX_E_HIP);
+  if (qh) {
+    char* w2 = (char*)ex->head_w + (size_t)c.head_hidden * d * es;
+    if (!ok(hipMemcpyAsync(w2, head->w2, (size_t)2 * c.head_hidden * es, hipMemcpyDeviceToDevice, s), "copy head w2") ||
+        !ok(hipMemcpyAsync(ex->head_b, head->b, sizeof(float) * c.head_hidden, hipMemcpyDeviceToDevice, s), "copy head b") ||
+        !ok(hipMemcpyAsync(ex->head_b + c.head_hidden, head->b2, sizeof(float) * 2, hipMemcpyDeviceToDevice, s),
+            "copy head b2"))
+      return cleanup(FSX_E_HIP);
+    ex->qhead.w1 = ex->head_w;
+    ex->qhead.b1 = ex->head_b;
+    ex->qhead.w2 = w2;
+    ex->qhead.b2 = ex->head_b + c.head_hidden;
+    ex->qhead.hidden = c.head_hidden;
+  }
+  ex->qhead.wdtype = c.dtype;
 
   char* wp = (char*)ex->wbuf;
   if (ex->path == 0) {
@@ -317,6 +350,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
     t.final_norm = ex->final_norm;
     t.head_w = ex->head_w;
     t.head_dtype = c.dtype;
+    t.qhead = ex->qhead;
     t.q = ex->ws.q;
     t.kself = ex->ws.kself;
     t.vself = ex->ws.vself;
@@ -346,8 +380,9 @@ static int validate_cache(const fsx_expert* ex, const fsx_cache_desc* c, int bat
     return fail(FSX_E_INVALID, "cache dtype must be F32, BF16 or FP8_E4M3");
   if (ex && (c->n_layers != ex->cfg.n_layers || c->n_heads != ex->cfg.n_heads || c->head_dim != ex->cfg.head_dim))
     return fail(FSX_E_INVALID, "cache geometry (n_layers, n_heads, head_dim) differs from the expert's");
-  if (c->layout != FSX_CACHE_HEAD_MAJOR && c->layout != FSX_CACHE_TOKEN_MAJOR)
-    return fail(FSX_E_INVALID, "cache layout must be FSX_CACHE_HEAD_MAJOR or FSX_CACHE_TOKEN_MAJOR");
+  if (c->layout & ~(FSX_CACHE_TOKEN_MAJOR | FSX_CACHE_SHARED))
+    return fail(FSX_E_INVALID, "cache layout must be FSX_CACHE_HEAD_MAJOR or FSX_CACHE_TOKEN_MAJOR, optionally with "
+                               "FSX_CACHE_SHARED");
   if (c->batch <= 0 || c->batch > FSX_MAX_BATCH) return fail(FSX_E_INVALID, "cache batch must be in 1..64");
   if (batch > c->batch) return fail(FSX_E_INVALID, "batch exceeds the cache descriptor's batch");
   if (c->capacity < 0 || c->capacity > (int64_t)INT32_MAX) return fail(FSX_E_INVALID, "capacity out of range");
@@ -469,12 +504,15 @@ static int forward_impl(fsx_expert* ex, const fsx_cache_desc* cache, const void*
   }
   Dims dm{};
   dm.d = c.d_model; dm.H = c.n_heads; dm.Dh = c.head_dim; dm.A = ex->A; dm.F = c.d_ffn; dm.n_layers = c.n_layers;
-  dm.n_out = c.n_out; dm.eps = c.rms_eps; dm.rope_base = c.rope_base;
+  dm.n_out = c.n_out; dm.eps = c.rms_eps; dm.rope_base = c.rope_base; dm.head_kind = c.head_kind;
   CacheView cv{};
   cv.k = cache->k; cv.v = cache->v; cv.k_scale = cache->k_scale; cv.v_scale = cache->v_scale;
   cv.cap = cache->capacity; cv.n_layers = cache->n_layers; cv.layer = 0; cv.dtype = cache->dtype;
   cv.H = cache->n_heads; cv.Dh = cache->head_dim;
-  if (cache->layout == FSX_CACHE_TOKEN_MAJOR) {
+  const bool shared = (cache->layout & FSX_CACHE_SHARED) != 0;
+  cv.bs = shared ? 0 : (int64_t)cache->n_layers * cache->n_heads * cache->capacity * cache->head_dim;
+  cv.sbs = shared ? 0 : cache->n_layers * cache->n_heads;
+  if (cache->layout & FSX_CACHE_TOKEN_MAJOR) {
     cv.hs = cache->head_dim;
     cv.rs = (int64_t)cache->n_heads * cache->head_dim;
   } else {
@@ -486,8 +524,8 @@ static int forward_impl(fsx_expert* ex, const fsx_cache_desc* cache, const void*
     return fail(FSX_E_UNSUPPORTED, "the allocation-free entry point runs the persistent tick kernel only (bf16 expert "
                                    "whose heads and FFN columns fit the per-XCD split, no FSX_FLAG_MULTI_LAUNCH)");
   if (ex->path == 1) {
-    HIP_TRY(generic_tick(ex->gw.data(), ex->final_norm, ex->head_w, c.dtype, tokens, cv, tp, dm, ex->gws, waypoints,
-                         hidden, s));
+    HIP_TRY(generic_tick(ex->gw.data(), ex->final_norm, ex->head_w, ex->qhead, c.dtype, tokens, cv, tp, dm, ex->gws,
+                         waypoints, hidden, s));
     HIP_TRY(hipEventRecord(ex->done, s));
     g_err.clear();
     return FSX_OK;
@@ -582,7 +620,10 @@ static int forward_impl(fsx_expert* ex, const fsx_cache_desc* cache, const void*
     const float* gnext = l + 1 < c.n_layers ? ex->fw[l + 1].attn_norm : ex->final_norm;
     HIP_TRY(launch_reduce_norm(tp, dm, ex->ws, ks_d, gnext, hidden ? hidden + (int64_t)l * tp.M * dm.d : nullptr, s));
   }
-  HIP_TRY(launch_head(tp, dm, ex->ws, ex->final_norm, ex->head_w, c.dtype, waypoints, s));
+  if (c.head_kind == FSX_HEAD_QUERY_MLP)
+    HIP_TRY(launch_query_head(ex->ws.h, tp, dm, ex->final_norm, ex->qhead, waypoints, s));
+  else
+    HIP_TRY(launch_head(tp, dm, ex->ws, ex->final_norm, ex->head_w, c.dtype, waypoints, s));
   HIP_TRY(hipEventRecord(ex->done, s));
   g_err.clear();
   return FSX_OK;
@@ -611,6 +652,9 @@ extern "C" int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, 
   }
   if (!k_rows || !v_rows || !cache->k || !cache->v) return fail(FSX_E_INVALID, "row and cache pointers must be non-NULL");
   if (n_rows > cache->capacity) return fail(FSX_E_CAPACITY, "n_rows exceeds the ring capacity");
+  if (cache->layout & FSX_CACHE_SHARED)
+    return fail(FSX_E_UNSUPPORTED, "a shared cache is a set of views of one agent's rings; append through a "
+                                   "descriptor of that agent alone");
   if (cache->n_layers <= 0 || cache->n_heads <= 0 || cache->head_dim <= 0)
     return fail(FSX_E_INVALID, "cache geometry must be positive");
   const int64_t head_row_bytes = (int64_t)cache->head_dim * esize(cache->dtype);

@@ -340,7 +340,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a, TickParams tp) {
     const int64_t off = cache_head_base(a.cv, b, a.cv.layer, h) * ES;
     float ks = 1.f, vs = 1.f;
     if (KT == 1) {
-      const int64_t si = ((int64_t)b * a.cv.n_layers + a.cv.layer) * a.H + h;
+      const int64_t si = cache_scale_index(a.cv, b, a.cv.layer, h);
       ks = a.cv.k_scale[si];
       vs = a.cv.v_scale[si];
     }
@@ -474,6 +474,23 @@ __global__ __launch_bounds__(256) void k_head(const float* __restrict__ h, int S
   }
 }
 
+__global__ __launch_bounds__(256) void k_query_head(const float* __restrict__ h, int S, int T, int d, float eps,
+                                                    const float* __restrict__ gfin, QueryHead qh, int nq,
+                                                    float* __restrict__ wp) {
+  extern __shared__ float qlds[];
+  const int b = blockIdx.x;
+  query_head_wg([&](int t, int c) { return h[((int64_t)b * S + t) * d + c]; }, T, nq, d, eps, gfin, qh,
+                [&](int o, float v) { wp[(int64_t)b * 2 * nq + o] = v; }, qlds);
+}
+
+hipError_t launch_query_head(const float* h, const TickParams& tp, const Dims& dm, const float* final_norm,
+                             const QueryHead& qh, float* waypoints, hipStream_t s) {
+  const int nq = dm.n_out / 2;
+  hipLaunchKernelGGL(k_query_head, dim3(tp.B), dim3(256), (size_t)nq * (dm.d + qh.hidden) * sizeof(float), s, h,
+                     tp.S, tp.T, dm.d, dm.eps, final_norm, qh, nq, waypoints);
+  return hipGetLastError();
+}
+
 hipError_t launch_head(const TickParams& tp, const Dims& dm, const Workspace& ws, const float* final_norm,
                        const void* head_w, int head_dtype, float* waypoints, hipStream_t s) {
   hipLaunchKernelGGL(k_head, dim3(tp.B), dim3(256), dm.d * sizeof(float), s, (const float*)ws.h, tp.S, tp.T, dm.d,
@@ -533,7 +550,7 @@ hipError_t launch_append(const fsx_cache_desc& c, const void* k_rows, const void
   a.ks = (const uint4*)k_rows; a.vs = (const uint4*)v_rows; a.kc = (uint4*)c.k; a.vc = (uint4*)c.v;
   a.cap = c.capacity; a.row_chunks = (int64_t)c.head_dim * es / 16;
   a.n_layers = c.n_layers; a.n_heads = c.n_heads; a.n_rows = n_rows; a.B = c.batch;
-  a.token_major = c.layout == FSX_CACHE_TOKEN_MAJOR;
+  a.token_major = (c.layout & FSX_CACHE_TOKEN_MAJOR) != 0;
   for (int b = 0; b < c.batch; ++b) a.first[b] = first[b];
   const int64_t total = (int64_t)a.B * a.n_layers * a.n_heads * a.n_rows * a.row_chunks;
   if (total == 0) return hipSuccess;

@@ -85,8 +85,8 @@ __global__ void g_attention(CacheView cv, TickParams tp, const float* q, const f
   const int64_t hb = cache_head_base(cv, b, cv.layer, h);  // ring slot 0 of (agent, layer, head)
   float ks = 1.f, vs = 1.f;
   if (cv.dtype == FSX_FP8_E4M3) {
-    ks = cv.k_scale[((int64_t)b * cv.n_layers + cv.layer) * H + h];
-    vs = cv.v_scale[((int64_t)b * cv.n_layers + cv.layer) * H + h];
+    ks = cv.k_scale[cache_scale_index(cv, b, cv.layer, h)];
+    vs = cv.v_scale[cache_scale_index(cv, b, cv.layer, h)];
   }
   auto cache_off = [&](int r) {
     int64_t slot = tp.start[b] + r;
@@ -168,7 +168,8 @@ __global__ void g_head(const float* h, int S, int T, int d, float eps, const flo
 
 static inline unsigned nblk(int64_t n, int bs) { return (unsigned)((n + bs - 1) / bs); }
 
-hipError_t generic_tick(const GenericWeights* L, const float* final_norm, const void* head_w, int wdt,
+hipError_t generic_tick(const GenericWeights* L, const float* final_norm, const void* head_w, const QueryHead& qhead,
+                        int wdt,
                         const void* tokens, const CacheView& cv0, const TickParams& tp, const Dims& dm,
                         const GenericWorkspace& ws, float* waypoints, float* hidden, hipStream_t s) {
   const int M = tp.M, d = dm.d, A = dm.A, F = dm.F;
@@ -201,6 +202,11 @@ hipError_t generic_tick(const GenericWeights* L, const float* final_norm, const 
     if (hidden)
       hipLaunchKernelGGL(g_copy, dim3(nblk((int64_t)M * d, 256)), dim3(256), 0, s, (const float*)ws.h,
                          hidden + (int64_t)l * M * d, (int64_t)M * d);
+  }
+  if (dm.head_kind == 1) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_query_head((const float*)ws.h, tp, dm, final_norm, qhead, waypoints, s);
   }
   hipLaunchKernelGGL(g_head, dim3(tp.B), dim3(256), d * sizeof(float), s, (const float*)ws.h, tp.S, tp.T, d, dm.eps,
                      final_norm, head_w, wdt, dm.n_out, waypoints);

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "../../include/fsx.h"
+#include "head_device.h"
 
 namespace fsx {
 
@@ -30,16 +31,19 @@ struct TickParams {
 };
 
 // Cache view of one layer.  Element offset of (agent b, layer l, head h, ring slot j, channel c):
-// ((b * n_layers + l) * H * cap) * Dh + h * hs + j * rs + c, with (hs, rs) = (cap * Dh, Dh) for a head-major
-// cache and (Dh, H * Dh) for a token-major one.
+// b * bs + l * H * cap * Dh + h * hs + j * rs + c, with (hs, rs) = (cap * Dh, Dh) for a head-major cache and
+// (Dh, H * Dh) for a token-major one; bs = n_layers * H * cap * Dh, or 0 when every agent reads the same rings
+// (a shared cache).  fp8 scale of (b, l, h): [b * sbs + l * H + h], sbs = n_layers * H or 0.
 struct CacheView {
   const void* k;     // base of the whole cache tensor
   const void* v;
-  const float* k_scale;  // fp8 only: [batch][n_layers][H]
+  const float* k_scale;  // fp8 only: [batch][n_layers][H] ([1][n_layers][H] when shared)
   const float* v_scale;
   int64_t cap;           // ring rows
   int64_t hs;            // elements between the rows of two heads of one slot
   int64_t rs;            // elements between two ring slots of one head
+  int64_t bs;            // elements between the rings of two agents (0: shared)
+  int32_t sbs;           // scales between two agents (0: shared)
   int32_t n_layers;
   int32_t layer;
   int32_t dtype;         // fsx_dtype
@@ -47,7 +51,10 @@ struct CacheView {
 };
 // Element offset of row slot 0 of (agent b, layer l, head h).
 __host__ __device__ inline int64_t cache_head_base(const CacheView& cv, int b, int l, int h) {
-  return ((int64_t)b * cv.n_layers + l) * cv.H * cv.cap * cv.Dh + (int64_t)h * cv.hs;
+  return (int64_t)b * cv.bs + (int64_t)l * cv.H * cv.cap * cv.Dh + (int64_t)h * cv.hs;
+}
+__host__ __device__ inline int64_t cache_scale_index(const CacheView& cv, int b, int l, int h) {
+  return (int64_t)b * cv.sbs + (int64_t)l * cv.H + h;
 }
 
 // ------------------------------------------------------------------ packing (create time)
@@ -82,6 +89,7 @@ struct Workspace {
 struct Dims {
   int d, H, Dh, A, F, n_layers, n_out;
   float eps, rope_base;
+  int head_kind;  // 0: mean over the expert tokens + linear; 1: two-layer head over the waypoint queries
 };
 
 hipError_t launch_embed(const void* tokens, int tok_dtype, const float* g0, const TickParams& tp, const Dims& dm,
@@ -101,6 +109,9 @@ hipError_t launch_reduce_norm(const TickParams& tp, const Dims& dm, const Worksp
                               const float* gain, float* hidden_layer, hipStream_t s);
 hipError_t launch_head(const TickParams& tp, const Dims& dm, const Workspace& ws, const float* final_norm,
                        const void* head_w, int head_dtype, float* waypoints, hipStream_t s);
+// The two-layer query head of every agent from a row-major residual h [M][d] (both per-op paths).
+hipError_t launch_query_head(const float* h, const TickParams& tp, const Dims& dm, const float* final_norm,
+                             const QueryHead& qh, float* waypoints, hipStream_t s);
 
 // ------------------------------------------------------------------ persistent tick kernel
 // The tick kernel splits every layer over the chip's XCDs the way a tensor-parallel layer is split over
@@ -117,6 +128,7 @@ struct TickArgs {
   const float* final_norm;
   const void* head_w;
   int head_dtype;
+  QueryHead qhead;     // head kind 1
   int tok_dtype;
   const void* tokens;
   CacheView cv;
@@ -189,7 +201,8 @@ struct GenericWeights {
 struct GenericWorkspace {
   float* h; float* x; float* q; float* k; float* v; float* attn; float* g; float* u; float* rope;
 };
-hipError_t generic_tick(const GenericWeights* layers, const float* final_norm, const void* head_w, int wdtype,
+hipError_t generic_tick(const GenericWeights* layers, const float* final_norm, const void* head_w,
+                        const QueryHead& qhead, int wdtype,
                         const void* tokens, const CacheView& cv0, const TickParams& tp, const Dims& dm,
                         const GenericWorkspace& ws, float* waypoints, float* hidden, hipStream_t s);
 

@@ -1739,7 +1739,7 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
     U.vs = (const char*)a.vself + ((int64_t)b * tp.S * A + (int64_t)h * DH) * 2;
     U.ksc = U.vsc = 1.f;
     if (KT == 1) {
-      const int64_t si = ((int64_t)b * a.cv.n_layers + l) * H + h;
+      const int64_t si = cache_scale_index(a.cv, b, l, h);
       U.ksc = a.cv.k_scale[si];
       U.vsc = a.cv.v_scale[si];
     }
@@ -1952,6 +1952,13 @@ __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& 
       return;
     }
     const float* h = a.hres;  // replica of XCD rank 0, tile-major [d/16][Mp][16]
+    if (dm.head_kind == 1) {
+      query_head_wg([&](int t, int col) { return ld_dev_f(h + ((int64_t)(col >> 4) * tp.Mp + b * tp.S + t) * 16 + (col & 15)); },
+                    T, dm.n_out / 2, d, dm.eps, a.final_norm, a.qhead,
+                    [&](int o, float v) { st_dev_f(a.waypoints + (int64_t)b * dm.n_out + o, v); },
+                    reinterpret_cast<float*>(&L.u));
+      continue;
+    }
     const int n0 = tid, n1 = tid + NTHR;
     auto hv = [&](int m, int col) { return ld_dev_f(h + ((int64_t)(col >> 4) * tp.Mp + m) * 16 + (col & 15)); };
     float xm0 = 0.f, xm1 = 0.f;

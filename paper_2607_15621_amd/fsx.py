@@ -19,8 +19,9 @@ LIB_PATH = os.path.join(HERE, "libfsx.so")
 
 F32, BF16, FP8_E4M3 = 0, 1, 2
 APPEND_RING, APPEND_ERROR = 0, 1
-CACHE_HEAD_MAJOR, CACHE_TOKEN_MAJOR = 0, 1
+CACHE_HEAD_MAJOR, CACHE_TOKEN_MAJOR, CACHE_SHARED = 0, 1, 2
 FLAG_GENERIC, FLAG_MULTI_LAUNCH, FLAG_TRACE = 1, 2, 4
+HEAD_MEAN_LINEAR, HEAD_QUERY_MLP = 0, 1
 MAX_BATCH = 64
 STATUS = {0: "FSX_OK", 1: "FSX_E_INVALID", 2: "FSX_E_UNSUPPORTED", 3: "FSX_E_CAPACITY", 4: "FSX_E_OOM",
           5: "FSX_E_HIP"}
@@ -40,7 +41,12 @@ class ExpertCfg(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("n_expert_tokens", ctypes.c_int32),
                 ("n_out", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("max_frame_tokens", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float),
-                ("flags", ctypes.c_int32), ("tick_timeout_us", ctypes.c_int32)]
+                ("flags", ctypes.c_int32), ("tick_timeout_us", ctypes.c_int32), ("head_kind", ctypes.c_int32),
+                ("head_hidden", ctypes.c_int32)]
+
+
+class HeadWeights(ctypes.Structure):
+    _fields_ = [("w", ctypes.c_void_p), ("b", ctypes.c_void_p), ("w2", ctypes.c_void_p), ("b2", ctypes.c_void_p)]
 
 
 class LayerWeights(ctypes.Structure):
@@ -68,8 +74,8 @@ def lib() -> ctypes.CDLL:
             raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_15621_amd.build`")
         L = ctypes.CDLL(LIB_PATH)
         vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
-        L.fsx_expert_create.argtypes = [ctypes.POINTER(ExpertCfg), ctypes.POINTER(LayerWeights), vp, vp, vp,
-                                        ctypes.POINTER(vp)]
+        L.fsx_expert_create.argtypes = [ctypes.POINTER(ExpertCfg), ctypes.POINTER(LayerWeights), vp,
+                                        ctypes.POINTER(HeadWeights), vp, ctypes.POINTER(vp)]
         L.fsx_expert_forward.argtypes = [vp, ctypes.POINTER(CacheDescC), vp, i32, i32, vp, vp, vp]
         L.fsx_cache_append_rows.argtypes = [ctypes.POINTER(CacheDescC), vp, vp, i32, i32, vp]
         L.fsx_expert_status.argtypes = [vp, vp]
@@ -123,9 +129,9 @@ def _stream(stream) -> int:
 
 def make_cfg(n_layers, d_model, n_heads, head_dim, d_ffn, n_expert_tokens=10, n_out=10, max_batch=1,
              max_frame_tokens=0, dtype=BF16, rope_base=10000.0, rms_eps=1e-6, flags=0,
-             tick_timeout_us=0) -> ExpertCfg:
+             tick_timeout_us=0, head_kind=HEAD_MEAN_LINEAR, head_hidden=0) -> ExpertCfg:
     return ExpertCfg(n_layers, d_model, n_heads, head_dim, d_ffn, n_expert_tokens, n_out, max_batch,
-                     max_frame_tokens, dtype, rope_base, rms_eps, flags, tick_timeout_us)
+                     max_frame_tokens, dtype, rope_base, rms_eps, flags, tick_timeout_us, head_kind, head_hidden)
 
 
 class Expert:
@@ -147,16 +153,21 @@ class Expert:
             pass
 
 
-def expert_create(cfg: ExpertCfg, layers: Sequence[dict], final_norm, head_w, stream=None) -> Expert:
+def expert_create(cfg: ExpertCfg, layers: Sequence[dict], final_norm, head, stream=None) -> Expert:
     """fsx_expert_create.  layers: per layer a dict of device tensors (wq, wk, wv, wo, w_gate, w_up,
-    w_down, attn_norm, ffn_norm) in nn.Linear layout."""
+    w_down, attn_norm, ffn_norm) in nn.Linear layout.  head: the mean-pool head's weight [n_out][d], or a dict
+    w1, b1, w2, b2 of device tensors for the query head."""
     arr = (LayerWeights * len(layers))()
     for i, lw in enumerate(layers):
         arr[i] = LayerWeights(*[_ptr(lw[n]) for n in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down",
                                                         "attn_norm", "ffn_norm")])
+    if isinstance(head, dict):
+        hw = HeadWeights(_ptr(head["w1"]), _ptr(head["b1"]), _ptr(head["w2"]), _ptr(head["b2"]))
+    else:
+        hw = HeadWeights(_ptr(head), None, None, None)
     out = ctypes.c_void_p(0)
     _check(lib().fsx_expert_create(ctypes.byref(cfg), arr if len(layers) else None, _ptr(final_norm),
-                                   _ptr(head_w), _stream(stream), ctypes.byref(out)))
+                                   ctypes.byref(hw), _stream(stream), ctypes.byref(out)))
     return Expert(out.value, cfg)
 
 

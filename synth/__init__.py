@@ -62,6 +62,8 @@ class Workload:
     rope_base: float = 10000.0
     rms_eps: float = 1e-6
     append_rows: int = 0  # rows appended per (agent, layer) by the append step
+    head_kind: int = 0  # 0: mean-pool + linear head; 1: two-layer head over the waypoint queries
+    head_hidden: int = 0  # hidden width of the two-layer head
 
     @property
     def seq(self) -> int:
@@ -140,7 +142,8 @@ def _normal(key, shape, std=1.0) -> np.ndarray:
 # ----------------------------------------------------------------------------- weights and tokens
 
 def make_weights(wl: Workload):
-    """Per-layer weight dicts (nn.Linear [out][in] layout) + final norm gain + head weight."""
+    """Per-layer weight dicts (nn.Linear [out][in] layout) + final norm gain + the head: its weight [n_out][d], or
+    for the two-layer head a dict w1 [hidden][d], b1 [hidden], w2 [2][hidden], b2 [2] (biases ~N(0, 0.02^2), fp32)."""
     d, A, F = wl.d_model, wl.attn_width, wl.d_ffn
     shapes = {"wq": (A, d), "wk": (A, d), "wv": (A, d), "wo": (d, A),
               "w_gate": (F, d), "w_up": (F, d), "w_down": (d, F)}
@@ -153,6 +156,13 @@ def make_weights(wl: Workload):
         lw["ffn_norm"] = np.ones(d, np.float32)
         layers.append(lw)
     final_norm = np.ones(d, np.float32)
+    if wl.head_kind == 1:
+        hid = wl.head_hidden
+        head = {"w1": round_to(_normal([wl.wid, TAG_WEIGHT, wl.n_layers, 0], (hid, d), 0.02), wl.dtype),
+                "b1": _normal([wl.wid, TAG_WEIGHT, wl.n_layers, 1], (hid,), 0.02),
+                "w2": round_to(_normal([wl.wid, TAG_WEIGHT, wl.n_layers, 2], (2, hid), 0.02), wl.dtype),
+                "b2": _normal([wl.wid, TAG_WEIGHT, wl.n_layers, 3], (2,), 0.02)}
+        return layers, final_norm, head
     head_w = round_to(_normal([wl.wid, TAG_WEIGHT, wl.n_layers, 0], (wl.n_out, d), 0.02), wl.dtype)
     return layers, final_norm, head_w
 

@@ -37,10 +37,15 @@ class Model:
             self.dev_layers.append({k: torch.from_numpy(v).to(device=device, dtype=torch.float32 if k in NORMS else td)
                                     for k, v in lw.items()})
         self.dev_final = torch.from_numpy(self.final_norm).to(device)
-        self.dev_head = torch.from_numpy(self.head_w).to(device=device, dtype=td)
+        if isinstance(self.head_w, dict):
+            self.dev_head = {k: torch.from_numpy(v).to(device=device, dtype=td if k in ("w1", "w2") else torch.float32)
+                             for k, v in self.head_w.items()}
+        else:
+            self.dev_head = torch.from_numpy(self.head_w).to(device=device, dtype=td)
         cfg = fsx.make_cfg(wl.n_layers, wl.d_model, wl.n_heads, wl.head_dim, wl.d_ffn, wl.n_expert_tokens, wl.n_out,
                            max_batch or wl.batch, wl.n_frame_tokens if max_frame_tokens is None else max_frame_tokens,
-                           fsx_dtype(wl.dtype), wl.rope_base, wl.rms_eps, flags, tick_timeout_us)
+                           fsx_dtype(wl.dtype), wl.rope_base, wl.rms_eps, flags, tick_timeout_us, wl.head_kind,
+                           wl.head_hidden)
         ex = fsx.expert_create(cfg, self.dev_layers, self.dev_final, self.dev_head)
         torch.cuda.synchronize()
         # the library packed its own copy; the caller's tensors may go

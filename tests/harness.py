@@ -23,7 +23,8 @@ from gpu_inputs import head_major_rows, rel_err, run_forward, tokens_for  # noqa
 def shape_of(wl: synth.Workload) -> oracle.ExpertShape:
     return oracle.ExpertShape(n_layers=wl.n_layers, d_model=wl.d_model, n_heads=wl.n_heads, head_dim=wl.head_dim,
                               d_ffn=wl.d_ffn, n_expert_tokens=wl.n_expert_tokens, n_out=wl.n_out,
-                              rope_base=wl.rope_base, rms_eps=wl.rms_eps)
+                              rope_base=wl.rope_base, rms_eps=wl.rms_eps, head_kind=wl.head_kind,
+                              head_hidden=wl.head_hidden)
 
 
 class Model(_Model):
