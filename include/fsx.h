@@ -214,6 +214,47 @@ int fsx_expert_forward_noalloc(fsx_expert* ex, const fsx_cache_desc* cache, cons
 int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, const void* v_rows, int32_t n_rows,
                           int32_t policy, void* stream);
 
+/* The slow system's rows, quantised on the way in: rows in BF16 or F32 (rows_dtype) are stored into an
+ * FP8_E4M3 cache as code = round-to-nearest-even(clamp(x / scale, -448, 448)) with the cache's existing
+ * per-(agent, layer, head) k_scale / v_scale (Sec. 3.3 append; the fp8 cache of the long-context workload).
+ * Layout, policy, ring update and errors as fsx_cache_append_rows; FSX_E_INVALID if the cache is not FP8 or has
+ * no scales.  head_dim must be a multiple of 16. */
+int fsx_cache_append_rows_quantize(fsx_cache_desc* cache, const void* k_rows, const void* v_rows, int32_t rows_dtype,
+                                   int32_t n_rows, int32_t policy, void* stream);
+
+/* ---- The asynchronous deployment loop (Sec. 3.3, "Asynchronous Deployment"; Fig. 1) ----
+ * The expert runs every tick on `expert_stream`; the slow system's rows are appended on `append_stream` (a
+ * different stream of the same priority).  The loop keeps two copies of the ring state: ticks read the front
+ * copy, appends advance the back copy.  An append is handed to the ticks (front = back, the tick's stream waiting
+ * on the append's event) at the first tick after it has completed, and at the latest on the K-1-th tick after it
+ * was submitted, so a tick never lags the newest submitted rows by more than K-1 ticks.  An append that overwrites
+ * rows the ticks can see (ring full) first waits for the ticks already enqueued and is handed over at the next
+ * tick.  The cache descriptor's device buffers must outlive the loop; its host arrays are copied at create. */
+typedef struct fsx_loop fsx_loop;
+typedef struct {
+  int64_t tick;        /* index of this tick */
+  int32_t published;   /* 1 if this tick is the first to see the rows of earlier appends */
+  int32_t staleness;   /* ticks (this one included) that ran without the newest submitted rows; 0 = up to date */
+  int64_t start[FSX_MAX_BATCH], len[FSX_MAX_BATCH], pos[FSX_MAX_BATCH];  /* the ring state this tick read */
+} fsx_loop_tick_info;
+
+/* append_every = K >= 1 (the paper: 4); policy FSX_APPEND_RING or FSX_APPEND_ERROR. */
+int fsx_loop_create(fsx_expert* ex, const fsx_cache_desc* cache, int32_t append_every, int32_t policy,
+                    void* expert_stream, void* append_stream, fsx_loop** out);
+/* One control tick (arguments as fsx_expert_forward); info (nullable, HOST) receives the ring state it read. */
+int fsx_loop_tick(fsx_loop* lp, const void* tokens, int32_t batch, int32_t n_frame_tokens, float* waypoints,
+                  float* hidden, fsx_loop_tick_info* info);
+/* Submit n_rows new rows per (agent, layer) (layout as fsx_cache_append_rows); rows_dtype equal to the cache's
+ * dtype copies them, BF16 / F32 rows into an FP8 cache are quantised.  The row buffers are read on the append
+ * stream: keep them unchanged until a later tick reports them published or fsx_loop_sync returns. */
+int fsx_loop_append(fsx_loop* lp, const void* k_rows, const void* v_rows, int32_t rows_dtype, int32_t n_rows);
+/* Wait for both streams; cache_out (nullable) receives the newest ring state (start/len/pos). */
+int fsx_loop_sync(fsx_loop* lp, fsx_cache_desc* cache_out);
+/* Wait for the loop's last tick and append, then free it (the expert and the cache stay the caller's). */
+void fsx_loop_destroy(fsx_loop* lp);
+/* Message of the calling thread's last failed loop call. */
+const char* fsx_loop_last_error(void);
+
 /* Synchronise `stream` and report whether the ticks enqueued on this handle completed: FSX_OK, or
  * FSX_E_HIP if a tick kernel gave up on a wait (its waypoints were then written as NaN).  The
  * failure is reported once per failed tick and cleared by reporting it. */

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfsx.so")
-SOURCES = ["api.hip", "fast_kernels.hip", "generic_kernels.hip", "tick_kernel.hip", "probe.hip"]
+SOURCES = ["api.hip", "fast_kernels.hip", "generic_kernels.hip", "tick_kernel.hip", "probe.hip", "loop.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC",

@@ -640,12 +640,18 @@ extern "C" int fsx_expert_forward_noalloc(fsx_expert* ex, const fsx_cache_desc* 
   return forward_impl(ex, cache, tokens, batch, n_frame_tokens, waypoints, hidden, stream, true);
 }
 
-extern "C" int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, const void* v_rows, int32_t n_rows,
-                                     int32_t policy, void* stream) {
+// rows_dtype < 0: rows in the cache's dtype (bit copy); else bf16 / fp32 rows encoded into an fp8 cache.
+static int append_impl(fsx_cache_desc* cache, const void* k_rows, const void* v_rows, int rows_dtype, int32_t n_rows,
+                       int32_t policy, void* stream) {
   int rc = validate_cache(nullptr, cache, cache ? cache->batch : 0);
   if (rc) return rc;
   if (n_rows < 0) return fail(FSX_E_INVALID, "n_rows must be >= 0");
   if (policy != FSX_APPEND_RING && policy != FSX_APPEND_ERROR) return fail(FSX_E_INVALID, "unknown append policy");
+  if (rows_dtype >= 0) {
+    if (cache->dtype != FSX_FP8_E4M3) return fail(FSX_E_INVALID, "quantising append needs an FP8_E4M3 cache");
+    if (rows_dtype != FSX_BF16 && rows_dtype != FSX_F32) return fail(FSX_E_INVALID, "rows must be BF16 or F32");
+    if (!cache->k_scale || !cache->v_scale) return fail(FSX_E_INVALID, "fp8 cache needs k_scale and v_scale");
+  }
   if (n_rows == 0) {
     g_err.clear();
     return FSX_OK;
@@ -671,7 +677,10 @@ extern "C" int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, 
     const int64_t st = cache->len[b] > 0 ? cache->start[b] : 0;
     first[b] = (st + cache->len[b]) % cache->capacity;
   }
-  HIP_TRY(launch_append(*cache, k_rows, v_rows, n_rows, first.data(), (hipStream_t)stream));
+  if (rows_dtype >= 0)
+    HIP_TRY(launch_append_quantize(*cache, k_rows, v_rows, rows_dtype, n_rows, first.data(), (hipStream_t)stream));
+  else
+    HIP_TRY(launch_append(*cache, k_rows, v_rows, n_rows, first.data(), (hipStream_t)stream));
   for (int b = 0; b < B; ++b) {
     const int64_t st = cache->len[b] > 0 ? cache->start[b] : first[b];
     const int64_t nl = cache->len[b] + n_rows;
@@ -686,6 +695,17 @@ extern "C" int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, 
   }
   g_err.clear();
   return FSX_OK;
+}
+
+extern "C" int fsx_cache_append_rows(fsx_cache_desc* cache, const void* k_rows, const void* v_rows, int32_t n_rows,
+                                     int32_t policy, void* stream) {
+  return append_impl(cache, k_rows, v_rows, -1, n_rows, policy, stream);
+}
+
+extern "C" int fsx_cache_append_rows_quantize(fsx_cache_desc* cache, const void* k_rows, const void* v_rows,
+                                              int32_t rows_dtype, int32_t n_rows, int32_t policy, void* stream) {
+  if (rows_dtype < 0) return fail(FSX_E_INVALID, "rows must be BF16 or F32");
+  return append_impl(cache, k_rows, v_rows, rows_dtype, n_rows, policy, stream);
 }
 
 extern "C" int fsx_expert_status(fsx_expert* ex, void* stream) {

@@ -543,6 +543,123 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a) {
   a.vc[dst] = a.vs[i];
 }
 
+// Quantising append into an fp8 cache: the rows arrive in bf16 or fp32 and each element is stored as the E4M3 code
+// RNE(clamp(x / scale, -448, 448)) with the (agent, layer, head) scale the cache already has.  The encoding follows
+// the format's definition step by step (exact in fp32: the quotient is rounded once by the division, the mantissa
+// rounding is a rint of an exactly scaled value), so the codes are reproducible bit for bit.
+__device__ __forceinline__ uint32_t e4m3_encode(float x, float scale) {
+  float y = x / scale;
+  if (y != y) return 0x7Fu | (__float_as_uint(y) >> 31 << 7);
+  y = fminf(fmaxf(y, -448.0f), 448.0f);
+  const uint32_t sign = __float_as_uint(y) >> 31 << 7;
+  const float a = fabsf(y);
+  uint32_t code;
+  if (a < 0.015625f) {  // below the smallest normal 2^-6: subnormal steps of 2^-9
+    code = (uint32_t)rintf(a * 512.0f);  // 8 -> the smallest normal, code 0x08
+  } else {
+    int e;
+    const float m = frexpf(a, &e);  // a = m 2^e, m in [0.5, 1)
+    uint32_t mant = (uint32_t)rintf((m * 2.0f - 1.0f) * 8.0f);
+    int ex = e - 1;
+    if (mant == 8) {
+      mant = 0;
+      ++ex;
+    }
+    code = ((uint32_t)(ex + 7) << 3) | mant;
+  }
+  return sign | code;
+}
+
+struct QAppendArgs {
+  const void* ks;
+  const void* vs;
+  uint8_t* kc;
+  uint8_t* vc;
+  const float* kscale;
+  const float* vscale;
+  int64_t cap;
+  int n_layers, n_heads, head_dim, n_rows, B, token_major, src_f32;
+  int64_t first[FSX_MAX_BATCH];
+};
+
+// Thread i encodes 8 consecutive elements of one head row (8 bytes out).
+__global__ __launch_bounds__(256) void k_append_quantize(QAppendArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cpr = a.head_dim / 8;
+  const int64_t total = (int64_t)a.B * a.n_layers * a.n_heads * a.n_rows * cpr;
+  if (i >= total) return;
+  const int ch = (int)(i % cpr);
+  int64_t r = i / cpr;
+  int b, l, h, j;
+  if (a.token_major) {
+    h = (int)(r % a.n_heads);
+    r /= a.n_heads;
+    j = (int)(r % a.n_rows);
+    r /= a.n_rows;
+    l = (int)(r % a.n_layers);
+    b = (int)(r / a.n_layers);
+  } else {
+    j = (int)(r % a.n_rows);
+    r /= a.n_rows;
+    h = (int)(r % a.n_heads);
+    r /= a.n_heads;
+    l = (int)(r % a.n_layers);
+    b = (int)(r / a.n_layers);
+  }
+  int64_t slot = a.first[b] + j;
+  if (slot >= a.cap) slot -= a.cap;
+  const int64_t lb = ((int64_t)b * a.n_layers + l);
+  const int64_t dst = a.token_major ? ((lb * a.cap + slot) * a.n_heads + h) * a.head_dim + 8 * ch
+                                    : ((lb * a.n_heads + h) * a.cap + slot) * a.head_dim + 8 * ch;
+  const float sk = a.kscale[lb * a.n_heads + h], sv = a.vscale[lb * a.n_heads + h];
+  const int64_t src = i * 8;  // the source rows are dense in the same order as i
+  float xk[8], xv[8];
+  if (a.src_f32) {
+    const float4* pk = reinterpret_cast<const float4*>((const float*)a.ks + src);
+    const float4* pv = reinterpret_cast<const float4*>((const float*)a.vs + src);
+    const float4 k0 = pk[0], k1 = pk[1], v0 = pv[0], v1 = pv[1];
+    const float kk[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
+    const float vv[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      xk[e] = kk[e];
+      xv[e] = vv[e];
+    }
+  } else {
+    const uint4 k = *reinterpret_cast<const uint4*>((const uint16_t*)a.ks + src);
+    const uint4 v = *reinterpret_cast<const uint4*>((const uint16_t*)a.vs + src);
+    const uint32_t kw[4] = {k.x, k.y, k.z, k.w}, vw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      xk[2 * e] = __uint_as_float(kw[e] << 16);
+      xk[2 * e + 1] = __uint_as_float(kw[e] & 0xFFFF0000u);
+      xv[2 * e] = __uint_as_float(vw[e] << 16);
+      xv[2 * e + 1] = __uint_as_float(vw[e] & 0xFFFF0000u);
+    }
+  }
+  uint32_t ck[2] = {0, 0}, cv[2] = {0, 0};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    ck[e >> 2] |= e4m3_encode(xk[e], sk) << (8 * (e & 3));
+    cv[e >> 2] |= e4m3_encode(xv[e], sv) << (8 * (e & 3));
+  }
+  *reinterpret_cast<uint2*>(a.kc + dst) = make_uint2(ck[0], ck[1]);
+  *reinterpret_cast<uint2*>(a.vc + dst) = make_uint2(cv[0], cv[1]);
+}
+
+hipError_t launch_append_quantize(const fsx_cache_desc& c, const void* k_rows, const void* v_rows, int rows_dtype,
+                                  int n_rows, const int64_t* first, hipStream_t s) {
+  QAppendArgs a{};
+  a.ks = k_rows; a.vs = v_rows; a.kc = (uint8_t*)c.k; a.vc = (uint8_t*)c.v; a.kscale = c.k_scale; a.vscale = c.v_scale;
+  a.cap = c.capacity; a.n_layers = c.n_layers; a.n_heads = c.n_heads; a.head_dim = c.head_dim; a.n_rows = n_rows;
+  a.B = c.batch; a.token_major = (c.layout & FSX_CACHE_TOKEN_MAJOR) != 0; a.src_f32 = rows_dtype == FSX_F32;
+  for (int b = 0; b < c.batch; ++b) a.first[b] = first[b];
+  const int64_t total = (int64_t)a.B * a.n_layers * a.n_heads * a.n_rows * (a.head_dim / 8);
+  if (total == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_append_quantize, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_append(const fsx_cache_desc& c, const void* k_rows, const void* v_rows, int n_rows,
                          const int64_t* first, hipStream_t s) {
   AppendArgs a{};

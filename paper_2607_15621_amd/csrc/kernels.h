@@ -191,6 +191,9 @@ hipError_t launch_probe_read(const void* buf, int64_t bytes, int mode, uint32_t*
 // ------------------------------------------------------------------ cache append
 hipError_t launch_append(const fsx_cache_desc& c, const void* k_rows, const void* v_rows, int n_rows,
                          const int64_t* dst_first_slot /* host [batch] */, hipStream_t s);
+// bf16 / fp32 rows (rows_dtype) encoded into an fp8 cache with its existing scales.
+hipError_t launch_append_quantize(const fsx_cache_desc& c, const void* k_rows, const void* v_rows, int rows_dtype,
+                                  int n_rows, const int64_t* dst_first_slot, hipStream_t s);
 
 // ------------------------------------------------------------------ simple per-op path (any dtype)
 struct GenericWeights {

@@ -27,7 +27,9 @@ STATUS = {0: "FSX_OK", 1: "FSX_E_INVALID", 2: "FSX_E_UNSUPPORTED", 3: "FSX_E_CAP
           5: "FSX_E_HIP"}
 SYMBOLS = ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_status",
            "fsx_expert_trace", "fsx_expert_destroy", "fsx_last_error", "fsx_expert_info", "fsx_version",
-           "fsx_probe_hbm_read", "fsx_expert_forward_noalloc")
+           "fsx_probe_hbm_read", "fsx_expert_forward_noalloc", "fsx_cache_append_rows_quantize",
+           "fsx_loop_create", "fsx_loop_tick", "fsx_loop_append", "fsx_loop_sync", "fsx_loop_destroy",
+           "fsx_loop_last_error")
 
 
 class FsxError(RuntimeError):
@@ -52,6 +54,12 @@ class HeadWeights(ctypes.Structure):
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "attn_norm", "ffn_norm")]
+
+
+class LoopTickInfo(ctypes.Structure):
+    _fields_ = [("tick", ctypes.c_int64), ("published", ctypes.c_int32), ("staleness", ctypes.c_int32),
+                ("start", ctypes.c_int64 * MAX_BATCH), ("len", ctypes.c_int64 * MAX_BATCH),
+                ("pos", ctypes.c_int64 * MAX_BATCH)]
 
 
 class CacheDescC(ctypes.Structure):
@@ -89,6 +97,17 @@ def lib() -> ctypes.CDLL:
         L.fsx_probe_hbm_read.argtypes = [vp, i64, i32, vp, vp]
         L.fsx_expert_forward_noalloc.argtypes = [vp, ctypes.POINTER(CacheDescC), vp, i32, i32, vp, vp, vp]
         L.fsx_expert_forward_noalloc.restype = ctypes.c_int
+        L.fsx_cache_append_rows_quantize.argtypes = [ctypes.POINTER(CacheDescC), vp, vp, i32, i32, i32, vp]
+        L.fsx_loop_create.argtypes = [vp, ctypes.POINTER(CacheDescC), i32, i32, vp, vp, ctypes.POINTER(vp)]
+        L.fsx_loop_tick.argtypes = [vp, vp, i32, i32, vp, vp, ctypes.POINTER(LoopTickInfo)]
+        L.fsx_loop_append.argtypes = [vp, vp, vp, i32, i32]
+        L.fsx_loop_sync.argtypes = [vp, ctypes.POINTER(CacheDescC)]
+        L.fsx_loop_destroy.argtypes = [vp]
+        L.fsx_loop_destroy.restype = None
+        L.fsx_loop_last_error.restype = ctypes.c_char_p
+        for n in ("fsx_cache_append_rows_quantize", "fsx_loop_create", "fsx_loop_tick", "fsx_loop_append",
+                  "fsx_loop_sync"):
+            getattr(L, n).restype = ctypes.c_int
         for n in ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_info",
                   "fsx_expert_status", "fsx_expert_trace", "fsx_probe_hbm_read"):
             getattr(L, n).restype = ctypes.c_int
@@ -239,3 +258,53 @@ def cache_append_rows(cache: CacheDesc, k_rows, v_rows, n_rows: int, policy: int
 def probe_hbm_read(buf, nbytes: int, mode: int, sink, stream=None):
     """fsx_probe_hbm_read: enqueue one read-only pass over nbytes of buf (measurement helper)."""
     _check(lib().fsx_probe_hbm_read(_ptr(buf), nbytes, mode, _ptr(sink), _stream(stream)))
+
+
+def cache_append_rows_quantize(cache: CacheDesc, k_rows, v_rows, rows_dtype: int, n_rows: int,
+                               policy: int = APPEND_RING, stream=None):
+    """fsx_cache_append_rows_quantize: bf16 / fp32 rows encoded into an fp8 cache with its scales."""
+    _check(lib().fsx_cache_append_rows_quantize(ctypes.byref(cache.c), _ptr(k_rows), _ptr(v_rows), rows_dtype,
+                                                n_rows, policy, _stream(stream)))
+
+
+class Loop:
+    """fsx_loop: the asynchronous deployment loop (expert every tick, appends on a second stream)."""
+
+    def __init__(self, ex: Expert, cache: CacheDesc, append_every: int, expert_stream, append_stream,
+                 policy: int = APPEND_RING):
+        self.ex, self.cache = ex, cache  # the loop reads their device buffers
+        out = ctypes.c_void_p(0)
+        self._check(lib().fsx_loop_create(ctypes.c_void_p(ex.handle), ctypes.byref(cache.c), append_every, policy,
+                                          _stream(expert_stream), _stream(append_stream), ctypes.byref(out)))
+        self.handle = out.value
+
+    @staticmethod
+    def _check(code):
+        if code != 0:
+            raise FsxError(code, lib().fsx_loop_last_error().decode())
+
+    def tick(self, tokens, batch: int, n_frame_tokens: int, waypoints, hidden=None) -> dict:
+        info = LoopTickInfo()
+        self._check(lib().fsx_loop_tick(ctypes.c_void_p(self.handle), _ptr(tokens), batch, n_frame_tokens,
+                                        _ptr(waypoints), _ptr(hidden), ctypes.byref(info)))
+        return {"tick": info.tick, "published": info.published, "staleness": info.staleness,
+                "start": list(info.start[:batch]), "len": list(info.len[:batch]), "pos": list(info.pos[:batch])}
+
+    def append(self, k_rows, v_rows, rows_dtype: int, n_rows: int):
+        self._check(lib().fsx_loop_append(ctypes.c_void_p(self.handle), _ptr(k_rows), _ptr(v_rows), rows_dtype,
+                                          n_rows))
+
+    def sync(self, cache_out: Optional[CacheDesc] = None):
+        self._check(lib().fsx_loop_sync(ctypes.c_void_p(self.handle),
+                                        ctypes.byref(cache_out.c) if cache_out is not None else None))
+
+    def close(self):
+        if self.handle:
+            lib().fsx_loop_destroy(ctypes.c_void_p(self.handle))
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
