@@ -14,6 +14,9 @@ Attention", run once per control tick as in Sec. 3.3):
   two-layer head over the waypoint-query tokens; the staleness-augmented training
   form (Sec. 3.2): every frame's expert block of a clip in one forward, one
   attention over the whole clip with per-block masks.
+* ``backbone.py`` -- the backbone's incremental forward (Sec. 3.3): the n new
+  tokens of a frame through LLaMA decoder layers over the cache, giving the
+  rows to append.
 * ``fp8.py``     -- decoding of OCP FP8 E4M3 (e4m3fn) codes (the diagnostic
   reference for the fp8-stored cache) and their encoding against a scale
   (the reference of the quantising append).
@@ -44,3 +47,9 @@ from .expert import (  # noqa: F401
     masked_multiblock_forward,
 )
 from .fp8 import e4m3fn_decode, e4m3fn_encode  # noqa: F401
+from .backbone import (  # noqa: F401
+    BackboneShape,
+    causal_cache_attention,
+    backbone_layer,
+    backbone_incremental_forward,
+)
