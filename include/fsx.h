@@ -255,6 +255,41 @@ void fsx_loop_destroy(fsx_loop* lp);
 /* Message of the calling thread's last failed loop call. */
 const char* fsx_loop_last_error(void);
 
+/* ---- The slow system's producer of the appended rows: the backbone's incremental forward (Sec. 3.3) ----
+ * Every K ticks the current frame's tokens go through the frozen backbone (LLaMA-7B: 32 layers, width 4096, 32
+ * heads x 128, SwiGLU 11008) as an incremental forward over its cache: at every layer each new token attends to
+ * the cached rows and to the new tokens up to itself, and its rotated key and value become the layer's appended
+ * row.  The cost does not depend on the history length beyond the attention over the cached rows. */
+typedef struct fsx_backbone fsx_backbone;
+typedef struct {
+  int32_t n_layers, d_model, n_heads, head_dim, d_ffn;  /* head_dim 128; d_model and d_ffn multiples of 32 */
+  int32_t max_new_rows;  /* tokens appended per call and agent (4 per frame in the paper), 1..64 */
+  int32_t max_batch;     /* agents per call, 1..64 */
+  int32_t dtype;         /* FSX_BF16 */
+  float rope_base;       /* rotary base of the backbone (LLaMA: 10000) */
+  float rms_eps;
+} fsx_backbone_cfg;
+
+/* Pack the backbone's layers (fsx_layer_weights as for the expert: wq, wk, wv [H*Dh][d], wo [d][H*Dh], w_gate,
+ * w_up [d_ffn][d], w_down [d][d_ffn], norm gains [d]; DEVICE pointers, bf16) into library-owned memory.
+ * Synchronises `stream`; the caller may free its buffers afterwards. */
+int fsx_backbone_create(const fsx_backbone_cfg* cfg, const fsx_layer_weights* layers, void* stream,
+                        fsx_backbone** out);
+/* Append n_rows new tokens per agent to every layer of the cache through the incremental forward.
+ *   cache   geometry equal to the backbone's (n_layers, H, Dh); BF16 (rows stored as computed) or FP8_E4M3
+ *           (rows encoded with the cache's existing scales); batch must equal cache->batch; not shared
+ *   tokens  DEVICE [batch][n_rows][d] bf16 embeddings of the new tokens, at positions pos[b] .. pos[b]+n_rows-1
+ *   hidden  DEVICE [n_layers][batch][n_rows][d] fp32 output of every layer, or NULL
+ *   policy  FSX_APPEND_RING / FSX_APPEND_ERROR as fsx_cache_append_rows; the new tokens attend to every row the
+ *           ring held before the call, also to rows the append then overwrites
+ * The ring state (start, len, pos) is updated on the host before returning, as fsx_cache_append_rows does. */
+int fsx_backbone_append(fsx_backbone* bb, fsx_cache_desc* cache, const void* tokens, int32_t batch, int32_t n_rows,
+                        float* hidden, int32_t policy, void* stream);
+/* Bytes of the packed weight matrices (streamed once per call) and of the workspace. */
+int fsx_backbone_info(const fsx_backbone* bb, int64_t* weight_bytes, int64_t* workspace_bytes);
+/* Wait for the handle's last call, then free it. */
+void fsx_backbone_destroy(fsx_backbone* bb);
+
 /* Synchronise `stream` and report whether the ticks enqueued on this handle completed: FSX_OK, or
  * FSX_E_HIP if a tick kernel gave up on a wait (its waypoints were then written as NaN).  The
  * failure is reported once per failed tick and cleared by reporting it. */

@@ -60,6 +60,7 @@ struct fsx_expert {
   uint64_t epoch = 0;
   uint64_t status_seen = 0;
   hipEvent_t done = nullptr;  // recorded after every tick enqueued on the handle (destroy waits for it)
+  bool backbone = false;      // the backbone's layers (fsx_backbone_*), not an expert
   int wg_per_xcd_max = 0;     // most workgroups the create-time probe placed on one XCD
 };
 
@@ -99,14 +100,18 @@ static int validate_cfg(const fsx_expert_cfg* c) {
   return FSX_OK;
 }
 
-extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weights* layers, const float* final_norm,
-                                 const fsx_head_weights* head, void* stream, fsx_expert** out) {
+// backbone: the layers only (no final norm, no head), run as one launch per phase with causal own rows (the
+// backbone's incremental forward, fsx_backbone_*).
+static int create_impl(const fsx_expert_cfg* cfg, const fsx_layer_weights* layers, const float* final_norm,
+                       const fsx_head_weights* head, void* stream, fsx_expert** out, bool backbone) {
   if (!out) return fail(FSX_E_INVALID, "out is NULL");
   *out = nullptr;
   int rc = validate_cfg(cfg);
   if (rc) return rc;
-  if (!layers || !final_norm || !head || !head->w) return fail(FSX_E_INVALID, "layers, final_norm and head->w must be non-NULL");
-  if (cfg->head_kind == FSX_HEAD_QUERY_MLP && (!head->b || !head->w2 || !head->b2))
+  if (!backbone && (!layers || !final_norm || !head || !head->w))
+    return fail(FSX_E_INVALID, "layers, final_norm and head->w must be non-NULL");
+  if (backbone && !layers) return fail(FSX_E_INVALID, "layers must be non-NULL");
+  if (!backbone && cfg->head_kind == FSX_HEAD_QUERY_MLP && (!head->b || !head->w2 || !head->b2))
     return fail(FSX_E_INVALID, "the query head needs w, b, w2 and b2");
   const fsx_expert_cfg& c = *cfg;
   for (int l = 0; l < c.n_layers; ++l) {
@@ -128,10 +133,19 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   ex->M_max = c.max_batch * ex->S_max;
   const bool fused_ok = c.dtype == FSX_BF16 && Dh == 128 && d % 32 == 0 && F % 32 == 0;
   ex->path = (fused_ok && !(c.flags & FSX_FLAG_GENERIC)) ? 0 : 1;
+  ex->backbone = backbone;
+  if (backbone) {
+    if (ex->path != 0) {
+      delete ex;
+      return fail(FSX_E_UNSUPPORTED, "the backbone runs bf16 weights with head_dim 128 and d, d_ffn multiples of 32");
+    }
+    ex->cfg.flags |= FSX_FLAG_MULTI_LAUNCH;
+  }
   const int es = esize(c.dtype);
   const int64_t per_layer = (int64_t)4 * A * d + (int64_t)3 * F * d;  // elements
   const bool qh = c.head_kind == FSX_HEAD_QUERY_MLP;
-  const int64_t head_elems = qh ? (int64_t)c.head_hidden * d + 2 * (int64_t)c.head_hidden : (int64_t)c.n_out * d;
+  const int64_t head_elems =
+      backbone ? 0 : (qh ? (int64_t)c.head_hidden * d + 2 * (int64_t)c.head_hidden : (int64_t)c.n_out * d);
   ex->weight_bytes = (per_layer * c.n_layers + head_elems) * es;
 
   int last = FSX_OK;
@@ -151,7 +165,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   if (!ok(hipMalloc(&ex->wbuf, (size_t)(per_layer * c.n_layers * es)), "hipMalloc(weights)")) return cleanup(FSX_E_OOM);
   if (!ok(hipMalloc((void**)&ex->fbuf, sizeof(float) * ((size_t)2 * c.n_layers * d + d)), "hipMalloc(norms)"))
     return cleanup(FSX_E_OOM);
-  if (!ok(hipMalloc(&ex->head_w, (size_t)head_elems * es), "hipMalloc(head)")) return cleanup(FSX_E_OOM);
+  if (!backbone && !ok(hipMalloc(&ex->head_w, (size_t)head_elems * es), "hipMalloc(head)")) return cleanup(FSX_E_OOM);
   if (qh && !ok(hipMalloc((void**)&ex->head_b, sizeof(float) * ((size_t)c.head_hidden + 2)), "hipMalloc(head bias)"))
     return cleanup(FSX_E_OOM);
 
@@ -164,12 +178,14 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
       return cleanup(FSX_E_HIP);
   }
   ex->final_norm = ex->fbuf + (size_t)2 * c.n_layers * d;
-  if (!ok(hipMemcpyAsync((void*)ex->final_norm, final_norm, sizeof(float) * d, hipMemcpyDeviceToDevice, s),
+  if (backbone) {
+    // no final norm and no head: the incremental forward's product is the appended rows (and hidden states)
+  } else if (!ok(hipMemcpyAsync((void*)ex->final_norm, final_norm, sizeof(float) * d, hipMemcpyDeviceToDevice, s),
           "copy final_norm") ||
       !ok(hipMemcpyAsync(ex->head_w, head->w, (size_t)(qh ? (int64_t)c.head_hidden * d : (int64_t)c.n_out * d) * es,
                          hipMemcpyDeviceToDevice, s), "copy head"))
     return cleanup(FSX_E_HIP);
-  if (qh) {
+  if (qh && !backbone) {
     char* w2 = (char*)ex->head_w + (size_t)c.head_hidden * d * es;
     if (!ok(hipMemcpyAsync(w2, head->w2, (size_t)2 * c.head_hidden * es, hipMemcpyDeviceToDevice, s), "copy head w2") ||
         !ok(hipMemcpyAsync(ex->head_b, head->b, sizeof(float) * c.head_hidden, hipMemcpyDeviceToDevice, s), "copy head b") ||
@@ -270,7 +286,7 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
              {(void**)&ex->gws.rope, (size_t)M * Dh * 4}};
   }
   const int nflag_attn = c.max_batch * H;
-  if (ex->path == 0 && !(c.flags & FSX_FLAG_MULTI_LAUNCH)) {
+  if (ex->path == 0 && !(ex->cfg.flags & FSX_FLAG_MULTI_LAUNCH)) {
     // The tick kernel splits heads and FFN columns over the XCDs; find how many there are and check that
     // every XCD's share fits the kernel (at most 4 heads of width 128 and 512 FFN columns per XCD).
     int nx = 0;
@@ -372,6 +388,11 @@ extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weig
   *out = ex;
   g_err.clear();
   return FSX_OK;
+}
+
+extern "C" int fsx_expert_create(const fsx_expert_cfg* cfg, const fsx_layer_weights* layers, const float* final_norm,
+                                 const fsx_head_weights* head, void* stream, fsx_expert** out) {
+  return create_impl(cfg, layers, final_norm, head, stream, out, false);
 }
 
 static int validate_cache(const fsx_expert* ex, const fsx_cache_desc* c, int batch) {
@@ -765,4 +786,161 @@ extern "C" int fsx_probe_hbm_read(const void* buf, int64_t bytes, int32_t mode, 
   HIP_TRY(launch_probe_read(buf, bytes, mode, sink, (hipStream_t)stream));
   g_err.clear();
   return FSX_OK;
+}
+
+// ------------------------------------------------------------------------------------------------------------
+// The backbone's incremental forward (Sec. 3.3): the slow system's producer of the appended rows.  The layers run
+// as one launch per phase (split-K MFMA projections streaming the packed weights, split-K attention over the
+// cached rows plus the new rows under a causal mask); after each layer's attention the new rows' rotated keys and
+// values are written into that layer's ring slots.
+struct fsx_backbone {
+  fsx_expert* ex = nullptr;
+};
+
+extern "C" int fsx_backbone_create(const fsx_backbone_cfg* cfg, const fsx_layer_weights* layers, void* stream,
+                                   fsx_backbone** out) {
+  if (!out) return fail(FSX_E_INVALID, "out is NULL");
+  *out = nullptr;
+  if (!cfg) return fail(FSX_E_INVALID, "cfg is NULL");
+  if (cfg->dtype != FSX_BF16) return fail(FSX_E_UNSUPPORTED, "the backbone runs bf16 weights");
+  if (cfg->max_new_rows < 1 || cfg->max_new_rows > 64) return fail(FSX_E_INVALID, "max_new_rows must be in 1..64");
+  fsx_expert_cfg c{};
+  c.n_layers = cfg->n_layers; c.d_model = cfg->d_model; c.n_heads = cfg->n_heads; c.head_dim = cfg->head_dim;
+  c.d_ffn = cfg->d_ffn; c.n_expert_tokens = cfg->max_new_rows; c.n_out = 2; c.max_batch = cfg->max_batch;
+  c.max_frame_tokens = 0; c.dtype = cfg->dtype; c.rope_base = cfg->rope_base; c.rms_eps = cfg->rms_eps;
+  c.flags = FSX_FLAG_MULTI_LAUNCH; c.head_kind = FSX_HEAD_MEAN_LINEAR;
+  fsx_expert* ex = nullptr;
+  const int rc = create_impl(&c, layers, nullptr, nullptr, stream, &ex, true);
+  if (rc) return rc;
+  fsx_backbone* bb = new fsx_backbone();
+  bb->ex = ex;
+  *out = bb;
+  g_err.clear();
+  return FSX_OK;
+}
+
+extern "C" int fsx_backbone_append(fsx_backbone* bb, fsx_cache_desc* cache, const void* tokens, int32_t batch,
+                                   int32_t n_rows, float* hidden, int32_t policy, void* stream) {
+  if (!bb || !bb->ex) return fail(FSX_E_INVALID, "backbone handle is NULL");
+  fsx_expert* ex = bb->ex;
+  const fsx_expert_cfg& c = ex->cfg;
+  if (!tokens) return fail(FSX_E_INVALID, "tokens must be non-NULL");
+  if (n_rows < 1 || n_rows > c.n_expert_tokens) return fail(FSX_E_CAPACITY, "n_rows outside 1..max_new_rows");
+  if (policy != FSX_APPEND_RING && policy != FSX_APPEND_ERROR) return fail(FSX_E_INVALID, "unknown append policy");
+  int rc = validate_cache(ex, cache, batch);
+  if (rc) return rc;
+  if (batch != cache->batch) return fail(FSX_E_INVALID, "the backbone appends to every agent of the descriptor: batch "
+                                                        "must equal cache->batch");
+  if (batch > c.max_batch) return fail(FSX_E_CAPACITY, "batch exceeds max_batch");
+  if (cache->layout & FSX_CACHE_SHARED) return fail(FSX_E_UNSUPPORTED, "a shared cache cannot be appended to");
+  if (cache->dtype != FSX_BF16 && cache->dtype != FSX_FP8_E4M3)
+    return fail(FSX_E_UNSUPPORTED, "the backbone writes BF16 or FP8 caches");
+  if (!cache->k || !cache->v) return fail(FSX_E_INVALID, "cache k/v pointers are NULL");
+  if (cache->dtype == FSX_FP8_E4M3 && (!cache->k_scale || !cache->v_scale))
+    return fail(FSX_E_INVALID, "fp8 cache needs k_scale and v_scale");
+  if (!aligned16(tokens) || !aligned16(cache->k) || !aligned16(cache->v))
+    return fail(FSX_E_INVALID, "tokens and cache buffers must be 16-byte aligned");
+  if (n_rows > cache->capacity) return fail(FSX_E_CAPACITY, "n_rows exceeds the ring capacity");
+  if (policy == FSX_APPEND_ERROR)
+    for (int b = 0; b < batch; ++b)
+      if (cache->len[b] + n_rows > cache->capacity)
+        return fail(FSX_E_CAPACITY, "agent " + std::to_string(b) + ": ring full (policy FSX_APPEND_ERROR)");
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev != ex->device) return fail(FSX_E_INVALID, "current device differs from the one the backbone was created on");
+  hipStream_t s = (hipStream_t)stream;
+
+  TickParams tp{};
+  tp.B = batch;
+  tp.S = n_rows;
+  tp.T = n_rows;
+  tp.M = batch * n_rows;
+  tp.n_tt = (tp.S + 15) / 16;
+  int64_t rows = 0;
+  std::vector<int64_t> first(batch);
+  for (int b = 0; b < batch; ++b) {
+    tp.pos[b] = cache->pos[b];  // the new tokens sit at positions pos .. pos + n_rows - 1
+    tp.start[b] = cache->len[b] > 0 ? cache->start[b] : 0;
+    tp.len[b] = (int32_t)cache->len[b];
+    rows += cache->len[b];
+    first[b] = (tp.start[b] + cache->len[b]) % cache->capacity;
+  }
+  Dims dm{};
+  dm.d = c.d_model; dm.H = c.n_heads; dm.Dh = c.head_dim; dm.A = ex->A; dm.F = c.d_ffn; dm.n_layers = c.n_layers;
+  dm.n_out = c.n_out; dm.eps = c.rms_eps; dm.rope_base = c.rope_base; dm.head_kind = 0;
+  CacheView cv{};
+  cv.k = cache->k; cv.v = cache->v; cv.k_scale = cache->k_scale; cv.v_scale = cache->v_scale;
+  cv.cap = cache->capacity; cv.n_layers = cache->n_layers; cv.dtype = cache->dtype;
+  cv.H = cache->n_heads; cv.Dh = cache->head_dim;
+  cv.bs = (int64_t)cache->n_layers * cache->n_heads * cache->capacity * cache->head_dim;
+  cv.sbs = cache->n_layers * cache->n_heads;
+  if (cache->layout & FSX_CACHE_TOKEN_MAJOR) {
+    cv.hs = cache->head_dim;
+    cv.rs = (int64_t)cache->n_heads * cache->head_dim;
+  } else {
+    cv.hs = cache->capacity * cache->head_dim;
+    cv.rs = cache->head_dim;
+  }
+  // split plan of the attention over the cached rows (as the per-phase expert tick)
+  const int target = 2048;
+  const int64_t work = rows * dm.H * tp.n_tt;
+  int64_t cr = std::max<int64_t>(32, (((work + target - 1) / target + 31) / 32) * 32);
+  for (;;) {
+    int64_t slots = 0;
+    for (int b = 0; b < batch; ++b) slots += (tp.len[b] + cr - 1) / cr + 1;
+    if (slots * dm.H * tp.n_tt <= ex->items_max) {
+      tp.n_items = (int)(slots * dm.H * tp.n_tt);
+      break;
+    }
+    cr *= 2;
+  }
+  tp.chunk_rows = (int)cr;
+  tp.chunk_prefix[0] = 0;
+  for (int b = 0; b < batch; ++b) tp.chunk_prefix[b + 1] = tp.chunk_prefix[b] + (int)((tp.len[b] + cr - 1) / cr) + 1;
+  const int wpg = tp.n_items >= 1024 ? 4 : 1;
+  auto kspl = [](int KB) { return KB % 8 == 0 ? 8 : (KB % 4 == 0 ? 4 : (KB % 2 == 0 ? 2 : 1)); };
+  const int ks_o = kspl(dm.A / 32), ks_d = kspl(dm.F / 32);
+  HIP_TRY(launch_embed(tokens, c.dtype, ex->fw[0].attn_norm, tp, dm, ex->ws, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const FastWeights& w = ex->fw[l];
+    cv.layer = l;
+    HIP_TRY(launch_gemm_qkv(w, tp, dm, ex->ws, s));
+    HIP_TRY(launch_attention(cv, tp, dm, ex->ws, wpg, s, true));
+    HIP_TRY(launch_combine(tp, dm, ex->ws, s));
+    HIP_TRY(launch_write_rows(cv, ex->ws, batch, n_rows, first.data(), s));  // after the old rows were read
+    HIP_TRY(launch_gemm_o(w, tp, dm, ex->ws, ks_o, s));
+    HIP_TRY(launch_reduce_norm(tp, dm, ex->ws, ks_o, w.ffn_norm, nullptr, s));
+    HIP_TRY(launch_gemm_gu(w, tp, dm, ex->ws, s));
+    HIP_TRY(launch_gemm_down(w, tp, dm, ex->ws, ks_d, s));
+    const float* gnext = l + 1 < c.n_layers ? ex->fw[l + 1].attn_norm : ex->final_norm;
+    HIP_TRY(launch_reduce_norm(tp, dm, ex->ws, ks_d, gnext, hidden ? hidden + (int64_t)l * tp.M * dm.d : nullptr, s));
+  }
+  HIP_TRY(hipEventRecord(ex->done, s));
+  for (int b = 0; b < batch; ++b) {  // the ring state after the append, as fsx_cache_append_rows
+    const int64_t st = cache->len[b] > 0 ? cache->start[b] : first[b];
+    const int64_t nl = cache->len[b] + n_rows;
+    if (nl <= cache->capacity) {
+      cache->start[b] = st;
+      cache->len[b] = nl;
+    } else {
+      cache->start[b] = (st + (nl - cache->capacity)) % cache->capacity;
+      cache->len[b] = cache->capacity;
+    }
+    cache->pos[b] += n_rows;
+  }
+  g_err.clear();
+  return FSX_OK;
+}
+
+extern "C" int fsx_backbone_info(const fsx_backbone* bb, int64_t* weight_bytes, int64_t* workspace_bytes) {
+  if (!bb || !bb->ex) return fail(FSX_E_INVALID, "backbone handle is NULL");
+  if (weight_bytes) *weight_bytes = bb->ex->weight_bytes;
+  if (workspace_bytes) *workspace_bytes = bb->ex->ws_bytes;
+  return FSX_OK;
+}
+
+extern "C" void fsx_backbone_destroy(fsx_backbone* bb) {
+  if (!bb) return;
+  fsx_expert_destroy(bb->ex);
+  delete bb;
 }

@@ -50,15 +50,18 @@ __device__ __forceinline__ uint4 load8(const char* p) {
 }
 
 // rows i in [i0, i1) of one (agent, head): row i lives at base + slot(i) * row_bytes, where
-// slot(i) = (start + i) mod cap for a ring and i for the expert's own rows.
+// slot(i) = (start + i) mod cap for a ring and i for the expert's own rows.  The query of lane column c sees only
+// rows i <= qmax0 + c (a causal mask among new rows; pass a large qmax0 for none).
 // COH_ROWS: rows are read with device-coherent loads (rows produced inside the same launch);
 // COH_OUT: the partial is written with device-coherent stores (consumed inside the same launch).
 template <int KT, bool RING, bool COH_ROWS, bool COH_OUT>
 __device__ void attn_rows(const char* __restrict__ kbase, const char* __restrict__ vbase, int64_t row_bytes,
                           int64_t start, int64_t cap, int i0, int i1, const uint4 qf[4], float kscale, float vscale,
-                          int lane, float* __restrict__ out_o, float* __restrict__ out_ml, int Dh) {
+                          int lane, float* __restrict__ out_o, float* __restrict__ out_ml, int Dh,
+                          int qmax0 = 1 << 30) {
   constexpr int ES = KT == 0 ? 2 : 1;
   const int c = lane & 15, grp = lane >> 4;
+  const int qmax = qmax0 + c;
   auto roff = [&](int i) -> int64_t {
     int64_t slot = i;
     if (RING) {
@@ -101,7 +104,7 @@ __device__ void attn_rows(const char* __restrict__ kbase, const char* __restrict
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int rr = r0 + 16 * rt + 4 * grp + i;
-        const float v = rr < i1 ? s[rt][i] * kscale : -INFINITY;
+        const float v = rr < i1 && rr <= qmax ? s[rt][i] * kscale : -INFINITY;
         s[rt][i] = v;
         mx = fmaxf(mx, v);
       }

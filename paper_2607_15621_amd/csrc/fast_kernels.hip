@@ -305,6 +305,7 @@ struct AttnArgs {
   float* att_ml;
   uint16_t* attn_out;  // [M][A] bf16 (combine output)
   int H, Dh, A;
+  int causal;          // the own rows are masked causally (new token t sees own rows 0..t)
 };
 
 template <int KT>
@@ -331,7 +332,7 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a, TickParams tp) {
     load_q_frag<0, false>(a.q, qrow, tv, grp, qf);
     const int64_t off = ((int64_t)b * tp.S * a.A + (int64_t)h * a.Dh) * 2;
     attn_rows<0, false, false, false>((const char*)a.kself + off, (const char*)a.vself + off, (int64_t)a.A * 2, 0, 0, 0, tp.S, qf,
-                        1.f, 1.f, lane, out_o, out_ml, a.Dh);
+                        1.f, 1.f, lane, out_o, out_ml, a.Dh, a.causal ? tt * 16 : 1 << 30);
   } else {
     const int i0 = cidx * tp.chunk_rows;
     const int i1 = min(i0 + tp.chunk_rows, tp.len[b]);
@@ -351,10 +352,10 @@ __global__ __launch_bounds__(256) void k_attention(AttnArgs a, TickParams tp) {
 }
 
 hipError_t launch_attention(const CacheView& cv, const TickParams& tp, const Dims& dm, const Workspace& ws,
-                            int waves_per_wg, hipStream_t s) {
+                            int waves_per_wg, hipStream_t s, bool causal) {
   AttnArgs a{};
   a.cv = cv; a.q = ws.q; a.kself = ws.kself; a.vself = ws.vself; a.att_o = ws.att_o; a.att_ml = ws.att_ml;
-  a.H = dm.H; a.Dh = dm.Dh; a.A = dm.A;
+  a.H = dm.H; a.Dh = dm.Dh; a.A = dm.A; a.causal = causal ? 1 : 0;
   const dim3 grid((unsigned)((tp.n_items + waves_per_wg - 1) / waves_per_wg)), block(64 * waves_per_wg);
   if (cv.dtype == FSX_FP8_E4M3)
     hipLaunchKernelGGL(k_attention<1>, grid, block, 0, s, a, tp);
@@ -657,6 +658,63 @@ hipError_t launch_append_quantize(const fsx_cache_desc& c, const void* k_rows, c
   const int64_t total = (int64_t)a.B * a.n_layers * a.n_heads * a.n_rows * (a.head_dim / 8);
   if (total == 0) return hipSuccess;
   hipLaunchKernelGGL(k_append_quantize, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// The new tokens' rotated keys and values of one layer (kself / vself, bf16 [B*n][H*Dh]) written into that layer's
+// ring slots (first[b] + t) mod cap, bf16 copies or fp8 codes against the cache's scales.  Thread i handles 8
+// channels of one head row.
+struct RowsArgs {
+  CacheView cv;
+  const uint16_t* ks;
+  const uint16_t* vs;
+  int B, n;
+  int64_t first[FSX_MAX_BATCH];
+};
+
+__global__ __launch_bounds__(256) void k_write_rows(RowsArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cpr = a.cv.Dh / 8, A = a.cv.H * a.cv.Dh;
+  const int64_t total = (int64_t)a.B * a.n * a.cv.H * cpr;
+  if (i >= total) return;
+  const int ch = (int)(i % cpr);
+  int64_t r = i / cpr;
+  const int h = (int)(r % a.cv.H);
+  const int64_t m = r / a.cv.H;  // token row b * n + t
+  const int b = (int)(m / a.n), t = (int)(m % a.n);
+  int64_t slot = a.first[b] + t;
+  if (slot >= a.cv.cap) slot -= a.cv.cap;
+  const int64_t dst = cache_head_base(a.cv, b, a.cv.layer, h) + slot * a.cv.rs + 8 * ch;
+  const int64_t src = m * A + (int64_t)h * a.cv.Dh + 8 * ch;
+  const uint4 kv = *reinterpret_cast<const uint4*>(a.ks + src), vv = *reinterpret_cast<const uint4*>(a.vs + src);
+  if (a.cv.dtype == FSX_FP8_E4M3) {
+    const int64_t si = cache_scale_index(a.cv, b, a.cv.layer, h);
+    const float sk = a.cv.k_scale[si], sv = a.cv.v_scale[si];
+    const uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w}, vw[4] = {vv.x, vv.y, vv.z, vv.w};
+    uint32_t ck[2] = {0, 0}, cv[2] = {0, 0};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t kbits = e & 1 ? kw[e >> 1] & 0xFFFF0000u : kw[e >> 1] << 16;
+      const uint32_t vbits = e & 1 ? vw[e >> 1] & 0xFFFF0000u : vw[e >> 1] << 16;
+      ck[e >> 2] |= e4m3_encode(__uint_as_float(kbits), sk) << (8 * (e & 3));
+      cv[e >> 2] |= e4m3_encode(__uint_as_float(vbits), sv) << (8 * (e & 3));
+    }
+    *reinterpret_cast<uint2*>((uint8_t*)a.cv.k + dst) = make_uint2(ck[0], ck[1]);
+    *reinterpret_cast<uint2*>((uint8_t*)a.cv.v + dst) = make_uint2(cv[0], cv[1]);
+  } else {
+    *reinterpret_cast<uint4*>((uint16_t*)a.cv.k + dst) = kv;
+    *reinterpret_cast<uint4*>((uint16_t*)a.cv.v + dst) = vv;
+  }
+}
+
+hipError_t launch_write_rows(const CacheView& cv, const Workspace& ws, int B, int n, const int64_t* first,
+                             hipStream_t s) {
+  RowsArgs a{};
+  a.cv = cv; a.ks = ws.kself; a.vs = ws.vself; a.B = B; a.n = n;
+  for (int b = 0; b < B; ++b) a.first[b] = first[b];
+  const int64_t total = (int64_t)B * n * cv.H * (cv.Dh / 8);
+  if (total == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_write_rows, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

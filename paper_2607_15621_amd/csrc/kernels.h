@@ -97,7 +97,10 @@ hipError_t launch_embed(const void* tokens, int tok_dtype, const float* g0, cons
 hipError_t launch_gemm_qkv(const FastWeights& w, const TickParams& tp, const Dims& dm, const Workspace& ws,
                            hipStream_t s);
 hipError_t launch_attention(const CacheView& cv, const TickParams& tp, const Dims& dm, const Workspace& ws,
-                            int waves_per_wg, hipStream_t s);
+                            int waves_per_wg, hipStream_t s, bool causal = false);
+// The new rows of layer cv.layer (ws.kself / ws.vself, B agents x n tokens) into ring slots (first[b] + t) mod cap.
+hipError_t launch_write_rows(const CacheView& cv, const Workspace& ws, int B, int n, const int64_t* first,
+                             hipStream_t s);
 hipError_t launch_combine(const TickParams& tp, const Dims& dm, const Workspace& ws, hipStream_t s);
 hipError_t launch_gemm_o(const FastWeights& w, const TickParams& tp, const Dims& dm, const Workspace& ws,
                          int ksplit, hipStream_t s);

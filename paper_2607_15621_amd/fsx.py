@@ -29,7 +29,8 @@ SYMBOLS = ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "
            "fsx_expert_trace", "fsx_expert_destroy", "fsx_last_error", "fsx_expert_info", "fsx_version",
            "fsx_probe_hbm_read", "fsx_expert_forward_noalloc", "fsx_cache_append_rows_quantize",
            "fsx_loop_create", "fsx_loop_tick", "fsx_loop_append", "fsx_loop_sync", "fsx_loop_destroy",
-           "fsx_loop_last_error")
+           "fsx_loop_last_error", "fsx_backbone_create", "fsx_backbone_append", "fsx_backbone_info",
+           "fsx_backbone_destroy")
 
 
 class FsxError(RuntimeError):
@@ -54,6 +55,13 @@ class HeadWeights(ctypes.Structure):
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "attn_norm", "ffn_norm")]
+
+
+class BackboneCfg(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("max_new_rows", ctypes.c_int32),
+                ("max_batch", ctypes.c_int32), ("dtype", ctypes.c_int32), ("rope_base", ctypes.c_float),
+                ("rms_eps", ctypes.c_float)]
 
 
 class LoopTickInfo(ctypes.Structure):
@@ -107,6 +115,14 @@ def lib() -> ctypes.CDLL:
         L.fsx_loop_last_error.restype = ctypes.c_char_p
         for n in ("fsx_cache_append_rows_quantize", "fsx_loop_create", "fsx_loop_tick", "fsx_loop_append",
                   "fsx_loop_sync"):
+            getattr(L, n).restype = ctypes.c_int
+        L.fsx_backbone_create.argtypes = [ctypes.POINTER(BackboneCfg), ctypes.POINTER(LayerWeights), vp,
+                                          ctypes.POINTER(vp)]
+        L.fsx_backbone_append.argtypes = [vp, ctypes.POINTER(CacheDescC), vp, i32, i32, vp, i32, vp]
+        L.fsx_backbone_info.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(i64)]
+        L.fsx_backbone_destroy.argtypes = [vp]
+        L.fsx_backbone_destroy.restype = None
+        for n in ("fsx_backbone_create", "fsx_backbone_append", "fsx_backbone_info"):
             getattr(L, n).restype = ctypes.c_int
         for n in ("fsx_expert_create", "fsx_expert_forward", "fsx_cache_append_rows", "fsx_expert_info",
                   "fsx_expert_status", "fsx_expert_trace", "fsx_probe_hbm_read"):
@@ -301,6 +317,40 @@ class Loop:
     def close(self):
         if self.handle:
             lib().fsx_loop_destroy(ctypes.c_void_p(self.handle))
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Backbone:
+    """fsx_backbone: the backbone's incremental forward that produces the appended cache rows."""
+
+    def __init__(self, cfg: BackboneCfg, layers: Sequence[dict], stream=None):
+        arr = (LayerWeights * len(layers))()
+        for i, lw in enumerate(layers):
+            arr[i] = LayerWeights(*[_ptr(lw[n]) for n in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down",
+                                                            "attn_norm", "ffn_norm")])
+        out = ctypes.c_void_p(0)
+        _check(lib().fsx_backbone_create(ctypes.byref(cfg), arr, _stream(stream), ctypes.byref(out)))
+        self.handle, self.cfg = out.value, cfg
+
+    def append(self, cache: CacheDesc, tokens, batch: int, n_rows: int, hidden=None, policy: int = APPEND_RING,
+               stream=None):
+        _check(lib().fsx_backbone_append(ctypes.c_void_p(self.handle), ctypes.byref(cache.c), _ptr(tokens), batch,
+                                         n_rows, _ptr(hidden), policy, _stream(stream)))
+
+    def info(self):
+        wb, wsb = ctypes.c_int64(), ctypes.c_int64()
+        _check(lib().fsx_backbone_info(ctypes.c_void_p(self.handle), ctypes.byref(wb), ctypes.byref(wsb)))
+        return {"weight_bytes": wb.value, "workspace_bytes": wsb.value}
+
+    def close(self):
+        if self.handle:
+            lib().fsx_backbone_destroy(ctypes.c_void_p(self.handle))
             self.handle = 0
 
     def __del__(self):
