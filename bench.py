@@ -6,7 +6,8 @@ By default every full-size workload is timed in one run: the 40-frame single age
 4096-row history with 64 frame tokens, 16 batched agents with their 4-row append, and 8 ragged agents on an fp8
 cache; the one JSON line carries the headline workload's fields plus a `workloads` object with each workload's
 µs/tick, ticks/s, roofline fraction, HBM traffic and a variant with the 256 MB Infinity Cache flushed before every
-tick, an `append` object and the device's measured HBM read ceiling (`hbm_read_ceiling`).
+tick, an `append` object, the backbone's incremental forward that produces the appended rows at LLaMA-7B shapes
+(`backbone_append`) and the device's measured HBM read ceiling (`hbm_read_ceiling`).
 
 Measurement helpers (used by the commands recorded in profiles/):
     python bench.py --copy-calibration BYTES      plain device copies of BYTES (counter calibration)
@@ -349,6 +350,58 @@ def run_workload(name: str, steps: int, warmup: int, multi_launch: bool, cold_st
     return wl, r, extra
 
 
+def run_backbone(batches=(1, 16), n_new: int = 4, steps: int = 10, warmup: int = 2):
+    """The backbone's incremental forward (the producer of the appended rows) at LLaMA-7B shapes -- 32 layers, width
+    4096, 32 x 128 heads, SwiGLU 11008, synthetic weights N(0, 0.02^2) drawn on the GPU -- appending n_new tokens per
+    agent: one agent over a 224-row cache (the 40-frame history) and 16 agents over 1024-row caches (the batched
+    workload's append).  ms per append and the bandwidth of the bytes one call must read (packed weights + cached
+    rows)."""
+    import torch
+
+    from paper_2607_15621_amd import fsx
+
+    nl, d, H, Dh, F = 32, 4096, 32, 128, 11008
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2024)
+    bf = torch.bfloat16
+
+    def w(*shape):
+        return (torch.randn(shape, generator=g, device="cuda") * 0.02).to(bf)
+
+    layers = []
+    for _ in range(nl):
+        layers.append({"wq": w(H * Dh, d), "wk": w(H * Dh, d), "wv": w(H * Dh, d), "wo": w(d, H * Dh),
+                       "w_gate": w(F, d), "w_up": w(F, d), "w_down": w(d, F),
+                       "attn_norm": torch.ones(d, device="cuda"), "ffn_norm": torch.ones(d, device="cuda")})
+    cfg = fsx.BackboneCfg(nl, d, H, Dh, F, n_new, max(batches), fsx.BF16, 10000.0, 1e-6)
+    bb = fsx.Backbone(cfg, layers)
+    torch.cuda.synchronize()
+    del layers
+    torch.cuda.empty_cache()
+    wbytes = bb.info()["weight_bytes"]
+    stream = torch.cuda.current_stream()
+    out = {"model": "LLaMA-7B shapes (32 layers, d 4096, 32 x 128 heads, SwiGLU 11008), synthetic weights",
+           "new_tokens_per_agent": n_new, "weight_bytes": wbytes, "paper_ms_per_append_rtx3090ti": 21.1}
+    for B in batches:
+        L = 224 if B == 1 else 1024
+        cap = L + n_new
+        k = torch.randn((B, nl, H, cap, Dh), generator=g, device="cuda").to(bf)
+        v = torch.randn((B, nl, H, cap, Dh), generator=g, device="cuda").to(bf)
+        desc = fsx.CacheDesc(k, v, fsx.BF16, nl, H, Dh, cap, [L] * B)
+        tok = torch.randn((B, n_new, d), generator=g, device="cuda").to(bf)
+        torch.cuda.synchronize()
+        t = time_launches(lambda: bb.append(desc, tok, B, n_new, None, fsx.APPEND_RING, stream), stream, steps, warmup)
+        nbytes = wbytes + B * L * nl * 2 * H * Dh * 2
+        out[f"agents_{B}"] = {"cache_rows": L, "ms_per_append": round(t * 1e3, 3), "bytes_read": nbytes,
+                              "achieved_gbs": round(nbytes / t / 1e9, 1),
+                              "frac": round(nbytes / t / 1e9 / HBM_PEAK_GBS, 4)}
+        del k, v, desc, tok
+        torch.cuda.empty_cache()
+    bb.close()
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -359,6 +412,7 @@ def main():
     ap.add_argument("--cold-steps", type=int, default=10, help="ticks timed with the Infinity Cache flushed (0: none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-hbm-probe", action="store_true")
+    ap.add_argument("--no-backbone", action="store_true", help="skip the backbone's incremental forward")
     ap.add_argument("--multi-launch", action="store_true", help="one launch per phase instead of the tick kernel")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
     ap.add_argument("--summarize-trace", metavar="DIR")
@@ -408,6 +462,7 @@ def main():
     del flush_buf
     torch.cuda.empty_cache()
     ceiling = None if args.no_hbm_probe else hbm_ceiling(stream)
+    backbone = None if args.no_backbone else run_backbone()
     wl = head_wl
     h = results[names[0]]
     per_tick = h["us_per_tick"] / 1e6
@@ -439,6 +494,7 @@ def main():
                      "frac": h["frac"], "traffic": h["traffic"], "algorithmic_bytes_per_launch": h["algorithmic_bytes"]},
         "workloads": results,
         "append": append,
+        "backbone_append": backbone,
         "hbm_read_ceiling": ceiling,
     }
     if not args.no_cpu_baseline:
