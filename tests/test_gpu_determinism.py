@@ -1,0 +1,79 @@
+"""Run-to-run reproducibility of every forward path: the same inputs give bit-identical waypoints and per-layer
+hidden states on repeated launches.
+
+The tick kernel's work split depends only on the shapes (the XCD ranks and slots come from the hardware placement
+but every partial sum is taken in a fixed order), so any difference between two launches is a race: a value read
+before it was written, or an LDS tile read while it is being refilled.  A tolerance-based comparison with the
+oracle cannot see such races when they only perturb the last bits (near-uniform attention over random keys hides
+a wrong query row almost entirely), so these tests compare launches with each other, bit for bit.
+
+Cases: the many-query attention (64 frame tokens, five query tiles per agent) with one and with two heads per XCD,
+the single-query attention of 16 heads, the fp8 cache, and the per-phase launches and the generic path.
+"""
+
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from harness import Cache, Model, tokens_for
+from paper_2607_15621_amd import fsx
+
+pytestmark = pytest.mark.gpu
+
+REPS = 12
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def small(wid, n_frame, n_heads, cache_dtype="bf16"):
+    return synth.Workload(name=f"det{wid}", wid=wid, n_layers=2, d_model=128, n_heads=n_heads, head_dim=128,
+                          d_ffn=256, n_expert_tokens=10, n_frame_tokens=n_frame, batch=3, lengths=(300, 0, 77),
+                          dtype="bf16", cache_dtype=cache_dtype, capacity=320, rope_base=10000.0)
+
+
+def launch(ex, cache, tok, wl):
+    S = wl.n_expert_tokens + wl.n_frame_tokens
+    wp = torch.full((wl.batch, wl.n_out), float("nan"), device="cuda")
+    hid = torch.full((wl.n_layers, wl.batch, S, wl.d_model), float("nan"), device="cuda")
+    fsx.expert_forward(ex, cache.desc, tok, wl.batch, wl.n_frame_tokens, wp, hid)
+    torch.cuda.synchronize()
+    return wp.cpu().numpy(), hid.cpu().numpy()
+
+
+CASES = {
+    "many-query, 1 head per XCD": (dict(n_frame=64, n_heads=4), 0),
+    "many-query, 2 heads per XCD": (dict(n_frame=64, n_heads=16), 0),
+    "single-query, 16 heads": (dict(n_frame=0, n_heads=16), 0),
+    "many-query, fp8 cache": (dict(n_frame=64, n_heads=16, cache_dtype="fp8"), 0),
+    "per-phase launches": (dict(n_frame=64, n_heads=16), fsx.FLAG_MULTI_LAUNCH),
+    "generic path": (dict(n_frame=64, n_heads=4), fsx.FLAG_GENERIC),
+}
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_repeated_launches_are_bit_identical(case):
+    kw, flags = CASES[case]
+    wl = small(700 + sorted(CASES).index(case), **kw)
+    say(f"case determinism: {case}")
+    model = Model(wl)
+    cache = Cache(wl, starts=(100, 0, 310))
+    _, tok = tokens_for(wl)
+    ex = model.create(flags=flags)
+    wp0, h0 = launch(ex, cache, tok, wl)
+    assert np.isfinite(wp0).all() and np.isfinite(h0).all()
+    differ = []
+    for r in range(REPS):
+        wp, h = launch(ex, cache, tok, wl)
+        if not (np.array_equal(wp, wp0) and np.array_equal(h, h0)):
+            rows = np.nonzero((h != h0).any(axis=(0, 3)))
+            differ.append((r, sorted(set(zip(rows[0].tolist(), (rows[1] // 16).tolist())))[:6]))
+    ex.close()
+    assert not differ, f"launches differ from the first (run, [(agent, query tile)]): {differ}"
