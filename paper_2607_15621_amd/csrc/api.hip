@@ -277,7 +277,8 @@ static int create_impl(const fsx_expert_cfg* cfg, const fsx_layer_weights* layer
              {(void**)&ex->ws.part, (size_t)KSPLIT_MAX * M * d * 4},  // split factors are <= KSPLIT_MAX
              {(void**)&ex->ws.att_o, (size_t)ex->items_max * 16 * Dh * 4},
              {(void**)&ex->ws.att_ml, (size_t)ex->items_max * 32 * 4},
-             {(void**)&ex->ws.rope, (size_t)M * Dh * 4}};
+             {(void**)&ex->ws.rope, (size_t)M * Dh * 4},
+             {(void**)&ex->ws.ss, (size_t)M * (d / 512 + 1) * 4}};
   } else {
     parts = {{(void**)&ex->gws.h, (size_t)M * d * 4},   {(void**)&ex->gws.x, (size_t)M * d * 4},
              {(void**)&ex->gws.q, (size_t)M * A * 4},   {(void**)&ex->gws.k, (size_t)M * A * 4},

@@ -208,7 +208,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   const int KB = g.K / 32;
   const int kbs = KB / g.ksplit;
   const int kb0 = ks * kbs, kb1 = kb0 + kbs;
-  const uint4* wt = g.w + (int64_t)nt * KB * WAVE + lane;
+  const uint4* __restrict__ wt = g.w + (int64_t)nt * KB * WAVE + lane;
   const int n_mt = (g.M + 15) / 16;
   for (int mg = 0; mg < n_mt; mg += MT) {
     f32x4 acc[MT];
@@ -221,8 +221,26 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       ok[mt] = row < g.M;
       xr[mt] = g.x + (int64_t)(ok[mt] ? row : 0) * g.ldx + 8 * grp;
     }
-    for (int kb = kb0 + wave; kb < kb1; kb += 4) {
-      const uint4 wv = wt[(int64_t)kb * WAVE];
+    // Batches of U k-blocks of this wave: every weight block and x operand of the batch is loaded before the first
+    // MFMA, so U KiB of weights per wave are in flight (one at a time leaves the stream latency-bound).
+    constexpr int U = MT <= 1 ? 8 : (MT <= 2 ? 6 : (MT <= 4 ? 4 : 2));
+    int kb = kb0 + wave;
+    for (; kb + 4 * (U - 1) < kb1; kb += 4 * U) {
+      uint4 wv[U], xv[U][MT];
+#pragma unroll
+      for (int u = 0; u < U; ++u) wv[u] = ld_global(wt + (int64_t)(kb + 4 * u) * WAVE);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          xv[u][mt] = ok[mt] ? *reinterpret_cast<const uint4*>(xr[mt] + (kb + 4 * u) * 32) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[mt] = mfma_bf16(xv[u][mt], wv[u], acc[mt]);
+    }
+    for (; kb < kb1; kb += 4) {
+      const uint4 wv = ld_global(wt + (int64_t)kb * WAVE);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const uint4 xv = ok[mt] ? *reinterpret_cast<const uint4*>(xr[mt] + kb * 32) : make_uint4(0, 0, 0, 0);
@@ -434,8 +452,68 @@ __global__ __launch_bounds__(256) void k_reduce_norm(float* __restrict__ h, cons
   }
 }
 
+// Wide rows (the backbone's d = 4096 over a handful of tokens): one workgroup per row leaves the partial sums'
+// loads latency-bound on a few CUs, so the rows are cut into 512-column chunks, one workgroup each: h += sum of the
+// partials, the chunk's sum of squares to ss[m][chunk]; then one workgroup per row forms the row's scale and writes
+// the bf16 input of the next projection.
+__global__ __launch_bounds__(256) void k_reduce_chunks(float* __restrict__ h, const float* __restrict__ part,
+                                                       int M, int d, int ksplit, float* __restrict__ ss,
+                                                       float* __restrict__ hidden) {
+  __shared__ float red[16];
+  const int nch = d / RN_CHUNK, m = blockIdx.x / nch, ch = blockIdx.x % nch;
+  float acc[2] = {0.f, 0.f};
+  int64_t idx[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) idx[e] = (int64_t)m * d + ch * RN_CHUNK + threadIdx.x + 256 * e;
+  for (int s0 = 0; s0 < ksplit; s0 += 8) {
+    float v[8][2];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int e = 0; e < 2; ++e) v[j][e] = s0 + j < ksplit ? part[(int64_t)(s0 + j) * M * d + idx[e]] : 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int e = 0; e < 2; ++e) acc[e] += v[j][e];
+  }
+  float sq = 0.f;
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const float val = h[idx[e]] + acc[e];
+    h[idx[e]] = val;
+    if (hidden) hidden[idx[e]] = val;
+    sq += val * val;
+  }
+  sq = block_sum(sq, red);
+  if (threadIdx.x == 0) ss[(int64_t)m * nch + ch] = sq;
+}
+
+// Row m of a wide row set: r = 1 / sqrt(sum over chunks of ss[m][chunk] / d + eps) (chunks added in order), and
+// xb[m] = bf16(h[m] * r) (the norm's gain is folded into the next projection's weights).
+__global__ __launch_bounds__(256) void k_row_norm(const float* __restrict__ h, const float* __restrict__ ss,
+                                                  uint16_t* __restrict__ xb, int d, float eps) {
+  const int m = blockIdx.x, nch = d / RN_CHUNK;
+  float tot = 0.f;
+  for (int c = 0; c < nch; ++c) tot += ss[(int64_t)m * nch + c];
+  const float r = 1.0f / sqrtf(tot / (float)d + eps);
+  const float* hr = h + (int64_t)m * d;
+  uint16_t* xr = xb + (int64_t)m * d;
+  for (int c = 2 * threadIdx.x; c < d; c += 512) {
+    const float2 v = *reinterpret_cast<const float2*>(hr + c);
+    *reinterpret_cast<uint32_t*>(xr + c) = pack_bf16x2(v.x * r, v.y * r);
+  }
+}
+
 hipError_t launch_reduce_norm(const TickParams& tp, const Dims& dm, const Workspace& ws, int ksplit,
                               const float* gain, float* hidden_layer, hipStream_t s) {
+  if (wide_rows(dm)) {
+    const int nch = dm.d / RN_CHUNK;
+    hipLaunchKernelGGL(k_reduce_chunks, dim3(tp.M * nch), dim3(256), 0, s, ws.h, (const float*)ws.part, tp.M, dm.d,
+                       ksplit, ws.ss, hidden_layer);
+    hipLaunchKernelGGL(k_row_norm, dim3(tp.M), dim3(256), 0, s, (const float*)ws.h, (const float*)ws.ss, ws.xb, dm.d,
+                       dm.eps);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_reduce_norm, dim3(tp.M), dim3(256), 0, s, ws.h, (const float*)ws.part, ws.xb, tp.M, dm.d,
                      ksplit, gain, dm.eps, hidden_layer);
   return hipGetLastError();

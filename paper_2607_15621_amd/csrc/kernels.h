@@ -84,6 +84,7 @@ struct Workspace {
   float* att_o;      // [items][16][Dh] unnormalised partial attention outputs
   float* att_ml;     // [items][16][2] running max (log2 units) and sum
   float* rope;       // [M][Dh/2][2] cos, sin
+  float* ss;         // [M][d/512] per-chunk sums of squares (wide rows)
 };
 
 struct Dims {
@@ -91,6 +92,11 @@ struct Dims {
   float eps, rope_base;
   int head_kind;  // 0: mean over the expert tokens + linear; 1: two-layer head over the waypoint queries
 };
+
+// Rows wide enough (the backbone's width) that the per-phase reductions split them into chunks of RN_CHUNK columns,
+// one workgroup each, before a per-row normalisation.
+constexpr int RN_CHUNK = 512;
+__host__ __device__ inline bool wide_rows(const Dims& dm) { return dm.d >= 4 * RN_CHUNK && dm.d % RN_CHUNK == 0; }
 
 hipError_t launch_embed(const void* tokens, int tok_dtype, const float* g0, const TickParams& tp, const Dims& dm,
                         const Workspace& ws, hipStream_t s);
