@@ -322,26 +322,23 @@ static int create_impl(const fsx_expert_cfg* cfg, const fsx_layer_weights* layer
     auto r256 = [](size_t b) { return (b + 255) & ~(size_t)255; };
     const size_t rep_f = r256(Mp * d * 4), rep_b = r256(Mp * d * 2), rep_s = r256(dt * Ms * 4),
                  rep_r = r256((size_t)M * Dh * 4);
-    t.x_stride_f = (int64_t)(rep_f / 4);
-    t.x_stride_b = (int64_t)(rep_b / 2);
-    t.x_stride_s = (int64_t)(rep_s / 4);
     t.x_stride_r = (int64_t)(rep_r / 4);
     const size_t G = (size_t)ex->cu_count;
     // data first, then everything that must start at zero (flags, stamped words, registration, status)
     std::vector<std::pair<void**, size_t>> tp = {
-        {(void**)&t.hres, NXMAX * rep_f},
-        {(void**)&t.xb_mid, NXMAX * rep_b},
-        {(void**)&t.xb_out, NXMAX * rep_b},
-        {(void**)&t.ssq_mid, NXMAX * rep_s},
-        {(void**)&t.ssq_out, NXMAX * rep_s},
+        {(void**)&t.hres, rep_f},
+        {(void**)&t.xb_mid, rep_b},
+        {(void**)&t.xb_out, rep_b},
+        {(void**)&t.ssq_mid, rep_s},
+        {(void**)&t.ssq_out, rep_s},
         {(void**)&t.rope, NXMAX * rep_r},
         {(void**)&t.z, Mp * F * 2},
         {(void**)&t.po, NXMAX * dt * Mp * 16 * 8},
         {(void**)&t.pd, NXMAX * dt * Mp * 16 * 8},
         {(void**)&t.reg, G * 8},
         {(void**)&t.f_rope, (size_t)NXMAX * XFLAGS * FPAD * 8},
-        {(void**)&t.f_out, (size_t)NXMAX * XFLAGS * FPAD * 8},
-        {(void**)&t.f_mid, (size_t)NXMAX * XFLAGS * FPAD * 8},
+        {(void**)&t.f_out, (size_t)XFLAGS * FPAD * 8},
+        {(void**)&t.f_mid, (size_t)XFLAGS * FPAD * 8},
         {(void**)&t.f_q, (size_t)3 * A / 16 * FPAD * 8},
         {(void**)&t.f_attn, (size_t)nflag_attn * n_tt_max * FPAD * 8},
         {(void**)&t.f_rng, (size_t)ex->items_max * FPAD * 8},
@@ -463,21 +460,18 @@ size_t static_tick_layout(const fsx_expert* ex, const TickParams& tp, char* base
   const size_t items = (size_t)NXR * tp.slot_x * tp.n_tt;
   auto r256 = [](size_t b) { return (b + 255) & ~(size_t)255; };
   const size_t rep_f = r256(Mp * d * 4), rep_b = r256(Mp * d * 2), rep_s = r256(dt * Ms * 4), rep_r = r256(M * Dh * 4);
-  t.x_stride_f = (int64_t)(rep_f / 4);
-  t.x_stride_b = (int64_t)(rep_b / 2);
-  t.x_stride_s = (int64_t)(rep_s / 4);
   t.x_stride_r = (int64_t)(rep_r / 4);
   void* dummy;
   const std::pair<void**, size_t> parts[] = {
       {(void**)&t.q, M * A * 4},  {(void**)&t.kself, M * A * 2}, {(void**)&t.vself, M * A * 2},
       {(void**)&t.attn, M * A * 2}, {(void**)&t.att_o, items * 16 * Dh * 4}, {(void**)&t.att_ml, items * 32 * 4},
-      {(void**)&t.hres, NXS * rep_f}, {(void**)&t.xb_mid, NXS * rep_b}, {(void**)&t.xb_out, NXS * rep_b},
-      {(void**)&t.ssq_mid, NXS * rep_s}, {(void**)&t.ssq_out, NXS * rep_s}, {(void**)&t.rope, NXS * rep_r},
+      {(void**)&t.hres, rep_f}, {(void**)&t.xb_mid, rep_b}, {(void**)&t.xb_out, rep_b},
+      {(void**)&t.ssq_mid, rep_s}, {(void**)&t.ssq_out, rep_s}, {(void**)&t.rope, NXS * rep_r},
       {(void**)&t.z, Mp * F * 2},
       {&dummy, 0},  // start of the part that must start at zero
       {(void**)&t.po, NXS * dt * Mp * 16 * 8}, {(void**)&t.pd, NXS * dt * Mp * 16 * 8},
       {(void**)&t.reg, (size_t)ex->cu_count * 8}, {(void**)&t.f_rope, NXS * XFLAGS * FPAD * 8},
-      {(void**)&t.f_out, NXS * XFLAGS * FPAD * 8}, {(void**)&t.f_mid, NXS * XFLAGS * FPAD * 8},
+      {(void**)&t.f_out, XFLAGS * FPAD * 8}, {(void**)&t.f_mid, XFLAGS * FPAD * 8},
       {(void**)&t.f_q, 3 * A / 16 * FPAD * 8}, {(void**)&t.f_attn, (size_t)tp.B * c.n_heads * tp.n_tt * FPAD * 8},
       {(void**)&t.f_rng, items * FPAD * 8}, {(void**)&t.f_z, F / 8 * R * FPAD * 8}, {(void**)&t.status, 256}};
   size_t off = 0;
@@ -580,6 +574,9 @@ static int forward_impl(fsx_expert* ex, const fsx_cache_desc* cache, const void*
     const int G = ex->cu_count;
     tp.Mp = (tp.M + 7) / 8 * 8;
     tp.Ms = (tp.M + 31) / 32 * 32;
+    // row blocks per residual column tile: about one piece per workgroup, pieces of at least 16 rows (the pieces
+    // number at most G <= XFLAGS, the flag slots of f_out and f_mid)
+    tp.rblk = std::max(1, std::min(G / (dm.d / 16), (tp.M + 15) / 16));
     // Attention work (the kernel slices it): agents longest first; per head, agent b weighs its 32-row cache
     // tiles (at least one, for the expert's own rows)
     std::vector<int> ord(batch);

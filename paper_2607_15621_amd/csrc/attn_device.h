@@ -108,8 +108,7 @@ __device__ void attn_rows(const char* __restrict__ kbase, const char* __restrict
         s[rt][i] = v;
         mx = fmaxf(mx, v);
       }
-    mx = fmaxf(mx, shfl_xor(mx, 16));
-    mx = fmaxf(mx, shfl_xor(mx, 32));
+    mx = rows_max(mx);
     const float m_new = fmaxf(m_run, mx);
     const float alpha = exp2f(m_run - m_new);
     float p[8], ps = 0.f;
@@ -130,7 +129,7 @@ __device__ void attn_rows(const char* __restrict__ kbase, const char* __restrict
       pf = make_uint4(pack_f16x2(p[0], p[1]), pack_f16x2(p[2], p[3]), pack_f16x2(p[4], p[5]), pack_f16x2(p[6], p[7]));
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float a_i = shfl(alpha, 4 * grp + i);
+      const float a_i = col_pick(alpha, grp, i);
 #pragma unroll
       for (int k = 0; k < 8; ++k) o[k][i] *= a_i;
     }
@@ -139,8 +138,7 @@ __device__ void attn_rows(const char* __restrict__ kbase, const char* __restrict
 #pragma unroll
     for (int k = 0; k < 8; ++k) o[k] = KT == 0 ? mfma_bf16(pf, vt[k], o[k]) : mfma_f16(pf, vt[k], o[k]);
   }
-  float lt = l_run + shfl_xor(l_run, 16);
-  lt += shfl_xor(lt, 32);
+  const float lt = rows_sum(l_run);
   if (grp == 0) {
     stf<COH_OUT>(out_ml + c * 2 + 0, m_run);
     stf<COH_OUT>(out_ml + c * 2 + 1, lt);

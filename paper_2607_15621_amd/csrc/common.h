@@ -66,9 +66,10 @@ __device__ __forceinline__ f32x4 mfma_f16(uint4 a, uint4 b, f32x4 c) {
 }
 
 // ---------------------------------------------------------------- cross-lane helpers
-
-__device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v, m, WAVE); }
-__device__ __forceinline__ float shfl(float v, int src) { return __shfl(v, src, WAVE); }
+// No cross-lane move in these kernels goes through the LDS crossbar (ds_bpermute, ds_swizzle: what __shfl and
+// __shfl_xor compile to).  In a wave whose direct loads into LDS were still landing, such shuffles returned wrong
+// values now and then (the attention's running-max rescale gave launch-to-launch differences); DPP, the permlane
+// swaps and readlane do not use the LDS path.
 
 // Cross-lane moves without the LDS crossbar (DPP and the gfx950 permlane swaps):
 //   xor1(v)      value of lane l ^ 1 (quad_perm [1,0,3,2])
@@ -116,6 +117,17 @@ __device__ __forceinline__ float rows_sum(float v) {
   const unsigned mu = __builtin_bit_cast(unsigned, m);
   const auto b = __builtin_amdgcn_permlane32_swap(mu, mu, false, false);
   return __builtin_bit_cast(float, (unsigned)b[0]) + __builtin_bit_cast(float, (unsigned)b[1]);
+}
+// Sum over the 64 lanes, in every lane.
+__device__ __forceinline__ float wave_sum(float v) { return rows_sum(row_sum16(v)); }
+// For the lanes of 16-lane row grp: the value of lane 4 grp + i, where lanes 0..15 hold one value per column and
+// every row repeats them (a per-query running statistic); four lane reads selected by row.
+__device__ __forceinline__ float col_pick(float v, int grp, int i) {
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 4 + i));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 8 + i));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 12 + i));
+  return grp == 0 ? r0 : (grp == 1 ? r1 : (grp == 2 ? r2 : r3));
 }
 
 // Transpose an 8x8 block of 16-bit values held as 8 x uint4 (in[j] = row j, 8 columns) into
@@ -254,8 +266,7 @@ __device__ __forceinline__ void st16(void* p, uint4 v) {
 }
 
 __device__ __forceinline__ float block_sum(float v, float* scratch /* >= 16 floats */) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += shfl_xor(v, m);
+  v = wave_sum(v);
   const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
   const int nw = (blockDim.x + WAVE - 1) / WAVE;
   __syncthreads();

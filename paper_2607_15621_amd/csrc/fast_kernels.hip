@@ -156,7 +156,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x4 s, int ro
   } else if constexpr (EPI == EPI_SWIGLU) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float up = shfl_xor(s[i], 8);
+      const float up = xor8(s[i]);
       const int row = row0 + 4 * grp + i;
       if (c < 8 && row < g.M) {
         const float gt = s[i];
@@ -180,7 +180,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x4 s, int ro
       const int dch = c < 8 ? j : half + j;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float other = shfl_xor(s[i], 8);
+        const float other = xor8(s[i]);
         const int row = row0 + 4 * grp + i;
         const int rrow = row < g.M ? row : 0;
         const float cs = g.rope[((int64_t)rrow * half + j) * 2 + 0];
@@ -547,8 +547,7 @@ __global__ __launch_bounds__(256) void k_head(const float* __restrict__ h, int S
                                           : ((const float*)w)[(int64_t)o * d + n];
       acc += xm[n] * wv;
     }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) acc += shfl_xor(acc, m);
+    acc = wave_sum(acc);
     if (lane == 0) wp[(int64_t)b * n_out + o] = acc / (float)T;
   }
 }

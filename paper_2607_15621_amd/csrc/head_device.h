@@ -23,12 +23,6 @@ __device__ __forceinline__ float qh_weight(const void* w, int wdtype, int64_t i)
   return wdtype == FSX_BF16 ? bf16_to_f32(reinterpret_cast<const uint16_t*>(w)[i]) : reinterpret_cast<const float*>(w)[i];
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, WAVE);
-  return v;
-}
-
 // row(t, col): residual of expert token t (0 <= t < T), column col.  out(o, v) stores output o (2q + {0: x, 1: y}).
 // lds: nq * (d + hidden) floats.  Ends with a barrier; every thread of the workgroup must call it.
 template <typename Row, typename Out>

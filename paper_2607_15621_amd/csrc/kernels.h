@@ -28,6 +28,8 @@ struct TickParams {
   int32_t seg_w[FSX_MAX_BATCH];
   int32_t seg_p[FSX_MAX_BATCH + 1];
   int32_t slot_x;
+  // tick kernel: row blocks of every residual column tile in the cross-XCD reductions (pieces; see reduce_piece)
+  int32_t rblk;
 };
 
 // Cache view of one layer.  Element offset of (agent b, layer l, head h, ring slot j, channel c):
@@ -125,8 +127,8 @@ hipError_t launch_query_head(const float* h, const TickParams& tp, const Dims& d
 // ------------------------------------------------------------------ persistent tick kernel
 // The tick kernel splits every layer over the chip's XCDs the way a tensor-parallel layer is split over
 // devices: XCD X owns a contiguous range of heads and of FFN columns.  Buffers marked "per XCD" hold one
-// replica per XCD rank (at most NXMAX); the others are indexed by head or FFN unit, so each of their
-// cache lines is written and read by one XCD only.
+// replica per XCD rank (at most NXMAX); those indexed by head or FFN unit are written and read by one XCD only;
+// the residual and its bf16 copies are written once (each piece by one workgroup) and read by every XCD.
 constexpr int NXMAX = 16;
 constexpr int NXR = 8;      // XCDs the cross-XCD reductions read at most (the XCD count of gfx950 parts)
 constexpr int FPAD = 16;     // flags are 64-bit stamps, one per 128-byte line (index * FPAD)
@@ -144,17 +146,14 @@ struct TickArgs {
   float* waypoints;
   float* hidden;       // optional caller buffer [n_layers][M][d]
   uint64_t* reg;       // [grid] registration words: epoch << 8 | hardware XCD id
-  // per XCD
-  float* hres;         // residual stream, tile-major [d/16 column tiles][Mp rows][16 columns], each tile touched
-                       // only by its owner workgroup
+  // written by the owner of each piece, read by every XCD
+  float* hres;         // residual stream, tile-major [d/16 column tiles][Mp rows][16 columns]
   uint16_t* xb_mid;    // [Mp][d] bf16 copy of the residual after attention (input of the FFN)
   uint16_t* xb_out;    // [Mp][d] bf16 copy of the residual after the FFN (input of the next layer)
   float* ssq_mid;      // [d/16][Ms] per-tile sums of squares
   float* ssq_out;
+  // per XCD
   float* rope;         // [M][Dh/2][2] cos, sin
-  int64_t x_stride_f;  // floats between replicas of hres
-  int64_t x_stride_b;  // bf16 elements between replicas of xb_mid / xb_out
-  int64_t x_stride_s;  // floats between replicas of ssq_mid / ssq_out
   int64_t x_stride_r;  // floats between replicas of rope
   // by head / FFN unit
   float* q;            // [M][A] rotated, pre-scaled queries
@@ -169,8 +168,8 @@ struct TickArgs {
   uint64_t* pd;        // [NXMAX][d/16][Mp][16] down-projection partials
   // flags (stamps), each in its own 128-byte line: element [i] lives at f[i * FPAD]
   uint64_t* f_rope;    // [NXMAX][XFLAGS] by workgroup slot
-  uint64_t* f_out;     // [NXMAX][XFLAGS] by column tile
-  uint64_t* f_mid;     // [NXMAX][XFLAGS] by column tile
+  uint64_t* f_out;     // [XFLAGS] by residual piece (column tile * rblk + row block)
+  uint64_t* f_mid;     // [XFLAGS] by residual piece
   uint64_t* f_q;       // [3A/16]
   uint64_t* f_attn;    // [B*H][n_tt] per query tile
   uint64_t* f_rng;     // [slot] partial states written

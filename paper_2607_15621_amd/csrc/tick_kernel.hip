@@ -10,14 +10,16 @@
 //        others (log-sum-exp)
 //   O  : output projection restricted to X's heads: a partial sum over X's attention columns for each
 //        16-column tile of the residual
-//   R1 : reduction across XCDs: the owner of column tile i in EVERY XCD reads the 8 partials of tile i
-//        (stamped words, polled directly), adds them in a fixed order to its copy of the residual and
-//        publishes the bf16 tile and its sums of squares inside its XCD
+//   R1 : reduction across XCDs: column tile i of the residual belongs to one XCD, whose workgroups each
+//        take a block of its rows (a piece), read the 8 partials of the piece (stamped words, polled
+//        directly), add them in a fixed order to the residual and publish the piece's bf16 values and
+//        sums of squares to every XCD
 //   F1 : RMSNorm + gate/up projection with SwiGLU for X's FFN columns
 //   D  : down projection restricted to X's FFN columns (partials)
 //   R2 : reduction across XCDs as R1, giving the layer output
-// All exchanges except R1 and R2 stay inside an XCD.  Every XCD keeps a bit-identical replica of the
-// residual stream (same values, same summation order).  The head pools the first T tokens at the end.
+// All exchanges except R1 and R2 (and the residual they publish) stay inside an XCD.  Each residual element
+// is reduced once, in a fixed order, so every XCD reads the same values.  The head pools the first T tokens at
+// the end.
 //
 // Placement.  Each workgroup reads its hardware XCD id at the start of the tick and publishes it; from the
 // published ids every workgroup derives its XCD rank X, its slot s among that XCD's n workgroups, and the
@@ -233,7 +235,7 @@ __device__ __forceinline__ bool xcd_register(const TickArgs& a, TickLds& L) {
 #pragma unroll
       for (int e = 0; e < EPL; ++e)
         if (e == w / WAVE) sel = xc[e];
-      const uint32_t mine = (uint32_t)__shfl((int)sel, w % WAVE, WAVE);
+      const uint32_t mine = (uint32_t)__builtin_amdgcn_readlane((int)sel, w % WAVE);
       int X = 0, NX = 0, n = 0, s = 0, n0 = 0;
       for (uint32_t x = 0; x < 16; ++x) {
         int cnt = 0;
@@ -428,22 +430,31 @@ __device__ __forceinline__ void wave_gemm(const uint4 w[16], int mt_n, TickLds& 
 }
 
 // ------------------------------------------------------------------------------------------ reductions
-// Column tile i of the residual, in the owner workgroup of XCD X: h[m][i] += sum over XCDs x (fixed order)
-// of part[x][i][m][:], where part holds stamped words.  Thread t owns the elements e = t + 256 k (e = m*16 + c,
-// k < EB); all of its words are loaded before any is checked, then it polls its own stale words until their
-// stamps are right.  The new tile goes to hres (owner-private), to the row-major bf16 copy xb and the per-row
-// sums of squares ssq (read by the whole XCD), and, if given, to hidden; then the tile's flag is published.
-constexpr int EB = 5;  // element batches per pass: M <= 80 rows in one pass
-__device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, int i,
-                                            const uint64_t* part, uint16_t* xb, float* ssq, uint64_t* flag,
-                                            float* hidden_l, TickLds& L) {
-  const int M = tp.M, X = uni(L.X), NX = uni(L.NX), nt = dm.d / 16;
+// Pieces of the cross-XCD reductions: column tile i (16 columns) of the residual belongs to the XCD of rank X
+// with tile_lo(X) <= i < tile_lo(X + 1); its rows are cut into tp.rblk blocks, rows [piece_row(rb),
+// piece_row(rb + 1)).  Piece (i, rb) is the q-th of its XCD, q = (i - tile_lo(X)) * rblk + rb, and goes to the
+// workgroup of slot q mod n, in the embedding and in every reduction, so each residual element is always
+// updated by the same workgroup.  Its flag is f[(i * rblk + rb) * FPAD].
+__device__ __forceinline__ int tile_lo(int X, int NX, int nt) { return X * nt / NX; }
+__device__ __forceinline__ int piece_row(const TickParams& tp, int rb) { return rb * tp.M / tp.rblk; }
+
+// Piece (i, rb): h[m][i] += sum over XCDs x (fixed order) of part[x][i][m][:] for its rows m, where part holds
+// stamped words.  Thread t owns the elements e = e_lo + t + 256 k (e = m*16 + c, k < EB); all of its words are
+// loaded before any is checked, then it polls its own stale words until their stamps are right.  The new values
+// go to the residual hres, to the row-major bf16 copy xb and the per-row sums of squares ssq (device-scope
+// stores: every XCD reads them), and, if given, to hidden; then the piece's flag is published.
+constexpr int EB = 5;  // element batches per pass: 80 rows in one pass
+__device__ __forceinline__ bool reduce_piece(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, int i,
+                                             int rb, const uint64_t* part, uint16_t* xb, float* ssq, uint64_t* flag,
+                                             float* hidden_l, TickLds& L) {
+  const int NX = uni(L.NX), nt = dm.d / 16;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
   const uint32_t st32 = (uint32_t)st;
-  float* hres = a.hres + (int64_t)X * a.x_stride_f + (int64_t)i * tp.Mp * 16;
+  float* hres = a.hres + (int64_t)i * tp.Mp * 16;
   const int64_t xs = (int64_t)nt * tp.Mp * 16;  // words between the partials of two XCDs
+  const int e_lo = piece_row(tp, rb) * 16, e_hi = piece_row(tp, rb + 1) * 16;
   bool ok = true;
-  for (int e0 = 0; e0 < M * 16 && ok; e0 += EB * NTHR) {
+  for (int e0 = e_lo; e0 < e_hi && ok; e0 += EB * NTHR) {
     // Batch k is skipped as a whole when none of its elements exists; in a partial batch the threads past the
     // end load the last element (in bounds) and ignore it, so no load depends on a per-thread branch.  Words
     // are used only where use[k] bit x is set (x < NX and the element exists).
@@ -453,12 +464,12 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
 #pragma unroll
     for (int k = 0; k < EB; ++k) {
       const int e = e0 + k * NTHR + tix();
-      const uint64_t* src = part + (int64_t)i * tp.Mp * 16 + min(e, M * 16 - 1);
-      use[k] = e < M * 16 ? (1u << NX) - 1 : 0u;
-      if (e0 + k * NTHR < M * 16) {
+      const uint64_t* src = part + (int64_t)i * tp.Mp * 16 + min(e, e_hi - 1);
+      use[k] = e < e_hi ? (1u << NX) - 1 : 0u;
+      if (e0 + k * NTHR < e_hi) {
 #pragma unroll
         for (int x = 0; x < NXR; ++x) v[k][x] = ld_dev(src + (x < NX ? x : 0) * xs);
-        hold[k] = hres[min(e, M * 16 - 1)];
+        hold[k] = ld_dev_f(hres + min(e, e_hi - 1));
       } else {
 #pragma unroll
         for (int x = 0; x < NXR; ++x) v[k][x] = 0;
@@ -512,47 +523,50 @@ __device__ __forceinline__ bool reduce_tile(const TickArgs& a, const TickParams&
         if (use[k] & (1u << x)) acc += __uint_as_float((uint32_t)v[k][x]);
       const float hv = hold[k] + acc;
       if (in) {
-        hres[e] = hv;
+        st_dev_f(hres + e, hv);
         if (hidden_l) hidden_l[(int64_t)m * dm.d + i * 16 + c] = hv;
       }
       const float vn = xor1(hv);
       if (in && (c & 1) == 0)
-        st_loc(reinterpret_cast<uint32_t*>(xb + (int64_t)m * dm.d + i * 16 + c), pack_bf16x2(hv, vn));
+        st_dev(reinterpret_cast<uint32_t*>(xb + (int64_t)m * dm.d + i * 16 + c), pack_bf16x2(hv, vn));
       const float sq = row_sum16(hv * hv);
-      if (in && c == 0) st_loc_f(ssq + (int64_t)i * tp.Ms + m, sq);
+      if (in && c == 0) st_dev_f(ssq + (int64_t)i * tp.Ms + m, sq);
     }
   }
   stores_done();
   __syncthreads();
-  if (tix() == 0) st_loc(flag + (int64_t)i * FPAD, st);
+  if (tix() == 0) st_dev(flag + ((int64_t)i * tp.rblk + rb) * FPAD, st);
   return __syncthreads_and(ok);
 }
 
 // ------------------------------------------------------------------------------------------ embed
-// In every XCD: the owner of column tile i copies the tokens' tile into the residual, its bf16 copy and sums of
-// squares (the input of layer 0) and publishes it; rotary rows m = s, s + n, ... (fp64 angles) are written for
-// the XCD's own use.
+// The owner of each residual piece copies the tokens' values into the residual, its bf16 copy and sums of squares
+// (the input of layer 0) and publishes the piece; rotary rows m = s, s + n, ... (fp64 angles) are written in every
+// XCD for its own use.
 __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams& tp, const Dims& dm, TickLds& L) {
-  const int X = uni(L.X), s = uni(L.s), n = uni(L.n), d = dm.d, M = tp.M, half = dm.Dh / 2, nt = d / 16;
+  const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX), d = dm.d, M = tp.M, half = dm.Dh / 2;
+  const int nt = d / 16, t0 = tile_lo(X, NX, nt), t1 = tile_lo(X + 1, NX, nt);
   const uint64_t st = stamp_of(a, -1, dm.n_layers);
-  float* hres = a.hres + (int64_t)X * a.x_stride_f;
-  uint16_t* xb = a.xb_out + (int64_t)X * a.x_stride_b;
-  float* ssq = a.ssq_out + (int64_t)X * a.x_stride_s;
+  float* hres = a.hres;
+  uint16_t* xb = a.xb_out;
+  float* ssq = a.ssq_out;
   float* rope = a.rope + (int64_t)X * a.x_stride_r;
-  for (int i = s; i < nt; i += n) {
-    for (int e = tix(); e < M * 16; e += NTHR) {
+  for (int q = s; q < (t1 - t0) * tp.rblk; q += n) {
+    const int i = t0 + q / tp.rblk, rb = q % tp.rblk;
+    // whole rows of 16 elements per 16-lane group, so the neighbour and row-sum shuffles stay inside live lanes
+    for (int e = piece_row(tp, rb) * 16 + tix(); e < piece_row(tp, rb + 1) * 16; e += NTHR) {
       const int m = e >> 4, c = e & 15;
       const int64_t idx = (int64_t)m * d + i * 16 + c;
       const float v = a.tok_dtype == FSX_BF16 ? bf16_to_f32(((const uint16_t*)a.tokens)[idx]) : ((const float*)a.tokens)[idx];
-      hres[(int64_t)i * tp.Mp * 16 + e] = v;
+      st_dev_f(hres + (int64_t)i * tp.Mp * 16 + e, v);
       const float vn = xor1(v);
-      if ((c & 1) == 0) st_loc(reinterpret_cast<uint32_t*>(xb + (int64_t)m * d + i * 16 + c), pack_bf16x2(v, vn));
+      if ((c & 1) == 0) st_dev(reinterpret_cast<uint32_t*>(xb + (int64_t)m * d + i * 16 + c), pack_bf16x2(v, vn));
       const float sq = row_sum16(v * v);
-      if (c == 0) st_loc_f(ssq + (int64_t)i * tp.Ms + m, sq);
+      if (c == 0) st_dev_f(ssq + (int64_t)i * tp.Ms + m, sq);
     }
     stores_done();
     __syncthreads();
-    if (tix() == 0) st_loc(a.f_out + ((int64_t)X * XFLAGS + i) * FPAD, st);
+    if (tix() == 0) st_dev(a.f_out + ((int64_t)i * tp.rblk + rb) * FPAD, st);
   }
   for (int m = s; m < M; m += n) {
     const int b = m / tp.S, t = m % tp.S;
@@ -587,8 +601,8 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
   const LayerW W = layer_w(a, dm, l);
   const int KB = d / 32;
   const float qs = LOG2E / sqrtf((float)DH);
-  const uint16_t* xb = a.xb_out + (int64_t)X * a.x_stride_b;
-  const float* ssq = a.ssq_out + (int64_t)X * a.x_stride_s;
+  const uint16_t* xb = a.xb_out;
+  const float* ssq = a.ssq_out;
   const float* rope = a.rope + (int64_t)X * a.x_stride_r;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
   const int nseg = tp.B * nh, nq = n - nseg;  // attention workgroups, and the others
@@ -605,7 +619,7 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
     if (mine) load_unit_w_full(W.wqkv + (int64_t)tile * KB * WAVE, KB, w);
     if (!waited) {
       TICK_SUB(l, 0);
-      bool ok = wg_wait(a.f_out + (int64_t)X * XFLAGS * FPAD, nt, stamp_of(a, l - 1, dm.n_layers), a, L);
+      bool ok = wg_wait(a.f_out, nt * tp.rblk, stamp_of(a, l - 1, dm.n_layers), a, L);
       if (ok && l == 0) ok = wg_wait(a.f_rope + (int64_t)X * XFLAGS * FPAD, n, stamp_of(a, -1, dm.n_layers), a, L);
       if (!ok) return false;
       waited = true;
@@ -841,7 +855,7 @@ __device__ __forceinline__ void tile_jobs(const RawTile<KT>& t, QF qf, int r0, i
         m_run[j] = m_new;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float a_i = shfl(alpha, 4 * grp + i);
+          const float a_i = col_pick(alpha, grp, i);
 #pragma unroll
           for (int k = 0; k < 8; ++k) o[j][k][i] *= a_i;
         }
@@ -919,7 +933,7 @@ __device__ __forceinline__ void tile_pair_compute(const RawTile<KT>& ta, const R
     m_run = m_new;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float a_i = shfl(alpha, 4 * grp + i);
+      const float a_i = col_pick(alpha, grp, i);
 #pragma unroll
       for (int k = 0; k < 8; ++k) o[k][i] *= a_i;
     }
@@ -1242,12 +1256,11 @@ __device__ __forceinline__ void read_tile(const uint8_t* slot, const TileLanes<K
   else
     read_tile_fp8(slot, tl, t);
 }
-// Ring geometry: slots per tile, tiles the ring holds, direct-load instructions per tile.
+// Ring geometry: slots per tile, tiles the ring holds.
 template <int KT>
 struct RingOf {
   static constexpr int spt = KT == 0 ? 2 : 1;
   static constexpr int tiles = RSLOTS / spt;
-  static constexpr int loads = KT == 0 ? 16 : 8;
 };
 
 // The tiles of one unit for the agent's single query tile: wave w takes tiles w, w+4, ... of the unit's sequence,
@@ -1303,21 +1316,14 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
   const int tt_one[1] = {0};
   load_q<1, KT == 1>(a, tp, dm, U.b, U.h, tt_one, 1, qr);
   auto qf = [&](int, int k) -> uint4 { return qr[0][k]; };
-  // Pairs of tiles (i, i + 1) at ring places i % T, i % T + 1 (T = tiles the ring holds).  The memory operations
-  // issued after tile i + 1 are the direct loads of tiles i + 2 .. i + T - 1, so once at most that many loads are
-  // pending the pair has landed; once both are read into registers their places take tiles i + T and i + T + 1,
-  // which stream in while the pair is computed.  (An own-row tile has as many direct loads as a bf16 cache tile.)
-  static_assert(RG::tiles == 2 || RG::tiles == 4, "the waits below cover rings of two or four tiles");
+  // Pairs of tiles (i, i + 1) at ring places i % T, i % T + 1 (T = tiles the ring holds).  The pair is read once
+  // every direct load this wave has issued has landed (no LDS read of this wave runs while its own direct loads
+  // are in flight: reads in that window returned wrong values now and then); then the pair's places take tiles
+  // i + T and i + T + 1, which stream in while the pair is computed.
 #pragma unroll 1
   for (int i = 0; i < n; i += 2) {
     const bool two = i + 1 < n;
-    const int after = RG::tiles == 4 ? min(n - 2 - i, 2) : 0;  // tiles in flight behind the pair (when two)
-    if (two && after == 2)
-      vm_wait_below_c<2 * RG::loads>();
-    else if (two && after == 1)
-      vm_wait_below_c<RG::loads>();
-    else
-      vm_wait_all();
+    vm_wait_all();
     RawTile<TK> ta, tb;
     read_tile<TK>(slot_of(i), tl, ta);
     if (two) read_tile<TK>(slot_of(i + 1), tl, tb);
@@ -1349,18 +1355,6 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
   return true;
 }
 
-// Wait until at most `behind` tiles of LOADS direct loads each are pending (behind <= MAXB).
-template <int LOADS, int MAXB>
-__device__ __forceinline__ void vm_wait_tiles(int behind) {
-  if constexpr (MAXB == 0) {
-    vm_wait_all();
-  } else {
-    if (behind >= MAXB)
-      vm_wait_below_c<MAXB * LOADS>();
-    else
-      vm_wait_tiles<LOADS, MAXB - 1>(behind);
-  }
-}
 
 // One wave writes out a whole state from its LDS slots (rows [16][128], (m, l)[16]; see state_to_lds): lane l takes
 // row l / 4, channels 32 (l % 4) .. + 31; normalised into the attention output if the agent has one range, else as
@@ -1410,7 +1404,6 @@ template <int KT>
 struct WRingOf {
   static constexpr int tb = KT == 0 ? 2 * RSLOT : RSLOT;  // bytes of a staged tile
   static constexpr int tiles = 4 * RSLOTS * RSLOT / tb;    // 8 (bf16) or 16 (fp8)
-  static constexpr int loads = KT == 0 ? 4 : 2;           // direct loads of a thread per tile
   static constexpr int own = 4 * RSLOTS * RSLOT / (2 * RSLOT);  // bf16 own-row tiles the ring holds
 };
 template <int KT>
@@ -1478,15 +1471,17 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
   };
   // Groups of G tiles i .. i + G - 1: once they have landed and every wave is done with the previous group, that
   // group's places take tiles i + T - G .. i + T - 1.  A barrier per group of four (not per tile) lets the key-split
-  // jobs, which take one tile in four, even out within the group.
+  // jobs, which take one tile in four, even out within the group.  The group is read only once this wave's direct
+  // loads of the next one have landed too: no LDS read of a wave runs while its own direct loads are in flight
+  // (reads in that window returned wrong values now and then).
 #pragma unroll 1
   for (int i = 0; i < nc; i += G) {
-    // tiles issued: 0 .. min(i + T - G - 1, nc - 1); those after tile i + G - 1 (or the last) may stay in flight
-    vm_wait_tiles<WR::loads, WR::tiles - 2 * G>(max(0, min(WR::tiles - 2 * G, nc - G - i)));
+    vm_wait_all();  // this wave's loads of tiles i .. i + G - 1
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < G; ++e)
       if (i + WR::tiles - G + e < nc) stage(i + WR::tiles - G + e);
+    vm_wait_all();
 #pragma unroll 1
     for (int e = 0; e < G; ++e) {
       if (i + e < nc && act_of(i + e)) {
@@ -1559,9 +1554,10 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
 // queries and the first tiles, merging the waves' states) followed by one unit per 32-row cache tile (an agent with
 // no cached rows has one tile, for the expert's own rows).  With enough work every workgroup takes an equal run of
 // work units (slice); a segment whose tiles fall into several slices leaves one partial state per slice, merged
-// afterwards by separate items (agent, head, query tile) in a fixed order.  With little work (fewer than 16 tiles per
-// workgroup) and few segments, workgroup s takes segment s whole.  Equal slices keep every workgroup streaming until
-// the phase ends.
+// afterwards by separate items (agent, head, query tile) in a fixed order.  With little work (fewer than 4 tiles per
+// workgroup on average) and few segments, workgroup s takes segment s whole and the others compute the projections
+// (one agent of 32 heads: up to 1,023 cached rows).  Equal slices keep every workgroup streaming until the phase
+// ends; the threshold is where the two plans measured equal (one agent, 32 heads, 8 XCDs of 32 workgroups).
 // Many-query units weigh no extra start-up: every slice pays one (its queries, its first group of tiles), and without
 // the padding equal segments split into whole slices when the workgroups divide them evenly.
 constexpr int SEG_COST = 24;
@@ -1571,7 +1567,7 @@ __device__ __forceinline__ bool attn_plan(const TickArgs& a, const TickParams& t
   const int nh = head_lo(X + 1, NX, dm.H) - head_lo(X, NX, dm.H);
   const int nseg = tp.B * nh;  // <= NSEG = NTHR
   const int NT = nh * tp.seg_p[tp.B];  // cache (work) tiles
-  const int mode = NT < 16 * n && nseg <= n ? 1 : 0;
+  const int mode = NT < 4 * n && nseg <= n ? 1 : 0;
   const int SC = tp.n_tt > 1 ? SEG_COST_MQ : SEG_COST;
   const int NC = NT + nseg * SC;  // work units
   const int g = tix();
@@ -1747,9 +1743,9 @@ __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams&
     if (first) TICK_SUB(l, 6);
     first = false;
   }
-  for (int i = s; i < nt; i += n)
-    if (!reduce_tile(a, tp, dm, l, i, a.po, a.xb_mid + (int64_t)X * a.x_stride_b, a.ssq_mid + (int64_t)X * a.x_stride_s,
-                     a.f_mid + (int64_t)X * XFLAGS * FPAD, nullptr, L))
+  const int t0 = tile_lo(X, NX, nt), t1 = tile_lo(X + 1, NX, nt);
+  for (int q = s; q < (t1 - t0) * tp.rblk; q += n)
+    if (!reduce_piece(a, tp, dm, l, t0 + q / tp.rblk, q % tp.rblk, a.po, a.xb_mid, a.ssq_mid, a.f_mid, nullptr, L))
       return false;
   return true;
 }
@@ -1764,8 +1760,8 @@ __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams
   const int u0 = f0 / 8, nu = (f1 - f0) / 8;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
   const LayerW W = layer_w(a, dm, l);
-  const uint16_t* xb = a.xb_mid + (int64_t)X * a.x_stride_b;
-  const float* ssq = a.ssq_mid + (int64_t)X * a.x_stride_s;
+  const uint16_t* xb = a.xb_mid;
+  const float* ssq = a.ssq_mid;
   const int KB = d / 32;
   bool waited = false;
   int staged = -1;
@@ -1774,7 +1770,7 @@ __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams
     uint4 w[4];
     load_unit_w(W.wgu + (int64_t)u * KB * WAVE, 0, KB, w);
     if (!waited) {
-      if (!wg_wait(a.f_mid + (int64_t)X * XFLAGS * FPAD, nt, st, a, L)) return false;
+      if (!wg_wait(a.f_mid, nt * tp.rblk, st, a, L)) return false;
       waited = true;
       TICK_SUB(l, 7);
     }
@@ -1814,7 +1810,7 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
   const uint32_t st32 = (uint32_t)st;
   const LayerW W = layer_w(a, dm, l);
   uint64_t* pd = a.pd + (int64_t)X * nt * tp.Mp * 16;
-  float* hidden_l = (a.hidden && X == 0) ? a.hidden + (int64_t)l * M * d : nullptr;
+  float* hidden_l = a.hidden ? a.hidden + (int64_t)l * M * d : nullptr;
   bool waited = false;
   int staged = -1;
   for (int item = s; item < nt * R; item += n) {
@@ -1838,9 +1834,9 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
     });
     if (item == s) TICK_SUB(l, 10);
   }
-  for (int i = s; i < nt; i += n)
-    if (!reduce_tile(a, tp, dm, l, i, a.pd, a.xb_out + (int64_t)X * a.x_stride_b, a.ssq_out + (int64_t)X * a.x_stride_s,
-                     a.f_out + (int64_t)X * XFLAGS * FPAD, hidden_l, L))
+  const int t0 = tile_lo(X, NX, nt), t1 = tile_lo(X + 1, NX, nt);
+  for (int q = s; q < (t1 - t0) * tp.rblk; q += n)
+    if (!reduce_piece(a, tp, dm, l, t0 + q / tp.rblk, q % tp.rblk, a.pd, a.xb_out, a.ssq_out, a.f_out, hidden_l, L))
       return false;
   return true;
 }
@@ -1870,12 +1866,12 @@ __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& 
   if (uni(L.X) != 0) return;
   const int s = uni(L.s), n = uni(L.n0);
   for (int b = s; b < tp.B; b += n) {
-    ok = wg_wait(a.f_out, d / 16, stamp_of(a, nl - 1, nl), a, L);  // XCD rank 0's flags
+    ok = wg_wait(a.f_out, d / 16 * tp.rblk, stamp_of(a, nl - 1, nl), a, L);  // every piece of the last layer
     if (!ok) {
       poison_waypoints(a, tp, dm);
       return;
     }
-    const float* h = a.hres;  // replica of XCD rank 0, tile-major [d/16][Mp][16]
+    const float* h = a.hres;  // tile-major [d/16][Mp][16]
     if (dm.head_kind == 1) {
       query_head_wg([&](int t, int col) { return ld_dev_f(h + ((int64_t)(col >> 4) * tp.Mp + b * tp.S + t) * 16 + (col & 15)); },
                     T, dm.n_out / 2, d, dm.eps, a.final_norm, a.qhead,
@@ -1898,8 +1894,7 @@ __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& 
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
         float sq = v0[t] * v0[t] + v1[t] * v1[t];
-#pragma unroll
-        for (int m = 32; m >= 1; m >>= 1) sq += shfl_xor(sq, m);
+        sq = wave_sum(sq);
         if (lane == 0) L.red2[wave][t] = sq;
       }
       __syncthreads();
@@ -1929,8 +1924,7 @@ __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& 
                                                  : ((const float*)a.head_w)[(int64_t)o * d + c];
         acc += xm[c] * wv;
       }
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) acc += shfl_xor(acc, m);
+      acc = wave_sum(acc);
       if (lane == 0) st_dev_f(a.waypoints + (int64_t)b * dm.n_out + o, acc);
     }
     __syncthreads();
