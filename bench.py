@@ -402,6 +402,62 @@ def run_backbone(batches=(1, 16), n_new: int = 4, steps: int = 10, warmup: int =
     return out
 
 
+# Tick time across cache lengths (one agent) and agent counts (1,024 rows each) of the full-size expert, bf16 cache,
+# no frame tokens: the shapes of Sec. 4.4's latency discussion, at the history lengths the cache can hold.
+SWEEP_LENGTHS = (0, 224, 1024, 4096, 16384)
+SWEEP_BATCHES = (1, 4, 16, 32)
+
+
+def run_sweep(steps: int, warmup: int, out_md: str, command: str):
+    import torch
+
+    import synth
+    from gpu_inputs import Model, tokens_for
+    from paper_2607_15621_amd import fsx
+
+    points = [(1, L) for L in SWEEP_LENGTHS] + [(B, 1024) for B in SWEEP_BATCHES if B != 1]
+    rows = []
+    stream = torch.cuda.current_stream()
+    for i, (B, L) in enumerate(points):
+        wl = synth.Workload(name=f"sweep_B{B}_L{L}", wid=100 + i, n_frame_tokens=0, batch=B, lengths=(L,) * B,
+                            dtype="bf16", cache_dtype="bf16", capacity=max(L, 1), **synth.FULL)
+        model = Model(wl)
+        ex = model.create()
+        info = fsx.expert_info(ex)
+        desc, keep = gpu_cache(wl, seed=2000 + i)
+        _, tok = tokens_for(wl)
+        wp = torch.zeros(wl.batch, wl.n_out, device="cuda")
+        per_tick = time_launches(lambda: fsx.expert_forward(ex, desc, tok, B, 0, wp, None, stream), stream, steps,
+                                 warmup)
+        fsx.expert_status(ex, stream)
+        assert torch.isfinite(wp).all(), f"non-finite waypoints ({wl.name})"
+        nbytes = algorithmic_bytes(wl, info["weight_bytes"])
+        gbs = nbytes / per_tick / 1e9
+        rows.append({"agents": B, "cache_rows": L, "us_per_tick": round(per_tick * 1e6, 1),
+                     "agent_ticks_per_s": round(B / per_tick, 1), "algorithmic_mb": round(nbytes / 1e6, 1),
+                     "achieved_gbs": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)})
+        print(f"# sweep B={B} L={L}: {rows[-1]['us_per_tick']} us/tick, frac {rows[-1]['frac']}", file=sys.stderr,
+              flush=True)
+        ex.close()
+        del keep, desc
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    out = ["# Tick time across cache lengths and agent counts", "",
+           "Full-size expert (32 layers, width 512, 32 heads x 128, SwiGLU 2048, 10 expert tokens), bf16 weights "
+           "and cache, no frame tokens, seeded synthetic inputs; one persistent tick-kernel launch per tick, "
+           f"{steps} back-to-back launches timed with HIP events after {warmup} warm-up launches. `frac` is the "
+           "algorithmic bytes (weights once, every cached K/V row once) per tick over 8 TB/s.", "",
+           f"Command: `{command}`", "",
+           "| agents | cache rows per agent | µs/tick | agent-ticks/s | algorithmic MB | GB/s | frac |",
+           "|---:|---:|---:|---:|---:|---:|---:|"]
+    for r in rows:
+        out.append(f"| {r['agents']} | {r['cache_rows']} | {r['us_per_tick']} | {r['agent_ticks_per_s']} | "
+                   f"{r['algorithmic_mb']} | {r['achieved_gbs']} | {r['frac']} |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(out) + "\n")
+    print(json.dumps({"sweep": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -423,6 +479,8 @@ def main():
     ap.add_argument("--copy-bytes", type=int, default=0)
     ap.add_argument("--summarize-parity", metavar="JSONL", help="write profiles/parity_errors.md from the parity log")
     ap.add_argument("--command", action="append", default=[], help="command recorded in a summary")
+    ap.add_argument("--sweep", metavar="MD", help="time the tick across cache lengths and agent counts and write "
+                    "the table to MD")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -444,6 +502,11 @@ def main():
     import torch
 
     torch.cuda.set_device(0)
+    if args.sweep:
+        run_sweep(args.steps, args.warmup, args.sweep, " ".join(["python", "bench.py"] + sys.argv[1:]))
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        return
     stream = torch.cuda.current_stream()
     names = [n for n in args.workload.split(",") if n]
     flush_buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda") if args.cold_steps > 0 else None
