@@ -122,11 +122,13 @@ def copy_calibration(nbytes: int, reps: int = 5):
     print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
 
 
-def summarize_trace(d: str, workload: str, bench_line: str, command: str):
-    """profiles/tick_kernel_<workload>.md from a rocprofv3 --kernel-trace --stats directory."""
+def summarize_trace(d: str, workload: str, bench_line: str, command: str, name: str = ""):
+    """profiles/tick_kernel_<workload>.md (or profiles/<name>.md) from a rocprofv3 --kernel-trace --stats
+    directory."""
     rows = _csv_rows(d, "kernel_stats.csv")
     line = json.loads(open(bench_line).read().strip().splitlines()[-1])
-    out = [f"# Kernel trace: tick kernel, workload `{workload}`", "", "Command (from the repository root, on one MI355X):",
+    title = f"tick kernel, workload `{workload}`" if not name else f"`{name}` (bench.py run of workload `{workload}`)"
+    out = [f"# Kernel trace: {title}", "", "Command (from the repository root, on one MI355X):",
            "", "```", command, "```", "", "| kernel | calls | total ms | avg µs | min µs | max µs |",
            "|---|---|---|---|---|---|"]
     for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
@@ -136,7 +138,9 @@ def summarize_trace(d: str, workload: str, bench_line: str, command: str):
                 f"back-to-back ticks), {line['value']} agent-ticks/s, algorithmic bytes "
                 f"{line['roofline']['algorithmic_bytes_per_launch']:,} per launch, achieved "
                 f"{line['roofline']['achieved']} GB/s = {line['roofline']['frac']} of 8000 GB/s.", ""]
-    path = os.path.join(ROOT, "profiles", f"tick_kernel_{workload}.md")
+    if line.get("backbone_append"):
+        out += [f"Backbone incremental forward of the same run: {json.dumps(line['backbone_append'])}", ""]
+    path = os.path.join(ROOT, "profiles", f"{name}.md" if name else f"tick_kernel_{workload}.md")
     open(path, "w").write("\n".join(out))
     print(path)
 
@@ -197,7 +201,7 @@ def summarize_parity(log: str, command: str):
            f"{all(r['ok'] for r in rows)}.", "",
            "| test | comparisons | worst error | tolerance | measure |", "|---|---|---|---|---|"]
     for case, v in by.items():
-        w = max(v, key=lambda r: r["err"] / r["tol"])
+        w = max(v, key=lambda r: r["err"] / r["tol"] if r["tol"] > 0 else (0.0 if r["err"] == 0 else float("inf")))
         out.append(f"| `{case.split('::', 1)[-1]}` | {len(v)} | {w['err']:.2e} | {w['tol']:g} | {w['what'].replace('|', chr(92) + '|')} |")
     full = [r for r in rows if any(k in r["case"] for k in ("batched", "ragged", "full_", "maximum_batch"))]
     out += ["", "Every comparison of the full-size workloads (and of the 64-agent case):", "",
@@ -473,6 +477,7 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
     ap.add_argument("--summarize-trace", metavar="DIR")
     ap.add_argument("--bench-line", metavar="FILE")
+    ap.add_argument("--trace-name", default="", help="with --summarize-trace: write profiles/<NAME>.md")
     ap.add_argument("--summarize-traffic", nargs=4, metavar="DIR")
     ap.add_argument("--dram", action="store_true", help="with --summarize-traffic: the directories hold "
                     "TCC_EA0_RDREQ_DRAM_sum / TCC_EA0_WRREQ_DRAM_sum runs")
@@ -486,7 +491,7 @@ def main():
         copy_calibration(args.copy_calibration)
         return
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace, args.workload, args.bench_line, " && ".join(args.command))
+        summarize_trace(args.summarize_trace, args.workload, args.bench_line, " && ".join(args.command), args.trace_name)
         return
     if args.summarize_parity:
         summarize_parity(args.summarize_parity, " && ".join(args.command))
