@@ -278,7 +278,9 @@ static int create_impl(const fsx_expert_cfg* cfg, const fsx_layer_weights* layer
              {(void**)&ex->ws.att_o, (size_t)ex->items_max * 16 * Dh * 4},
              {(void**)&ex->ws.att_ml, (size_t)ex->items_max * 32 * 4},
              {(void**)&ex->ws.rope, (size_t)M * Dh * 4},
-             {(void**)&ex->ws.ss, (size_t)M * (d / 512 + 1) * 4}};
+             {(void**)&ex->ws.ss, (size_t)M * (d / 512 + 1) * 4},
+             {(void**)&ex->ws.rs, (size_t)M * 4},
+             {(void**)&ex->ws.rcnt, (size_t)M * 4}};
   } else {
     parts = {{(void**)&ex->gws.h, (size_t)M * d * 4},   {(void**)&ex->gws.x, (size_t)M * d * 4},
              {(void**)&ex->gws.q, (size_t)M * A * 4},   {(void**)&ex->gws.k, (size_t)M * A * 4},
@@ -355,6 +357,9 @@ static int create_impl(const fsx_expert_cfg* cfg, const fsx_layer_weights* layer
     *p.first = q;
     q += (p.second + 255) & ~(size_t)255;
   }
+  // the per-row chunk counters of the wide-row reductions start at zero (each reduction leaves them at zero)
+  if (ex->path == 0 && !ok(hipMemsetAsync(ex->ws.rcnt, 0, (size_t)M * 4, s), "hipMemsetAsync(row counters)"))
+    return cleanup(FSX_E_HIP);
   if (ex->tick) {
     // stamped words, flags, registration and status start at zero; stamps only grow
     TickArgs& t = ex->ta;
@@ -456,7 +461,7 @@ int scratch_of(int dev, void** out) {
 size_t static_tick_layout(const fsx_expert* ex, const TickParams& tp, char* base, TickArgs& t, size_t* zero_off) {
   const fsx_expert_cfg& c = ex->cfg;
   const size_t d = c.d_model, F = c.d_ffn, Dh = c.head_dim, A = ex->A, M = tp.M, Mp = tp.Mp, Ms = tp.Ms;
-  const size_t dt = d / 16, R = ((size_t)tp.M + 79) / 80, NXS = NXR;  // replicas: the tick path runs on <= NXR XCDs
+  const size_t dt = d / 16, R = ((size_t)tp.M + 79) / 80, NXS = NXR;  // per-XCD copies (rope, partials, registration): the tick path runs on <= NXR XCDs
   const size_t items = (size_t)NXR * tp.slot_x * tp.n_tt;
   auto r256 = [](size_t b) { return (b + 255) & ~(size_t)255; };
   const size_t rep_f = r256(Mp * d * 4), rep_b = r256(Mp * d * 2), rep_s = r256(dt * Ms * 4), rep_r = r256(M * Dh * 4);
@@ -629,7 +634,7 @@ static int forward_impl(fsx_expert* ex, const fsx_cache_desc* cache, const void*
   for (int l = 0; l < c.n_layers; ++l) {
     const FastWeights& w = ex->fw[l];
     cv.layer = l;
-    HIP_TRY(launch_gemm_qkv(w, tp, dm, ex->ws, s));
+    HIP_TRY(launch_gemm_qkv(w, tp, dm, ex->ws, s, l > 0));
     HIP_TRY(launch_attention(cv, tp, dm, ex->ws, wpg, s));
     HIP_TRY(launch_combine(tp, dm, ex->ws, s));
     HIP_TRY(launch_gemm_o(w, tp, dm, ex->ws, ks_o, s));
@@ -902,7 +907,7 @@ extern "C" int fsx_backbone_append(fsx_backbone* bb, fsx_cache_desc* cache, cons
   for (int l = 0; l < c.n_layers; ++l) {
     const FastWeights& w = ex->fw[l];
     cv.layer = l;
-    HIP_TRY(launch_gemm_qkv(w, tp, dm, ex->ws, s));
+    HIP_TRY(launch_gemm_qkv(w, tp, dm, ex->ws, s, l > 0));
     HIP_TRY(launch_attention(cv, tp, dm, ex->ws, wpg, s, true));
     HIP_TRY(launch_combine(tp, dm, ex->ws, s));
     HIP_TRY(launch_write_rows(cv, ex->ws, batch, n_rows, first.data(), s));  // after the old rows were read

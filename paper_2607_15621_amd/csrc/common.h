@@ -182,9 +182,6 @@ __device__ __forceinline__ float4 ld_dev_f4(const float* p) {
   const uint4 u = ld_dev16(p);
   return make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w));
 }
-__device__ __forceinline__ uint32_t atomic_add_dev(uint32_t* p, uint32_t v) {
-  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 // Wait until every vector memory operation this thread issued has completed (s_waitcnt vmcnt(0), GFX9
 // encoding).  Through the builtin, so the compiler knows those loads are complete and adds no later wait
 // for them; the empty asm statements keep memory accesses from moving across it.

@@ -142,6 +142,9 @@ struct GemmArgs {
   const float* rope; // [M][Dh/2][2]
   int A, Dh;
   float q_scale;
+  // optional RMSNorm scale of each row [M], applied to the products (wide rows: x then holds the unscaled residual
+  // in bf16; the gain is folded into the weights)
+  const float* rscale;
 };
 
 template <int EPI>
@@ -214,12 +217,18 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     f32x4 acc[MT];
     const uint16_t* xr[MT];
     bool ok[MT];
+    float rsc[MT][4];  // row scales of this lane's epilogue rows, loaded before the weight stream
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
       const int row = (mg + mt) * 16 + c;
       ok[mt] = row < g.M;
       xr[mt] = g.x + (int64_t)(ok[mt] ? row : 0) * g.ldx + 8 * grp;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int er = (mg + mt) * 16 + 4 * grp + i;
+        rsc[mt][i] = EPI != EPI_PARTIAL && g.rscale && er < g.M ? g.rscale[er] : 1.f;
+      }
     }
     // Batches of U k-blocks of this wave: every weight block and x operand of the batch is loaded before the first
     // MFMA, so U KiB of weights per wave are in flight (one at a time leaves the stream latency-bound).
@@ -250,8 +259,12 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) red[wave][mt][lane] = acc[mt];
     __syncthreads();
-    for (int mt = wave; mt < MT; mt += 4) {
-      const f32x4 s = red[0][mt][lane] + red[1][mt][lane] + red[2][mt][lane] + red[3][mt][lane];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      if (mt % 4 != wave) continue;
+      f32x4 s = red[0][mt][lane] + red[1][mt][lane] + red[2][mt][lane] + red[3][mt][lane];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s[i] *= rsc[mt][i];
       gemm_epilogue<EPI>(g, s, (mg + mt) * 16, nt, ks, c, grp);
     }
     __syncthreads();
@@ -277,10 +290,17 @@ static hipError_t gemm_dispatch(const GemmArgs& g, hipStream_t s) {
   return hipGetLastError();
 }
 
+// After a reduction of wide rows xb holds the unscaled residual and ws.rs each row's RMSNorm scale: the
+// projection applies the scales to its products.
+static void row_scale_from_chunks(GemmArgs& g, const Dims& dm, const Workspace& ws, bool after_reduction) {
+  if (after_reduction && wide_rows(dm)) g.rscale = ws.rs;
+}
+
 hipError_t launch_gemm_qkv(const FastWeights& w, const TickParams& tp, const Dims& dm, const Workspace& ws,
-                           hipStream_t s) {
+                           hipStream_t s, bool after_reduction) {
   GemmArgs g{};
   g.x = ws.xb; g.ldx = dm.d; g.w = w.wqkv; g.M = tp.M; g.K = dm.d; g.N = 3 * dm.A; g.ksplit = 1;
+  row_scale_from_chunks(g, dm, ws, after_reduction);
   g.out_f = ws.q; g.out_k = ws.kself; g.out_v = ws.vself; g.rope = ws.rope; g.A = dm.A; g.Dh = dm.Dh;
   g.q_scale = LOG2E / sqrtf((float)dm.Dh);
   return gemm_dispatch<EPI_QKV>(g, s);
@@ -299,6 +319,7 @@ hipError_t launch_gemm_gu(const FastWeights& w, const TickParams& tp, const Dims
   GemmArgs g{};
   g.x = ws.xb; g.ldx = dm.d; g.w = w.wgu; g.M = tp.M; g.K = dm.d; g.N = 2 * dm.F; g.ksplit = 1;
   g.out_z = ws.z;
+  row_scale_from_chunks(g, dm, ws, true);
   return gemm_dispatch<EPI_SWIGLU>(g, s);
 }
 
@@ -454,11 +475,14 @@ __global__ __launch_bounds__(256) void k_reduce_norm(float* __restrict__ h, cons
 
 // Wide rows (the backbone's d = 4096 over a handful of tokens): one workgroup per row leaves the partial sums'
 // loads latency-bound on a few CUs, so the rows are cut into 512-column chunks, one workgroup each: h += sum of the
-// partials, the chunk's sum of squares to ss[m][chunk]; then one workgroup per row forms the row's scale and writes
-// the bf16 input of the next projection.
+// partials, xb = bf16(h) unscaled, and the chunk's sum of squares to ss[m][chunk]; the last chunk of the row forms
+// the row's RMSNorm scale, which the next projection applies to its products, so no launch forms the normalised
+// input.
 __global__ __launch_bounds__(256) void k_reduce_chunks(float* __restrict__ h, const float* __restrict__ part,
                                                        int M, int d, int ksplit, float* __restrict__ ss,
-                                                       float* __restrict__ hidden) {
+                                                       uint16_t* __restrict__ xb, float* __restrict__ hidden,
+                                                       float* __restrict__ rs, uint32_t* __restrict__ rcnt,
+                                                       float eps) {
   __shared__ float red[16];
   const int nch = d / RN_CHUNK, m = blockIdx.x / nch, ch = blockIdx.x % nch;
   float acc[2] = {0.f, 0.f};
@@ -481,26 +505,22 @@ __global__ __launch_bounds__(256) void k_reduce_chunks(float* __restrict__ h, co
   for (int e = 0; e < 2; ++e) {
     const float val = h[idx[e]] + acc[e];
     h[idx[e]] = val;
+    xb[idx[e]] = f32_to_bf16(val);
     if (hidden) hidden[idx[e]] = val;
     sq += val * val;
   }
   sq = block_sum(sq, red);
-  if (threadIdx.x == 0) ss[(int64_t)m * nch + ch] = sq;
-}
-
-// Row m of a wide row set: r = 1 / sqrt(sum over chunks of ss[m][chunk] / d + eps) (chunks added in order), and
-// xb[m] = bf16(h[m] * r) (the norm's gain is folded into the next projection's weights).
-__global__ __launch_bounds__(256) void k_row_norm(const float* __restrict__ h, const float* __restrict__ ss,
-                                                  uint16_t* __restrict__ xb, int d, float eps) {
-  const int m = blockIdx.x, nch = d / RN_CHUNK;
-  float tot = 0.f;
-  for (int c = 0; c < nch; ++c) tot += ss[(int64_t)m * nch + c];
-  const float r = 1.0f / sqrtf(tot / (float)d + eps);
-  const float* hr = h + (int64_t)m * d;
-  uint16_t* xr = xb + (int64_t)m * d;
-  for (int c = 2 * threadIdx.x; c < d; c += 512) {
-    const float2 v = *reinterpret_cast<const float2*>(hr + c);
-    *reinterpret_cast<uint32_t*>(xr + c) = pack_bf16x2(v.x * r, v.y * r);
+  // the last chunk of row m to finish adds the chunk sums in chunk order and writes the row's scale; it then resets
+  // the row's counter for the next reduction (the next launch)
+  if (threadIdx.x == 0) {
+    st_dev_f(ss + (int64_t)m * nch + ch, sq);
+    const uint32_t done = __hip_atomic_fetch_add(rcnt + m, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    if (done == (uint32_t)(nch - 1)) {
+      float tot = 0.f;
+      for (int c = 0; c < nch; ++c) tot += ld_dev_f(ss + (int64_t)m * nch + c);
+      rs[m] = 1.0f / sqrtf(tot / (float)d + eps);
+      __hip_atomic_store(rcnt + m, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 
@@ -509,9 +529,7 @@ hipError_t launch_reduce_norm(const TickParams& tp, const Dims& dm, const Worksp
   if (wide_rows(dm)) {
     const int nch = dm.d / RN_CHUNK;
     hipLaunchKernelGGL(k_reduce_chunks, dim3(tp.M * nch), dim3(256), 0, s, ws.h, (const float*)ws.part, tp.M, dm.d,
-                       ksplit, ws.ss, hidden_layer);
-    hipLaunchKernelGGL(k_row_norm, dim3(tp.M), dim3(256), 0, s, (const float*)ws.h, (const float*)ws.ss, ws.xb, dm.d,
-                       dm.eps);
+                       ksplit, ws.ss, ws.xb, hidden_layer, ws.rs, ws.rcnt, dm.eps);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_reduce_norm, dim3(tp.M), dim3(256), 0, s, ws.h, (const float*)ws.part, ws.xb, tp.M, dm.d,

@@ -87,6 +87,8 @@ struct Workspace {
   float* att_ml;     // [items][16][2] running max (log2 units) and sum
   float* rope;       // [M][Dh/2][2] cos, sin
   float* ss;         // [M][d/512] per-chunk sums of squares (wide rows)
+  float* rs;         // [M] RMSNorm scale of each row (wide rows)
+  uint32_t* rcnt;    // [M] chunks of the row reduced so far (wide rows; zero between launches)
 };
 
 struct Dims {
@@ -96,14 +98,16 @@ struct Dims {
 };
 
 // Rows wide enough (the backbone's width) that the per-phase reductions split them into chunks of RN_CHUNK columns,
-// one workgroup each, before a per-row normalisation.
+// one workgroup each, and leave the RMSNorm scale to the next projection.
 constexpr int RN_CHUNK = 512;
 __host__ __device__ inline bool wide_rows(const Dims& dm) { return dm.d >= 4 * RN_CHUNK && dm.d % RN_CHUNK == 0; }
 
 hipError_t launch_embed(const void* tokens, int tok_dtype, const float* g0, const TickParams& tp, const Dims& dm,
                         const Workspace& ws, hipStream_t s);
+// after_reduction: xb comes from a reduction (not from the embedding); for wide rows it is then unscaled and the
+// projection applies the RMSNorm row scales from the chunk sums of squares.
 hipError_t launch_gemm_qkv(const FastWeights& w, const TickParams& tp, const Dims& dm, const Workspace& ws,
-                           hipStream_t s);
+                           hipStream_t s, bool after_reduction);
 hipError_t launch_attention(const CacheView& cv, const TickParams& tp, const Dims& dm, const Workspace& ws,
                             int waves_per_wg, hipStream_t s, bool causal = false);
 // The new rows of layer cv.layer (ws.kself / ws.vself, B agents x n tokens) into ring slots (first[b] + t) mod cap.

@@ -1843,8 +1843,8 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
 
 // ------------------------------------------------------------------------------------------ head
 // wp[b] = mean over t < T of RMSNorm(h[b][t]) * g_final, times W_head^T, on the workgroups of XCD rank 0
-// (agent b on slot b mod n0), from that XCD's replica of the residual.  Thread tid owns columns tid and
-// tid + 256 and holds the pooled rows in registers (16 rows per pass).
+// (agent b on slot b mod n0), from the residual once every piece of the last layer is published.  Thread tid
+// owns columns tid and tid + 256 and holds the pooled rows in registers (16 rows per pass).
 // Every workgroup that gave up (its failure is in the status word before it gets here) stores NaN into ALL
 // waypoints, after its status store has completed.  The head workgroups store valid waypoints, wait for those
 // stores, then read the status word and store NaN if a failure is recorded.  Either the head sees the failure, or
