@@ -909,8 +909,7 @@ extern "C" int fsx_backbone_append(fsx_backbone* bb, fsx_cache_desc* cache, cons
     cv.layer = l;
     HIP_TRY(launch_gemm_qkv(w, tp, dm, ex->ws, s, l > 0));
     HIP_TRY(launch_attention(cv, tp, dm, ex->ws, wpg, s, true));
-    HIP_TRY(launch_combine(tp, dm, ex->ws, s));
-    HIP_TRY(launch_write_rows(cv, ex->ws, batch, n_rows, first.data(), s));  // after the old rows were read
+    HIP_TRY(launch_combine(tp, dm, ex->ws, s, &cv));  // and the new rows, after the old ones were read
     HIP_TRY(launch_gemm_o(w, tp, dm, ex->ws, ks_o, s));
     HIP_TRY(launch_reduce_norm(tp, dm, ex->ws, ks_o, w.ffn_norm, nullptr, s));
     HIP_TRY(launch_gemm_gu(w, tp, dm, ex->ws, s));

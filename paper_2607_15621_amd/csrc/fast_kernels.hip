@@ -345,6 +345,7 @@ struct AttnArgs {
   uint16_t* attn_out;  // [M][A] bf16 (combine output)
   int H, Dh, A;
   int causal;          // the own rows are masked causally (new token t sees own rows 0..t)
+  int write_rows;      // combine launch: also store the new rows (kself/vself) into the cache rings (cv)
 };
 
 template <int KT>
@@ -404,7 +405,16 @@ hipError_t launch_attention(const CacheView& cv, const TickParams& tp, const Dim
 }
 
 // Log-sum-exp merge of the work items of one (agent, head, query tile), in item order.
+__device__ __forceinline__ void write_row_chunk(const CacheView& cv, const uint16_t* ks, const uint16_t* vs,
+                                                const TickParams& tp, int64_t i);
+
+// Workgroups past the B * H * n_tt merges (when a.write_rows is set) store the layer's new rows into the cache.
 __global__ __launch_bounds__(256) void k_combine(AttnArgs a, TickParams tp) {
+  const int n_merge = tp.B * a.H * tp.n_tt;
+  if ((int)blockIdx.x >= n_merge) {
+    write_row_chunk(a.cv, a.kself, a.vself, tp, (int64_t)(blockIdx.x - n_merge) * blockDim.x + threadIdx.x);
+    return;
+  }
   const int tt = blockIdx.x % tp.n_tt;
   const int rest = blockIdx.x / tp.n_tt;
   const int h = rest % a.H;
@@ -437,10 +447,19 @@ __global__ __launch_bounds__(256) void k_combine(AttnArgs a, TickParams tp) {
   }
 }
 
-hipError_t launch_combine(const TickParams& tp, const Dims& dm, const Workspace& ws, hipStream_t s) {
+hipError_t launch_combine(const TickParams& tp, const Dims& dm, const Workspace& ws, hipStream_t s,
+                          const CacheView* rows_into) {
   AttnArgs a{};
   a.att_o = ws.att_o; a.att_ml = ws.att_ml; a.attn_out = ws.attn; a.H = dm.H; a.Dh = dm.Dh; a.A = dm.A;
-  hipLaunchKernelGGL(k_combine, dim3((unsigned)(tp.B * dm.H * tp.n_tt)), dim3(256), 0, s, a, tp);
+  int64_t blocks = (int64_t)tp.B * dm.H * tp.n_tt;
+  if (rows_into) {
+    a.cv = *rows_into;
+    a.kself = ws.kself;
+    a.vself = ws.vself;
+    a.write_rows = 1;
+    blocks += ((int64_t)tp.B * tp.S * rows_into->H * (rows_into->Dh / 8) + 255) / 256;
+  }
+  hipLaunchKernelGGL(k_combine, dim3((unsigned)blocks), dim3(256), 0, s, a, tp);
   return hipGetLastError();
 }
 
@@ -759,58 +778,43 @@ hipError_t launch_append_quantize(const fsx_cache_desc& c, const void* k_rows, c
 // The new tokens' rotated keys and values of one layer (kself / vself, bf16 [B*n][H*Dh]) written into that layer's
 // ring slots (first[b] + t) mod cap, bf16 copies or fp8 codes against the cache's scales.  Thread i handles 8
 // channels of one head row.
-struct RowsArgs {
-  CacheView cv;
-  const uint16_t* ks;
-  const uint16_t* vs;
-  int B, n;
-  int64_t first[FSX_MAX_BATCH];
-};
-
-__global__ __launch_bounds__(256) void k_write_rows(RowsArgs a) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int cpr = a.cv.Dh / 8, A = a.cv.H * a.cv.Dh;
-  const int64_t total = (int64_t)a.B * a.n * a.cv.H * cpr;
+// Chunk i (8 elements) of the new rows [B][n][H][Dh] (kself/vself layout, row b * n + t) into ring slot
+// (start + len + t) mod capacity of (agent b, layer cv.layer, head h): a bf16 copy, or E4M3 codes with the cache's
+// per-(agent, layer, head) scales.  Runs after the attention that read the old rows (a full ring overwrites its
+// oldest rows).
+__device__ __forceinline__ void write_row_chunk(const CacheView& cv, const uint16_t* ks, const uint16_t* vs,
+                                                const TickParams& tp, int64_t i) {
+  const int cpr = cv.Dh / 8, A = cv.H * cv.Dh, n = tp.S;
+  const int64_t total = (int64_t)tp.B * n * cv.H * cpr;
   if (i >= total) return;
   const int ch = (int)(i % cpr);
   int64_t r = i / cpr;
-  const int h = (int)(r % a.cv.H);
-  const int64_t m = r / a.cv.H;  // token row b * n + t
-  const int b = (int)(m / a.n), t = (int)(m % a.n);
-  int64_t slot = a.first[b] + t;
-  if (slot >= a.cv.cap) slot -= a.cv.cap;
-  const int64_t dst = cache_head_base(a.cv, b, a.cv.layer, h) + slot * a.cv.rs + 8 * ch;
-  const int64_t src = m * A + (int64_t)h * a.cv.Dh + 8 * ch;
-  const uint4 kv = *reinterpret_cast<const uint4*>(a.ks + src), vv = *reinterpret_cast<const uint4*>(a.vs + src);
-  if (a.cv.dtype == FSX_FP8_E4M3) {
-    const int64_t si = cache_scale_index(a.cv, b, a.cv.layer, h);
-    const float sk = a.cv.k_scale[si], sv = a.cv.v_scale[si];
+  const int h = (int)(r % cv.H);
+  const int64_t m = r / cv.H;  // token row b * n + t
+  const int b = (int)(m / n), t = (int)(m % n);
+  int64_t slot = (tp.start[b] + tp.len[b]) % cv.cap + t;
+  if (slot >= cv.cap) slot -= cv.cap;
+  const int64_t dst = cache_head_base(cv, b, cv.layer, h) + slot * cv.rs + 8 * ch;
+  const int64_t src = m * A + (int64_t)h * cv.Dh + 8 * ch;
+  const uint4 kv = *reinterpret_cast<const uint4*>(ks + src), vv = *reinterpret_cast<const uint4*>(vs + src);
+  if (cv.dtype == FSX_FP8_E4M3) {
+    const int64_t si = cache_scale_index(cv, b, cv.layer, h);
+    const float sk = cv.k_scale[si], sv = cv.v_scale[si];
     const uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w}, vw[4] = {vv.x, vv.y, vv.z, vv.w};
-    uint32_t ck[2] = {0, 0}, cv[2] = {0, 0};
+    uint32_t ck[2] = {0, 0}, cvw[2] = {0, 0};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const uint32_t kbits = e & 1 ? kw[e >> 1] & 0xFFFF0000u : kw[e >> 1] << 16;
       const uint32_t vbits = e & 1 ? vw[e >> 1] & 0xFFFF0000u : vw[e >> 1] << 16;
       ck[e >> 2] |= e4m3_encode(__uint_as_float(kbits), sk) << (8 * (e & 3));
-      cv[e >> 2] |= e4m3_encode(__uint_as_float(vbits), sv) << (8 * (e & 3));
+      cvw[e >> 2] |= e4m3_encode(__uint_as_float(vbits), sv) << (8 * (e & 3));
     }
-    *reinterpret_cast<uint2*>((uint8_t*)a.cv.k + dst) = make_uint2(ck[0], ck[1]);
-    *reinterpret_cast<uint2*>((uint8_t*)a.cv.v + dst) = make_uint2(cv[0], cv[1]);
+    *reinterpret_cast<uint2*>((uint8_t*)cv.k + dst) = make_uint2(ck[0], ck[1]);
+    *reinterpret_cast<uint2*>((uint8_t*)cv.v + dst) = make_uint2(cvw[0], cvw[1]);
   } else {
-    *reinterpret_cast<uint4*>((uint16_t*)a.cv.k + dst) = kv;
-    *reinterpret_cast<uint4*>((uint16_t*)a.cv.v + dst) = vv;
+    *reinterpret_cast<uint4*>((uint16_t*)cv.k + dst) = kv;
+    *reinterpret_cast<uint4*>((uint16_t*)cv.v + dst) = vv;
   }
-}
-
-hipError_t launch_write_rows(const CacheView& cv, const Workspace& ws, int B, int n, const int64_t* first,
-                             hipStream_t s) {
-  RowsArgs a{};
-  a.cv = cv; a.ks = ws.kself; a.vs = ws.vself; a.B = B; a.n = n;
-  for (int b = 0; b < B; ++b) a.first[b] = first[b];
-  const int64_t total = (int64_t)B * n * cv.H * (cv.Dh / 8);
-  if (total == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_write_rows, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
-  return hipGetLastError();
 }
 
 hipError_t launch_append(const fsx_cache_desc& c, const void* k_rows, const void* v_rows, int n_rows,

@@ -110,10 +110,11 @@ hipError_t launch_gemm_qkv(const FastWeights& w, const TickParams& tp, const Dim
                            hipStream_t s, bool after_reduction);
 hipError_t launch_attention(const CacheView& cv, const TickParams& tp, const Dims& dm, const Workspace& ws,
                             int waves_per_wg, hipStream_t s, bool causal = false);
-// The new rows of layer cv.layer (ws.kself / ws.vself, B agents x n tokens) into ring slots (first[b] + t) mod cap.
-hipError_t launch_write_rows(const CacheView& cv, const Workspace& ws, int B, int n, const int64_t* first,
-                             hipStream_t s);
-hipError_t launch_combine(const TickParams& tp, const Dims& dm, const Workspace& ws, hipStream_t s);
+// Merges the attention's partial states; with rows_into, the same launch also stores the layer's new rows
+// (ws.kself / ws.vself, B agents x S tokens) into ring slots (start + len + t) mod capacity of cache layer
+// rows_into->layer (after the attention has read the old rows).
+hipError_t launch_combine(const TickParams& tp, const Dims& dm, const Workspace& ws, hipStream_t s,
+                          const CacheView* rows_into = nullptr);
 hipError_t launch_gemm_o(const FastWeights& w, const TickParams& tp, const Dims& dm, const Workspace& ws,
                          int ksplit, hipStream_t s);
 hipError_t launch_gemm_gu(const FastWeights& w, const TickParams& tp, const Dims& dm, const Workspace& ws,
