@@ -9,10 +9,15 @@ a wrong query row almost entirely), so these tests compare launches with each ot
 
 Cases: the many-query attention (64 frame tokens, five query tiles per agent) with one and with two heads per XCD,
 the single-query attention of 16 heads, the fp8 cache, and the per-phase launches and the generic path.
+
+The alternating-inputs test runs two token sets in turn on one handle and requires each launch to reproduce the
+first result of its own set, bit for bit: nothing a launch leaves in the workspace (flags, stamped words, partial
+states, activations) may leak into the next one.
 """
 
 from __future__ import annotations
 
+import dataclasses
 import sys
 
 import numpy as np
@@ -33,8 +38,8 @@ def say(*a):
     sys.stdout.flush()
 
 
-def small(wid, n_frame, n_heads, cache_dtype="bf16"):
-    return synth.Workload(name=f"det{wid}", wid=wid, n_layers=2, d_model=128, n_heads=n_heads, head_dim=128,
+def small(wid, n_frame, n_heads, cache_dtype="bf16", d_model=128):
+    return synth.Workload(name=f"det{wid}", wid=wid, n_layers=2, d_model=d_model, n_heads=n_heads, head_dim=128,
                           d_ffn=256, n_expert_tokens=10, n_frame_tokens=n_frame, batch=3, lengths=(300, 0, 77),
                           dtype="bf16", cache_dtype=cache_dtype, capacity=320, rope_base=10000.0)
 
@@ -49,6 +54,8 @@ def launch(ex, cache, tok, wl):
 
 
 CASES = {
+    "width 512, many-query": (dict(n_frame=64, n_heads=8, d_model=512), 0),
+    "width 512, single-query": (dict(n_frame=0, n_heads=8, d_model=512), 0),
     "many-query, 1 head per XCD": (dict(n_frame=64, n_heads=4), 0),
     "many-query, 2 heads per XCD": (dict(n_frame=64, n_heads=16), 0),
     "single-query, 16 heads": (dict(n_frame=0, n_heads=16), 0),
@@ -77,3 +84,23 @@ def test_repeated_launches_are_bit_identical(case):
             differ.append((r, sorted(set(zip(rows[0].tolist(), (rows[1] // 16).tolist())))[:6]))
     ex.close()
     assert not differ, f"launches differ from the first (run, [(agent, query tile)]): {differ}"
+
+
+@pytest.mark.parametrize("n_frame", [0, 64])
+def test_alternating_inputs_reproduce_their_results(n_frame):
+    wl = small(720 + n_frame, n_frame=n_frame, n_heads=8, d_model=512)
+    say(f"case alternating inputs: width 512, {n_frame} frame tokens")
+    model = Model(wl)
+    cache = Cache(wl, starts=(100, 0, 310))
+    toks = [tokens_for(wl)[1], tokens_for(dataclasses.replace(wl, wid=wl.wid + 1000))[1]]
+    ex = model.create()
+    first = [launch(ex, cache, toks[0], wl), launch(ex, cache, toks[1], wl)]
+    assert not np.array_equal(first[0][0], first[1][0]), "the two token sets give the same waypoints"
+    differ = []
+    for r in range(6):
+        for k in (0, 1):
+            wp, h = launch(ex, cache, toks[k], wl)
+            if not (np.array_equal(wp, first[k][0]) and np.array_equal(h, first[k][1])):
+                differ.append((r, k, int((h != first[k][1]).sum())))
+    ex.close()
+    assert not differ, f"launches differ from the first of their token set (run, set, elements): {differ}"
