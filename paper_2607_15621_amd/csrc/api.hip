@@ -583,7 +583,7 @@ static int forward_impl(fsx_expert* ex, const fsx_cache_desc* cache, const void*
     // number at most G <= XFLAGS, the flag slots of f_out and f_mid)
     tp.rblk = std::max(1, std::min(G / (dm.d / 16), (tp.M + 15) / 16));
     // Attention work (the kernel slices it): agents longest first; per head, agent b weighs its 32-row cache
-    // tiles (at least one, for the expert's own rows)
+    // tiles followed by the 32-row tiles of the expert's own rows
     std::vector<int> ord(batch);
     for (int b = 0; b < batch; ++b) ord[b] = b;
     std::stable_sort(ord.begin(), ord.end(), [&](int x, int y) { return tp.len[x] > tp.len[y]; });
@@ -591,7 +591,7 @@ static int forward_impl(fsx_expert* ex, const fsx_cache_desc* cache, const void*
     for (int k = 0; k < batch; ++k) {
       const int b = ord[k];
       tp.order[k] = b;
-      tp.seg_w[k] = std::max<int>(1, (int)((tp.len[b] + 31) / 32));
+      tp.seg_w[k] = (int)((tp.len[b] + 31) / 32) + (tp.S + 31) / 32;
       tp.seg_p[k + 1] = tp.seg_p[k] + tp.seg_w[k];
     }
     // partial-state slots per XCD: at most one per segment (<= 4 local heads per agent) plus one per slice boundary

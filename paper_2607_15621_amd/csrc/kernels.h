@@ -22,7 +22,8 @@ struct TickParams {
   int32_t len[FSX_MAX_BATCH];                 // valid cache rows
   int32_t chunk_prefix[FSX_MAX_BATCH + 1];    // per-phase path: chunk slots before agent b (ceil(len/chunk_rows) + 1 each)
   // tick kernel attention: agents in the order order[0..B-1]; the k-th weighs seg_w[k] work tiles per head
-  // (its 32-row cache tiles, at least 1), seg_p[k] = seg_w[0] + ... + seg_w[k-1]; partial-state slots of XCD X
+  // (its 32-row cache tiles, then the 32-row tiles of the expert's own rows), seg_p[k] = seg_w[0] + ... +
+  // seg_w[k-1]; partial-state slots of XCD X
   // are X * slot_x .. X * slot_x + slot_x - 1
   int32_t order[FSX_MAX_BATCH];
   int32_t seg_w[FSX_MAX_BATCH];

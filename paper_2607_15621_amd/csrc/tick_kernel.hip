@@ -1551,13 +1551,15 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
 
 // Attention work of XCD X: the segments (local head, agent) laid end to end, head-major (the short segments of
 // ragged agents then fall into different slices), each weighing SEG_COST work units for its start-up (loading the
-// queries and the first tiles, merging the waves' states) followed by one unit per 32-row cache tile (an agent with
-// no cached rows has one tile, for the expert's own rows).  With enough work every workgroup takes an equal run of
-// work units (slice); a segment whose tiles fall into several slices leaves one partial state per slice, merged
-// afterwards by separate items (agent, head, query tile) in a fixed order.  With little work (fewer than 4 tiles per
-// workgroup on average) and few segments, workgroup s takes segment s whole and the others compute the projections
-// (one agent of 32 heads: up to 1,023 cached rows).  Equal slices keep every workgroup streaming until the phase
-// ends; the threshold is where the two plans measured equal (one agent, 32 heads, 8 XCDs of 32 workgroups).
+// queries and the first tiles, merging the waves' states) followed by one unit per 32-row cache tile and one per
+// 32-row tile of the expert's own rows.  The slice that holds a segment's first own-row unit takes all its own rows
+// (a later slice that holds only own-row units of the segment leaves an empty partial).  With enough work every
+// workgroup takes an equal run of work units (slice); a segment whose tiles fall into several slices leaves one
+// partial state per slice, merged afterwards by separate items (agent, head, query tile) in a fixed order.  With
+// little work (fewer than about 4 cache tiles per workgroup) and few segments, workgroup s takes segment s whole and
+// the others compute the projections (one agent of 32 heads: up to 992 cached rows).  Equal slices keep every
+// workgroup streaming until the phase ends; the threshold is where the two plans measured equal (one agent, 32
+// heads, 8 XCDs of 32 workgroups).
 // Many-query units weigh no extra start-up: every slice pays one (its queries, its first group of tiles), and without
 // the padding equal segments split into whole slices when the workgroups divide them evenly.
 constexpr int SEG_COST = 24;
@@ -1566,8 +1568,8 @@ __device__ __forceinline__ bool attn_plan(const TickArgs& a, const TickParams& t
   const int X = uni(L.X), NX = uni(L.NX), n = uni(L.n);
   const int nh = head_lo(X + 1, NX, dm.H) - head_lo(X, NX, dm.H);
   const int nseg = tp.B * nh;  // <= NSEG = NTHR
-  const int NT = nh * tp.seg_p[tp.B];  // cache (work) tiles
-  const int mode = NT < 4 * n && nseg <= n ? 1 : 0;
+  const int NT = nh * tp.seg_p[tp.B];  // work tiles (cache and own rows)
+  const int mode = NT < 4 * n + nseg && nseg <= n ? 1 : 0;
   const int SC = tp.n_tt > 1 ? SEG_COST_MQ : SEG_COST;
   const int NC = NT + nseg * SC;  // work units
   const int g = tix();
@@ -1639,7 +1641,7 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
   bool first = true;
   for (; w0 < w1 && g < nseg && uni(L.seg0[g]) < w1; ++g) {
     const int g0 = uni(L.seg0[g]), g1 = g0 + uni(L.segw[g]);
-    const int t0 = max(w0, g0) - g0, t1 = min(w1, g1) - g0;  // the segment's tiles in this slice
+    const int t0 = max(w0, g0) - g0, t1 = min(w1, g1) - g0;  // the segment's units in this slice
     const int b = tp.order[g % B], h = h0 + g / B;
     const int npart = uni(L.np[g]);
     AUnit U;
@@ -1647,10 +1649,11 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
     U.h = h;
     U.final_out = npart == 1;
     U.slot = X * tp.slot_x + uni(L.pb[g]) + (mode == 1 ? 0 : s - uni(L.sf[g]));
-    U.i0 = 32 * t0;
-    U.i1 = min(32 * t1, tp.len[b]);
+    const int cu = (tp.len[b] + 31) / 32;  // the segment's cache units; units cu .. are its own rows
+    U.i0 = 32 * min(t0, cu);
+    U.i1 = min(32 * min(t1, cu), tp.len[b]);
     U.nct = U.i1 > U.i0 ? (U.i1 - U.i0 + 31) / 32 : 0;
-    U.nst = t1 == g1 - g0 ? (tp.S + 31) / 32 : 0;  // the segment's last slice also takes the expert's own rows
+    U.nst = t0 <= cu && cu < t1 ? (tp.S + 31) / 32 : 0;  // the slice with the first own-row unit takes them all
     const int64_t hb = cache_head_base(a.cv, b, l, h);  // ring slot 0 of (b, l, h)
     U.kc = (const char*)a.cv.k + hb * ES;
     U.vc = (const char*)a.cv.v + hb * ES;
