@@ -1389,17 +1389,20 @@ __device__ __forceinline__ void write_state_rows(const TickArgs& a, const TickPa
   }
 }
 
-// Many-query unit (query tiles tt0 .. tt0+nq-1, nq <= NQW = 6).  Every cache tile of the unit is staged once into a
-// workgroup ring of T tiles by direct loads (each wave issues its share of every tile), in groups of four, and the
-// waves split the arithmetic as jobs (query tile u, key class): a job takes the tiles i with i mod P = p.  The first
-// F = 4 query tiles (when nq >= 4) are one whole job each (wave w: tile w, P = 1); the R = nq - F others are split
-// by keys: one tile over all four waves (P = 4, p = w), or two tiles over two waves each (tile F + w/2, P = 2,
-// p = w mod 2), or, for R = 3 (then F = 0), both.  So a wave has at most two jobs, and within a group of four tiles
-// every wave does the same work.  At group step i a barrier follows this wave's wait for its share of tiles
-// i .. i + 3, so they have landed and every wave is done with the previous group.  The own rows follow through the
-// same ring, under the same key classes (own tile index j).  A whole job's state is written out by its wave; the
-// key-split tiles are merged through LDS, one query tile at a time.  Output: normalised if the agent has one range,
-// else the partial of this range.
+// Many-query unit (query tiles tt0 .. tt0+nq-1, nq <= NQW = 6).  Wave 3 is the unit's loader: it stages every tile
+// of the unit (cache tiles, then the own rows) into the workgroup ring of T tiles with direct loads, and never
+// reads the ring; waves 0-2 only read the ring and compute (no wave reads LDS while its own direct loads are in
+// flight: reads in that window returned wrong values now and then, so a wave that both loaded and computed could
+// not overlap the two).  The ring holds two steps of G = T / 2 tiles: while the compute waves work on step k, the
+// loader brings in step k + 1 and waits for it; a barrier then opens step k + 1 and frees step k's places.
+//
+// The compute waves split the arithmetic as jobs (query tile u, key class): a job takes the tiles i with
+// i mod P = p (P = 1: the whole tile).  Per nq, with at most two jobs per wave w (w < 3):
+//   1: tile 0, P = 3, p = w            2: tiles 0 and 1, P = 3, p = w        3: tile w whole
+//   4: tile w whole; tile 3, P = 3, p = w                                    6: tiles w and w + 3 whole
+//   5: tile w whole; tile 3, P = 2, p = w for w < 2; tile 4 whole for w = 2
+// A whole job's state is written out by its wave; the key-split tiles are merged through LDS, one query tile at a
+// time.  Output: normalised if the agent has one range, else the partial of this range.
 template <int KT>
 struct WRingOf {
   static constexpr int tb = KT == 0 ? 2 * RSLOT : RSLOT;  // bytes of a staged tile
@@ -1412,38 +1415,54 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
   using WR = WRingOf<KT>;
   constexpr int TK = KT;  // tile kind of the cache tiles
   constexpr int OK = 0;   // tile kind of the own rows (bf16)
-  const int wave = tix() >> 6, lane = tix() & 63, c16 = lane & 15, grp = lane >> 4;
+  constexpr int G = WR::tiles / 2;  // tiles per step
+  const int wave = tix() >> 6;
+  const bool loader = wave == 3;
   const uint64_t st = stamp_of(a, l, dm.n_layers);
   const int nc = U.nct;
-  // this wave's jobs: query tile ju[j] (relative to tt0), key class (jp[j] = P - 1 as a mask, jk[j] = p)
-  const int F = nq >= 4 ? 4 : 0, R = nq - F;
-  int nj = 0, ju[2] = {0, 0}, jp[2] = {0, 0}, jk[2] = {0, 0};
+  // this wave's jobs: query tile ju[j] (relative to tt0), key class p = jk[j] of jP[j]
+  int nj = 0, ju[2] = {0, 0}, jP[2] = {1, 1}, jk[2] = {0, 0};
   auto add_job = [&](int u, int P, int pk) {
     ju[nj] = u;
-    jp[nj] = P - 1;
+    jP[nj] = P;
     jk[nj] = pk;
     ++nj;
   };
-  if (F) add_job(wave, 1, 0);
-  if (R == 1) add_job(F, 4, wave);
-  if (R >= 2) add_job(F + (wave >> 1), 2, wave & 1);
-  if (R == 3) add_job(F + 2, 4, wave);
-  auto act_of = [&](int i) { return (nj > 0 && (i & jp[0]) == jk[0] ? 1 : 0) | (nj > 1 && (i & jp[1]) == jk[1] ? 2 : 0); };
+  if (!loader) {
+    if (nq <= 2) {
+      add_job(0, 3, wave);
+      if (nq == 2) add_job(1, 3, wave);
+    } else if (nq == 5) {
+      add_job(wave, 1, 0);
+      if (wave < 2) add_job(3, 2, wave);
+      else add_job(4, 1, 0);
+    } else {
+      add_job(wave, 1, 0);
+      if (nq == 4) add_job(3, 3, wave);
+      if (nq == 6) add_job(wave + 3, 1, 0);
+    }
+  }
+  // the key-split query tiles [s_lo, s_hi)
+  const int s_lo = nq <= 2 ? 0 : 3, s_hi = nq <= 2 ? nq : (nq == 4 || nq == 5 ? 4 : 3);
+  auto act_of = [&](int i) {
+    return (nj > 0 && (jP[0] == 1 || i % jP[0] == jk[0]) ? 1 : 0) | (nj > 1 && (jP[1] == 1 || i % jP[1] == jk[1]) ? 2 : 0);
+  };
   uint8_t* base = &L.u.a.ring[0][0][0];
   auto place = [&](int i) { return base + (i % WR::tiles) * WR::tb; };
-  auto stage = [&](int i) {
+  auto stage = [&](int i) {  // the loader's loads of cache tile i
     if constexpr (KT == 0)
-      stage_tile_bf16<2>(U.kc, U.vc, U.rsb, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * i, U.i1, place(i), 2 * wave);
+      stage_tile_bf16<8>(U.kc, U.vc, U.rsb, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * i, U.i1, place(i), 0);
     else
-      stage_tile_fp8<1>(U.kc, U.vc, U.rsb, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * i, U.i1, place(i), wave);
+      stage_tile_fp8<4>(U.kc, U.vc, U.rsb, tp.start[U.b], a.cv.cap, U.i0, U.i0 + 32 * i, U.i1, place(i), 0);
   };
-  constexpr int G = 4;  // tiles per barrier step
-  auto prefetch = [&]() {
-    for (int i = 0; i < WR::tiles - G && i < nc; ++i) stage(i);
-  };
-  if (wave < 3) prefetch();
-  if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16, 3)) return false;
-  if (wave == 3) prefetch();
+  // The first step's tiles do not depend on this layer's projections: the loader issues them before the wait, and
+  // wave 0 (no loads in flight) polls the q, k and v column tiles of this head.
+  if (loader)
+    for (int i = 0; i < G && i < nc; ++i) stage(i);
+  if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16, 0)) {
+    vm_wait_all();
+    return false;
+  }
   f32x4 o[2][8];
   float m_run[2], l_run[2];
 #pragma unroll
@@ -1456,7 +1475,7 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
   const int tts[2] = {tt0 + ju[0], tt0 + ju[1]};
   uint4 qr[2][4];
   const TileLanes<TK> tl = tile_lanes<TK>();
-  load_q<2, KT == 1>(a, tp, dm, U.b, U.h, tts, nj, qr);
+  if (!loader) load_q<2, KT == 1>(a, tp, dm, U.b, U.h, tts, nj, qr);
   auto qf = [&](int j, int k) -> uint4 { return qr[j][k]; };
   // one step of the online softmax for the jobs that take tile i (index in its sequence)
   auto update = [&](auto kind, const auto& t, int i, int r0, int i1, float ksc) {
@@ -1469,28 +1488,25 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
     else if (act == 2)
       tile_jobs<K, 2, 2>(t, qf, r0, i1, ksc, o, m_run, l_run);
   };
-  // Groups of G tiles i .. i + G - 1: once they have landed and every wave is done with the previous group, that
-  // group's places take tiles i + T - G .. i + T - 1.  A barrier per group of four (not per tile) lets the key-split
-  // jobs, which take one tile in four, even out within the group.  The group is read only once this wave's direct
-  // loads of the next one have landed too: no LDS read of a wave runs while its own direct loads are in flight
-  // (reads in that window returned wrong values now and then).
 #pragma unroll 1
   for (int i = 0; i < nc; i += G) {
-    vm_wait_all();  // this wave's loads of tiles i .. i + G - 1
-    __syncthreads();
-#pragma unroll
-    for (int e = 0; e < G; ++e)
-      if (i + WR::tiles - G + e < nc) stage(i + WR::tiles - G + e);
-    vm_wait_all();
+    if (loader) vm_wait_all();  // tiles i .. i + G - 1 have landed
+    __syncthreads();            // and every compute wave is done with tiles i - G .. i - 1
+    if (loader) {
+      for (int e = 0; e < G; ++e)
+        if (i + G + e < nc) stage(i + G + e);
+    } else {
 #pragma unroll 1
-    for (int e = 0; e < G; ++e) {
-      if (i + e < nc && act_of(i + e)) {
-        RawTile<TK> t;
-        read_tile<TK>(place(i + e), tl, t);
-        update(std::integral_constant<int, TK>(), t, i + e, U.i0 + 32 * (i + e), U.i1, U.ksc);
+      for (int e = 0; e < G; ++e) {
+        if (i + e < nc && act_of(i + e)) {
+          RawTile<TK> t;
+          read_tile<TK>(place(i + e), tl, t);
+          update(std::integral_constant<int, TK>(), t, i + e, U.i0 + 32 * (i + e), U.i1, U.ksc);
+        }
       }
     }
   }
+  if (loader) vm_wait_all();
   if (KT == 1) {
     // fp8 values carry their scale: apply it to the cache part of the output before the own rows join
 #pragma unroll
@@ -1502,40 +1518,48 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
   for (int j0 = 0; j0 < U.nst; j0 += WR::own) {
     const int nown = min(WR::own, U.nst - j0);
     __syncthreads();  // every wave is done with the ring
-    for (int j = 0; j < nown; ++j)
-      stage_own_tile<2>(U.ks, U.vs, (int64_t)dm.A * 2, 32 * (j0 + j), tp.S, base + j * 2 * RSLOT, 2 * wave);
-    if (KT == 1 && j0 == 0) load_q<2, false>(a, tp, dm, U.b, U.h, tts, nj, qr);  // the queries as bf16
-    vm_wait_all();
+    if (loader) {
+      for (int j = 0; j < nown; ++j)
+        stage_own_tile<8>(U.ks, U.vs, (int64_t)dm.A * 2, 32 * (j0 + j), tp.S, base + j * 2 * RSLOT, 0);
+      vm_wait_all();
+    } else if (KT == 1 && j0 == 0) {
+      load_q<2, false>(a, tp, dm, U.b, U.h, tts, nj, qr);  // the queries as bf16
+    }
     __syncthreads();
-    const TileLanes<OK> tlo = tile_lanes<OK>();
-    for (int j = 0; j < nown; ++j) {
-      if (act_of(j0 + j)) {
-        RawTile<OK> t;
-        read_tile<OK>(base + j * 2 * RSLOT, tlo, t);
-        update(std::integral_constant<int, OK>(), t, j0 + j, 32 * (j0 + j), tp.S, 1.f);
+    if (!loader) {
+      const TileLanes<OK> tlo = tile_lanes<OK>();
+      for (int j = 0; j < nown; ++j) {
+        if (act_of(j0 + j)) {
+          RawTile<OK> t;
+          read_tile<OK>(base + j * 2 * RSLOT, tlo, t);
+          update(std::integral_constant<int, OK>(), t, j0 + j, 32 * (j0 + j), tp.S, 1.f);
+        }
       }
     }
   }
-  // whole jobs (at most one per wave, job 0): the state goes through this wave's LDS slots into row order
+  // whole jobs: each state goes through this wave's LDS slots into row order
   __syncthreads();  // every wave is done with the ring
-  if (nj > 0 && jp[0] == 0) {
-    float* stw = state_of(L, wave);
-    state_to_lds(stw, o[0], m_run[0], l_run[0]);
-    write_state_rows(a, tp, dm, U, tt0 + ju[0], (int64_t)U.slot * tp.n_tt + tt0 + ju[0], stw);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (j < nj && jP[j] == 1) {
+      float* stw = state_of(L, wave);
+      state_to_lds(stw, o[j], m_run[j], l_run[j]);
+      write_state_rows(a, tp, dm, U, tt0 + ju[j], (int64_t)U.slot * tp.n_tt + tt0 + ju[j], stw);
+    }
   }
-  // key-split query tiles F .. nq-1: each wave's state (empty if it has no job on the tile), merged in LDS
-  for (int u = F; u < nq; ++u) {
+  // key-split query tiles: each wave's state (empty if it has no job on the tile), merged in LDS
+  for (int u = s_lo; u < s_hi; ++u) {
     __syncthreads();  // the ring (and the previous merge) is free
     f32x4 oe[8];
     float me = -INFINITY, le = 0.f;
 #pragma unroll
     for (int k = 0; k < 8; ++k) oe[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (nj > 0 && jp[0] != 0 && ju[0] == u) {
+    if (nj > 0 && jP[0] != 1 && ju[0] == u) {
 #pragma unroll
       for (int k = 0; k < 8; ++k) oe[k] = o[0][k];
       me = m_run[0];
       le = l_run[0];
-    } else if (nj > 1 && jp[1] != 0 && ju[1] == u) {
+    } else if (nj > 1 && jP[1] != 1 && ju[1] == u) {
 #pragma unroll
       for (int k = 0; k < 8; ++k) oe[k] = o[1][k];
       me = m_run[1];
