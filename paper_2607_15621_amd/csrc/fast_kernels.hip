@@ -271,12 +271,121 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   }
 }
 
+// Projection of batched rows: CT column tiles per workgroup, so each row operand loaded from L2 serves CT tiles (with
+// one tile per workgroup the rows' bytes were MT times the weights' for MT row tiles).  The 4 waves split K as in
+// k_gemm; wave w holds U batches of CT weight blocks and MT row operands, then runs CT x MT MFMA chains.
+template <int MT, int CT, int EPI>
+__global__ __launch_bounds__(256) void k_gemm_ct(GemmArgs g) {
+  __shared__ f32x4 red[4][CT][MT][WAVE];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c = lane & 15, grp = lane >> 4;
+  const int n_groups = g.N / (16 * CT);
+  const int ng = blockIdx.x % n_groups, ks = blockIdx.x / n_groups;
+  const int KB = g.K / 32;
+  const int kbs = KB / g.ksplit;
+  const int kb0 = ks * kbs, kb1 = kb0 + kbs;
+  const uint4* __restrict__ wt = g.w + (int64_t)ng * CT * KB * WAVE + lane;  // tile ct at wt + ct * KB * WAVE
+  const int n_mt = (g.M + 15) / 16;
+  for (int mg = 0; mg < n_mt; mg += MT) {
+    f32x4 acc[CT][MT];
+    const uint16_t* xr[MT];
+    bool ok[MT];
+    float rsc[MT][4];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) acc[ct][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int row = (mg + mt) * 16 + c;
+      ok[mt] = row < g.M;
+      xr[mt] = g.x + (int64_t)(ok[mt] ? row : 0) * g.ldx + 8 * grp;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int er = (mg + mt) * 16 + 4 * grp + i;
+        rsc[mt][i] = EPI != EPI_PARTIAL && g.rscale && er < g.M ? g.rscale[er] : 1.f;
+      }
+    }
+    constexpr int U = 2;
+    int kb = kb0 + wave;
+    for (; kb + 4 * (U - 1) < kb1; kb += 4 * U) {
+      uint4 wv[U][CT], xv[U][MT];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) wv[u][ct] = ld_global(wt + ((int64_t)ct * KB + kb + 4 * u) * WAVE);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          xv[u][mt] = ok[mt] ? *reinterpret_cast<const uint4*>(xr[mt] + (kb + 4 * u) * 32) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) acc[ct][mt] = mfma_bf16(xv[u][mt], wv[u][ct], acc[ct][mt]);
+    }
+    for (; kb < kb1; kb += 4) {
+      uint4 wv[CT], xv[MT];
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) wv[ct] = ld_global(wt + ((int64_t)ct * KB + kb) * WAVE);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        xv[mt] = ok[mt] ? *reinterpret_cast<const uint4*>(xr[mt] + kb * 32) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[ct][mt] = mfma_bf16(xv[mt], wv[ct], acc[ct][mt]);
+    }
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) red[wave][ct][mt][lane] = acc[ct][mt];
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < CT * MT; ++p) {
+      if (p % 4 != wave) continue;
+      const int ct = p / MT, mt = p % MT;
+      f32x4 sm = red[0][ct][mt][lane] + red[1][ct][mt][lane] + red[2][ct][mt][lane] + red[3][ct][mt][lane];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sm[i] *= rsc[mt][i];
+      gemm_epilogue<EPI>(g, sm, (mg + mt) * 16, ng * CT + ct, ks, c, grp);
+    }
+    __syncthreads();
+  }
+}
+
 template <int EPI>
 static hipError_t gemm_dispatch(const GemmArgs& g, hipStream_t s) {
   const int n_mt = (g.M + 15) / 16;
   const int groups = (n_mt + 7) / 8;
   const int mt = (n_mt + groups - 1) / groups;
-  const dim3 grid((unsigned)((g.N / 16) * g.ksplit)), block(256);
+  // several column tiles per workgroup when the rows span more than one tile and the grid still fills the chip
+  const int tiles = g.N / 16;
+  auto fills = [&](int ct) { return tiles % ct == 0 && (tiles / ct) * g.ksplit >= 256; };
+  const dim3 block(256);
+  if (mt >= 2 && mt <= 4 && fills(4)) {
+    const dim3 grid((unsigned)((tiles / 4) * g.ksplit));
+    switch (mt) {
+      case 2: hipLaunchKernelGGL((k_gemm_ct<2, 4, EPI>), grid, block, 0, s, g); break;
+      case 3: hipLaunchKernelGGL((k_gemm_ct<3, 4, EPI>), grid, block, 0, s, g); break;
+      default: hipLaunchKernelGGL((k_gemm_ct<4, 4, EPI>), grid, block, 0, s, g); break;
+    }
+    return hipGetLastError();
+  }
+  if (mt >= 2 && fills(2)) {
+    const dim3 grid((unsigned)((tiles / 2) * g.ksplit));
+    switch (mt) {
+      case 2: hipLaunchKernelGGL((k_gemm_ct<2, 2, EPI>), grid, block, 0, s, g); break;
+      case 3: hipLaunchKernelGGL((k_gemm_ct<3, 2, EPI>), grid, block, 0, s, g); break;
+      case 4: hipLaunchKernelGGL((k_gemm_ct<4, 2, EPI>), grid, block, 0, s, g); break;
+      case 5: hipLaunchKernelGGL((k_gemm_ct<5, 2, EPI>), grid, block, 0, s, g); break;
+      case 6: hipLaunchKernelGGL((k_gemm_ct<6, 2, EPI>), grid, block, 0, s, g); break;
+      case 7: hipLaunchKernelGGL((k_gemm_ct<7, 2, EPI>), grid, block, 0, s, g); break;
+      default: hipLaunchKernelGGL((k_gemm_ct<8, 2, EPI>), grid, block, 0, s, g); break;
+    }
+    return hipGetLastError();
+  }
+  const dim3 grid((unsigned)(tiles * g.ksplit));
   switch (mt) {
     case 1: hipLaunchKernelGGL((k_gemm<1, EPI>), grid, block, 0, s, g); break;
     case 2: hipLaunchKernelGGL((k_gemm<2, EPI>), grid, block, 0, s, g); break;

@@ -165,6 +165,32 @@ def test_backbone_full_llama_widths():
     bb.bb.close()
 
 
+@pytest.mark.slow
+@pytest.mark.parametrize("batch", [8, 16])
+def test_backbone_batched_llama_widths(batch):
+    # 32 or 64 new rows at LLaMA-7B widths: the projections take the several-column-tiles-per-workgroup kernel
+    lengths = tuple(40 + 17 * b for b in range(batch))
+    wl = bb_workload(760 + batch, lengths=lengths, n_new=4, capacity=320, d=4096, H=32, F=11008, n_layers=2)
+    say(f"case backbone at LLaMA-7B widths, {batch} agents, 2 layers")
+    bb = BB(wl)
+    cache = Cache(wl)
+    host_tok, tok = tokens_for(wl)
+    first = [int((cache.desc.start[b] + cache.desc.len[b]) % wl.capacity) for b in range(wl.batch)]
+    pos0 = [int(p) for p in cache.desc.pos]
+    hid = torch.full((wl.n_layers, wl.batch, 4, wl.d_model), float("nan"), device="cuda")
+    bb.bb.append(cache.desc, tok, wl.batch, 4, hid)
+    torch.cuda.synchronize()
+    hid = hid.cpu().numpy()
+    got = [appended(cache, b, first[b], 4) for b in range(wl.batch)]
+    refs = synth.parallel_map(lambda b: bb.oracle(host_tok[b], cache.oracle_rows(b), pos0[b]), list(range(wl.batch)))
+    for b, (k_ref, v_ref, h_ref) in enumerate(refs):
+        record(b, rel_err(got[b][0], k_ref), TOL, what="appended keys (rotated), max|d| / max|ref|")
+        record(b, rel_err(got[b][1], v_ref), TOL, what="appended values, max|d| / max|ref|")
+        record(b, max(rel_err(hid[l, b], h_ref[l]) for l in range(wl.n_layers)), TOL,
+               what="worst layer hidden, max|d| / max|ref|")
+    bb.bb.close()
+
+
 def test_expert_tick_over_rows_the_backbone_appended():
     # producer -> consumer: the backbone extends the cache, then the expert reads it
     wl = bb_workload(740, lengths=(100, 64), n_new=4, capacity=128, d=512, H=16, F=1024)
