@@ -606,43 +606,49 @@ __global__ __launch_bounds__(256) void k_reduce_norm(float* __restrict__ h, cons
 // partials, xb = bf16(h) unscaled, and the chunk's sum of squares to ss[m][chunk]; the last chunk of the row forms
 // the row's RMSNorm scale, which the next projection applies to its products, so no launch forms the normalised
 // input.
-__global__ __launch_bounds__(256) void k_reduce_chunks(float* __restrict__ h, const float* __restrict__ part,
-                                                       int M, int d, int ksplit, float* __restrict__ ss,
-                                                       uint16_t* __restrict__ xb, float* __restrict__ hidden,
-                                                       float* __restrict__ rs, uint32_t* __restrict__ rcnt,
-                                                       float eps) {
+__global__ __launch_bounds__(RN_CHUNK / 4) void k_reduce_chunks(float* __restrict__ h, const float* __restrict__ part,
+                                                                int M, int d, int ksplit, float* __restrict__ ss,
+                                                                uint16_t* __restrict__ xb, float* __restrict__ hidden,
+                                                                float* __restrict__ rs, uint32_t* __restrict__ rcnt,
+                                                                float eps) {
   __shared__ float red[16];
   const int nch = d / RN_CHUNK, m = blockIdx.x / nch, ch = blockIdx.x % nch;
-  float acc[2] = {0.f, 0.f};
-  int64_t idx[2];
-#pragma unroll
-  for (int e = 0; e < 2; ++e) idx[e] = (int64_t)m * d + ch * RN_CHUNK + threadIdx.x + 256 * e;
+  // thread t: the 4 columns ch * RN_CHUNK + 4t .. + 3, 16-byte loads (every partial's load issued before any add)
+  const int64_t idx = (int64_t)m * d + ch * RN_CHUNK + 4 * threadIdx.x;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int s0 = 0; s0 < ksplit; s0 += 8) {
-    float v[8][2];
+    float4 v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j)
+      v[j] = s0 + j < ksplit ? *reinterpret_cast<const float4*>(part + (int64_t)(s0 + j) * M * d + idx)
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-      for (int e = 0; e < 2; ++e) v[j][e] = s0 + j < ksplit ? part[(int64_t)(s0 + j) * M * d + idx[e]] : 0.f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-#pragma unroll
-      for (int e = 0; e < 2; ++e) acc[e] += v[j][e];
+    for (int j = 0; j < 8; ++j) {
+      acc.x += v[j].x;
+      acc.y += v[j].y;
+      acc.z += v[j].z;
+      acc.w += v[j].w;
+    }
   }
-  float sq = 0.f;
-#pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    const float val = h[idx[e]] + acc[e];
-    h[idx[e]] = val;
-    xb[idx[e]] = f32_to_bf16(val);
-    if (hidden) hidden[idx[e]] = val;
-    sq += val * val;
+  const float4 h0 = *reinterpret_cast<const float4*>(h + idx);
+  const float4 val = make_float4(h0.x + acc.x, h0.y + acc.y, h0.z + acc.z, h0.w + acc.w);
+  *reinterpret_cast<float4*>(h + idx) = val;
+  *reinterpret_cast<uint2*>(xb + idx) = make_uint2(pack_bf16x2(val.x, val.y), pack_bf16x2(val.z, val.w));
+  if (hidden) {  // the caller's buffer: 4-byte alignment only
+    hidden[idx] = val.x;
+    hidden[idx + 1] = val.y;
+    hidden[idx + 2] = val.z;
+    hidden[idx + 3] = val.w;
   }
+  float sq = val.x * val.x + val.y * val.y + val.z * val.z + val.w * val.w;
   sq = block_sum(sq, red);
   // the last chunk of row m to finish adds the chunk sums in chunk order and writes the row's scale; it then resets
-  // the row's counter for the next reduction (the next launch)
+  // the row's counter for the next reduction (the next launch).  The sums are device-scope stores completed before
+  // the count (no release fence: at device scope that writes back the whole L2) and read with device-scope loads.
   if (threadIdx.x == 0) {
     st_dev_f(ss + (int64_t)m * nch + ch, sq);
-    const uint32_t done = __hip_atomic_fetch_add(rcnt + m, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    stores_done();
+    const uint32_t done = __hip_atomic_fetch_add(rcnt + m, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (done == (uint32_t)(nch - 1)) {
       float tot = 0.f;
       for (int c = 0; c < nch; ++c) tot += ld_dev_f(ss + (int64_t)m * nch + c);
@@ -656,7 +662,7 @@ hipError_t launch_reduce_norm(const TickParams& tp, const Dims& dm, const Worksp
                               const float* gain, float* hidden_layer, hipStream_t s) {
   if (wide_rows(dm)) {
     const int nch = dm.d / RN_CHUNK;
-    hipLaunchKernelGGL(k_reduce_chunks, dim3(tp.M * nch), dim3(256), 0, s, ws.h, (const float*)ws.part, tp.M, dm.d,
+    hipLaunchKernelGGL(k_reduce_chunks, dim3(tp.M * nch), dim3(RN_CHUNK / 4), 0, s, ws.h, (const float*)ws.part, tp.M, dm.d,
                        ksplit, ws.ss, ws.xb, hidden_layer, ws.rs, ws.rcnt, dm.eps);
     return hipGetLastError();
   }
