@@ -401,6 +401,19 @@ __device__ __forceinline__ void unit_gemm(const uint4 w[4], int nkb, int mt_n, T
   __syncthreads();
 }
 
+// The row-split projections (O, F1, D) load the weights of IPF items of a workgroup (items it0 + j n) together, so
+// that with several row blocks the second item's weights are not fetched after the first item's product.
+constexpr int IPF = 2;
+__device__ __forceinline__ void pick_w(const uint4 (&w)[IPF][4], int j, uint4 (&out)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = w[0][i];
+#pragma unroll
+  for (int jj = 1; jj < IPF; ++jj)
+    if (j == jj)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) out[i] = w[jj][i];
+}
+
 // One wave per projection unit: the wave holds the unit's 16-column tile for every k-block (K <= 512) in
 // registers and multiplies all staged row tiles.
 __device__ __forceinline__ void load_unit_w_full(const uint4* __restrict__ wtile, int nkb, uint4 w[16]) {
@@ -1748,27 +1761,35 @@ __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams&
   uint64_t* po = a.po + (int64_t)X * nt * tp.Mp * 16;
   bool first = true;
   int staged = -1;  // row block in L.x
-  for (int item = s; item < nt * R; item += n) {
-    const int k = item / R, r = item % R;
-    uint4 w[4];
-    load_unit_w(W.wo + (int64_t)k * (A / 32) * WAVE, kb0, nkb, w);
+  const int total = nt * R;
+  for (int it0 = s; it0 < total; it0 += IPF * n) {
+    uint4 wg[IPF][4];
+#pragma unroll
+    for (int j = 0; j < IPF; ++j)
+      if (it0 + j * n < total) load_unit_w(W.wo + (int64_t)((it0 + j * n) / R) * (A / 32) * WAVE, kb0, nkb, wg[j]);
     if (first && nh > 0 &&
         !wg_wait(a.f_attn + (int64_t)h0 * tp.n_tt * FPAD, tp.B * nh * tp.n_tt, st, a, L, nh * tp.n_tt, H * tp.n_tt))
       return false;
     if (first) TICK_SUB(l, 5);
-    const int m0 = r * MTMAX * 16, rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-    if (nh > 0 && staged != r) stage(a.attn + h0 * DH, A, m0, rows, nh * DH, nullptr, 0, 0, 0.f, L);
-    staged = r;
-    unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
+#pragma unroll 1
+    for (int j = 0; j < IPF && it0 + j * n < total; ++j) {
+      const int item = it0 + j * n, k = item / R, r = item % R;
+      uint4 w[4];
+      pick_w(wg, j, w);
+      const int m0 = r * MTMAX * 16, rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
+      if (nh > 0 && staged != r) stage(a.attn + h0 * DH, A, m0, rows, nh * DH, nullptr, 0, 0, 0.f, L);
+      staged = r;
+      unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int row = m0 + mt * 16 + 4 * grp + q;
-        if (row < M)
-          st_dev(po + ((int64_t)k * tp.Mp + row) * 16 + c, ((uint64_t)st32 << 32) | __float_as_uint(sacc[q]));
-      }
-    });
-    if (first) TICK_SUB(l, 6);
-    first = false;
+        for (int q = 0; q < 4; ++q) {
+          const int row = m0 + mt * 16 + 4 * grp + q;
+          if (row < M)
+            st_dev(po + ((int64_t)k * tp.Mp + row) * 16 + c, ((uint64_t)st32 << 32) | __float_as_uint(sacc[q]));
+        }
+      });
+      if (first) TICK_SUB(l, 6);
+      first = false;
+    }
   }
   const int t0 = tile_lo(X, NX, nt), t1 = tile_lo(X + 1, NX, nt);
   for (int q = s; q < (t1 - t0) * tp.rblk; q += n)
@@ -1792,35 +1813,43 @@ __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams
   const int KB = d / 32;
   bool waited = false;
   int staged = -1;
-  for (int item = s; item < nu * R; item += n) {
-    const int u = u0 + item / R, r = item % R;
-    uint4 w[4];
-    load_unit_w(W.wgu + (int64_t)u * KB * WAVE, 0, KB, w);
+  const int total = nu * R;
+  for (int it0 = s; it0 < total; it0 += IPF * n) {
+    uint4 wg[IPF][4];
+#pragma unroll
+    for (int j = 0; j < IPF; ++j)
+      if (it0 + j * n < total) load_unit_w(W.wgu + (int64_t)(u0 + (it0 + j * n) / R) * KB * WAVE, 0, KB, wg[j]);
     if (!waited) {
       if (!wg_wait(a.f_mid, nt * tp.rblk, st, a, L)) return false;
       waited = true;
       TICK_SUB(l, 7);
     }
-    const int m0 = r * MTMAX * 16, rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-    if (staged != r) stage(xb, d, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
-    staged = r;
-    unit_gemm(w, KB, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
+#pragma unroll 1
+    for (int j = 0; j < IPF && it0 + j * n < total; ++j) {
+      const int item = it0 + j * n, u = u0 + item / R, r = item % R;
+      uint4 w[4];
+      pick_w(wg, j, w);
+      const int m0 = r * MTMAX * 16, rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
+      if (staged != r) stage(xb, d, m0, rows, d, ssq, tp.Ms, d, dm.eps, L);
+      staged = r;
+      unit_gemm(w, KB, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        sacc[q] *= L.r[mt * 16 + 4 * grp + q];  // RMSNorm row scale
-        const float up = xor8(sacc[q]);
-        const float gt = sacc[q];
-        const float zz = gt / (1.0f + expf(-gt)) * up;
-        const float zn = xor1(zz);
-        const int row = m0 + mt * 16 + 4 * grp + q;
-        if (c < 8 && (c & 1) == 0 && row < M)
-          st_loc(reinterpret_cast<uint32_t*>(a.z + (int64_t)row * F + u * 8 + c), pack_bf16x2(zz, zn));
-      }
-    });
-    if (item == s) TICK_SUB(l, 8);
-    stores_done();
-    __syncthreads();
-    if (tix() == 0) st_loc(a.f_z + ((int64_t)u * R + r) * FPAD, st);
+        for (int q = 0; q < 4; ++q) {
+          sacc[q] *= L.r[mt * 16 + 4 * grp + q];  // RMSNorm row scale
+          const float up = xor8(sacc[q]);
+          const float gt = sacc[q];
+          const float zz = gt / (1.0f + expf(-gt)) * up;
+          const float zn = xor1(zz);
+          const int row = m0 + mt * 16 + 4 * grp + q;
+          if (c < 8 && (c & 1) == 0 && row < M)
+            st_loc(reinterpret_cast<uint32_t*>(a.z + (int64_t)row * F + u * 8 + c), pack_bf16x2(zz, zn));
+        }
+      });
+      if (item == s) TICK_SUB(l, 8);
+      stores_done();
+      __syncthreads();
+      if (tix() == 0) st_loc(a.f_z + ((int64_t)u * R + r) * FPAD, st);
+    }
   }
   return true;
 }
@@ -1840,26 +1869,34 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
   float* hidden_l = a.hidden ? a.hidden + (int64_t)l * M * d : nullptr;
   bool waited = false;
   int staged = -1;
-  for (int item = s; item < nt * R; item += n) {
-    const int k = item / R, r = item % R;
-    uint4 w[4];
-    load_unit_w(W.wd + (int64_t)k * (F / 32) * WAVE, kb0, nkb, w);
+  const int total = nt * R;
+  for (int it0 = s; it0 < total; it0 += IPF * n) {
+    uint4 wg[IPF][4];
+#pragma unroll
+    for (int j = 0; j < IPF; ++j)
+      if (it0 + j * n < total) load_unit_w(W.wd + (int64_t)((it0 + j * n) / R) * (F / 32) * WAVE, kb0, nkb, wg[j]);
     if (!waited && nkb > 0 && !wg_wait(a.f_z + (int64_t)(f0 / 8) * R * FPAD, (f1 - f0) / 8 * R, st, a, L))
       return false;
     if (!waited) TICK_SUB(l, 9);
     waited = true;
-    const int m0 = r * MTMAX * 16, rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
-    if (nkb > 0 && staged != r) stage(a.z + f0, F, m0, rows, f1 - f0, nullptr, 0, 0, 0.f, L);
-    staged = r;
-    unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
+#pragma unroll 1
+    for (int j = 0; j < IPF && it0 + j * n < total; ++j) {
+      const int item = it0 + j * n, k = item / R, r = item % R;
+      uint4 w[4];
+      pick_w(wg, j, w);
+      const int m0 = r * MTMAX * 16, rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
+      if (nkb > 0 && staged != r) stage(a.z + f0, F, m0, rows, f1 - f0, nullptr, 0, 0, 0.f, L);
+      staged = r;
+      unit_gemm(w, nkb, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int row = m0 + mt * 16 + 4 * grp + q;
-        if (row < M)
-          st_dev(pd + ((int64_t)k * tp.Mp + row) * 16 + c, ((uint64_t)st32 << 32) | __float_as_uint(sacc[q]));
-      }
-    });
-    if (item == s) TICK_SUB(l, 10);
+        for (int q = 0; q < 4; ++q) {
+          const int row = m0 + mt * 16 + 4 * grp + q;
+          if (row < M)
+            st_dev(pd + ((int64_t)k * tp.Mp + row) * 16 + c, ((uint64_t)st32 << 32) | __float_as_uint(sacc[q]));
+        }
+      });
+      if (item == s) TICK_SUB(l, 10);
+    }
   }
   const int t0 = tile_lo(X, NX, nt), t1 = tile_lo(X + 1, NX, nt);
   for (int q = s; q < (t1 - t0) * tp.rblk; q += n)
