@@ -341,7 +341,7 @@ static int create_impl(const fsx_expert_cfg* cfg, const fsx_layer_weights* layer
         {(void**)&t.f_rope, (size_t)NXMAX * XFLAGS * FPAD * 8},
         {(void**)&t.f_out, (size_t)XFLAGS * FPAD * 8},
         {(void**)&t.f_mid, (size_t)XFLAGS * FPAD * 8},
-        {(void**)&t.f_q, (size_t)3 * A / 16 * FPAD * 8},
+        {(void**)&t.f_q, (size_t)3 * A / 16 * ((M + 79) / 80) * FPAD * 8},  // per (tile, row block of 80 rows)
         {(void**)&t.f_attn, (size_t)nflag_attn * n_tt_max * FPAD * 8},
         {(void**)&t.f_rng, (size_t)ex->items_max * FPAD * 8},
         {(void**)&t.f_z, (size_t)F / 8 * ((M + 79) / 80) * FPAD * 8},
@@ -477,7 +477,7 @@ size_t static_tick_layout(const fsx_expert* ex, const TickParams& tp, char* base
       {(void**)&t.po, NXS * dt * Mp * 16 * 8}, {(void**)&t.pd, NXS * dt * Mp * 16 * 8},
       {(void**)&t.reg, (size_t)ex->cu_count * 8}, {(void**)&t.f_rope, NXS * XFLAGS * FPAD * 8},
       {(void**)&t.f_out, XFLAGS * FPAD * 8}, {(void**)&t.f_mid, XFLAGS * FPAD * 8},
-      {(void**)&t.f_q, 3 * A / 16 * FPAD * 8}, {(void**)&t.f_attn, (size_t)tp.B * c.n_heads * tp.n_tt * FPAD * 8},
+      {(void**)&t.f_q, 3 * A / 16 * R * FPAD * 8}, {(void**)&t.f_attn, (size_t)tp.B * c.n_heads * tp.n_tt * FPAD * 8},
       {(void**)&t.f_rng, items * FPAD * 8}, {(void**)&t.f_z, F / 8 * R * FPAD * 8}, {(void**)&t.status, 256}};
   size_t off = 0;
   for (const auto& p : parts) {

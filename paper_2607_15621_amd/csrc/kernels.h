@@ -176,7 +176,7 @@ struct TickArgs {
   uint64_t* f_rope;    // [NXMAX][XFLAGS] by workgroup slot
   uint64_t* f_out;     // [XFLAGS] by residual piece (column tile * rblk + row block)
   uint64_t* f_mid;     // [XFLAGS] by residual piece
-  uint64_t* f_q;       // [3A/16]
+  uint64_t* f_q;       // [3A/16][row blocks of 80 rows]
   uint64_t* f_attn;    // [B*H][n_tt] per query tile
   uint64_t* f_rng;     // [slot] partial states written
   uint64_t* f_z;       // [F/8][row blocks of 80 rows]

@@ -58,6 +58,8 @@ constexpr int NSEG = FSX_MAX_BATCH * 4;  // attention segments (agent, local hea
 
 // A value read from LDS that is the same in every lane, moved to a scalar register.
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+// Row blocks of MTMAX * 16 rows: the projections stage and multiply one block of the M rows at a time.
+__device__ __forceinline__ int row_blocks(int M) { return (M + MTMAX * 16 - 1) / (MTMAX * 16); }
 
 struct TickLds {
   union {
@@ -607,7 +609,7 @@ __device__ __forceinline__ void phase_embed(const TickArgs& a, const TickParams&
 // those take all units, so that the attention workgroups start streaming their cache tiles at once.
 __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
-  const int d = dm.d, M = tp.M, A = dm.A, H = dm.H, half = DH / 2, nt = d / 16;
+  const int d = dm.d, M = tp.M, A = dm.A, H = dm.H, half = DH / 2, nt = d / 16, R = row_blocks(M);
   const int wave = uni(tix() >> 6);  // scalar, so the unit's section is a uniform branch
   const int h0 = head_lo(X, NX, H), nh = head_lo(X + 1, NX, H) - h0;
   const int n_units = 24 * nh;
@@ -621,15 +623,33 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
   const int nseg = tp.B * nh, nq = n - nseg;  // attention workgroups, and the others
   const bool spare = uni(L.amode) == 1 && nq > 0 && n_units <= 4 * nq;
   const int s0 = spare ? s - nseg : s, nw = spare ? nq : n;  // this workgroup's index among the Q workgroups
+  // With several row blocks (and n a multiple of R) workgroup s takes row block s mod R only, staged once, and the
+  // units s / R + (n / R)(w + 4k); otherwise every row block of units s0 + nw (w + 4k).
+  const bool by_rows = R > 1 && !spare && n % R == 0;
+  const int rb0 = by_rows ? s % R : 0, rb1 = by_rows ? rb0 + 1 : R;
+  const int ub = by_rows ? s / R : s0, us = by_rows ? n / R : nw;
   bool waited = false;
-  for (int u0 = s0; s0 >= 0 && u0 < n_units; u0 += 4 * nw) {
-    const int u = u0 + wave * nw;  // this wave's unit in this round
+  int staged = -1;  // row block in L.x
+  uint4 w[16], wn[16];
+  {
+    const int u = ub + us * wave;
+    if (s0 >= 0 && u < n_units) {
+      const int tile = ((u % 24) / 8) * (A / 16) + (h0 + u / 24) * (DH / 16) + u % 8;
+      load_unit_w_full(W.wqkv + (int64_t)tile * KB * WAVE, KB, w);
+    }
+  }
+  for (int u0 = ub; s0 >= 0 && u0 < n_units; u0 += 4 * us) {
+    const int u = u0 + wave * us;  // this wave's unit in this round
     const bool mine = u < n_units;
     const int hl = u / 24, sec = (u % 24) / 8, t = u % 8;
     const int h = h0 + hl;
     const int tile = sec * (A / 16) + h * (DH / 16) + t;  // 16-row tile of packed [q; k; v]
-    uint4 w[16];
-    if (mine) load_unit_w_full(W.wqkv + (int64_t)tile * KB * WAVE, KB, w);
+    // the next round's weights stream in during this round (one row block: the rows are staged once)
+    const int un = u + 4 * us;
+    if (by_rows && un < n_units) {
+      const int tn = ((un % 24) / 8) * (A / 16) + (h0 + un / 24) * (DH / 16) + un % 8;
+      load_unit_w_full(W.wqkv + (int64_t)tn * KB * WAVE, KB, wn);
+    }
     if (!waited) {
       TICK_SUB(l, 0);
       bool ok = wg_wait(a.f_out, nt * tp.rblk, stamp_of(a, l - 1, dm.n_layers), a, L);
@@ -639,8 +659,8 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
       TICK_SUB(l, 1);
     }
     const int nl0 = h * DH + t * 16;  // first column of the unit inside its section
-    for (int m0 = 0; m0 < M; m0 += MTMAX * 16) {
-      const int rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
+    for (int r = rb0; r < rb1; ++r) {
+      const int m0 = r * MTMAX * 16, rows = min(MTMAX * 16, M - m0), mt_n = (rows + 15) / 16;
       // this wave's rotary slice: rope[row][8t .. 8t+7][2] (64 bytes per row), 16 rows per direct load
       auto rope_loads = [&]() {
         if (mine && sec < 2) {
@@ -651,7 +671,13 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
           }
         }
       };
-      stage(xb, d, m0, rows, d, ssq, tp.Ms, d, dm.eps, L, rope_loads);
+      if (staged != r) {
+        stage(xb, d, m0, rows, d, ssq, tp.Ms, d, dm.eps, L, rope_loads);
+        staged = r;
+      } else {
+        rope_loads();  // the wave's own slice only; read once its loads have landed
+        vm_wait_all();
+      }
       TICK_SUB(l, 2);
       if (mine) {
         wave_gemm(w, mt_n, L, [&](int mt, f32x4 sacc, int c, int grp) {
@@ -677,25 +703,37 @@ __device__ __forceinline__ bool phase_qkv(const TickArgs& a, const TickParams& t
             for (int i = 0; i < 4; ++i) {
               const float v = sacc[i] * rs[i];
               const float partner = xor8(v);
-              const float r = c < 8 ? v * cs[i].x - partner * cs[i].y : v * cs[i].x + partner * cs[i].y;
+              const float rr = c < 8 ? v * cs[i].x - partner * cs[i].y : v * cs[i].x + partner * cs[i].y;
               const int row = m0 + rb + i;
               const int64_t o = (int64_t)row * A + h * DH + dch;
               if (sec == 0) {
-                if (row < M) st_loc_f(a.q + o, r * qs);
+                if (row < M) st_loc_f(a.q + o, rr * qs);
               } else {
-                const float nb = xor1(r);  // neighbouring channel dch+1 sits in lane c+1
-                if ((c & 1) == 0 && row < M) st_loc(reinterpret_cast<uint32_t*>(a.kself + o), pack_bf16x2(r, nb));
+                const float nb = xor1(rr);  // neighbouring channel dch+1 sits in lane c+1
+                if ((c & 1) == 0 && row < M) st_loc(reinterpret_cast<uint32_t*>(a.kself + o), pack_bf16x2(rr, nb));
               }
             }
           }
         });
       }
-      __syncthreads();  // the next chunk overwrites the staged rows
+      if (!by_rows) __syncthreads();  // the next chunk overwrites the staged rows
     }
-    // publish this wave's unit
+    // publish this wave's unit: flag (tile, r) for each of its row blocks
     stores_done();
-    if (mine && (tix() & 63) == 0) st_loc(a.f_q + (int64_t)tile * FPAD, st);
+    if (mine && (tix() & 63) == 0)
+      for (int r = rb0; r < rb1; ++r) st_loc(a.f_q + ((int64_t)tile * R + r) * FPAD, st);
+    if (by_rows) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) w[i] = wn[i];
+    } else if (u0 + 4 * us < n_units) {
+      const int un2 = u + 4 * us;
+      if (un2 < n_units) {
+        const int tn = ((un2 % 24) / 8) * (A / 16) + (h0 + un2 / 24) * (DH / 16) + un2 % 8;
+        load_unit_w_full(W.wqkv + (int64_t)tn * KB * WAVE, KB, w);
+      }
+    }
   }
+  if (by_rows) __syncthreads();  // the next phase overwrites the staged rows
   TICK_SUB(l, 3);
   return true;
 }
@@ -1315,7 +1353,10 @@ __device__ __forceinline__ bool attn_unit(const TickArgs& a, const TickParams& t
       if (dd < nc) ring_tile(dd);
   };
   if (wave < 3) prefetch();
-  if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16, 3)) return false;
+  const int RQ = row_blocks(tp.M);  // the flags of the head's q, k and v tiles, per row block
+  if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * RQ * FPAD, 3 * (DH / 16) * RQ, st, a, L, DH / 16 * RQ, dm.A / 16 * RQ,
+               3))
+    return false;
   if (wave == 3) prefetch();
 #pragma unroll
   for (int dd = 0; dd < RG::tiles; ++dd)
@@ -1472,7 +1513,9 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
   // wave 0 (no loads in flight) polls the q, k and v column tiles of this head.
   if (loader)
     for (int i = 0; i < G && i < nc; ++i) stage(i);
-  if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * FPAD, 3 * (DH / 16), st, a, L, DH / 16, dm.A / 16, 0)) {
+  const int RQ = row_blocks(tp.M);  // the flags of the head's q, k and v tiles, per row block
+  if (!wg_wait(a.f_q + (int64_t)U.h * (DH / 16) * RQ * FPAD, 3 * (DH / 16) * RQ, st, a, L, DH / 16 * RQ, dm.A / 16 * RQ,
+               0)) {
     vm_wait_all();
     return false;
   }
@@ -1741,15 +1784,14 @@ __device__ __forceinline__ bool phase_attn(const TickArgs& a, const TickParams& 
   return true;
 }
 
-// ------------------------------------------------------------------------------------------ O (+ R1)
+// ------------------------------------------------------------------------------------------ O
 // The row-split projections (O, F1, D) work on items (column tile or unit k, row block r) of MTMAX*16 rows,
 // item = k * R + r with R row blocks; workgroup s takes items s, s + n, ... (when n is a multiple of R, all of one
 // workgroup's items share a row block, which it stages once).  With more than one row block this halves (or more)
 // the rows a workgroup stages and multiplies, against every workgroup taking all rows of fewer tiles.
-__device__ __forceinline__ int row_blocks(int M) { return (M + MTMAX * 16 - 1) / (MTMAX * 16); }
 
 // Column tile k (of the residual) of the output projection over X's attention columns, rows of block r, as stamped
-// partial words; then the reduction of every tile i this workgroup owns (slot i mod n) over the XCDs into h_mid.
+// partial words (reduced across the XCDs by phase_reduce).
 __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
   const int d = dm.d, M = tp.M, A = dm.A, H = dm.H, nt = d / 16, R = row_blocks(M);
@@ -1791,10 +1833,6 @@ __device__ __forceinline__ bool phase_oproj(const TickArgs& a, const TickParams&
       first = false;
     }
   }
-  const int t0 = tile_lo(X, NX, nt), t1 = tile_lo(X + 1, NX, nt);
-  for (int q = s; q < (t1 - t0) * tp.rblk; q += n)
-    if (!reduce_piece(a, tp, dm, l, t0 + q / tp.rblk, q % tp.rblk, a.po, a.xb_mid, a.ssq_mid, a.f_mid, nullptr, L))
-      return false;
   return true;
 }
 
@@ -1854,9 +1892,9 @@ __device__ __forceinline__ bool phase_gateup(const TickArgs& a, const TickParams
   return true;
 }
 
-// ------------------------------------------------------------------------------------------ D (+ R2)
-// Items (column tile k, row block r) of the down projection over X's FFN columns, as stamped partial words; then the
-// reduction of every tile this workgroup owns into the layer output.
+// ------------------------------------------------------------------------------------------ D
+// Items (column tile k, row block r) of the down projection over X's FFN columns, as stamped partial words (reduced
+// across the XCDs by phase_reduce into the layer output).
 __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, TickLds& L) {
   const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX);
   const int d = dm.d, M = tp.M, F = dm.F, nt = d / 16, R = row_blocks(M);
@@ -1866,7 +1904,6 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
   const uint32_t st32 = (uint32_t)st;
   const LayerW W = layer_w(a, dm, l);
   uint64_t* pd = a.pd + (int64_t)X * nt * tp.Mp * 16;
-  float* hidden_l = a.hidden ? a.hidden + (int64_t)l * M * d : nullptr;
   bool waited = false;
   int staged = -1;
   const int total = nt * R;
@@ -1898,10 +1935,24 @@ __device__ __forceinline__ bool phase_down(const TickArgs& a, const TickParams& 
       if (item == s) TICK_SUB(l, 10);
     }
   }
+  return true;
+}
+
+// ------------------------------------------------------------------------------------------ R1, R2
+// The reduction across XCDs after the output projection (R1, second = false: into the FFN's input) or the down
+// projection (R2: into the layer's output): every piece this workgroup owns (slot q mod n).  One call site in the
+// layer loop, so the kernel holds one copy of this code.
+__device__ __forceinline__ bool phase_reduce(const TickArgs& a, const TickParams& tp, const Dims& dm, int l, bool second,
+                                             TickLds& L) {
+  const int X = uni(L.X), s = uni(L.s), n = uni(L.n), NX = uni(L.NX), nt = dm.d / 16;
   const int t0 = tile_lo(X, NX, nt), t1 = tile_lo(X + 1, NX, nt);
+  const uint64_t* part = second ? a.pd : a.po;
+  uint16_t* xb = second ? a.xb_out : a.xb_mid;
+  float* ssq = second ? a.ssq_out : a.ssq_mid;
+  uint64_t* flag = second ? a.f_out : a.f_mid;
+  float* hidden_l = second && a.hidden ? a.hidden + (int64_t)l * tp.M * dm.d : nullptr;
   for (int q = s; q < (t1 - t0) * tp.rblk; q += n)
-    if (!reduce_piece(a, tp, dm, l, t0 + q / tp.rblk, q % tp.rblk, a.pd, a.xb_out, a.ssq_out, a.f_out, hidden_l, L))
-      return false;
+    if (!reduce_piece(a, tp, dm, l, t0 + q / tp.rblk, q % tp.rblk, part, xb, ssq, flag, hidden_l, L)) return false;
   return true;
 }
 
@@ -2018,12 +2069,19 @@ __global__ __launch_bounds__(NTHR, 1) void k_tick(TickArgs a, TickParams tp, Dim
     trace_mark(a, 2 + 16 * l, nl);
     ok = ok && phase_attn<KT, MQ>(a, tp, dm, l, L);
     trace_mark(a, 3 + 16 * l, nl);
-    ok = ok && phase_oproj(a, tp, dm, l, L);
-    trace_mark(a, 4 + 16 * l, nl);
-    ok = ok && phase_gateup(a, tp, dm, l, L);
-    trace_mark(a, 5 + 16 * l, nl);
-    ok = ok && phase_down(a, tp, dm, l, L);
-    trace_mark(a, 6 + 16 * l, nl);
+    // O + R1, then F1, D + R2: the two reductions share one copy of their code (a loop of two passes)
+#pragma unroll 1
+    for (int second = 0; second < 2 && ok; ++second) {
+      if (!second) {
+        ok = phase_oproj(a, tp, dm, l, L);
+      } else {
+        ok = phase_gateup(a, tp, dm, l, L);
+        trace_mark(a, 5 + 16 * l, nl);
+        ok = ok && phase_down(a, tp, dm, l, L);
+      }
+      ok = ok && phase_reduce(a, tp, dm, l, second != 0, L);
+      trace_mark(a, (second ? 6 : 4) + 16 * l, nl);
+    }
   }
   phase_head(a, tp, dm, ok, L);
   trace_mark(a, 2 + 16 * nl, nl);
