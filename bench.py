@@ -508,7 +508,9 @@ def main():
 
     torch.cuda.set_device(0)
     if args.sweep:
-        run_sweep(args.steps, args.warmup, args.sweep, " ".join(["python", "bench.py"] + sys.argv[1:]))
+        # the recorded command names the output file by its base name (the directory is the caller's choice)
+        argv = [os.path.basename(x) if x == args.sweep else x for x in sys.argv[1:]]
+        run_sweep(args.steps, args.warmup, args.sweep, " ".join(["python", "bench.py"] + argv))
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
         return
