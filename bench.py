@@ -500,7 +500,7 @@ def main():
         summarize_traffic(args.summarize_traffic, args.workload, args.copy_bytes, args.command, args.dram)
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+        print(f"bench.py runs on one GPU only: the library has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
 

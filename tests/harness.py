@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import json
 import os
+import tempfile
 import threading
 
 import numpy as np
@@ -53,7 +54,9 @@ class Cache(_Cache):
 
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-ERR_LOG = os.environ.get("FSX_PARITY_LOG") or os.path.join(ROOT, "gpurun_out", "parity_errors.jsonl")
+# the parity log (one JSON line per comparison; profiles/parity_errors.md is made from it): FSX_PARITY_LOG, else a
+# file in the system's temporary directory
+ERR_LOG = os.environ.get("FSX_PARITY_LOG") or os.path.join(tempfile.gettempdir(), "fsx_parity_errors.jsonl")
 _log_lock = threading.Lock()
 
 
