@@ -248,13 +248,23 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[mt] = mfma_bf16(xv[u][mt], wv[u], acc[mt]);
     }
-    for (; kb < kb1; kb += 4) {
-      const uint4 wv = ld_global(wt + (int64_t)kb * WAVE);
+    if (kb < kb1) {
+      // the last, partial batch: its k-blocks loaded together too (the missing ones as zeros), so a short split-K
+      // range costs one load latency instead of one per k-block
+      uint4 wv[U], xv[U][MT];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const uint4 xv = ok[mt] ? *reinterpret_cast<const uint4*>(xr[mt] + kb * 32) : make_uint4(0, 0, 0, 0);
-        acc[mt] = mfma_bf16(xv, wv, acc[mt]);
+      for (int u = 0; u < U; ++u) {
+        const bool in = kb + 4 * u < kb1;
+        wv[u] = in ? ld_global(wt + (int64_t)(kb + 4 * u) * WAVE) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          xv[u][mt] = in && ok[mt] ? *reinterpret_cast<const uint4*>(xr[mt] + (kb + 4 * u) * 32) : make_uint4(0, 0, 0, 0);
       }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (kb + 4 * u < kb1)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) acc[mt] = mfma_bf16(xv[u][mt], wv[u], acc[mt]);
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) red[wave][mt][lane] = acc[mt];
@@ -324,17 +334,25 @@ __global__ __launch_bounds__(256) void k_gemm_ct(GemmArgs g) {
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) acc[ct][mt] = mfma_bf16(xv[u][mt], wv[u][ct], acc[ct][mt]);
     }
-    for (; kb < kb1; kb += 4) {
-      uint4 wv[CT], xv[MT];
+    if (kb < kb1) {  // the last, partial batch, loaded together as in k_gemm
+      uint4 wv[U][CT], xv[U][MT];
 #pragma unroll
-      for (int ct = 0; ct < CT; ++ct) wv[ct] = ld_global(wt + ((int64_t)ct * KB + kb) * WAVE);
+      for (int u = 0; u < U; ++u) {
+        const bool in = kb + 4 * u < kb1;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-        xv[mt] = ok[mt] ? *reinterpret_cast<const uint4*>(xr[mt] + kb * 32) : make_uint4(0, 0, 0, 0);
+        for (int ct = 0; ct < CT; ++ct)
+          wv[u][ct] = in ? ld_global(wt + ((int64_t)ct * KB + kb + 4 * u) * WAVE) : make_uint4(0, 0, 0, 0);
 #pragma unroll
-      for (int ct = 0; ct < CT; ++ct)
+        for (int mt = 0; mt < MT; ++mt)
+          xv[u][mt] = in && ok[mt] ? *reinterpret_cast<const uint4*>(xr[mt] + (kb + 4 * u) * 32) : make_uint4(0, 0, 0, 0);
+      }
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[ct][mt] = mfma_bf16(xv[mt], wv[ct], acc[ct][mt]);
+      for (int u = 0; u < U; ++u)
+        if (kb + 4 * u < kb1)
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) acc[ct][mt] = mfma_bf16(xv[u][mt], wv[u][ct], acc[ct][mt]);
     }
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
