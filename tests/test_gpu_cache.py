@@ -184,6 +184,31 @@ def test_small_fp8_cache_matches_oracle():
         record(b, rel_err(wp[b], refd), BF16_WP_TOL, what="waypoints vs decoded fp8, max|d| / max|ref|")
 
 
+# Equal lengths on power-of-two rings: with 16 heads (2 per XCD) and 4 agents every (agent, head) attention unit
+# takes its whole range and streams from tile (5h + 3b) mod n of its n tiles, wrapping around; 100 rows make four
+# tiles, the last one partial, and the rings wrap at different rows.  30 frame tokens: the many-query unit.
+@pytest.mark.parametrize("cache_dtype,n_frame", [("bf16", 0), ("fp8", 0), ("bf16", 30), ("fp8", 30)])
+def test_whole_range_units_on_power_of_two_rings_match_oracle(cache_dtype, n_frame):
+    wl = synth.Workload(name="whole", wid=64, n_layers=2, d_model=256, n_heads=16, head_dim=128, d_ffn=512,
+                        n_expert_tokens=10, n_frame_tokens=n_frame, batch=4, lengths=(100,) * 4, dtype="bf16",
+                        cache_dtype=cache_dtype, capacity=128)
+    say(f"case whole-range units, {cache_dtype}, {n_frame} frame tokens, capacity 128")
+    model = Model(wl)
+    ex = model.create()
+    cache = Cache(wl, starts=(120, 64, 0, 127))
+    host_tok, tok = tokens_for(wl)
+    wp, _ = run_forward(ex, cache, tok, wl.batch, n_frame)
+    for b in range(wl.batch):
+        ref, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b), cache.desc.pos[b])
+        if cache_dtype == "fp8":
+            refd, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b, decoded=True), cache.desc.pos[b])
+            record(b, rel_err(wp[b], ref), FP8_WP_TOL, what="waypoints vs bf16 source, max|d| / max|ref|")
+            record(b, rel_err(wp[b], refd), BF16_WP_TOL, what="waypoints vs decoded fp8, max|d| / max|ref|")
+        else:
+            record(b, rel_err(wp[b], ref), BF16_WP_TOL)
+    ex.close()
+
+
 # 30, 64, 90 frame tokens: 3, 5 and 7 query tiles per agent (key-split jobs only; four whole jobs and one
 # key-split; two passes over the cache)
 @pytest.mark.parametrize("n_frame", [30, 64, 90])
