@@ -265,6 +265,22 @@ def time_launches(fn, stream, steps: int, warmup: int) -> float:
     return e0.elapsed_time(e1) / 1e3 / steps
 
 
+def time_each(fn, stream, steps: int):
+    """Seconds of each of `steps` back-to-back calls of fn on `stream` (an event pair around every call, one
+    synchronisation at the end): (10th percentile, median, 90th percentile)."""
+    import numpy as np
+    import torch
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    t = np.array([e0.elapsed_time(e1) / 1e3 for e0, e1 in ev])
+    return tuple(float(x) for x in np.percentile(t, [10, 50, 90]))
+
+
 def time_cold(fn, stream, steps: int, flush) -> float:
     """Seconds per call with the Infinity Cache (256 MB) flushed before each call: a 1 GiB write runs before each
     call, outside its event pair; the per-call event times are averaged."""
@@ -329,6 +345,10 @@ def run_workload(name: str, steps: int, warmup: int, multi_launch: bool, cold_st
          "cache_dtype": wl.cache_dtype, "algorithmic_bytes": nbytes, "achieved_gbs": round(achieved, 1),
          "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(wl.name),
          "dram_traffic": measured_traffic(wl.name, "dram_bytes_per_launch")}
+    # the spread of single ticks (a separate pass, so the back-to-back figure above has no events between calls)
+    p10, p50, p90 = time_each(step, stream, steps)
+    r.update({"us_per_tick_p10": round(p10 * 1e6, 2), "us_per_tick_median": round(p50 * 1e6, 2),
+              "us_per_tick_p90": round(p90 * 1e6, 2)})
     if cold_steps > 0:
         cold = time_cold(step, stream, cold_steps, flush)
         r["us_per_tick_mall_flushed"] = round(cold * 1e6, 2)
@@ -408,8 +428,8 @@ def run_backbone(batches=(1, 16), n_new: int = 4, steps: int = 10, warmup: int =
 
 # Tick time across cache lengths (one agent) and agent counts (1,024 rows each) of the full-size expert, bf16 cache,
 # no frame tokens: the shapes of Sec. 4.4's latency discussion, at the history lengths the cache can hold.
-SWEEP_LENGTHS = (0, 224, 1024, 4096, 16384)
-SWEEP_BATCHES = (1, 4, 16, 32)
+SWEEP_LENGTHS = (0, 104, 224, 464, 1024, 2048, 4096, 8192, 16384)
+SWEEP_BATCHES = (1, 2, 4, 8, 16, 32)
 
 
 def run_sweep(steps: int, warmup: int, out_md: str, command: str):
@@ -528,7 +548,9 @@ def main():
             append = extra
         if i == 0:
             head_wl = wl
-        print(f"# {name}: {r['us_per_tick']} us/tick, frac {r['frac']}", file=sys.stderr, flush=True)
+        print(f"# {name}: {r['us_per_tick']} us/tick, frac {r['frac']} (single ticks p10 / median / p90: "
+              f"{r['us_per_tick_p10']} / {r['us_per_tick_median']} / {r['us_per_tick_p90']} us)", file=sys.stderr,
+              flush=True)
     del flush_buf
     torch.cuda.empty_cache()
     ceiling = None if args.no_hbm_probe else hbm_ceiling(stream)
