@@ -64,6 +64,7 @@ class Workload:
     append_rows: int = 0  # rows appended per (agent, layer) by the append step
     head_kind: int = 0  # 0: mean-pool + linear head; 1: two-layer head over the waypoint queries
     head_hidden: int = 0  # hidden width of the two-layer head
+    stress_keys: bool = False  # cached keys with outlier channels, a growing scale and a sink row (stress_keys())
 
     @property
     def seq(self) -> int:
@@ -186,7 +187,22 @@ def cache_slab(wl: Workload, b: int, layer: int, kind: str, rows: Optional[int] 
     L = wl.lengths[b] if rows is None else rows
     tag = TAG_CACHE_K if kind == "k" else TAG_CACHE_V
     a = _normal([wl.wid, tag, b, layer], (L, wl.n_heads, wl.head_dim))
+    if kind == "k" and wl.stress_keys:
+        a = stress_keys(a)
     return round_to(a, wl.cache_dtype)
+
+
+def stress_keys(a: np.ndarray) -> np.ndarray:
+    """Keys [L][H][Dh] made hard for an online softmax: channels 0-3 of every head 8x (outlier channels, as in
+    the caches of large language models), row i scaled by 1 + 3 i / L (scores grow along the sequence, so a query's
+    running maximum keeps moving), and row floor(2L/3) a further 8x (a sink row far past the first tiles)."""
+    L = a.shape[0]
+    a = a.astype(np.float32).copy()
+    a[:, :, :4] *= 8.0
+    a *= (1.0 + 3.0 * np.arange(L, dtype=np.float32) / max(L, 1))[:, None, None]
+    if L > 0:
+        a[(2 * L) // 3] *= 8.0
+    return a
 
 
 def append_rows(wl: Workload, step: int, kind: str, n_rows: int) -> np.ndarray:

@@ -209,6 +209,27 @@ def test_whole_range_units_on_power_of_two_rings_match_oracle(cache_dtype, n_fra
     ex.close()
 
 
+# Stress keys (outlier channels, keys growing along the sequence, a sink row two thirds in; synth.stress_keys): the
+# scores reach ~15 in log2 units, so queries' running maxima jump by more than 2^8 after their first tiles and the
+# accumulators are rescaled in the middle of a range.  fp8: compared with the decoded codes (the outliers make the
+# per-head scale coarse for the other rows, an input property rather than a kernel error).
+@pytest.mark.parametrize("cache_dtype,n_frame", [("bf16", 0), ("fp8", 0), ("bf16", 30), ("fp8", 30)])
+def test_stress_keys_rescale_within_a_range_match_oracle(cache_dtype, n_frame):
+    wl = small(66, lengths=(700, 333, 90), capacity=720, cache_dtype=cache_dtype).replace(
+        n_frame_tokens=n_frame, stress_keys=True)
+    say(f"case stress keys, {cache_dtype}, {n_frame} frame tokens")
+    model = Model(wl)
+    ex = model.create()
+    cache = Cache(wl, starts=(15, 700, 0))
+    host_tok, tok = tokens_for(wl)
+    wp, _ = run_forward(ex, cache, tok, wl.batch, n_frame)
+    for b in range(wl.batch):
+        ref, _ = model.oracle_agent(host_tok[b], cache.oracle_rows(b, decoded=True), cache.desc.pos[b])
+        record(b, rel_err(wp[b], ref), BF16_WP_TOL,
+               what="waypoints vs decoded fp8, max|d| / max|ref|" if cache_dtype == "fp8" else "waypoints, max|d| / max|ref|")
+    ex.close()
+
+
 # 30, 64, 90 frame tokens: 3, 5 and 7 query tiles per agent (key-split jobs only; four whole jobs and one
 # key-split; two passes over the cache)
 @pytest.mark.parametrize("n_frame", [30, 64, 90])

@@ -46,3 +46,19 @@ def test_ragged_lengths_of_the_fp8_workload():
     wl = synth.WORKLOADS["ragged_fp8_B8"]
     assert len(wl.lengths) == 8 and all(256 <= L <= 16384 for L in wl.lengths)
     assert max(wl.lengths) <= wl.capacity
+
+
+def test_stress_keys_scale_channels_rows_and_the_sink_row():
+    # ones through the transform: channel factor (8 for channels 0-3), row ramp 1 + 3 i / L, sink row 8x more
+    L, H, D = 30, 2, 8
+    got = synth.stress_keys(np.ones((L, H, D), np.float32))
+    ramp = 1.0 + 3.0 * np.arange(L) / L
+    for i in range(L):
+        sink = 8.0 if i == 20 else 1.0
+        np.testing.assert_allclose(got[i, :, 4:], ramp[i] * sink, rtol=1e-6)
+        np.testing.assert_allclose(got[i, :, :4], 8.0 * ramp[i] * sink, rtol=1e-6)
+    # only the keys of a stress workload change; values and ordinary workloads are untouched
+    wl = synth.WORKLOADS["tiny_fp32_L40"]
+    ws = wl.replace(stress_keys=True)
+    np.testing.assert_array_equal(synth.cache_slab(ws, 0, 0, "v"), synth.cache_slab(wl, 0, 0, "v"))
+    np.testing.assert_allclose(synth.cache_slab(ws, 0, 0, "k"), synth.stress_keys(synth.cache_slab(wl, 0, 0, "k")))
