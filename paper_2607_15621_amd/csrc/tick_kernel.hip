@@ -1539,13 +1539,13 @@ __device__ __forceinline__ bool attn_unit_mq(const TickArgs& a, const TickParams
   // one step of the online softmax for the jobs that take tile i (index in its sequence)
   auto update = [&](auto kind, const auto& t, int i, int r0, int i1, float ksc) {
     constexpr int K = decltype(kind)::value;
+    // the job sets that occur: {0} and {0, 1} (with two jobs, the second never runs without the first: they share
+    // a key class, or the first takes the whole tile)
     const int act = act_of(i);
     if (act == 3)
       tile_jobs<K, 2, 3>(t, qf, r0, i1, ksc, o, m_run, l_run);
     else if (act == 1)
       tile_jobs<K, 2, 1>(t, qf, r0, i1, ksc, o, m_run, l_run);
-    else if (act == 2)
-      tile_jobs<K, 2, 2>(t, qf, r0, i1, ksc, o, m_run, l_run);
   };
 #pragma unroll 1
   for (int i = 0; i < nc; i += G) {
