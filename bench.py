@@ -432,6 +432,70 @@ SWEEP_LENGTHS = (0, 104, 224, 464, 1024, 2048, 4096, 8192, 16384)
 SWEEP_BATCHES = (1, 2, 4, 8, 16, 32)
 
 
+PHASE_NAMES = ("Q", "A", "O + R1", "F1", "D + R2")
+
+
+def run_phase_trace(names, out_md: str, command: str, layers=(8, 16), ticks: int = 4):
+    """Per-phase times of the tick kernel from its own timestamps (FSX_FLAG_TRACE: every workgroup stamps the end of
+    each phase of each layer with the 100 MHz real-time counter).  For each workload and layer: each phase's end,
+    median and latest over the workgroups, relative to the latest end of the previous layer; a phase's time is the
+    difference of consecutive median ends (the attention also to its latest end)."""
+    import numpy as np
+    import torch
+
+    import synth
+    from gpu_inputs import Model, tokens_for
+    from paper_2607_15621_amd import fsx
+
+    stream = torch.cuda.current_stream()
+    out = ["# Tick phases from the kernel's own timestamps", "",
+           "Each workgroup of the persistent tick kernel stamps the end of every phase of every layer "
+           "(`FSX_FLAG_TRACE`, 100 MHz real-time counter); the last of " + str(ticks) + " back-to-back ticks is read. "
+           "Ends are µs after the latest workgroup's end of the previous layer (median / latest over the workgroups; "
+           "for the attention over those that ran an attention unit); a phase's time is the difference of "
+           "consecutive median ends (attention: also to its latest end).", "", f"Command: `{command}`", ""]
+    for name in names:
+        wl = synth.WORKLOADS[name]
+        model = Model(wl)
+        ex = model.create(flags=fsx.FLAG_TRACE)
+        desc, keep = gpu_cache(wl, seed=1000 + wl.wid)
+        _, tok = tokens_for(wl)
+        wp = torch.zeros(wl.batch, wl.n_out, device="cuda")
+        for _ in range(ticks):
+            fsx.expert_forward(ex, desc, tok, wl.batch, wl.n_frame_tokens, wp, None, stream)
+        torch.cuda.synchronize()
+        fsx.expert_status(ex, stream)
+        tr = fsx.expert_trace(ex).astype(np.int64)
+        nl = wl.n_layers
+        t0 = tr[:, 0].min()
+        out += [f"## `{name}`: tick {(tr[:, 2 + 16 * nl].max() - t0) / 100.0:.1f} µs", "",
+                "| layer | phase | end, median | end, latest | time |", "|---:|---|---:|---:|---:|"]
+        for l in layers:
+            base = tr[:, 2 + 16 * (l - 1) + 4].max()
+            prev = 0.0
+            # workgroups that ran an attention unit in this tick (their first unit's mark is from this tick): with
+            # few segments only those stream the cache, the others end the phase at once
+            att = tr[:, 2 + 16 * l + 5 + 4] >= t0
+            for e, ph in enumerate(PHASE_NAMES):
+                v = tr[:, 2 + 16 * l + e]
+                if ph == "A" and att.any():
+                    v = v[att]
+                v = (v[v >= t0] - base) / 100.0
+                med, last = float(np.median(v)), float(v.max())
+                t = f"{med - prev:.1f}" + (f" / {last - prev:.1f}" if ph == "A" else "")
+                out.append(f"| {l} | {ph} | {med:.1f} | {last:.1f} | {t} |")
+                prev = med
+            out.append(f"| {l} | layer | | {(tr[:, 2 + 16 * l + 4].max() - base) / 100.0:.1f} | |")
+        out.append("")
+        print(f"# phases {name}: done", file=sys.stderr, flush=True)
+        ex.close()
+        del keep, desc
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    with open(out_md, "w") as f:
+        f.write("\n".join(out))
+
+
 def run_sweep(steps: int, warmup: int, out_md: str, command: str):
     import torch
 
@@ -506,6 +570,8 @@ def main():
     ap.add_argument("--command", action="append", default=[], help="command recorded in a summary")
     ap.add_argument("--sweep", metavar="MD", help="time the tick across cache lengths and agent counts and write "
                     "the table to MD")
+    ap.add_argument("--phase-trace", metavar="MD", help="per-phase times of the workloads' ticks from the kernel's "
+                    "timestamps, written to MD")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -527,6 +593,11 @@ def main():
     import torch
 
     torch.cuda.set_device(0)
+    if args.phase_trace:
+        argv = [os.path.basename(x) if x == args.phase_trace else x for x in sys.argv[1:]]
+        run_phase_trace([n for n in args.workload.split(",") if n], args.phase_trace,
+                        " ".join(["python", "bench.py"] + argv))
+        return
     if args.sweep:
         # the recorded command names the output file by its base name (the directory is the caller's choice)
         argv = [os.path.basename(x) if x == args.sweep else x for x in sys.argv[1:]]
