@@ -470,6 +470,7 @@ def run_phase_trace(names, out_md: str, command: str, layers=(8, 16), ticks: int
         t0 = tr[:, 0].min()
         out += [f"## `{name}`: tick {(tr[:, 2 + 16 * nl].max() - t0) / 100.0:.1f} µs", "",
                 "| layer | phase | end, median | end, latest | time |", "|---:|---|---:|---:|---:|"]
+        xcd_notes = []
         for l in layers:
             base = tr[:, 2 + 16 * (l - 1) + 4].max()
             prev = 0.0
@@ -486,6 +487,14 @@ def run_phase_trace(names, out_md: str, command: str, layers=(8, 16), ticks: int
                 out.append(f"| {l} | {ph} | {med:.1f} | {last:.1f} | {t} |")
                 prev = med
             out.append(f"| {l} | layer | | {(tr[:, 2 + 16 * l + 4].max() - base) / 100.0:.1f} | |")
+            # the attention's latest end on each XCD (workgroup w runs on XCD w mod 8, as the create-time probe
+            # measures on this device)
+            a_end = (tr[:, 2 + 16 * l + 1] - base) / 100.0
+            per_x = [float(a_end[x::8][att[x::8]].max()) if att[x::8].any() else float(a_end[x::8].max())
+                     for x in range(8)]
+            xcd_notes.append(f"layer {l}: " + ", ".join(f"{v:.1f}" for v in per_x) +
+                             f" (spread {max(per_x) - min(per_x):.1f} µs)")
+        out += ["", "Latest attention end per XCD (µs, XCD 0..7):", ""] + [f"* {n}" for n in xcd_notes]
         out.append("")
         print(f"# phases {name}: done", file=sys.stderr, flush=True)
         ex.close()
