@@ -311,7 +311,24 @@ def hbm_ceiling(stream, nbytes: int = 4 << 30, reps: int = 10):
     for mode, name in ((0, "register_loads_gbs"), (1, "lds_direct_loads_gbs")):
         t = time_launches(lambda: fsx.probe_hbm_read(buf, nbytes, mode, sink, stream), stream, reps, 2)
         out[name] = round(nbytes / t / 1e9, 1)
-    del buf
+    # a 128 MiB pass (direct loads) right after a pass over the same bytes (held in the 256 MB Infinity Cache)
+    # against one after a pass over 1 GiB of other bytes: what the cache gives a re-read
+    small = 128 << 20
+    part, rest = buf[:small], buf[small:small + (1 << 30)]
+
+    def one_pass(before):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        fsx.probe_hbm_read(before, before.numel(), 1, sink, stream)
+        e0.record(stream)
+        fsx.probe_hbm_read(part, small, 1, sink, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / 1e3
+
+    for name, before in (("reread_128MiB_gbs", part), ("after_other_1GiB_128MiB_gbs", rest)):
+        t = sorted(one_pass(before) for _ in range(7))[3]
+        out[name] = round(small / t / 1e9, 1)
+    del buf, part, rest
     torch.cuda.empty_cache()
     return out
 
