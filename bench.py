@@ -186,6 +186,36 @@ def summarize_traffic(dirs, workload: str, copy_bytes: int, commands, dram: bool
     print(path, json.dumps({k: v for k, v in d.items() if k.endswith("bytes_per_launch")}))
 
 
+INSTR_COUNTERS = ("SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_INSTS_LDS", "SQ_INSTS_SALU", "SQ_INSTS_VMEM",
+                  "SQ_LDS_BANK_CONFLICT", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES")
+
+
+def summarize_counters(dirs, workloads, commands):
+    """profiles/instructions_tick.md: instruction counts of one tick-kernel launch per workload (wave-level
+    instructions summed over the device), LDS bank-conflict cycles and the MFMA busy fraction, from rocprofv3 --pmc
+    runs (dirs: for each workload in turn, one directory per pass)."""
+    per = len(dirs) // len(workloads)
+    out = ["# Instruction mix of the tick kernel", "",
+           "One tick-kernel launch per workload, counters summed over the device and averaged over the profiled "
+           "launches: wave-level instructions by kind, LDS bank-conflict cycles, and the busy cycles of the MFMA "
+           "units against those of the shader sequencers (SQ_VALU_MFMA_BUSY_CYCLES / SQ_BUSY_CYCLES; the counters "
+           "count in different units per block, so the ratio compares launches, not an absolute utilisation).", "",
+           "Commands (from the repository root, on one MI355X, one pass each):", "", "```"] + list(commands) + \
+          ["```", "", "| workload | " + " | ".join(c.replace("SQ_", "") for c in INSTR_COUNTERS) + " |",
+           "|---|" + "---:|" * len(INSTR_COUNTERS)]
+    for i, w in enumerate(workloads):
+        vals = {}
+        for d in dirs[i * per:(i + 1) * per]:
+            for r in _csv_rows(d, "counter_collection.csv"):
+                if "k_tick" in r["Kernel_Name"]:
+                    vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+        cells = [f"{sum(vals[c]) / len(vals[c]):,.0f}" if c in vals else "–" for c in INSTR_COUNTERS]
+        out.append(f"| `{w}` | " + " | ".join(cells) + " |")
+    path = os.path.join(ROOT, "profiles", "instructions_tick.md")
+    open(path, "w").write("\n".join(out) + "\n")
+    print(path)
+
+
 def summarize_parity(log: str, command: str):
     """profiles/parity_errors.md from the JSON lines the GPU parity tests append (one per comparison): per test, the
     number of comparisons and the worst error against its tolerance; then every comparison of the full-size
@@ -593,6 +623,8 @@ def main():
                     "TCC_EA0_RDREQ_DRAM_sum / TCC_EA0_WRREQ_DRAM_sum runs")
     ap.add_argument("--copy-bytes", type=int, default=0)
     ap.add_argument("--summarize-parity", metavar="JSONL", help="write profiles/parity_errors.md from the parity log")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="DIR", help="write profiles/instructions_tick.md from "
+                    "rocprofv3 --pmc runs of the workloads (in --workload order, the same number of passes each)")
     ap.add_argument("--command", action="append", default=[], help="command recorded in a summary")
     ap.add_argument("--sweep", metavar="MD", help="time the tick across cache lengths and agent counts and write "
                     "the table to MD")
@@ -607,6 +639,9 @@ def main():
         return
     if args.summarize_parity:
         summarize_parity(args.summarize_parity, " && ".join(args.command))
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, [n for n in args.workload.split(",") if n], args.command)
         return
     if args.summarize_traffic:
         summarize_traffic(args.summarize_traffic, args.workload, args.copy_bytes, args.command, args.dram)
