@@ -515,7 +515,10 @@ def run_phase_trace(names, out_md: str, command: str, layers=(8, 16), ticks: int
         tr = fsx.expert_trace(ex).astype(np.int64)
         nl = wl.n_layers
         t0 = tr[:, 0].min()
-        out += [f"## `{name}`: tick {(tr[:, 2 + 16 * nl].max() - t0) / 100.0:.1f} µs", "",
+        pre = (tr[:, 1].max() - t0) / 100.0  # registration, attention plan, embedding: every workgroup done
+        post = (tr[:, 2 + 16 * nl].max() - tr[:, 2 + 16 * (nl - 1) + 4].max()) / 100.0  # the head
+        out += [f"## `{name}`: tick {(tr[:, 2 + 16 * nl].max() - t0) / 100.0:.1f} µs "
+                f"(before the first layer {pre:.1f} µs, after the last {post:.1f} µs)", "",
                 "| layer | phase | end, median | end, latest | time |", "|---:|---|---:|---:|---:|"]
         xcd_notes = []
         for l in layers:
