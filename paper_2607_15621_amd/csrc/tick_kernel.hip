@@ -1989,6 +1989,50 @@ __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& 
   }
   if (uni(L.X) != 0) return;
   const int s = uni(L.s), n = uni(L.n0);
+  // Thread tid's two columns (n0, n1) of the head weights for every output, and their final gains: independent of
+  // the last layer, so loaded before the wait, all at once (loaded one per step of the product they were as many
+  // dependent memory round trips as the product has steps)
+  constexpr int HO_MAX = 16;
+  const bool regs = dm.n_out <= HO_MAX && s < tp.B;
+  float hw0[HO_MAX], hw1[HO_MAX], g0 = 0.f, g1 = 0.f;
+  if (regs && dm.head_kind != 1) {
+    // every load unconditional (indices clamped in range, the unused values zeroed afterwards) and the dtype branch
+    // outside the loop, so the loads issue back to back and cost one round trip
+    const int no = dm.n_out, c0 = tid < d ? tid : d - 1, c1 = tid + NTHR < d ? tid + NTHR : d - 1;
+    const bool in0 = tid < d, in1 = tid + NTHR < d;
+    if (a.head_dtype == FSX_BF16) {
+      const uint16_t* hw = reinterpret_cast<const uint16_t*>(a.head_w);
+      uint16_t r0[HO_MAX], r1[HO_MAX];
+#pragma unroll
+      for (int o = 0; o < HO_MAX; ++o) {
+        const int64_t row = (int64_t)(o < no ? o : no - 1) * d;
+        r0[o] = hw[row + c0];
+        r1[o] = hw[row + c1];
+      }
+#pragma unroll
+      for (int o = 0; o < HO_MAX; ++o) {
+        hw0[o] = o < no && in0 ? bf16_to_f32(r0[o]) : 0.f;
+        hw1[o] = o < no && in1 ? bf16_to_f32(r1[o]) : 0.f;
+      }
+    } else {
+      const float* hw = reinterpret_cast<const float*>(a.head_w);
+#pragma unroll
+      for (int o = 0; o < HO_MAX; ++o) {
+        const int64_t row = (int64_t)(o < no ? o : no - 1) * d;
+        hw0[o] = hw[row + c0];
+        hw1[o] = hw[row + c1];
+      }
+#pragma unroll
+      for (int o = 0; o < HO_MAX; ++o) {
+        hw0[o] = o < no && in0 ? hw0[o] : 0.f;
+        hw1[o] = o < no && in1 ? hw1[o] : 0.f;
+      }
+    }
+    g0 = a.final_norm[c0];
+    g1 = a.final_norm[c1];
+    g0 = in0 ? g0 : 0.f;
+    g1 = in1 ? g1 : 0.f;
+  }
   for (int b = s; b < tp.B; b += n) {
     ok = wg_wait(a.f_out, d / 16 * tp.rblk, stamp_of(a, nl - 1, nl), a, L);  // every piece of the last layer
     if (!ok) {
@@ -2036,6 +2080,25 @@ __device__ __forceinline__ void phase_head(const TickArgs& a, const TickParams& 
         }
       }
       __syncthreads();
+    }
+    if (regs) {
+      // the pooled row's two columns of this thread times its weights, summed per wave, then over the 4 waves
+      const float x0 = xm0 * g0 / (float)T, x1 = xm1 * g1 / (float)T;
+#pragma unroll
+      for (int o = 0; o < HO_MAX; ++o) {
+        if (o < dm.n_out) {
+          const float p = wave_sum(x0 * hw0[o] + x1 * hw1[o]);
+          if (lane == 0) L.red2[wave][o] = p;
+        }
+      }
+      __syncthreads();
+      if (tid < dm.n_out) {
+        float acc = 0.f;
+        for (int w = 0; w < NTHR / WAVE; ++w) acc += L.red2[w][tid];
+        st_dev_f(a.waypoints + (int64_t)b * dm.n_out + tid, acc);
+      }
+      __syncthreads();
+      continue;
     }
     float* xm = L.tmp;
     if (n0 < d) xm[n0] = xm0 * a.final_norm[n0] / (float)T;
