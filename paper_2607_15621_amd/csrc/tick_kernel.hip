@@ -120,12 +120,15 @@ __device__ __forceinline__ bool wave_wait(const uint64_t* flags, int n, uint64_t
       fi[g] = i < n ? ((int64_t)(i / inner) * stride + i % inner) * FPAD : -1;
     }
     for (uint32_t spin = 0;; ++spin) {
+      // every group's loads issued, unconditionally, before any is checked: lanes past the end load flag 0 and ignore
+      // it (a load behind a branch, or selected against a constant, is waited for where the branches join, which
+      // made each group of a poll one more memory round trip)
       uint64_t v[GR];
 #pragma unroll
-      for (int g = 0; g < GR; ++g) v[g] = fi[g] >= 0 ? ld_dev(flags + fi[g]) : target;
+      for (int g = 0; g < GR; ++g) v[g] = ld_dev(flags + (fi[g] >= 0 ? fi[g] : 0));
       bool ok = true;
 #pragma unroll
-      for (int g = 0; g < GR; ++g) ok = ok && v[g] >= target;
+      for (int g = 0; g < GR; ++g) ok = ok && (fi[g] < 0 || v[g] >= target);
       if (__all(ok)) break;
       __builtin_amdgcn_s_sleep(1);
       if (timed_out(a, t0, spin)) {
@@ -211,13 +214,17 @@ __device__ __forceinline__ bool xcd_register(const TickArgs& a, TickLds& L) {
     bool ok = true;
     for (uint32_t spin = 0;; ++spin) {
       bool all = true;
+      // all of the lane's words loaded, unconditionally, before any is checked (a lane past the grid loads word 0
+      // and ignores it)
+      uint64_t v[EPL];
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) v[e] = ld_dev(a.reg + (e * WAVE + lane < G ? e * WAVE + lane : 0));
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
         if (!have[e]) {
-          const uint64_t v = ld_dev(a.reg + e * WAVE + lane);
-          if ((v >> 8) == a.epoch) {
+          if ((v[e] >> 8) == a.epoch) {
             have[e] = true;
-            xc[e] = (uint32_t)(v & 0xffu);
+            xc[e] = (uint32_t)(v[e] & 0xffu);
           } else {
             all = false;
           }
