@@ -545,6 +545,28 @@ def run_phase_trace(names, out_md: str, command: str, layers=(8, 16), ticks: int
             xcd_notes.append(f"layer {l}: " + ", ".join(f"{v:.1f}" for v in per_x) +
                              f" (spread {max(per_x) - min(per_x):.1f} µs)")
         out += ["", "Latest attention end per XCD (µs, XCD 0..7):", ""] + [f"* {n}" for n in xcd_notes]
+        # over every layer after the first: each XCD's latest attention end, and each slot's end against the median
+        # of its XCD (slot s of an XCD is workgroup 8 s + XCD; a slot's slice of the attention is the same in every
+        # layer), which tell a slow XCD from slices that the plan weighs wrongly
+        per_x, rel = [], []
+        for l in range(1, nl):
+            base = tr[:, 2 + 16 * (l - 1) + 4].max()
+            a_end = (tr[:, 2 + 16 * l + 1] - base) / 100.0
+            ran = tr[:, 2 + 16 * l + 5 + 4] >= t0
+            per_x.append([float(a_end[x::8][ran[x::8]].max()) if ran[x::8].any() else float(a_end[x::8].max())
+                          for x in range(8)])
+            r = np.zeros_like(a_end)
+            for x in range(8):
+                r[x::8] = a_end[x::8] - np.median(a_end[x::8])
+            rel.append(r)
+        px, rel = np.array(per_x).mean(0), np.array(rel)
+        n_slot = tr.shape[0] // 8
+        slot_mean = [float(rel[:, 8 * k:8 * k + 8].mean()) for k in range(n_slot)]
+        out += ["", f"Layers 2..{nl}: latest attention end per XCD, mean over the layers (µs, XCD 0..7): " +
+                ", ".join(f"{v:.1f}" for v in px) + f"; the latest of all, mean over the layers: "
+                f"{float(np.array(per_x).max(1).mean()):.1f}.", "",
+                "Attention end of each slot against the median of its XCD, mean over the layers and XCDs (µs, slot "
+                "0..): " + ", ".join(f"{v:+.1f}" for v in slot_mean) + "."]
         out.append("")
         print(f"# phases {name}: done", file=sys.stderr, flush=True)
         ex.close()
