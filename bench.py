@@ -482,6 +482,32 @@ SWEEP_BATCHES = (1, 2, 4, 8, 16, 32)
 PHASE_NAMES = ("Q", "A", "O + R1", "F1", "D + R2")
 
 
+def attention_tail(tr, nl: int, t0: int, nx: int = 8):
+    """Over every layer after the first, from a tick's phase trace (rows: workgroups, w on XCD w mod nx; words
+    2 + 16 l + e: end of phase e of layer l, 2 + 16 l + 5 + 4: end of the first attention unit, 100 MHz): each
+    XCD's latest attention end (µs after the previous layer's end) averaged over the layers, the latest of all
+    averaged over the layers, and each slot's attention end against the median of its XCD, averaged over the layers
+    and XCDs (slot k of an XCD is workgroup nx k + XCD; its slice of the attention is the same in every layer).
+    These tell an XCD that is slow from slices that the plan weighs wrongly."""
+    import numpy as np
+
+    per_x, rel = [], []
+    for l in range(1, nl):
+        base = tr[:, 2 + 16 * (l - 1) + 4].max()
+        a_end = (tr[:, 2 + 16 * l + 1] - base) / 100.0
+        ran = tr[:, 2 + 16 * l + 5 + 4] >= t0  # ran an attention unit in this tick
+        per_x.append([float(a_end[x::nx][ran[x::nx]].max()) if ran[x::nx].any() else float(a_end[x::nx].max())
+                      for x in range(nx)])
+        r = np.zeros_like(a_end)
+        for x in range(nx):
+            r[x::nx] = a_end[x::nx] - np.median(a_end[x::nx])
+        rel.append(r)
+    per_x, rel = np.array(per_x), np.array(rel)
+    n_slot = tr.shape[0] // nx
+    slot_mean = [float(rel[:, nx * k:nx * k + nx].mean()) for k in range(n_slot)]
+    return [float(v) for v in per_x.mean(0)], float(per_x.max(1).mean()), slot_mean
+
+
 def run_phase_trace(names, out_md: str, command: str, layers=(8, 16), ticks: int = 4):
     """Per-phase times of the tick kernel from its own timestamps (FSX_FLAG_TRACE: every workgroup stamps the end of
     each phase of each layer with the 100 MHz real-time counter).  For each workload and layer: each phase's end,
@@ -545,26 +571,9 @@ def run_phase_trace(names, out_md: str, command: str, layers=(8, 16), ticks: int
             xcd_notes.append(f"layer {l}: " + ", ".join(f"{v:.1f}" for v in per_x) +
                              f" (spread {max(per_x) - min(per_x):.1f} µs)")
         out += ["", "Latest attention end per XCD (µs, XCD 0..7):", ""] + [f"* {n}" for n in xcd_notes]
-        # over every layer after the first: each XCD's latest attention end, and each slot's end against the median
-        # of its XCD (slot s of an XCD is workgroup 8 s + XCD; a slot's slice of the attention is the same in every
-        # layer), which tell a slow XCD from slices that the plan weighs wrongly
-        per_x, rel = [], []
-        for l in range(1, nl):
-            base = tr[:, 2 + 16 * (l - 1) + 4].max()
-            a_end = (tr[:, 2 + 16 * l + 1] - base) / 100.0
-            ran = tr[:, 2 + 16 * l + 5 + 4] >= t0
-            per_x.append([float(a_end[x::8][ran[x::8]].max()) if ran[x::8].any() else float(a_end[x::8].max())
-                          for x in range(8)])
-            r = np.zeros_like(a_end)
-            for x in range(8):
-                r[x::8] = a_end[x::8] - np.median(a_end[x::8])
-            rel.append(r)
-        px, rel = np.array(per_x).mean(0), np.array(rel)
-        n_slot = tr.shape[0] // 8
-        slot_mean = [float(rel[:, 8 * k:8 * k + 8].mean()) for k in range(n_slot)]
+        px, latest, slot_mean = attention_tail(tr, nl, t0)
         out += ["", f"Layers 2..{nl}: latest attention end per XCD, mean over the layers (µs, XCD 0..7): " +
-                ", ".join(f"{v:.1f}" for v in px) + f"; the latest of all, mean over the layers: "
-                f"{float(np.array(per_x).max(1).mean()):.1f}.", "",
+                ", ".join(f"{v:.1f}" for v in px) + f"; the latest of all, mean over the layers: {latest:.1f}.", "",
                 "Attention end of each slot against the median of its XCD, mean over the layers and XCDs (µs, slot "
                 "0..): " + ", ".join(f"{v:+.1f}" for v in slot_mean) + "."]
         out.append("")

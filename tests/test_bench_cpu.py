@@ -86,3 +86,24 @@ def test_traffic_summary_scales_by_the_copy_calibration(tmp_path, monkeypatch):
     assert d["fetch_bytes_per_launch"] == int(2000 * (1 << 20) / 4000)
     assert d["write_bytes_per_launch"] == int(500 * (1 << 20) / 8000)
     assert d["source_hash"] == real_hash
+
+
+def test_attention_tail_separates_a_slow_xcd_from_a_late_slot():
+    """A synthetic phase trace (256 workgroups, workgroup w on XCD w mod 8, slot w // 8): XCD 3 ends every layer's
+    attention 5 µs late and slot 7 of every XCD 2 µs late."""
+    np = pytest.importorskip("numpy")
+    G, nl, t0 = 256, 4, 1000
+    tr = np.zeros((G, 2 + 16 * nl + 1), dtype=np.int64)
+    w = np.arange(G)
+    for l in range(nl):
+        start = t0 + 100_000 * l  # the previous layer's latest end
+        extra = 5.0 * (w % 8 == 3) + 2.0 * (w // 8 == 7)
+        tr[:, 2 + 16 * l + 1] = start + ((100.0 + extra) * 100).astype(np.int64)
+        tr[:, 2 + 16 * l + 4] = t0 + 100_000 * (l + 1)  # every workgroup ends the layer at once
+        tr[:, 2 + 16 * l + 5 + 4] = start + 50  # every workgroup ran an attention unit
+    per_x, latest, slot_mean = bench.attention_tail(tr, nl, t0)
+    assert per_x == pytest.approx([102.0] * 3 + [107.0] + [102.0] * 4)
+    assert latest == pytest.approx(107.0)
+    assert len(slot_mean) == 32
+    assert slot_mean[7] == pytest.approx(2.0)
+    assert all(v == pytest.approx(0.0) for k, v in enumerate(slot_mean) if k != 7)
