@@ -263,6 +263,8 @@ def gpu_cache(wl, seed: int):
     g.manual_seed(seed)
     for b in range(B):
         L = wl.lengths[b]
+        if L == 0:
+            continue  # no rows (and scales of 1)
         for l in range(nl):
             for t, sc in ((k, ks), (v, vs)):
                 x = torch.randn((H, L, Dh), generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
@@ -586,7 +588,7 @@ def run_phase_trace(names, out_md: str, command: str, layers=(8, 16), ticks: int
         f.write("\n".join(out))
 
 
-def run_sweep(steps: int, warmup: int, out_md: str, command: str):
+def run_sweep(steps: int, warmup: int, out_md: str, command: str, cache_dtype: str = "bf16"):
     import torch
 
     import synth
@@ -598,7 +600,7 @@ def run_sweep(steps: int, warmup: int, out_md: str, command: str):
     stream = torch.cuda.current_stream()
     for i, (B, L) in enumerate(points):
         wl = synth.Workload(name=f"sweep_B{B}_L{L}", wid=100 + i, n_frame_tokens=0, batch=B, lengths=(L,) * B,
-                            dtype="bf16", cache_dtype="bf16", capacity=max(L, 1), **synth.FULL)
+                            dtype="bf16", cache_dtype=cache_dtype, capacity=max(L, 1), **synth.FULL)
         model = Model(wl)
         ex = model.create()
         info = fsx.expert_info(ex)
@@ -621,8 +623,9 @@ def run_sweep(steps: int, warmup: int, out_md: str, command: str):
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
     out = ["# Tick time across cache lengths and agent counts", "",
-           "Full-size expert (32 layers, width 512, 32 heads x 128, SwiGLU 2048, 10 expert tokens), bf16 weights "
-           "and cache, no frame tokens, seeded synthetic inputs; one persistent tick-kernel launch per tick, "
+           "Full-size expert (32 layers, width 512, 32 heads x 128, SwiGLU 2048, 10 expert tokens), bf16 weights, "
+           f"{'fp8 (E4M3, a scale per agent, layer and head for K and for V)' if cache_dtype == 'fp8' else 'bf16'} cache, no frame tokens, seeded "
+           "synthetic inputs; one persistent tick-kernel launch per tick, "
            f"{steps} back-to-back launches timed with HIP events after {warmup} warm-up launches. `frac` is the "
            "algorithmic bytes (weights once, every cached K/V row once) per tick over 8 TB/s.", "",
            f"Command: `{command}`", "",
@@ -662,6 +665,7 @@ def main():
     ap.add_argument("--command", action="append", default=[], help="command recorded in a summary")
     ap.add_argument("--sweep", metavar="MD", help="time the tick across cache lengths and agent counts and write "
                     "the table to MD")
+    ap.add_argument("--sweep-cache", choices=("bf16", "fp8"), default="bf16", help="cache element type of --sweep")
     ap.add_argument("--phase-trace", metavar="MD", help="per-phase times of the workloads' ticks from the kernel's "
                     "timestamps, written to MD")
     args = ap.parse_args()
@@ -696,7 +700,7 @@ def main():
     if args.sweep:
         # the recorded command names the output file by its base name (the directory is the caller's choice)
         argv = [os.path.basename(x) if x == args.sweep else x for x in sys.argv[1:]]
-        run_sweep(args.steps, args.warmup, args.sweep, " ".join(["python", "bench.py"] + argv))
+        run_sweep(args.steps, args.warmup, args.sweep, " ".join(["python", "bench.py"] + argv), args.sweep_cache)
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
         return
